@@ -1,0 +1,175 @@
+"""Benchmark of the device-side LSTM while-loop: forward + gradient loop.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step = lstm_loop_fwd (save_for_backward) + lstm_loop_bwd over one batch
+of synthetic input already resident in device memory.  Prints one JSON line:
+throughput in timesteps*sequences per second (sum of the sequence lengths per
+step / step time), the matrix-core utilisation against the dense peak of the
+operand type, the time per loop iteration, a roofline entry for the dominant
+kernel (timed with HIP events on the launch stream inside the timed region),
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "LSTM fwd+bwd timesteps·seqs/sec at H=1024; MFMA util; per-iteration µs"
+PEAK = {"bf16": 2.5e15, "f32": 157.3e12}     # MI355X dense matrix-core peaks, flop/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="lstm_b128_h1024_tmax200_varlen_bf16")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU work of the oracle baseline sample (0 = skip)")
+    return ap.parse_args()
+
+
+def stage_flops(w, sum_len):
+    """Algorithmic flops per launch of each stage (per layer)."""
+    H = w.H
+    out = {}
+    for l in range(w.layers):
+        I = w.I if l == 0 else w.H
+        out.setdefault("fwd_loop", []).append(8.0 * H * H * sum_len)
+        out.setdefault("bwd_loop", []).append(8.0 * H * H * sum_len)
+        out.setdefault("input_proj", []).append(8.0 * H * I * sum_len)
+        out.setdefault("dw", []).append(8.0 * H * (I + H) * sum_len)
+        out.setdefault("dx", []).append(8.0 * H * I * sum_len)
+    return {k: float(np.mean(v)) for k, v in out.items()}
+
+
+def cpu_baseline(w, inp, target_s):
+    """The oracle as it is (float64, bf16-emulating for bf16 workloads), on the
+    full batch but only the first T_s time steps, T_s chosen for about
+    `target_s` seconds of work."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    precision = "bf16" if w.dtype == "bf16" else "fp64"
+
+    def run(Ts):
+        sl = np.minimum(inp["seq_len"], Ts)
+        x = inp["x"][:Ts].astype(np.float64)
+        dy = inp["dy"][:Ts].astype(np.float64) if inp["dy"] is not None else None
+        Ws = [a.astype(np.float64) for a in inp["W"]]
+        bs = [a.astype(np.float64) for a in inp["bias"]]
+        t0 = time.perf_counter()
+        y, hT, cT, tapes = oracle.stacked_forward(x, sl, Ws, bs, inp["h0"].astype(np.float64),
+                                                  inp["c0"].astype(np.float64), precision)
+        oracle.stacked_backward(tapes, dy, inp["dhT"].astype(np.float64),
+                                inp["dcT"].astype(np.float64))
+        return time.perf_counter() - t0, int(sl.sum())
+
+    T_eff = int(inp["seq_len"].max())
+    dt, _ = run(2)
+    Ts = int(max(2, min(T_eff, target_s / max(dt / 2, 1e-6))))
+    dt, n = run(Ts)
+    return {"value": n / dt, "unit": "timesteps·seqs/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"full batch B={w.B}, first {Ts} of {T_eff} loop iterations "
+                      f"({n} timesteps*seqs), {precision} oracle fwd+bwd, {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the data-parallel split over GPUs is described, not run)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_1805_01772_amd import workloads as wl
+    from paper_1805_01772_amd.runner import DeviceCase
+
+    w = wl.BY_NAME[args.workload]
+    inp = wl.generate(w)
+    sum_len = int(inp["seq_len"].sum())
+    T_eff = int(inp["seq_len"].max())
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, device="cuda:0")
+    plan = dc.plan()
+    for _ in range(args.warmup):
+        dc.fwd(plan)
+        dc.bwd(plan)
+    torch.cuda.synchronize()
+    if plan.status_sync() != 0:
+        raise RuntimeError("device error during warmup")
+    plan.set_timing(True)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        dc.fwd(plan)
+        dc.bwd(plan)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    stages = plan.read_timing()
+    plan.set_timing(False)
+    err = plan.status_sync()
+    if err:
+        raise RuntimeError(f"device error word {err}")
+    geom = plan.geometry()
+    plan.close()
+
+    ms_per_step = gpu_ms / args.steps
+    value = sum_len / (ms_per_step / 1e3)
+    flops = wl.algorithmic_flops(w, inp["seq_len"])
+    mfma_util = flops / (ms_per_step / 1e3) / PEAK[w.dtype]
+    sflops = stage_flops(w, sum_len)
+    per_launch = {k: (ms / n if n else 0.0) for k, (ms, n) in stages.items()}
+    dom = max(("fwd_loop", "bwd_loop", "input_proj", "dw", "dx"), key=lambda k: stages[k][0])
+    achieved = sflops[dom] / (per_launch[dom] / 1e3) / 1e12
+    peak_tf = PEAK[w.dtype] / 1e12
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "timesteps·seqs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "I": w.I, "H": w.H, "T_max": w.T_max,
+                   "layers": w.layers, "seq_len": f"U{{{w.len_lo}..{w.len_hi}}}",
+                   "sum_len": sum_len, "T_eff": T_eff, "loop_workgroups": geom["workgroups"],
+                   "units_per_workgroup": geom["units_per_workgroup"]},
+        "mfma_util": mfma_util,
+        "per_iteration_us": ms_per_step * 1e3 / T_eff if T_eff else None,
+        "algorithmic_tflops": flops / (ms_per_step / 1e3) / 1e12,
+        "host_wall_ms_per_step": wall * 1e3 / args.steps,
+        "stage_ms_per_step": {k: ms / args.steps for k, (ms, n) in stages.items()},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak_tf,
+                     "unit": "TFLOP/s", "frac": achieved / peak_tf, "traffic": None,
+                     "per_launch_ms": per_launch[dom],
+                     "algorithmic_flops_per_launch": sflops[dom]},
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

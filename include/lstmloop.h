@@ -1,0 +1,206 @@
+/*
+ * lstmloop: a device-side, data-dependent LSTM while-loop and its gradient
+ * loop for AMD Instinct MI355X (gfx950).
+ *
+ * What the library computes (Dynamic Control Flow in Large-Scale Machine
+ * Learning, Sections 2.1, 4.2, 5.1-5.3, 6.2):
+ *
+ *   while_loop(pred, body, inits) with pred = (t < T_eff), where
+ *   T_eff = max_b seq_len[b] is decided on the GPU (no host round trip per
+ *   step); a loop whose predicate is false at entry returns its inits
+ *   (Section 4.2).  The body is one LSTM step (textbook cell with forget
+ *   gate, gate column blocks i, f, g, o):
+ *       z = [x_t, h_{t-1}] W + b;  i,f,o = sigmoid;  g = tanh
+ *       c_t = f*c_{t-1} + i*g;     h_t = o*tanh(c_t)
+ *   Rows with t >= seq_len[b] keep their state and output y = 0.
+ *   Each iteration pushes what the gradient needs onto a stack (Section 5.1);
+ *   the gradient loop runs the same number of iterations in reverse, pops
+ *   the stack, carries dh/dc as loop variables and sums the gradients of the
+ *   loop constants (W, bias) over iterations (Section 5.1).  The gradient of
+ *   reading x_t is a write of dx_t (Section 5.2).  The stack can be swapped
+ *   out to pinned host memory on copy streams that run beside the compute
+ *   stream and prefetched back before the gradient loop needs it
+ *   (Section 5.3).
+ *
+ * Conventions for every entry point
+ *   - Array arguments are DEVICE pointers owned by the caller, contiguous,
+ *     row-major.  Sequences are time-major: x [T_max,B,I], y/dy [T_max,B,H],
+ *     dx [T_max,B,I].  Per-layer arrays are passed as HOST arrays of device
+ *     pointers (length = layers).
+ *   - W of layer l is [I_l + H, 4H]: rows 0..I_l-1 multiply x_t, rows
+ *     I_l..I_l+H-1 multiply h_{t-1}; column blocks are gates i, f, g, o.
+ *     I_0 = I, I_1 = H.  Its element type is desc.dtype (float or bfloat16
+ *     bits); bias is always float [4H].
+ *   - State, stack and accumulation are float32.  In LL_BF16 mode the
+ *     matrix-core operands are bfloat16 (round to nearest even): x, W,
+ *     h_{t-1} in the forward; dz, [x_t, h_{t-1}] and W in the backward.
+ *     Layer 2 reads bf16(y of layer 1).  db sums unrounded dz.
+ *   - `stream` is a hipStream_t passed as void*.  Compute calls are
+ *     asynchronous on it; they return after enqueueing.
+ *   - A plan serves one stream at a time.  Calls on one plan must not
+ *     overlap.
+ *   - Errors: checkable arguments give an error code synchronously and the
+ *     thread-local message of ll_last_error(); nothing is enqueued then.
+ *     Data-dependent errors (seq_len outside [0, T_max]) are detected on the
+ *     device: the loops then run zero iterations and ll_status_sync()
+ *     reports a nonzero device error word.  No exception or abort crosses
+ *     this interface.
+ */
+#ifndef LSTMLOOP_H
+#define LSTMLOOP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LL_OK = 0,
+  LL_EINVAL = 1,        /* bad argument (null pointer, shape, state)        */
+  LL_ENOMEM = 2,        /* device or pinned host allocation failed          */
+  LL_EHIP = 3,          /* a HIP runtime call failed                        */
+  LL_ESTATE = 4,        /* backward without a matching saved forward        */
+  LL_EUNSUPPORTED = 5   /* shape the kernels do not handle (see below)      */
+} ll_status;
+
+typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
+
+/* Device error word bits (ll_status_sync). */
+#define LL_DEVERR_SEQ_LEN 1      /* some seq_len[b] < 0 or > T_max          */
+#define LL_DEVERR_BARRIER 2      /* a grid-barrier wait exceeded its bound  */
+
+/*
+ * Problem description.
+ *   T_max, B, I, H >= 1; layers in {1, 2}; dtype an ll_dtype.
+ *   Supported tiling: H % 32 == 0, I % 8 == 0 (bf16) or I % 4 == 0 (f32),
+ *   B <= 4096; otherwise ll_plan_create returns LL_EUNSUPPORTED.
+ *   spill = 0: the stack lives in device memory (T_max*B rows capacity).
+ *   spill = 1: the stack is swapped to pinned host memory in chunks of
+ *     spill_chunk_steps time steps (0 = library default) on a device-to-host
+ *     copy stream while the forward runs, and prefetched back on a
+ *     host-to-device stream ahead of the gradient loop (Section 5.3).
+ *     device_stack_budget_bytes bounds the device ring that stages the
+ *     chunks (0 = the smallest ring that still overlaps, 3 chunks).
+ *   reserved must be 0.
+ */
+typedef struct {
+  int32_t T_max;
+  int32_t B;
+  int32_t I;
+  int32_t H;
+  int32_t layers;
+  int32_t dtype;
+  int32_t spill;
+  int32_t spill_chunk_steps;
+  int64_t device_stack_budget_bytes;
+  int64_t reserved;
+} ll_desc;
+
+typedef struct ll_plan ll_plan;   /* opaque: owns the stack, scratch arrays,
+                                     pinned host memory, copy streams, events
+                                     and the device error word */
+
+/* Validate `desc`, allocate the plan's device stack and scratch memory on
+ * `device` (and pinned host memory when spill = 1).  On success *out is a
+ * new plan; on failure *out is NULL and nothing stays allocated. */
+ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out);
+
+/* Free everything the plan owns.  Waits for the plan's outstanding work.
+ * NULL is accepted. */
+ll_status ll_plan_destroy(ll_plan* plan);
+
+/* Bytes of stack storage the plan holds in device memory and in pinned host
+ * memory.  Either output pointer may be NULL. */
+ll_status ll_plan_stack_bytes(const ll_plan* plan, int64_t* device_bytes,
+                              int64_t* host_bytes);
+
+/* Launch geometry the plan chose for the recurrent loops (for reports):
+ * work-groups of the forward loop, hidden units per work-group, work-groups
+ * per unit block.  Any output may be NULL. */
+ll_status ll_plan_geometry(const ll_plan* plan, int32_t* loop_workgroups,
+                           int32_t* units_per_workgroup,
+                           int32_t* row_groups);
+
+/*
+ * Forward while-loop (Sections 2.1, 4.2, 5.1).
+ *   x        [T_max,B,I] dtype; entries at t >= seq_len[b] are never read
+ *            into a kept result (they may hold NaN).
+ *   seq_len  [B] int32, each in [0, T_max].
+ *   W, bias  host arrays of `layers` device pointers (see conventions).
+ *   h0, c0   [layers,B,H] float, or NULL for zeros.
+ *   y        [T_max,B,H] float output of the top layer (0 where t >=
+ *            seq_len[b]), or NULL.
+ *   hT, cT   [layers,B,H] float: state after seq_len[b] steps (h0/c0 for
+ *            zero-length rows).  Required.
+ *   trip_count  device int32 scalar receiving T_eff, or NULL.
+ *   save_for_backward  nonzero: push the stack for lstm_loop_bwd; the plan
+ *            keeps x, seq_len, W, h0, c0 pointers, which must stay valid and
+ *            unchanged until the backward has been enqueued.
+ *            Zero: inference, nothing is saved.
+ */
+ll_status lstm_loop_fwd(ll_plan* plan, void* stream,
+                        const void* x, const int32_t* seq_len,
+                        const void* const* W, const float* const* bias,
+                        const float* h0, const float* c0,
+                        float* y, float* hT, float* cT,
+                        int32_t* trip_count, int32_t save_for_backward);
+
+/*
+ * Gradient while-loop (Sections 5.1, 5.2): runs T_eff iterations in reverse,
+ * popping the stack of the last lstm_loop_fwd(save_for_backward=1) on this
+ * plan.  Returns LL_ESTATE if there is none.  Consumes the saved stack.
+ *   dy       [T_max,B,H] float gradient of y, or NULL (zero).
+ *   dhT, dcT [layers,B,H] float gradients of hT/cT, or NULL (zero).
+ *   dx       [T_max,B,I] float output (0 where t >= seq_len[b]) or NULL.
+ *   dW       host array of `layers` device pointers to float [I_l+H,4H];
+ *            OVERWRITTEN with the gradient (not accumulated into).
+ *   dbias    host array of `layers` device pointers to float [4H];
+ *            overwritten.
+ *   dh0, dc0 [layers,B,H] float outputs, or NULL.
+ */
+ll_status lstm_loop_bwd(ll_plan* plan, void* stream,
+                        const float* dy, const float* dhT, const float* dcT,
+                        float* dx, float* const* dW, float* const* dbias,
+                        float* dh0, float* dc0);
+
+/* Wait for the plan's work on the stream of its last call, then read and
+ * clear the device error word (LL_DEVERR_* bits) into *device_error
+ * (may be NULL). */
+ll_status ll_status_sync(ll_plan* plan, int32_t* device_error);
+
+/* Message describing the last failure on the calling thread ("" if none). */
+const char* ll_last_error(void);
+
+/*
+ * Stage timing, for benchmarks.  While enabled, the plan records a pair of
+ * HIP events around every stage it enqueues, on the call's stream, so each
+ * pair brackets that stage's kernels exactly as the stream runs them.
+ * ll_plan_set_timing(plan, 1) clears the accumulators and starts recording;
+ * 0 stops.  ll_plan_read_timing waits for the recorded events, then returns
+ * the accumulated milliseconds and the number of recorded instances of
+ * `stage` (an ll_stage).  Outputs may be NULL.
+ */
+typedef enum {
+  LL_STAGE_PREP = 0,          /* trip count, length order, compact offsets   */
+  LL_STAGE_INPUT_PROJ = 1,    /* W transpose + x_t W_x + b of all rows        */
+  LL_STAGE_FWD_LOOP = 2,      /* forward recurrence (one launch per layer)   */
+  LL_STAGE_BWD_LOOP = 3,      /* gradient recurrence (one launch per layer)  */
+  LL_STAGE_BWD_OPERANDS = 4,  /* transposed operands of the dW products      */
+  LL_STAGE_DW = 5,            /* dW = sum_t [x_t, h_{t-1}]^T dz_t, db        */
+  LL_STAGE_DX = 6,            /* dx_t = dz_t W_x^T (and finished-row zeros)  */
+  LL_STAGE_COUNT = 7
+} ll_stage;
+
+ll_status ll_plan_set_timing(ll_plan* plan, int32_t enable);
+ll_status ll_plan_read_timing(ll_plan* plan, int32_t stage, double* total_ms,
+                              int64_t* instances);
+
+/* Library version string. */
+const char* ll_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LSTMLOOP_H */

@@ -1,0 +1,267 @@
+// Small kernels around the loops: trip count and length ordering, operand
+// transposes, zero fill of finished rows, deterministic reductions.
+#include "ll_kernels.h"
+
+namespace ll {
+
+// ---------------------------------------------------------------------------
+// Loop preparation (one work-group of 1024 threads).
+//   * range check of seq_len; a bad length sets LL_DEVERR_SEQ_LEN and makes
+//     the loops run zero iterations (every length treated as 0);
+//   * T_eff = max_b seq_len[b]: the loop predicate is t < T_eff, decided here
+//     on the device, and it is also the iteration count the gradient loop
+//     replays (the forward loop counter of the loop gradient);
+//   * perm: batch rows ordered by decreasing length (ties by index), so the
+//     rows still running at step t are the prefix r < active[t];
+//   * off[t] = sum_{t' < t} active[t']: rows of step t occupy compact rows
+//     off[t] .. off[t] + active[t] - 1 of every per-step array (stack,
+//     history, pre-activations, dz);  meta[1] = off[T_max] = sum of lengths;
+//   * rowmap[k] = t * B + perm[r] for compact row k = off[t] + r.
+//   * clears the barrier counters and the abort flag of this launch sequence.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_len, int B,
+                                                    int T_max, int* __restrict__ perm,
+                                                    int* __restrict__ active, int* __restrict__ off,
+                                                    int* __restrict__ rowmap, int* __restrict__ meta,
+                                                    int* __restrict__ trip_out) {
+  extern __shared__ int smem[];
+  int* s_len = smem;          // [B]
+  int* s_sorted = smem + B;   // [B] lengths in perm order
+  __shared__ int s_bad;
+  __shared__ int s_wsum[16];
+  __shared__ int s_carry;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int lane = tid & 63, wave = tid >> 6, nwaves = nt >> 6;
+  if (tid == 0) { s_bad = 0; s_carry = 0; }
+  __syncthreads();
+  for (int b = tid; b < B; b += nt) {
+    const int L = seq_len[b];
+    s_len[b] = L;
+    if (L < 0 || L > T_max) s_bad = 1;
+  }
+  __syncthreads();
+  const int bad = s_bad;
+  for (int b = tid; b < B; b += nt) {
+    const int L = s_len[b];
+    int rank = 0;
+    for (int o = 0; o < B; ++o) {
+      const int Lo = s_len[o];
+      rank += (Lo > L) || (Lo == L && o < b);
+    }
+    perm[rank] = b;
+    s_sorted[rank] = bad ? 0 : L;
+  }
+  __syncthreads();
+  const int T_eff = B > 0 ? s_sorted[0] : 0;
+  // active[t] = #{r : sorted length > t}; lengths are non-increasing in r
+  for (int t = tid; t <= T_max; t += nt) {
+    int lo = 0, hi = B;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (s_sorted[mid] > t) lo = mid + 1; else hi = mid;
+    }
+    active[t] = lo;
+  }
+  __syncthreads();
+  // exclusive prefix sum of active[0..T_max) into off[0..T_max]
+  for (int base = 0; base <= T_max; base += nt) {
+    const int t = base + tid;
+    const int v = (t < T_max) ? active[t] : 0;
+    int incl = v;
+    for (int d = 1; d < 64; d <<= 1) {
+      const int u = __shfl_up(incl, d, 64);
+      if (lane >= d) incl += u;
+    }
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    int wpre = 0, tot = 0;
+    for (int w = 0; w < nwaves; ++w) {
+      const int s = s_wsum[w];
+      if (w < wave) wpre += s;
+      tot += s;
+    }
+    const int carry = s_carry;
+    if (t <= T_max) off[t] = carry + wpre + incl - v;
+    __syncthreads();
+    if (tid == 0) s_carry = carry + tot;
+    __syncthreads();
+  }
+  const int total = off[T_max];
+  // rowmap: compact row -> t * B + b
+  for (int k = tid; k < total; k += nt) {
+    int lo = 0, hi = T_eff;          // largest t with off[t] <= k
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (off[mid] <= k) lo = mid; else hi = mid;
+    }
+    rowmap[k] = lo * B + perm[k - off[lo]];
+  }
+  if (tid == 0) {
+    meta[0] = T_eff;
+    meta[1] = total;
+    meta[3] = 0;                       // abort flag
+    for (int i = 0; i < 4; ++i) meta[4 + i] = 0;   // barrier counters
+    if (bad) atomicOr(&meta[2], LL_DEVERR_SEQ_LEN_BIT);
+    if (trip_out) *trip_out = T_eff;
+  }
+}
+
+// out[c * ldo + r] = in[r * ldi + c], r < R, c < C.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, int R, int C,
+                                                        int ldi, T* __restrict__ out, int ldo) {
+  __shared__ T tile[64][65];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    if (r < R && c < C) tile[i][tx] = in[(long)r * ldi + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < C && r < R) out[(long)c * ldo + r] = tile[tx][i];
+  }
+}
+
+// Gather compact rows and transpose: out[c * ldo + k] = src_k[c] for
+// k < meta[1] (sum of lengths), c < C.  Source row of compact row k:
+//   mode 0: in + rowmap[k] * C         (time-major input, original batch order)
+//   mode 1: in + k * C                 (already compact)
+//   mode 2: h_{t-1} of that row: t = rowmap[k] / B, r = k - off[t];
+//           t > 0: in + (off[t-1] + r) * C (compact history of h);
+//           t = 0: bf/fp conversion of h0f[perm[r] * C] (float, NULL = 0).
+template <typename T>
+__global__ __launch_bounds__(256) void gather_transpose_kernel(GatherTArgs g) {
+  __shared__ T tile[64][65];
+  const int total = g.meta[1];
+  const int k0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  if (k0 >= total) return;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const T* in = reinterpret_cast<const T*>(g.in);
+  for (int i = ty; i < 64; i += 4) {
+    const int k = k0 + i, c = c0 + tx;
+    if (k < total && c < g.C) {
+      T v;
+      if (g.mode == 0) {
+        v = in[(long)g.rowmap[k] * g.C + c];
+      } else if (g.mode == 1) {
+        v = in[(long)k * g.C + c];
+      } else {
+        const int t = g.rowmap[k] / g.B;
+        const int r = k - g.off[t];
+        if (t > 0) {
+          v = in[(long)(g.off[t - 1] + r) * g.C + c];
+        } else {
+          const float f = g.h0f ? g.h0f[(long)g.perm[r] * g.C + c] : 0.0f;
+          v = Op<T>::from_f32(f);
+        }
+      }
+      tile[i][tx] = v;
+    }
+  }
+  __syncthreads();
+  T* out = reinterpret_cast<T*>(g.out);
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, k = k0 + tx;
+    if (c < g.C && k < total) out[(long)c * g.ldo + k] = tile[tx][i];
+  }
+}
+
+// Zero the rows (t, b) of a [T_max, B, C] float array with t >= seq_len[b]
+// (all rows if the lengths failed the range check).  C % 4 == 0.
+__global__ __launch_bounds__(256) void zero_finished_rows_kernel(float* __restrict__ dst, int T_max,
+                                                                 int B, int C,
+                                                                 const int* __restrict__ seq_len,
+                                                                 const int* __restrict__ meta) {
+  const int bad = meta[2] & LL_DEVERR_SEQ_LEN_BIT;
+  const long rows = (long)T_max * B;
+  const int c4 = C >> 2;
+  for (long row = blockIdx.x * 4L + (threadIdx.x >> 6); row < rows; row += gridDim.x * 4L) {
+    const int t = (int)(row / B), b = (int)(row % B);
+    if (!bad && t < seq_len[b]) continue;
+    float4* p = reinterpret_cast<float4*>(dst + row * C);
+    for (int i = threadIdx.x & 63; i < c4; i += 64) p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+}
+
+// out[i] = sum_{s < S} ws[s * stride + i], fixed order.
+__global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict__ ws, int S,
+                                                         long stride, long n,
+                                                         float* __restrict__ out) {
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+    float acc = 0.0f;
+    for (int s = 0; s < S; ++s) acc += ws[s * stride + i];
+    out[i] = acc;
+  }
+}
+
+// float -> operand type copy (used for bf16(h0) and similar small arrays).
+template <typename T>
+__global__ __launch_bounds__(256) void convert_kernel(const float* __restrict__ in, long n,
+                                                      T* __restrict__ out) {
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L)
+    out[i] = Op<T>::from_f32(in[i]);
+}
+
+// ------------------------------------------------------------ launchers
+hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
+                       int* rowmap, int* meta, int* trip_out, hipStream_t s) {
+  const size_t smem = 2 * sizeof(int) * (size_t)B;
+  hipLaunchKernelGGL(prep_kernel, dim3(1), dim3(1024), smem, s, seq_len, B, T_max, perm, active,
+                     off, rowmap, meta, trip_out);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_transpose(const T* in, int R, int C, int ldi, T* out, int ldo, hipStream_t s) {
+  dim3 grid((C + 63) / 64, (R + 63) / 64);
+  hipLaunchKernelGGL(transpose_kernel<T>, grid, dim3(256), 0, s, in, R, C, ldi, out, ldo);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_gather_transpose(const GatherTArgs& g, int cap_rows, hipStream_t s) {
+  dim3 grid((cap_rows + 63) / 64, (g.C + 63) / 64);
+  hipLaunchKernelGGL(gather_transpose_kernel<T>, grid, dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_finished_rows(float* dst, int T_max, int B, int C, const int* seq_len,
+                                     const int* meta, hipStream_t s) {
+  const long rows = (long)T_max * B;
+  int blocks = (int)((rows + 3) / 4);
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(zero_finished_rows_kernel, dim3(blocks), dim3(256), 0, s, dst, T_max, B, C,
+                     seq_len, meta);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_slices(const float* ws, int S, long stride, long n, float* out,
+                             hipStream_t s) {
+  long blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(sum_slices_kernel, dim3((unsigned)blocks), dim3(256), 0, s, ws, S, stride, n,
+                     out);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s) {
+  long blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(convert_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, in, n, out);
+  return hipGetLastError();
+}
+
+template hipError_t launch_transpose<float>(const float*, int, int, int, float*, int, hipStream_t);
+template hipError_t launch_transpose<bf16_t>(const bf16_t*, int, int, int, bf16_t*, int,
+                                             hipStream_t);
+template hipError_t launch_gather_transpose<float>(const GatherTArgs&, int, hipStream_t);
+template hipError_t launch_gather_transpose<bf16_t>(const GatherTArgs&, int, hipStream_t);
+template hipError_t launch_convert<float>(const float*, long, float*, hipStream_t);
+template hipError_t launch_convert<bf16_t>(const float*, long, bf16_t*, hipStream_t);
+
+}  // namespace ll

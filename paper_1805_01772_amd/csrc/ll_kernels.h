@@ -1,0 +1,139 @@
+// Kernel argument blocks and launchers of the lstmloop library (internal).
+#pragma once
+
+#include "ll_device.h"
+
+namespace ll {
+
+constexpr int LL_DEVERR_SEQ_LEN_BIT = 1;
+constexpr int LL_DEVERR_BARRIER_BIT = 2;
+
+// meta[] layout (device int array owned by a plan)
+//   0: T_eff   1: total rows (sum of lengths)   2: error word   3: abort flag
+//   4..7: grid-barrier counters
+constexpr int META_INTS = 8;
+
+struct GatherTArgs {
+  const void* in;
+  void* out;
+  int C;
+  int ldo;
+  int mode;             // 0 rowmap gather, 1 compact, 2 previous-h history
+  int B;
+  const int* meta;
+  const int* rowmap;
+  const int* off;
+  const int* perm;
+  const float* h0f;     // mode 2, t = 0
+};
+
+// C[crow(m), n] = sum_k A[arow(m), k] * Bm[n, k] (+ bias[n]), both operands
+// K-contiguous ("NT").  M, K may come from device memory (sum of lengths).
+struct GemmArgs {
+  const void* A;
+  long lda;
+  const int* a_rowmap;   // NULL: arow(m) = m
+  const void* Bm;
+  long ldb;
+  float* C;
+  long ldc;
+  const int* c_rowmap;   // NULL: crow(m) = m
+  const float* bias;     // NULL: none
+  int M;                 // rows (capacity when M_dev is set)
+  const int* M_dev;      // NULL or device scalar: rows actually present
+  int N;
+  int K;
+  const int* K_dev;      // NULL or device scalar: reduction length
+  int splits;            // > 1: split-K; slice z written to C + z * split_stride
+  long split_stride;
+};
+
+struct LoopGeom {
+  int HJ;       // hidden units per work-group (multiple of 4)
+  int RG;       // work-groups per unit block (row groups)
+  int NRT;      // 16-row tiles covering the batch
+  int MRT;      // row tiles per work-group = ceil(NRT / RG)
+  int nwg;      // (H / HJ) * RG
+  size_t lds_fwd;
+  size_t lds_bwd;
+};
+
+struct FwdLoopArgs {
+  int B, H, T_max;
+  int HJ, RG, MRT;
+  const int* meta;
+  const int* active;
+  const int* off;
+  const int* perm;
+  const float* Zx;        // [cap, 4H] float: x_t W_x + b for every compact row
+  const void* WT;         // [4H, ldw] operand type: row n = gate column n of W
+  int ldw;
+  int woff;               // column of WT where the h rows of W start (= I_l)
+  const float* h0;        // [B, H] original order, or NULL
+  const float* c0;
+  void* HH;               // [cap, H] operand type: h_t history (compact rows)
+  float* stack;           // [cap, 5H] float: i, f, g, o, c_t (NULL = inference)
+  float* y;               // [T_max, B, H] or NULL
+  float* hT;
+  float* cT;
+  unsigned* bar;
+  int* abort_flag;
+  int* err;
+  unsigned long long limit;
+};
+
+struct BwdLoopArgs {
+  int B, H, T_max;
+  int HJ, RG, MRT;
+  const int* meta;
+  const int* active;
+  const int* off;
+  const int* perm;
+  const void* W;          // [rows, 4H] operand type, natural layout
+  int wrow0;              // first row of the h part of W (= I_l)
+  const float* stack;     // [cap, 5H]
+  const float* c0;        // [B, H] original order, or NULL
+  const float* dy;        // NULL, [T_max, B, H] (dy_compact = 0) or [cap, H] (= 1)
+  int dy_compact;
+  const float* dhT;
+  const float* dcT;
+  void* DZ;               // [cap, 4H] operand type (output)
+  float* db_part;         // [RG, 4H]
+  float* dh0;
+  float* dc0;
+  unsigned* bar;
+  int* abort_flag;
+  int* err;
+  unsigned long long limit;
+};
+
+hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
+                       int* rowmap, int* meta, int* trip_out, hipStream_t s);
+template <typename T>
+hipError_t launch_transpose(const T* in, int R, int C, int ldi, T* out, int ldo, hipStream_t s);
+template <typename T>
+hipError_t launch_gather_transpose(const GatherTArgs& g, int cap_rows, hipStream_t s);
+hipError_t launch_zero_finished_rows(float* dst, int T_max, int B, int C, const int* seq_len,
+                                     const int* meta, hipStream_t s);
+hipError_t launch_sum_slices(const float* ws, int S, long stride, long n, float* out,
+                             hipStream_t s);
+template <typename T>
+hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s);
+
+template <typename T>
+hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s);
+
+// Recurrent loops (cooperative launches).
+template <typename T>
+hipError_t loop_kernel_setup(int mrt, size_t lds_fwd, size_t lds_bwd, int* max_wg_per_cu_fwd,
+                             int* max_wg_per_cu_bwd);
+template <typename T>
+hipError_t launch_fwd_loop(const FwdLoopArgs& a, int nwg, size_t lds, hipStream_t s);
+template <typename T>
+hipError_t launch_bwd_loop(const BwdLoopArgs& a, int nwg, size_t lds, hipStream_t s);
+
+// LDS bytes the loops need for a geometry (see ll_loop.hip).
+size_t fwd_loop_lds(int H, int HJ, int elem_bytes);
+size_t bwd_loop_lds(int H, int HJ, int elem_bytes);
+
+}  // namespace ll

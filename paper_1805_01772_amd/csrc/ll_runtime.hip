@@ -1,0 +1,679 @@
+// Host runtime of lstmloop: plan (stack and scratch allocation, launch
+// geometry), argument validation, the enqueue order of the forward and
+// gradient loops, and the C ABI declared in include/lstmloop.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "lstmloop.h"
+#include "ll_kernels.h"
+
+using ll::bf16_t;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ll_status fail(ll_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+#define LL_HIP(call)                                                              \
+  do {                                                                            \
+    hipError_t e_ = (call);                                                       \
+    if (e_ != hipSuccess)                                                         \
+      return fail(LL_EHIP, "%s failed: %s", #call, hipGetErrorString(e_));        \
+  } while (0)
+
+enum PlanState { ST_EMPTY = 0, ST_FWD_DONE = 1 };
+
+class DeviceGuard {
+ public:
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev_) != hipSuccess) prev_ = -1;
+    if (prev_ != dev) hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev_ >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev_) hipSetDevice(prev_);
+  }
+
+ private:
+  int prev_ = -1;
+};
+
+long round_up(long v, long m) { return (v + m - 1) / m * m; }
+
+}  // namespace
+
+struct ll_plan {
+  ll_desc d{};
+  int device = 0;
+  int es = 4;            // operand element bytes
+  bool bf16 = false;
+  long cap = 0;          // compact-row capacity = T_max * B
+  long ldT = 0;          // leading dimension of transposed per-row arrays
+  ll::LoopGeom geom{};
+  int n_cu = 0;
+  unsigned long long barrier_ticks = 0;
+  int dw_splits[2] = {1, 1};   // split-K of the dW_x / dW_h products
+  // device memory
+  int* perm = nullptr;
+  int* active = nullptr;
+  int* off = nullptr;
+  int* rowmap = nullptr;
+  int* meta = nullptr;
+  void* WT[2] = {nullptr, nullptr};
+  float* Zx = nullptr;
+  float* stack[2] = {nullptr, nullptr};
+  void* HH[2] = {nullptr, nullptr};
+  void* DZ = nullptr;
+  void* DZT = nullptr;
+  void* XT = nullptr;
+  void* HPT = nullptr;
+  float* dyc = nullptr;
+  float* db_part = nullptr;
+  float* ws = nullptr;
+  long ws_floats = 0;
+  int64_t stack_device_bytes = 0;
+  int64_t stack_host_bytes = 0;
+  // saved forward
+  int state = ST_EMPTY;
+  const void* x = nullptr;
+  const int32_t* seq_len = nullptr;
+  const void* W[2] = {nullptr, nullptr};
+  const float* h0 = nullptr;
+  const float* c0 = nullptr;
+  hipStream_t last_stream = nullptr;
+  // stage timing
+  bool timing = false;
+  struct Rec {
+    int stage;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> ev_pool;
+  double t_ms[LL_STAGE_COUNT] = {};
+  int64_t t_n[LL_STAGE_COUNT] = {};
+};
+
+namespace {
+
+int in_width(const ll_plan* p, int l) { return l == 0 ? p->d.I : p->d.H; }
+
+hipEvent_t take_event(ll_plan* p) {
+  if (!p->ev_pool.empty()) {
+    hipEvent_t e = p->ev_pool.back();
+    p->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Stage bracket: tbeg records the opening event, tend the closing one.
+hipEvent_t tbeg(ll_plan* p, hipStream_t s) {
+  if (!p->timing) return nullptr;
+  hipEvent_t a = take_event(p);
+  if (a && hipEventRecord(a, s) != hipSuccess) {
+    p->ev_pool.push_back(a);
+    return nullptr;
+  }
+  return a;
+}
+
+void tend(ll_plan* p, hipStream_t s, int stage, hipEvent_t a) {
+  if (!p->timing || !a) return;
+  hipEvent_t b = take_event(p);
+  if (!b || hipEventRecord(b, s) != hipSuccess) {
+    p->ev_pool.push_back(a);
+    if (b) p->ev_pool.push_back(b);
+    return;
+  }
+  p->recs.push_back(ll_plan::Rec{stage, a, b});
+}
+
+void drain_timing(ll_plan* p) {
+  for (auto& r : p->recs) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      p->t_ms[r.stage] += ms;
+      p->t_n[r.stage] += 1;
+    }
+    p->ev_pool.push_back(r.a);
+    p->ev_pool.push_back(r.b);
+  }
+  p->recs.clear();
+}
+
+void free_plan_memory(ll_plan* p) {
+  void* ptrs[] = {p->perm, p->active, p->off, p->rowmap, p->meta, p->WT[0], p->WT[1], p->Zx,
+                  p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT, p->HPT,
+                  p->dyc, p->db_part, p->ws};
+  for (void* q : ptrs)
+    if (q) hipFree(q);
+}
+
+ll_status dalloc(void** out, size_t bytes, const char* what) {
+  *out = nullptr;
+  if (bytes == 0) bytes = 16;
+  hipError_t e = hipMalloc(out, bytes);
+  if (e != hipSuccess) {
+    *out = nullptr;
+    (void)hipGetLastError();
+    return fail(LL_ENOMEM, "device allocation of %zu bytes for %s failed: %s", bytes, what,
+                hipGetErrorString(e));
+  }
+  return LL_OK;
+}
+
+// Choose the loop work split: hidden units per work-group HJ in {16, 8, 4},
+// row groups RG; as many work-groups as compute units allow (one per CU,
+// the weight slice fills most of the LDS), then the widest HJ.
+bool choose_geometry(int B, int H, int es, int n_cu, size_t lds_max, ll::LoopGeom* out) {
+  const int NRT = (B + 15) / 16;
+  bool found = false;
+  ll::LoopGeom best{};
+  for (int HJ : {16, 8, 4}) {
+    if (H % HJ) continue;
+    const int NCB = H / HJ;
+    if (NCB > n_cu) continue;
+    const size_t lf = ll::fwd_loop_lds(H, HJ, es), lb = ll::bwd_loop_lds(H, HJ, es);
+    if (lf > lds_max || lb > lds_max) continue;
+    int RG = std::min(NRT, n_cu / NCB);
+    if (RG < 1) RG = 1;
+    const int MRT = (NRT + RG - 1) / RG;
+    if (MRT > 16) continue;
+    const int nwg = NCB * RG;
+    if (!found || nwg > best.nwg) {
+      best = ll::LoopGeom{HJ, RG, NRT, MRT, nwg, lf, lb};
+      found = true;
+    }
+  }
+  if (found) *out = best;
+  return found;
+}
+
+ll_status validate_desc(const ll_desc* d) {
+  if (!d) return fail(LL_EINVAL, "desc is NULL");
+  if (d->T_max < 1 || d->B < 1 || d->I < 1 || d->H < 1)
+    return fail(LL_EINVAL, "T_max, B, I, H must be >= 1 (got %d, %d, %d, %d)", d->T_max, d->B,
+                d->I, d->H);
+  if (d->layers != 1 && d->layers != 2)
+    return fail(LL_EINVAL, "layers must be 1 or 2 (got %d)", d->layers);
+  if (d->dtype != LL_F32 && d->dtype != LL_BF16)
+    return fail(LL_EINVAL, "dtype must be LL_F32 or LL_BF16 (got %d)", d->dtype);
+  if (d->spill != 0 && d->spill != 1) return fail(LL_EINVAL, "spill must be 0 or 1");
+  if (d->spill_chunk_steps < 0 || d->device_stack_budget_bytes < 0)
+    return fail(LL_EINVAL, "spill_chunk_steps and device_stack_budget_bytes must be >= 0");
+  if (d->reserved != 0) return fail(LL_EINVAL, "reserved must be 0");
+  if ((long)d->T_max * d->B > (1L << 30))
+    return fail(LL_EUNSUPPORTED, "T_max * B = %ld exceeds 2^30 rows", (long)d->T_max * d->B);
+  if (d->H % 32) return fail(LL_EUNSUPPORTED, "H = %d must be a multiple of 32", d->H);
+  const int ialign = d->dtype == LL_BF16 ? 8 : 4;
+  if (d->I % ialign)
+    return fail(LL_EUNSUPPORTED, "I = %d must be a multiple of %d for this dtype", d->I, ialign);
+  if (d->B > 4096) return fail(LL_EUNSUPPORTED, "B = %d exceeds 4096", d->B);
+  if (d->spill) return fail(LL_EUNSUPPORTED, "spill is not available in this build");
+  return LL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ll_last_error(void) { return g_last_error.c_str(); }
+
+const char* ll_version(void) { return "lstmloop 0.1 (gfx950)"; }
+
+ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
+  if (!out) return fail(LL_EINVAL, "out is NULL");
+  *out = nullptr;
+  ll_status st = validate_desc(desc);
+  if (st != LL_OK) return st;
+  int ndev = 0;
+  LL_HIP(hipGetDeviceCount(&ndev));
+  if (device < 0 || device >= ndev)
+    return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
+  DeviceGuard guard(device);
+  hipDeviceProp_t prop;
+  LL_HIP(hipGetDeviceProperties(&prop, device));
+  if (!prop.cooperativeLaunch)
+    return fail(LL_EUNSUPPORTED, "device %d does not support cooperative launches", device);
+
+  ll_plan* p = new (std::nothrow) ll_plan();
+  if (!p) return fail(LL_ENOMEM, "host allocation of the plan failed");
+  p->d = *desc;
+  p->device = device;
+  p->bf16 = desc->dtype == LL_BF16;
+  p->es = p->bf16 ? 2 : 4;
+  p->n_cu = prop.multiProcessorCount;
+  p->cap = (long)desc->T_max * desc->B;
+  p->ldT = round_up(p->cap, 64);
+  int wall_khz = 0;
+  if (hipDeviceGetAttribute(&wall_khz, hipDeviceAttributeWallClockRate, device) != hipSuccess ||
+      wall_khz <= 0)
+    wall_khz = 100000;
+  p->barrier_ticks = (unsigned long long)wall_khz * 5000ull;   // 5 s
+
+  const size_t lds_max = prop.sharedMemPerBlock > 0 ? (size_t)prop.sharedMemPerBlock : 65536;
+  size_t lds_limit = lds_max;
+  {
+    int optin = 0;
+    if (hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, device) ==
+            hipSuccess &&
+        optin > 0)
+      lds_limit = std::max(lds_limit, (size_t)optin);
+  }
+  const int H = desc->H, B = desc->B, L = desc->layers;
+  if (!choose_geometry(B, H, p->es, p->n_cu, lds_limit, &p->geom)) {
+    delete p;
+    return fail(LL_EUNSUPPORTED,
+                "no loop geometry fits: H = %d, B = %d, %d CUs, %zu bytes of LDS per group", H,
+                B, prop.multiProcessorCount, lds_limit);
+  }
+  int occ_f = 0, occ_b = 0;
+  hipError_t he = p->bf16 ? ll::loop_kernel_setup<bf16_t>(p->geom.MRT, p->geom.lds_fwd,
+                                                          p->geom.lds_bwd, &occ_f, &occ_b)
+                          : ll::loop_kernel_setup<float>(p->geom.MRT, p->geom.lds_fwd,
+                                                         p->geom.lds_bwd, &occ_f, &occ_b);
+  if (he != hipSuccess) {
+    delete p;
+    return fail(LL_EHIP, "loop kernel setup failed: %s", hipGetErrorString(he));
+  }
+  if ((long)occ_f * p->n_cu < p->geom.nwg || (long)occ_b * p->n_cu < p->geom.nwg) {
+    delete p;
+    return fail(LL_EUNSUPPORTED,
+                "loops need %d co-resident work-groups; occupancy allows %d/%d per CU x %d CUs",
+                p->geom.nwg, occ_f, occ_b, p->n_cu);
+  }
+
+  // dW split-K: enough work-groups to cover the chip.
+  for (int w = 0; w < 2; ++w) {
+    const int M = w == 0 ? desc->I : H;
+    const long tiles = (long)((M + 127) / 128) * ((4 * H + 127) / 128);
+    long s = (2L * p->n_cu + tiles - 1) / tiles;
+    s = std::max(1L, std::min(16L, s));
+    const long max_by_k = std::max(1L, p->cap / 256);
+    p->dw_splits[w] = (int)std::min(s, max_by_k);
+  }
+  const int maxI = std::max(desc->I, H);
+  p->ws_floats = 0;
+  for (int l = 0; l < L; ++l) {
+    const int Il = in_width(p, l);
+    if (p->dw_splits[0] > 1) p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[0] * Il * 4 * H);
+    if (p->dw_splits[1] > 1) p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[1] * H * 4 * H);
+  }
+
+  const size_t es = p->es;
+  const long cap = p->cap;
+#define ALLOC(ptr, bytes, what)                                      \
+  do {                                                               \
+    void* tmp_ = nullptr;                                            \
+    ll_status s_ = dalloc(&tmp_, (size_t)(bytes), what);             \
+    if (s_ != LL_OK) {                                               \
+      free_plan_memory(p);                                           \
+      delete p;                                                      \
+      return s_;                                                     \
+    }                                                                \
+    ptr = reinterpret_cast<decltype(ptr)>(tmp_);                     \
+  } while (0)
+  ALLOC(p->perm, sizeof(int) * B, "perm");
+  ALLOC(p->active, sizeof(int) * (desc->T_max + 1), "active");
+  ALLOC(p->off, sizeof(int) * (desc->T_max + 1), "off");
+  ALLOC(p->rowmap, sizeof(int) * cap, "rowmap");
+  ALLOC(p->meta, sizeof(int) * ll::META_INTS, "meta");
+  for (int l = 0; l < L; ++l) {
+    ALLOC(p->WT[l], es * 4 * H * (in_width(p, l) + H), "transposed W");
+    ALLOC(p->stack[l], sizeof(float) * cap * 5 * H, "stack");
+    ALLOC(p->HH[l], es * cap * H, "h history");
+  }
+  ALLOC(p->Zx, sizeof(float) * cap * 4 * H, "input projection");
+  ALLOC(p->DZ, es * cap * 4 * H, "dz");
+  ALLOC(p->DZT, es * 4 * H * p->ldT, "dz transposed");
+  ALLOC(p->XT, es * maxI * p->ldT, "x transposed");
+  ALLOC(p->HPT, es * H * p->ldT, "h_prev transposed");
+  if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
+  ALLOC(p->db_part, sizeof(float) * p->geom.RG * 4 * H, "db partials");
+  if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
+#undef ALLOC
+  if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess) {
+    free_plan_memory(p);
+    delete p;
+    return fail(LL_EHIP, "hipMemset of the plan's meta words failed");
+  }
+  p->stack_device_bytes = (int64_t)L * (int64_t)(sizeof(float) * cap * 5 * H + es * cap * H);
+  p->stack_host_bytes = 0;
+  *out = p;
+  return LL_OK;
+}
+
+ll_status ll_plan_destroy(ll_plan* p) {
+  if (!p) return LL_OK;
+  DeviceGuard guard(p->device);
+  hipDeviceSynchronize();
+  drain_timing(p);
+  for (hipEvent_t e : p->ev_pool) hipEventDestroy(e);
+  free_plan_memory(p);
+  delete p;
+  return LL_OK;
+}
+
+ll_status ll_plan_set_timing(ll_plan* p, int32_t enable) {
+  if (!p) return fail(LL_EINVAL, "plan is NULL");
+  DeviceGuard guard(p->device);
+  drain_timing(p);
+  for (int i = 0; i < LL_STAGE_COUNT; ++i) {
+    p->t_ms[i] = 0.0;
+    p->t_n[i] = 0;
+  }
+  p->timing = enable != 0;
+  return LL_OK;
+}
+
+ll_status ll_plan_read_timing(ll_plan* p, int32_t stage, double* total_ms, int64_t* n) {
+  if (!p) return fail(LL_EINVAL, "plan is NULL");
+  if (stage < 0 || stage >= LL_STAGE_COUNT) return fail(LL_EINVAL, "stage %d out of range", stage);
+  DeviceGuard guard(p->device);
+  drain_timing(p);
+  if (total_ms) *total_ms = p->t_ms[stage];
+  if (n) *n = p->t_n[stage];
+  return LL_OK;
+}
+
+ll_status ll_plan_stack_bytes(const ll_plan* p, int64_t* dev, int64_t* host) {
+  if (!p) return fail(LL_EINVAL, "plan is NULL");
+  if (dev) *dev = p->stack_device_bytes;
+  if (host) *host = p->stack_host_bytes;
+  return LL_OK;
+}
+
+ll_status ll_plan_geometry(const ll_plan* p, int32_t* nwg, int32_t* hj, int32_t* rg) {
+  if (!p) return fail(LL_EINVAL, "plan is NULL");
+  if (nwg) *nwg = p->geom.nwg;
+  if (hj) *hj = p->geom.HJ;
+  if (rg) *rg = p->geom.RG;
+  return LL_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+template <typename T>
+ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* seq_len,
+                      const void* const* W, const float* const* bias, const float* h0,
+                      const float* c0, float* y, float* hT, float* cT, int32_t* trip,
+                      bool save) {
+  const ll_desc& d = p->d;
+  const int H = d.H, B = d.B, L = d.layers;
+  hipEvent_t ev = tbeg(p, s);
+  LL_HIP(ll::launch_prep(seq_len, B, d.T_max, p->perm, p->active, p->off, p->rowmap, p->meta,
+                         trip, s));
+  tend(p, s, LL_STAGE_PREP, ev);
+  for (int l = 0; l < L; ++l) {
+    const int Il = in_width(p, l);
+    ev = tbeg(p, s);
+    // W^T: row n = gate column n, K-contiguous operand of both products
+    LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, 4 * H, 4 * H,
+                                   reinterpret_cast<T*>(p->WT[l]), Il + H, s));
+    // Zx = x_t W_x + b for every compact row (layer 0 gathers time-major x)
+    ll::GemmArgs g{};
+    g.A = l == 0 ? x : p->HH[0];
+    g.lda = Il;
+    g.a_rowmap = l == 0 ? p->rowmap : nullptr;
+    g.Bm = p->WT[l];
+    g.ldb = Il + H;
+    g.C = p->Zx;
+    g.ldc = 4L * H;
+    g.bias = bias[l];
+    g.M = (int)p->cap;
+    g.M_dev = p->meta + 1;
+    g.N = 4 * H;
+    g.K = Il;
+    g.splits = 1;
+    LL_HIP(ll::launch_gemm_nt<T>(g, s));
+    tend(p, s, LL_STAGE_INPUT_PROJ, ev);
+    ll::FwdLoopArgs a{};
+    a.B = B;
+    a.H = H;
+    a.T_max = d.T_max;
+    a.HJ = p->geom.HJ;
+    a.RG = p->geom.RG;
+    a.MRT = p->geom.MRT;
+    a.meta = p->meta;
+    a.active = p->active;
+    a.off = p->off;
+    a.perm = p->perm;
+    a.Zx = p->Zx;
+    a.WT = p->WT[l];
+    a.ldw = Il + H;
+    a.woff = Il;
+    a.h0 = h0 ? h0 + (long)l * B * H : nullptr;
+    a.c0 = c0 ? c0 + (long)l * B * H : nullptr;
+    a.HH = p->HH[l];
+    a.stack = save ? p->stack[l] : nullptr;
+    a.y = (l == L - 1) ? y : nullptr;
+    a.hT = hT + (long)l * B * H;
+    a.cT = cT + (long)l * B * H;
+    a.bar = reinterpret_cast<unsigned*>(p->meta + 4 + l);   // one counter per launch
+    a.abort_flag = p->meta + 3;
+    a.err = p->meta + 2;
+    a.limit = p->barrier_ticks;
+    ev = tbeg(p, s);
+    LL_HIP(ll::launch_fwd_loop<T>(a, p->geom.nwg, p->geom.lds_fwd, s));
+    tend(p, s, LL_STAGE_FWD_LOOP, ev);
+  }
+  return LL_OK;
+}
+
+template <typename T>
+ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* dhT,
+                      const float* dcT, float* dx, float* const* dW, float* const* dbias,
+                      float* dh0, float* dc0) {
+  const ll_desc& d = p->d;
+  const int H = d.H, B = d.B, L = d.layers;
+  hipEvent_t ev = tbeg(p, s);
+  if (dx) LL_HIP(ll::launch_zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta, s));
+  tend(p, s, LL_STAGE_DX, ev);
+  for (int l = L - 1; l >= 0; --l) {
+    const int Il = in_width(p, l);
+    ll::BwdLoopArgs a{};
+    a.B = B;
+    a.H = H;
+    a.T_max = d.T_max;
+    a.HJ = p->geom.HJ;
+    a.RG = p->geom.RG;
+    a.MRT = p->geom.MRT;
+    a.meta = p->meta;
+    a.active = p->active;
+    a.off = p->off;
+    a.perm = p->perm;
+    a.W = p->W[l];
+    a.wrow0 = Il;
+    a.stack = p->stack[l];
+    a.c0 = p->c0 ? p->c0 + (long)l * B * H : nullptr;
+    if (l == L - 1) {
+      a.dy = dy;
+      a.dy_compact = 0;
+    } else {
+      a.dy = p->dyc;
+      a.dy_compact = 1;
+    }
+    a.dhT = dhT ? dhT + (long)l * B * H : nullptr;
+    a.dcT = dcT ? dcT + (long)l * B * H : nullptr;
+    a.DZ = p->DZ;
+    a.db_part = p->db_part;
+    a.dh0 = dh0 ? dh0 + (long)l * B * H : nullptr;
+    a.dc0 = dc0 ? dc0 + (long)l * B * H : nullptr;
+    a.bar = reinterpret_cast<unsigned*>(p->meta + 6 + l);   // one counter per launch
+    a.abort_flag = p->meta + 3;
+    a.err = p->meta + 2;
+    a.limit = p->barrier_ticks;
+    ev = tbeg(p, s);
+    LL_HIP(ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s));
+    tend(p, s, LL_STAGE_BWD_LOOP, ev);
+    // db = sum of the row-group partials
+    ev = tbeg(p, s);
+    LL_HIP(ll::launch_sum_slices(p->db_part, p->geom.RG, 4L * H, 4L * H, dbias[l], s));
+    tend(p, s, LL_STAGE_DW, ev);
+    ev = tbeg(p, s);
+    // transposed operands of the dW products (reduction over compact rows)
+    ll::GatherTArgs gt{};
+    gt.B = B;
+    gt.meta = p->meta;
+    gt.rowmap = p->rowmap;
+    gt.off = p->off;
+    gt.perm = p->perm;
+    gt.ldo = (int)p->ldT;
+    gt.in = p->DZ;
+    gt.out = p->DZT;
+    gt.C = 4 * H;
+    gt.mode = 1;
+    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+    gt.in = l == 0 ? p->x : p->HH[0];
+    gt.out = p->XT;
+    gt.C = Il;
+    gt.mode = l == 0 ? 0 : 1;
+    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+    gt.in = p->HH[l];
+    gt.out = p->HPT;
+    gt.C = H;
+    gt.mode = 2;
+    gt.h0f = p->h0 ? p->h0 + (long)l * B * H : nullptr;
+    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+    tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
+    // dW_x = X^T DZ, dW_h = Hprev^T DZ
+    ev = tbeg(p, s);
+    for (int part = 0; part < 2; ++part) {
+      const int M = part == 0 ? Il : H;
+      ll::GemmArgs g{};
+      g.A = part == 0 ? p->XT : p->HPT;
+      g.lda = p->ldT;
+      g.Bm = p->DZT;
+      g.ldb = p->ldT;
+      g.M = M;
+      g.N = 4 * H;
+      g.K = (int)p->cap;
+      g.K_dev = p->meta + 1;
+      g.splits = p->dw_splits[part];
+      float* dst = dW[l] + (part == 0 ? 0L : (long)Il * 4 * H);
+      if (g.splits > 1) {
+        g.C = p->ws;
+        g.ldc = 4L * H;
+        g.split_stride = (long)M * 4 * H;
+        LL_HIP(ll::launch_gemm_nt<T>(g, s));
+        LL_HIP(ll::launch_sum_slices(p->ws, g.splits, g.split_stride, g.split_stride, dst, s));
+      } else {
+        g.C = dst;
+        g.ldc = 4L * H;
+        LL_HIP(ll::launch_gemm_nt<T>(g, s));
+      }
+    }
+    tend(p, s, LL_STAGE_DW, ev);
+    // dx_t = dz_t W_x^T: scattered to time-major dx (layer 0) or kept compact
+    // as the gradient of the layer below (layer 1)
+    if (l == 0 && !dx) continue;
+    ev = tbeg(p, s);
+    ll::GemmArgs g{};
+    g.A = p->DZ;
+    g.lda = 4L * H;
+    g.Bm = p->W[l];
+    g.ldb = 4L * H;
+    g.M = (int)p->cap;
+    g.M_dev = p->meta + 1;
+    g.N = Il;
+    g.K = 4 * H;
+    g.splits = 1;
+    if (l == 0) {
+      g.C = dx;
+      g.ldc = d.I;
+      g.c_rowmap = p->rowmap;
+    } else {
+      g.C = p->dyc;
+      g.ldc = H;
+    }
+    LL_HIP(ll::launch_gemm_nt<T>(g, s));
+    tend(p, s, LL_STAGE_DX, ev);
+  }
+  return LL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ll_status lstm_loop_fwd(ll_plan* p, void* stream, const void* x, const int32_t* seq_len,
+                        const void* const* W, const float* const* bias, const float* h0,
+                        const float* c0, float* y, float* hT, float* cT, int32_t* trip_count,
+                        int32_t save_for_backward) {
+  if (!p) return fail(LL_EINVAL, "plan is NULL");
+  if (!x || !seq_len || !W || !bias || !hT || !cT)
+    return fail(LL_EINVAL, "x, seq_len, W, bias, hT and cT are required");
+  for (int l = 0; l < p->d.layers; ++l)
+    if (!W[l] || !bias[l]) return fail(LL_EINVAL, "W[%d] or bias[%d] is NULL", l, l);
+  DeviceGuard guard(p->device);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  p->state = ST_EMPTY;
+  ll_status st = p->bf16 ? enqueue_fwd<bf16_t>(p, s, x, seq_len, W, bias, h0, c0, y, hT, cT,
+                                               trip_count, save_for_backward != 0)
+                         : enqueue_fwd<float>(p, s, x, seq_len, W, bias, h0, c0, y, hT, cT,
+                                              trip_count, save_for_backward != 0);
+  p->last_stream = s;
+  if (st != LL_OK) return st;
+  if (save_for_backward) {
+    p->state = ST_FWD_DONE;
+    p->x = x;
+    p->seq_len = seq_len;
+    for (int l = 0; l < p->d.layers; ++l) p->W[l] = W[l];
+    p->h0 = h0;
+    p->c0 = c0;
+  }
+  return LL_OK;
+}
+
+ll_status lstm_loop_bwd(ll_plan* p, void* stream, const float* dy, const float* dhT,
+                        const float* dcT, float* dx, float* const* dW, float* const* dbias,
+                        float* dh0, float* dc0) {
+  if (!p) return fail(LL_EINVAL, "plan is NULL");
+  if (p->state != ST_FWD_DONE)
+    return fail(LL_ESTATE, "no saved forward on this plan (call lstm_loop_fwd with "
+                           "save_for_backward=1 first)");
+  if (!dW || !dbias) return fail(LL_EINVAL, "dW and dbias are required");
+  for (int l = 0; l < p->d.layers; ++l)
+    if (!dW[l] || !dbias[l]) return fail(LL_EINVAL, "dW[%d] or dbias[%d] is NULL", l, l);
+  DeviceGuard guard(p->device);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  ll_status st = p->bf16 ? enqueue_bwd<bf16_t>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0)
+                         : enqueue_bwd<float>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
+  p->last_stream = s;
+  p->state = ST_EMPTY;
+  return st;
+}
+
+ll_status ll_status_sync(ll_plan* p, int32_t* device_error) {
+  if (!p) return fail(LL_EINVAL, "plan is NULL");
+  DeviceGuard guard(p->device);
+  LL_HIP(hipStreamSynchronize(p->last_stream));
+  int32_t e = 0;
+  LL_HIP(hipMemcpy(&e, p->meta + 2, sizeof(int32_t), hipMemcpyDeviceToHost));
+  const int32_t zero = 0;
+  LL_HIP(hipMemcpy(p->meta + 2, &zero, sizeof(int32_t), hipMemcpyHostToDevice));
+  if (device_error) *device_error = e;
+  return LL_OK;
+}
+
+}  // extern "C"

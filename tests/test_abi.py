@@ -1,0 +1,82 @@
+"""Host-side checks of the C-ABI library (no GPU needed).
+
+- the shared library loads and exports every function include/lstmloop.h
+  declares;
+- descriptor validation rejects bad problems before touching a device.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1805_01772_amd import lstmloop as ll
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lstmloop.h")
+
+
+def _lib():
+    if not os.path.exists(ll.LIB_PATH):
+        from paper_1805_01772_amd import build_lib
+        build_lib.build()
+    return ll.load_library()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*([a-z_][a-z0-9_]*)\s*\(",
+                       text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared_functions()
+    for n in ("ll_plan_create", "ll_plan_destroy", "lstm_loop_fwd", "lstm_loop_bwd",
+              "ll_status_sync", "ll_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib()
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    assert set(ll.EXPORTED) == set(_declared_functions())
+
+
+def test_version_string():
+    _lib()
+    assert "gfx950" in ll.ll_version()
+
+
+@pytest.mark.parametrize("fields,status", [
+    (dict(T_max=0), ll.LL_EINVAL),
+    (dict(B=0), ll.LL_EINVAL),
+    (dict(layers=3), ll.LL_EINVAL),
+    (dict(dtype=7), ll.LL_EINVAL),
+    (dict(reserved=1), ll.LL_EINVAL),
+    (dict(spill=2), ll.LL_EINVAL),
+    (dict(H=48), ll.LL_EUNSUPPORTED),
+    (dict(I=6), ll.LL_EUNSUPPORTED),
+    (dict(B=5000), ll.LL_EUNSUPPORTED),
+])
+def test_descriptor_validation(fields, status):
+    lib = _lib()
+    base = dict(T_max=8, B=4, I=32, H=32, layers=1, dtype=ll.LL_BF16, spill=0,
+                spill_chunk_steps=0, device_stack_budget_bytes=0, reserved=0)
+    base.update(fields)
+    d = ll.ll_desc(**base)
+    h = ctypes.c_void_p(123)
+    st = lib.ll_plan_create(ctypes.byref(d), 0, ctypes.byref(h))
+    assert st == status, ll.ll_last_error()
+    assert h.value is None
+    assert ll.ll_last_error() != ""
+
+
+def test_null_arguments_rejected():
+    lib = _lib()
+    assert lib.ll_plan_create(None, 0, None) == ll.LL_EINVAL
+    assert lib.lstm_loop_bwd(None, None, None, None, None, None, None, None, None, None) \
+        == ll.LL_EINVAL
+    assert lib.ll_plan_destroy(None) == ll.LL_OK

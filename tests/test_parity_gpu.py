@@ -1,0 +1,277 @@
+"""GPU parity: the HIP loops (through the C ABI) against the CPU oracle.
+
+Tolerance (per output tensor, max |gpu - oracle| / max |oracle|): 1e-5 for
+float32 runs against the float64 oracle, 2e-2 for bfloat16-operand runs
+against the bfloat16-emulating oracle.  Invariants that the method fixes
+exactly (finished rows, zero-trip loops, per-row independence) are checked
+bitwise between GPU runs.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1805_01772_amd import workloads as wl
+from paper_1805_01772_amd.lstmloop import LL_DEVERR_SEQ_LEN, LL_ESTATE, LoopError
+from paper_1805_01772_amd.runner import DeviceCase
+from _helpers import TOL, compare, oracle_reference, say
+
+pytestmark = pytest.mark.gpu
+
+W = wl.Workload
+SMALL = [
+    wl.TINY,
+    wl.TINY.with_(name="tiny_random_state_dy", random_state=True, with_dy=True, seed=7),
+    W("f32_b37_i48_h64_t23", B=37, I=48, H=64, T_max=23, dtype="f32", len_lo=0, len_hi=23,
+      w_scale=0.3, random_state=True, seed=11),
+    W("bf16_b50_i64_h96_t19", B=50, I=64, H=96, T_max=19, dtype="bf16", len_lo=0, len_hi=19,
+      w_scale=0.3, random_state=True, seed=12),
+    W("f32_b1_i4_h32_t1", B=1, I=4, H=32, T_max=1, dtype="f32", len_lo=1, len_hi=1,
+      random_state=True, seed=13),
+    W("f32_b100_i32_h512_t9_mrt2", B=100, I=32, H=512, T_max=9, dtype="f32", len_lo=0,
+      len_hi=9, random_state=True, seed=14),
+    W("bf16_b200_i64_h1024_t6_mrt4", B=200, I=64, H=1024, T_max=6, dtype="bf16", len_lo=1,
+      len_hi=6, random_state=True, seed=15),
+    W("bf16_b250_i64_h2048_t3_mrt16", B=250, I=64, H=2048, T_max=3, dtype="bf16", len_lo=0,
+      len_hi=3, random_state=True, seed=16),
+    W("f32_2layer_b21_i40_h32_t11", B=21, I=40, H=32, T_max=11, dtype="f32", layers=2,
+      len_lo=1, len_hi=11, w_scale=0.3, random_state=True, seed=17),
+    W("bf16_2layer_b33_i32_h64_t9", B=33, I=32, H=64, T_max=9, dtype="bf16", layers=2,
+      len_lo=0, len_hi=9, w_scale=0.3, random_state=True, seed=18),
+    W("f32_b300_i16_h64_t5_ragged", B=300, I=16, H=64, T_max=5, dtype="f32", len_lo=0,
+      len_hi=5, random_state=True, seed=19),
+]
+
+
+def run_case(w, inp, save=True, backward=True, with_dy=True):
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
+    plan = dc.plan()
+    dc.fwd(plan, save=save)
+    if backward:
+        dc.bwd(plan, with_dy=with_dy)
+    err = plan.status_sync()
+    res = dc.results()
+    plan.close()
+    return res, err
+
+
+@pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
+def test_small_parity(w):
+    say(f"[parity] {w.name}")
+    inp = wl.generate(w)
+    res, err = run_case(w, inp)
+    assert err == 0
+    ref = oracle_reference(inp, w.layers, w.dtype)
+    assert res["T_eff"] == ref["T_eff"] == int(inp["seq_len"].max())
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
+
+
+def test_zero_trip_loop_returns_inits_bitwise():
+    w = wl.TINY.with_(name="all_zero", random_state=True, with_dy=True, seed=21)
+    inp = wl.generate(w)
+    inp["seq_len"][:] = 0
+    say("[edge] all lengths zero")
+    res, err = run_case(w, inp)
+    assert err == 0 and res["T_eff"] == 0
+    assert (res["y"] == 0).all() and (res["dx"] == 0).all()
+    np.testing.assert_array_equal(res["hT"], inp["h0"])
+    np.testing.assert_array_equal(res["cT"], inp["c0"])
+    np.testing.assert_array_equal(res["dh0"], inp["dhT"])
+    np.testing.assert_array_equal(res["dc0"], inp["dcT"])
+    assert all((d == 0).all() for d in res["dW"]) and all((d == 0).all() for d in res["dbias"])
+
+
+def test_finished_rows_and_nan_padding():
+    w = W("nanpad", B=19, I=24, H=64, T_max=13, dtype="f32", len_lo=0, len_hi=13,
+          random_state=True, seed=22)
+    inp = wl.generate(w)
+    say("[edge] NaN padding")
+    clean, _ = run_case(w, inp)
+    inp_nan = wl.generate(w, nan_padding=True)
+    dirty, err = run_case(w, inp_nan)
+    assert err == 0
+    for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+        np.testing.assert_array_equal(dirty[k], clean[k], err_msg=k)
+    for a, b in zip(dirty["dW"] + dirty["dbias"], clean["dW"] + clean["dbias"]):
+        np.testing.assert_array_equal(a, b)
+    L = inp["seq_len"]
+    for b in range(w.B):
+        assert (clean["y"][L[b]:, b] == 0).all() and (clean["dx"][L[b]:, b] == 0).all()
+        if L[b] > 0:
+            np.testing.assert_array_equal(clean["hT"][0, b], clean["y"][L[b] - 1, b])
+        else:
+            np.testing.assert_array_equal(clean["hT"][0, b], inp["h0"][0, b])
+
+
+def test_rows_are_independent_and_permutation_equivariant():
+    w = W("perm", B=40, I=32, H=128, T_max=10, dtype="bf16", len_lo=0, len_hi=10,
+          random_state=True, seed=23)
+    inp = wl.generate(w)
+    say("[edge] permutation")
+    full, _ = run_case(w, inp)
+    p = np.random.default_rng(0).permutation(w.B)
+    pin = dict(inp)
+    pin["x"] = inp["x"][:, p].copy()
+    pin["dy"] = inp["dy"][:, p].copy()
+    pin["seq_len"] = inp["seq_len"][p].copy()
+    for k in ("h0", "c0", "dhT", "dcT"):
+        pin[k] = inp[k][:, p].copy()
+    perm, _ = run_case(w, pin)
+    for k in ("y", "dx"):
+        np.testing.assert_array_equal(perm[k], full[k][:, p], err_msg=k)
+    for k in ("hT", "cT", "dh0", "dc0"):
+        np.testing.assert_array_equal(perm[k], full[k][:, p], err_msg=k)
+    for a, b in zip(perm["dW"] + perm["dbias"], full["dW"] + full["dbias"]):
+        assert np.abs(a - b).max() <= 1e-5 * np.abs(b).max()
+    say("[edge] one row alone")
+    for b in (0, 7, 33):
+        one = {k: (v[:, b:b + 1].copy() if k in ("x", "dy", "h0", "c0", "dhT", "dcT") else v)
+               for k, v in inp.items()}
+        one["seq_len"] = inp["seq_len"][b:b + 1].copy()
+        res, _ = run_case(w.with_(B=1), one)
+        for k in ("y", "dx"):
+            np.testing.assert_array_equal(res[k][:, 0], full[k][:, b], err_msg=k)
+        for k in ("hT", "cT", "dh0", "dc0"):
+            np.testing.assert_array_equal(res[k][:, 0], full[k][:, b], err_msg=k)
+
+
+def test_tmax_padding_changes_nothing():
+    w = W("tpad", B=24, I=32, H=64, T_max=8, dtype="f32", len_lo=0, len_hi=8,
+          random_state=True, seed=24)
+    inp = wl.generate(w)
+    say("[edge] T_max padding")
+    a, _ = run_case(w, inp)
+    big = dict(inp)
+    rng = np.random.default_rng(1)
+    big["x"] = np.concatenate([inp["x"], rng.standard_normal((5, 24, 32), dtype=np.float32)])
+    big["dy"] = np.concatenate([inp["dy"], rng.standard_normal((5, 24, 64), dtype=np.float32)])
+    b, _ = run_case(w.with_(T_max=13), big)
+    for k in ("hT", "cT", "dh0", "dc0"):
+        np.testing.assert_array_equal(b[k], a[k], err_msg=k)
+    np.testing.assert_array_equal(b["y"][:8], a["y"])
+    np.testing.assert_array_equal(b["dx"][:8], a["dx"])
+    assert (b["y"][8:] == 0).all() and (b["dx"][8:] == 0).all()
+    for u, v in zip(b["dW"] + b["dbias"], a["dW"] + a["dbias"]):
+        assert np.abs(u - v).max() <= 1e-6 * np.abs(v).max()
+
+
+def test_repeat_calls_are_deterministic():
+    w = W("det", B=64, I=64, H=256, T_max=12, dtype="bf16", len_lo=1, len_hi=12,
+          random_state=True, seed=25)
+    inp = wl.generate(w)
+    say("[edge] determinism")
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
+    plan = dc.plan()
+    outs = []
+    for _ in range(3):
+        dc.fwd(plan)
+        dc.bwd(plan)
+        outs.append(dc.results())
+    plan.close()
+    for o in outs[1:]:
+        for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+            np.testing.assert_array_equal(o[k], outs[0][k])
+        for u, v in zip(o["dW"] + o["dbias"], outs[0]["dW"] + outs[0]["dbias"]):
+            np.testing.assert_array_equal(u, v)
+
+
+def test_two_layers_equal_two_single_layer_calls():
+    w = W("stack2", B=45, I=64, H=64, T_max=10, dtype="bf16", layers=2, len_lo=0, len_hi=10,
+          random_state=True, seed=26)
+    inp = wl.generate(w)
+    say("[edge] two layers vs two calls")
+    both, _ = run_case(w, inp)
+    w1 = w.with_(layers=1)
+    l1 = dict(inp, W=[inp["W"][0]], bias=[inp["bias"][0]], h0=inp["h0"][:1], c0=inp["c0"][:1],
+              dhT=inp["dhT"][:1], dcT=inp["dcT"][:1])
+    # forward of layer 1, then layer 2 on bf16(y1); backward in reverse order
+    dc1 = DeviceCase(l1, w.H, w.I, 1, "bf16")
+    p1 = dc1.plan()
+    dc1.fwd(p1)
+    y1 = dc1.y.detach().clone()
+    l2 = dict(inp, x=y1.to(torch.bfloat16).float().cpu().numpy(), W=[inp["W"][1]],
+              bias=[inp["bias"][1]], h0=inp["h0"][1:], c0=inp["c0"][1:], dhT=inp["dhT"][1:],
+              dcT=inp["dcT"][1:])
+    dc2 = DeviceCase(l2, w.H, w.H, 1, "bf16")
+    p2 = dc2.plan()
+    dc2.fwd(p2)
+    dc2.bwd(p2)
+    r2 = dc2.results()
+    dc1.dy = dc2.dx.detach().clone()
+    dc1.bwd(p1)
+    r1 = dc1.results()
+    p1.close()
+    p2.close()
+    np.testing.assert_array_equal(both["y"], r2["y"])
+    np.testing.assert_array_equal(both["hT"], np.concatenate([r1["hT"], r2["hT"]]))
+    np.testing.assert_array_equal(both["cT"], np.concatenate([r1["cT"], r2["cT"]]))
+    np.testing.assert_array_equal(both["dx"], r1["dx"])
+    np.testing.assert_array_equal(both["dh0"], np.concatenate([r1["dh0"], r2["dh0"]]))
+    np.testing.assert_array_equal(both["dW"][0], r1["dW"][0])
+    np.testing.assert_array_equal(both["dW"][1], r2["dW"][0])
+    np.testing.assert_array_equal(both["dbias"][1], r2["dbias"][0])
+
+
+def test_invalid_lengths_raise_device_error_and_recover():
+    w = W("badlen", B=8, I=32, H=32, T_max=6, dtype="f32", len_lo=1, len_hi=6,
+          random_state=True, seed=27)
+    inp = wl.generate(w)
+    say("[edge] invalid seq_len")
+    bad = dict(inp, seq_len=inp["seq_len"].copy())
+    bad["seq_len"][3] = 7
+    res, err = run_case(w, bad)
+    assert err & LL_DEVERR_SEQ_LEN
+    assert res["T_eff"] == 0 and (res["y"] == 0).all() and (res["dx"] == 0).all()
+    np.testing.assert_array_equal(res["hT"], inp["h0"])
+    good, err2 = run_case(w, inp)
+    assert err2 == 0 and good["T_eff"] == int(inp["seq_len"].max())
+
+
+def test_backward_without_forward_is_a_state_error():
+    w = wl.TINY
+    inp = wl.generate(w)
+    dc = DeviceCase(inp, w.H, w.I, 1, w.dtype)
+    plan = dc.plan()
+    with pytest.raises(LoopError) as e:
+        dc.bwd(plan)
+    assert e.value.status == LL_ESTATE
+    dc.fwd(plan, save=False)                 # inference saves nothing
+    with pytest.raises(LoopError):
+        dc.bwd(plan)
+    dc.fwd(plan, save=True)
+    dc.bwd(plan)
+    with pytest.raises(LoopError):           # the stack was consumed
+        dc.bwd(plan)
+    plan.close()
+
+
+# ----------------------------------------------------------- full sizes
+@pytest.mark.parametrize("w", [wl.FIXED_H512, wl.VAR_H1024], ids=lambda w: w.name)
+def test_full_size_parity(w):
+    say(f"[full] {w.name}")
+    inp = wl.generate(w)
+    res, err = run_case(w, inp)
+    assert err == 0
+    say("    oracle running")
+    ref = oracle_reference(inp, w.layers, w.dtype)
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
+
+
+def test_two_layer_full_size_sampled_rows():
+    w = wl.TWO_LAYER
+    say(f"[full] {w.name} (sampled rows)")
+    inp = wl.generate(w)
+    res, err = run_case(w, inp)
+    assert err == 0
+    rows = [int(np.argmax(inp["seq_len"])), int(np.argmin(inp["seq_len"])), 101]
+    sub = {k: (v[:, rows].copy() if k in ("x", "dy", "h0", "c0", "dhT", "dcT") else v)
+           for k, v in inp.items()}
+    sub["seq_len"] = inp["seq_len"][rows].copy()
+    ref = oracle_reference(sub, w.layers, w.dtype)
+    got = {k: res[k][:, rows] for k in ("y", "hT", "cT", "dx", "dh0", "dc0")}
+    errs, bad = compare(got, ref, TOL[w.dtype], keys=("y", "hT", "cT", "dx", "dh0", "dc0"))
+    say(f"    errors {errs}")
+    assert not bad, bad
