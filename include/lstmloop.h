@@ -116,11 +116,15 @@ ll_status ll_plan_stack_bytes(const ll_plan* plan, int64_t* device_bytes,
                               int64_t* host_bytes);
 
 /* Launch geometry the plan chose for the recurrent loops (for reports):
- * work-groups of the forward loop, hidden units per work-group, work-groups
- * per unit block.  Any output may be NULL. */
+ * work-groups per loop launch, hidden units per work-group, row groups
+ * (independent recurrences), and whether the XCD-local loops are used (1:
+ * each of the 8 XCDs runs the rows of its own group through its own L2; 0:
+ * one grid-wide barrier per step).  Any output may be NULL.
+ * The environment variable LSTMLOOP_LOOPS=grid at plan creation forces the
+ * grid-barrier loops. */
 ll_status ll_plan_geometry(const ll_plan* plan, int32_t* loop_workgroups,
                            int32_t* units_per_workgroup,
-                           int32_t* row_groups);
+                           int32_t* row_groups, int32_t* xcd_local);
 
 /*
  * Forward while-loop (Sections 2.1, 4.2, 5.1).

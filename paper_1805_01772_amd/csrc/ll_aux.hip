@@ -100,7 +100,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_
     meta[0] = T_eff;
     meta[1] = total;
     meta[3] = 0;                       // abort flag
-    for (int i = 0; i < 4; ++i) meta[4 + i] = 0;   // barrier counters
+    for (int i = 4; i < META_INTS; ++i) meta[i] = 0;   // barrier and rank counters
     if (bad) atomicOr(&meta[2], LL_DEVERR_SEQ_LEN_BIT);
     if (trip_out) *trip_out = T_eff;
   }

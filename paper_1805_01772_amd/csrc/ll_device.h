@@ -59,9 +59,15 @@ template <> struct Mfma<float> {
 };
 
 // ----------------------------------------------------- activations
-// sigmoid(u) = 1 / (1 + e^-u); tanh from the HIP math library.
-__device__ __forceinline__ float sigmoidf_(float u) { return 1.0f / (1.0f + expf(-u)); }
-__device__ __forceinline__ float tanhf_(float u) { return tanhf(u); }
+// sigmoid(u) = 1 / (1 + e^-u) and tanh(u) = 1 - 2 / (1 + e^{2u}), on the
+// hardware exponential and reciprocal.  Both saturate correctly (e^x -> inf
+// or 0); near u = 0 tanh keeps an absolute error of about one float ulp of 1.
+__device__ __forceinline__ float sigmoidf_(float u) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-u));
+}
+__device__ __forceinline__ float tanhf_(float u) {
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __expf(2.0f * u));
+}
 
 __device__ __forceinline__ uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
 

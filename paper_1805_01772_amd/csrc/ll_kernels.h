@@ -11,7 +11,10 @@ constexpr int LL_DEVERR_BARRIER_BIT = 2;
 // meta[] layout (device int array owned by a plan)
 //   0: T_eff   1: total rows (sum of lengths)   2: error word   3: abort flag
 //   4..7: grid-barrier counters
-constexpr int META_INTS = 8;
+//   16 + 8 * launch + xcd: per-XCD rank counters of the XCD-local loops
+//   (launch 0/1: forward layer 0/1, launch 2/3: backward layer 0/1)
+constexpr int META_INTS = 64;
+constexpr int META_RANK0 = 16;
 
 struct GatherTArgs {
   const void* in;
@@ -106,6 +109,54 @@ struct BwdLoopArgs {
   int* err;
   unsigned long long limit;
 };
+
+// XCD-local loops (ll_xloop.hip).  One argument block serves both directions.
+struct XLoopArgs {
+  int B, H, T_max;
+  int P;                  // members per XCD that own a unit block (H / HJ)
+  int MRT;                // row tiles per XCD = ceil(ceil(B/16) / 8)
+  const int* meta;
+  const int* active;
+  const int* off;
+  const int* perm;
+  const void* W;          // forward: W^T [4H, ldw]; backward: W [rows, 4H]
+  int ldw;
+  int woff;               // forward: column of the h part in W^T; backward: row of W_h
+  void* X;                // exchange array: forward h history [cap, H];
+                          // backward dz [cap, 4H] (operand type, pre-filled)
+  const float* Zx;        // forward: [cap, 4H]
+  const float* h0;
+  const float* c0;
+  float* stack;           // forward: push (NULL = inference); backward: pop
+  float* y;
+  float* hT;
+  float* cT;
+  const float* dy;
+  int dy_compact;
+  const float* dhT;
+  const float* dcT;
+  float* db_part;         // backward: [8, 4H]
+  float* dh0;
+  float* dc0;
+  unsigned* rank_ctr;     // [8], zero before the launch
+  int* abort_flag;
+  int* err;
+  unsigned long long limit;
+};
+
+struct XKernels {
+  const void* fwd;
+  const void* bwd;
+  size_t lds_fwd;
+  size_t lds_bwd;
+};
+
+template <typename T>
+XKernels x_kernels(int hc, int mrt);
+hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd);
+hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s);
+hipError_t launch_fill_pending(void* base, long row_bytes, const int* meta, long cap_rows,
+                               hipStream_t s);
 
 hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
                        int* rowmap, int* meta, int* trip_out, hipStream_t s);

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -69,6 +70,10 @@ struct ll_plan {
   int n_cu = 0;
   unsigned long long barrier_ticks = 0;
   int dw_splits[2] = {1, 1};   // split-K of the dW_x / dW_h products
+  bool xmode = false;          // XCD-local loops (ll_xloop.hip)
+  ll::XKernels xk{};
+  int xP = 0;                  // unit blocks per XCD
+  int xMRT = 0;                // row tiles per XCD
   // device memory
   int* perm = nullptr;
   int* active = nullptr;
@@ -301,6 +306,36 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
                 p->geom.nwg, occ_f, occ_b, p->n_cu);
   }
 
+  // XCD-local loops: 8 XCDs x 32 CUs, every exchanged row 128-byte aligned,
+  // H split 32 ways (bf16: 32 units per work-group, f32: 16).
+  {
+    const char* mode = getenv("LSTMLOOP_LOOPS");
+    const bool allow = !(mode && strcmp(mode, "grid") == 0);
+    const int HJx = p->bf16 ? 32 : 16;
+    const int P = H / HJx;
+    if (allow && p->n_cu == 256 && H % HJx == 0 && P >= 1 && P <= 32 &&
+        ((long)H * p->es) % 128 == 0) {
+      const int KS = p->bf16 ? H / 32 : H / 16;
+      const int need = (KS + 3) / 4;
+      const int hc = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : need <= 8 ? 8 : 0;
+      const int mrt = ((B + 15) / 16 + 7) / 8;
+      if (hc && mrt <= 16) {
+        ll::XKernels xk = p->bf16 ? ll::x_kernels<bf16_t>(hc, mrt) : ll::x_kernels<float>(hc, mrt);
+        if (xk.fwd && xk.bwd && xk.lds_fwd <= lds_limit && xk.lds_bwd <= lds_limit) {
+          int of = 0, ob = 0;
+          if (ll::x_setup(xk, &of, &ob) == hipSuccess && of >= 1 && ob >= 1) {
+            p->xmode = true;
+            p->xk = xk;
+            p->xP = P;
+            p->xMRT = mrt;
+          } else {
+            (void)hipGetLastError();
+          }
+        }
+      }
+    }
+  }
+
   // dW split-K: enough work-groups to cover the chip.
   for (int w = 0; w < 2; ++w) {
     const int M = w == 0 ? desc->I : H;
@@ -347,7 +382,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->XT, es * maxI * p->ldT, "x transposed");
   ALLOC(p->HPT, es * H * p->ldT, "h_prev transposed");
   if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
-  ALLOC(p->db_part, sizeof(float) * p->geom.RG * 4 * H, "db partials");
+  ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * 4 * H, "db partials");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
 #undef ALLOC
   if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess) {
@@ -401,11 +436,13 @@ ll_status ll_plan_stack_bytes(const ll_plan* p, int64_t* dev, int64_t* host) {
   return LL_OK;
 }
 
-ll_status ll_plan_geometry(const ll_plan* p, int32_t* nwg, int32_t* hj, int32_t* rg) {
+ll_status ll_plan_geometry(const ll_plan* p, int32_t* nwg, int32_t* hj, int32_t* rg,
+                           int32_t* xcd_local) {
   if (!p) return fail(LL_EINVAL, "plan is NULL");
-  if (nwg) *nwg = p->geom.nwg;
-  if (hj) *hj = p->geom.HJ;
-  if (rg) *rg = p->geom.RG;
+  if (nwg) *nwg = p->xmode ? 256 : p->geom.nwg;
+  if (hj) *hj = p->xmode ? (p->bf16 ? 32 : 16) : p->geom.HJ;
+  if (rg) *rg = p->xmode ? 8 : p->geom.RG;
+  if (xcd_local) *xcd_local = p->xmode ? 1 : 0;
   return LL_OK;
 }
 
@@ -447,6 +484,38 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     g.splits = 1;
     LL_HIP(ll::launch_gemm_nt<T>(g, s));
     tend(p, s, LL_STAGE_INPUT_PROJ, ev);
+    if (p->xmode) {
+      ev = tbeg(p, s);
+      LL_HIP(ll::launch_fill_pending(p->HH[l], (long)H * p->es, p->meta, p->cap, s));
+      ll::XLoopArgs xa{};
+      xa.B = B;
+      xa.H = H;
+      xa.T_max = d.T_max;
+      xa.P = p->xP;
+      xa.MRT = p->xMRT;
+      xa.meta = p->meta;
+      xa.active = p->active;
+      xa.off = p->off;
+      xa.perm = p->perm;
+      xa.W = p->WT[l];
+      xa.ldw = Il + H;
+      xa.woff = Il;
+      xa.X = p->HH[l];
+      xa.Zx = p->Zx;
+      xa.h0 = h0 ? h0 + (long)l * B * H : nullptr;
+      xa.c0 = c0 ? c0 + (long)l * B * H : nullptr;
+      xa.stack = save ? p->stack[l] : nullptr;
+      xa.y = (l == L - 1) ? y : nullptr;
+      xa.hT = hT + (long)l * B * H;
+      xa.cT = cT + (long)l * B * H;
+      xa.rank_ctr = reinterpret_cast<unsigned*>(p->meta + ll::META_RANK0 + 8 * l);
+      xa.abort_flag = p->meta + 3;
+      xa.err = p->meta + 2;
+      xa.limit = p->barrier_ticks;
+      LL_HIP(ll::x_launch(p->xk.fwd, xa, 256, p->xk.lds_fwd, s));
+      tend(p, s, LL_STAGE_FWD_LOOP, ev);
+      continue;
+    }
     ll::FwdLoopArgs a{};
     a.B = B;
     a.H = H;
@@ -491,6 +560,43 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
   tend(p, s, LL_STAGE_DX, ev);
   for (int l = L - 1; l >= 0; --l) {
     const int Il = in_width(p, l);
+    if (p->xmode) {
+      ev = tbeg(p, s);
+      LL_HIP(ll::launch_fill_pending(p->DZ, 4L * H * p->es, p->meta, p->cap, s));
+      ll::XLoopArgs xa{};
+      xa.B = B;
+      xa.H = H;
+      xa.T_max = d.T_max;
+      xa.P = p->xP;
+      xa.MRT = p->xMRT;
+      xa.meta = p->meta;
+      xa.active = p->active;
+      xa.off = p->off;
+      xa.perm = p->perm;
+      xa.W = p->W[l];
+      xa.woff = Il;
+      xa.X = p->DZ;
+      xa.c0 = p->c0 ? p->c0 + (long)l * B * H : nullptr;
+      xa.stack = p->stack[l];
+      if (l == L - 1) {
+        xa.dy = dy;
+        xa.dy_compact = 0;
+      } else {
+        xa.dy = p->dyc;
+        xa.dy_compact = 1;
+      }
+      xa.dhT = dhT ? dhT + (long)l * B * H : nullptr;
+      xa.dcT = dcT ? dcT + (long)l * B * H : nullptr;
+      xa.db_part = p->db_part;
+      xa.dh0 = dh0 ? dh0 + (long)l * B * H : nullptr;
+      xa.dc0 = dc0 ? dc0 + (long)l * B * H : nullptr;
+      xa.rank_ctr = reinterpret_cast<unsigned*>(p->meta + ll::META_RANK0 + 8 * (2 + l));
+      xa.abort_flag = p->meta + 3;
+      xa.err = p->meta + 2;
+      xa.limit = p->barrier_ticks;
+      LL_HIP(ll::x_launch(p->xk.bwd, xa, 256, p->xk.lds_bwd, s));
+      tend(p, s, LL_STAGE_BWD_LOOP, ev);
+    }
     ll::BwdLoopArgs a{};
     a.B = B;
     a.H = H;
@@ -523,12 +629,15 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     a.abort_flag = p->meta + 3;
     a.err = p->meta + 2;
     a.limit = p->barrier_ticks;
-    ev = tbeg(p, s);
-    LL_HIP(ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s));
-    tend(p, s, LL_STAGE_BWD_LOOP, ev);
+    if (!p->xmode) {
+      ev = tbeg(p, s);
+      LL_HIP(ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s));
+      tend(p, s, LL_STAGE_BWD_LOOP, ev);
+    }
     // db = sum of the row-group partials
     ev = tbeg(p, s);
-    LL_HIP(ll::launch_sum_slices(p->db_part, p->geom.RG, 4L * H, 4L * H, dbias[l], s));
+    LL_HIP(ll::launch_sum_slices(p->db_part, p->xmode ? 8 : p->geom.RG, 4L * H, 4L * H,
+                                 dbias[l], s));
     tend(p, s, LL_STAGE_DW, ev);
     ev = tbeg(p, s);
     // transposed operands of the dW products (reduction over compact rows)

@@ -54,13 +54,17 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         raise RuntimeError(
             f"{path} is missing: build it with `python -m paper_1805_01772_amd.build_lib` "
             "(or __graft_entry__.build()); there is no CPU fallback")
+    # torch ships its own HIP runtime (SONAME libamdhip64.so.7).  Loading torch
+    # first makes the library bind to that same runtime instead of a second
+    # copy, so torch's streams and device pointers are valid here.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     lib.ll_plan_create.argtypes = [ctypes.POINTER(ll_desc), ctypes.c_int, ctypes.POINTER(vp)]
     lib.ll_plan_destroy.argtypes = [vp]
     lib.ll_plan_stack_bytes.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.ll_plan_geometry.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32),
-                                     ctypes.POINTER(i32)]
+                                     ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.lstm_loop_fwd.argtypes = [vp, vp, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp),
                                   vp, vp, vp, vp, vp, vp, i32]
     lib.lstm_loop_bwd.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.POINTER(vp),
@@ -159,10 +163,11 @@ class Plan:
         return d.value, h.value
 
     def geometry(self):
-        n, hj, rg = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        n, hj, rg, xl = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
         _check(self._lib.ll_plan_geometry(self._h, ctypes.byref(n), ctypes.byref(hj),
-                                          ctypes.byref(rg)))
-        return dict(workgroups=n.value, units_per_workgroup=hj.value, row_groups=rg.value)
+                                          ctypes.byref(rg), ctypes.byref(xl)))
+        return dict(workgroups=n.value, units_per_workgroup=hj.value, row_groups=rg.value,
+                    xcd_local=bool(xl.value))
 
     def fwd(self, x, seq_len, W: Sequence, bias: Sequence, h0, c0, y, hT, cT,
             trip_count=None, save_for_backward: bool = True, stream=None) -> None:

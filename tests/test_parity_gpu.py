@@ -54,10 +54,27 @@ def run_case(w, inp, save=True, backward=True, with_dy=True):
     return res, err
 
 
+@pytest.fixture(params=["auto", "grid"])
+def loop_mode(request, monkeypatch):
+    """auto: the library's choice (XCD-local loops where the shape allows);
+    grid: the grid-barrier loops, forced through LSTMLOOP_LOOPS."""
+    if request.param == "grid":
+        monkeypatch.setenv("LSTMLOOP_LOOPS", "grid")
+    else:
+        monkeypatch.delenv("LSTMLOOP_LOOPS", raising=False)
+    return request.param
+
+
 @pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
-def test_small_parity(w):
-    say(f"[parity] {w.name}")
+def test_small_parity(w, loop_mode):
     inp = wl.generate(w)
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
+    plan = dc.plan()
+    geom = plan.geometry()
+    plan.close()
+    say(f"[parity] {w.name} mode={loop_mode} geometry={geom}")
+    if loop_mode == "grid":
+        assert not geom["xcd_local"]
     res, err = run_case(w, inp)
     assert err == 0
     ref = oracle_reference(inp, w.layers, w.dtype)
