@@ -122,6 +122,7 @@ struct XLoopArgs {
   const void* W;          // forward: W^T [4H, ldw]; backward: W [rows, 4H]
   int ldw;
   int woff;               // forward: column of the h part in W^T; backward: row of W_h
+  const void* H0;         // forward: h0 rows in length order, operand type [B, H]
   void* X;                // exchange array: forward h history [cap, H];
                           // backward dz [cap, 4H] (operand type, pre-filled)
   const float* Zx;        // forward: [cap, 4H]
@@ -157,6 +158,9 @@ hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd);
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s);
 hipError_t launch_fill_pending(void* base, long row_bytes, const int* meta, long cap_rows,
                                hipStream_t s);
+template <typename T>
+hipError_t launch_h0_sorted(const float* h0, const int* perm, int B, int H, void* out,
+                            hipStream_t s);
 
 hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
                        int* rowmap, int* meta, int* trip_out, hipStream_t s);

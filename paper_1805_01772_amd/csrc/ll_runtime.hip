@@ -89,6 +89,7 @@ struct ll_plan {
   void* XT = nullptr;
   void* HPT = nullptr;
   float* dyc = nullptr;
+  void* H0s = nullptr;         // h0 rows in length order, operand type [B, H]
   float* db_part = nullptr;
   float* ws = nullptr;
   long ws_floats = 0;
@@ -167,7 +168,7 @@ void drain_timing(ll_plan* p) {
 void free_plan_memory(ll_plan* p) {
   void* ptrs[] = {p->perm, p->active, p->off, p->rowmap, p->meta, p->WT[0], p->WT[1], p->Zx,
                   p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT, p->HPT,
-                  p->dyc, p->db_part, p->ws};
+                  p->dyc, p->H0s, p->db_part, p->ws};
   for (void* q : ptrs)
     if (q) hipFree(q);
 }
@@ -315,9 +316,9 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     const int P = H / HJx;
     if (allow && p->n_cu == 256 && H % HJx == 0 && P >= 1 && P <= 32 &&
         ((long)H * p->es) % 128 == 0) {
-      const int KS = p->bf16 ? H / 32 : H / 16;
-      const int need = (KS + 3) / 4;
-      const int hc = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : need <= 8 ? 8 : 0;
+      const int KS = p->bf16 ? H / 32 : H / 16;      // forward k-steps, 8 waves share them
+      const int need = (KS + 7) / 8;
+      const int hc = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 0;
       const int mrt = ((B + 15) / 16 + 7) / 8;
       if (hc && mrt <= 16) {
         ll::XKernels xk = p->bf16 ? ll::x_kernels<bf16_t>(hc, mrt) : ll::x_kernels<float>(hc, mrt);
@@ -382,6 +383,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->XT, es * maxI * p->ldT, "x transposed");
   ALLOC(p->HPT, es * H * p->ldT, "h_prev transposed");
   if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
+  ALLOC(p->H0s, es * B * H, "sorted h0");
   ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * 4 * H, "db partials");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
 #undef ALLOC
@@ -487,7 +489,9 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     if (p->xmode) {
       ev = tbeg(p, s);
       LL_HIP(ll::launch_fill_pending(p->HH[l], (long)H * p->es, p->meta, p->cap, s));
+      LL_HIP(ll::launch_h0_sorted<T>(h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->H0s, s));
       ll::XLoopArgs xa{};
+      xa.H0 = p->H0s;
       xa.B = B;
       xa.H = H;
       xa.T_max = d.T_max;

@@ -21,6 +21,8 @@
 // Each work-group keeps its recurrent weight slice on chip for the whole
 // loop, in registers (the first KSR k-steps of each wave's share; any rest in
 // LDS).
+#include <type_traits>
+
 #include "ll_kernels.h"
 
 namespace ll {
@@ -37,16 +39,25 @@ __device__ __forceinline__ unsigned long long ld_u64_agent(const void* p) {
 // True if any element of the 8-byte word still holds the fill pattern.
 template <typename T> __device__ __forceinline__ bool pending(unsigned long long v);
 template <> __device__ __forceinline__ bool pending<bf16_t>(unsigned long long v) {
-  const unsigned long long m = v & (v >> 1) & 0x7fff7fff7fff7fffull;   // low 15 bits all ones
-  const unsigned long long t = m & (m >> 2);
-  const unsigned long long t2 = t & (t >> 4);
-  const unsigned long long t3 = t2 & (t2 >> 8);
-  // element e is all-ones iff bit 0 of t3 (in its 16-bit lane) and bit 15 are set
-  const unsigned long long full = t3 & (v >> 15) & 0x0001000100010001ull;
-  return full != 0;
+  // an element is all ones iff its 16 bits of ~v are zero (zero-lane test)
+  const unsigned long long x = ~v;
+  return ((x - 0x0001000100010001ull) & ~x & 0x8000800080008000ull) != 0;
 }
 template <> __device__ __forceinline__ bool pending<float>(unsigned long long v) {
   return ((unsigned)v == 0xffffffffu) || ((unsigned)(v >> 32) == 0xffffffffu);
+}
+
+// 16-byte chunk read with two agent-scope (L1-bypassing) 64-bit loads.
+template <typename T>
+__device__ __forceinline__ uint4 ld_chunk_agent(const T* p) {
+  const unsigned long long lo = ld_u64_agent(p);
+  const unsigned long long hi = ld_u64_agent(p + 8 / sizeof(T));
+  return make_uint4((unsigned)lo, (unsigned)(lo >> 32), (unsigned)hi, (unsigned)(hi >> 32));
+}
+template <typename T>
+__device__ __forceinline__ bool pending_chunk(uint4 v) {
+  return pending<T>((unsigned long long)v.x | ((unsigned long long)v.y << 32)) ||
+         pending<T>((unsigned long long)v.z | ((unsigned long long)v.w << 32));
 }
 
 // Store forms of an exchanged value: NaN in canonical form (never all ones).
@@ -56,22 +67,6 @@ template <> __device__ __forceinline__ float to_exchange<float>(float v) {
 }
 template <> __device__ __forceinline__ bf16_t to_exchange<bf16_t>(float v) {
   return v != v ? (bf16_t)0x7fc0 : f32_to_bf16(v);
-}
-
-// 16-byte operand chunk from float data (h0 at step 0), converted.
-template <typename T> __device__ __forceinline__ uint4 xchunk_from_f32(const float* p);
-template <> __device__ __forceinline__ uint4 xchunk_from_f32<float>(const float* p) {
-  return ld16(p);
-}
-template <> __device__ __forceinline__ uint4 xchunk_from_f32<bf16_t>(const float* p) {
-  const float4 a = *reinterpret_cast<const float4*>(p);
-  const float4 b = *reinterpret_cast<const float4*>(p + 4);
-  uint4 r;
-  r.x = (uint32_t)f32_to_bf16(a.x) | ((uint32_t)f32_to_bf16(a.y) << 16);
-  r.y = (uint32_t)f32_to_bf16(a.z) | ((uint32_t)f32_to_bf16(a.w) << 16);
-  r.z = (uint32_t)f32_to_bf16(b.x) | ((uint32_t)f32_to_bf16(b.y) << 16);
-  r.w = (uint32_t)f32_to_bf16(b.z) | ((uint32_t)f32_to_bf16(b.w) << 16);
-  return r;
 }
 
 // Group of this work-group: (XCD, rank within the XCD).
@@ -86,36 +81,66 @@ __device__ __forceinline__ void join_group(unsigned* rank_ctr, int* s_info) {
 
 }  // namespace
 
-size_t xfwd_lds(int KSW, int KSR, int NCT) {
+// 8 waves per work-group, two per SIMD: the weight slice of a work-group is
+// split over 8 waves' registers (the reduction dimension is split 8 ways).
+constexpr int XNW = 8;
+constexpr int XNT = 64 * XNW;
+// Per-step loop metadata (active rows, compact offsets) for steps
+// lo .. lo+WIN, kept in LDS so that no step waits on a global load for it.
+constexpr int WIN = 256;
+
+// Forward partial products in LDS: [wave][element i of the MFMA result]
+// [column tile][lane], one slice of xfwd_is floats per (wave, i).  The pad of
+// 16 floats puts the four rows a 16-lane group of the cell reads in distinct
+// LDS banks.
+constexpr int xfwd_is(int NCT) { return NCT * 64 + 16; }
+
+// LDS of the forward kernel: weight k-steps not in registers, partial
+// products, metadata window, perm rows.
+size_t xfwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
   const int KSL = KSW > KSR ? KSW - KSR : 0;
-  return (size_t)4 * KSL * NCT * 64 * 16 + (size_t)3 * NCT * 256 * sizeof(float);
+  return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)XNW * 4 * xfwd_is(NCT) * 4 +
+         (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
 }
-size_t xbwd_lds(int KSW, int KSR, int NCT) {
+size_t xbwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
   const int KSL = KSW > KSR ? KSW - KSR : 0;
-  size_t red = (size_t)4 * NCT * 256 * sizeof(float);
-  const size_t dbr = (size_t)16 * 4 * 16 * NCT * sizeof(float);
+  const size_t HJ = 16 * NCT;
+  size_t red = (size_t)XNW * NCT * 256 * 4;
+  const size_t dbr = 16 * 4 * HJ * 4;
   if (red < dbr) red = dbr;
-  return (size_t)4 * KSL * NCT * 64 * 16 + red;
+  return (size_t)XNW * KSL * NCT * 64 * 16 + red + (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
+}
+
+__device__ __forceinline__ void load_window(const XLoopArgs& a, int* win, int lo) {
+  __syncthreads();
+  for (int i = threadIdx.x; i <= WIN; i += blockDim.x) {
+    const int t = lo + i;
+    win[i] = t <= a.T_max ? a.active[t] : 0;
+    win[WIN + 1 + i] = t <= a.T_max ? a.off[t] : 0;
+  }
+  __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
 // Forward loop, XCD-local.  Member `rank` of XCD x owns hidden units
 // j0 .. j0+HJ-1 (HJ = 4 NCT: all four gates of each unit, NCT column tiles of
 // 16 gate columns) of the rows in tiles x, x+8, ...  Step t for a row tile:
-//   poll h_{t-1} rows (K split across the 4 waves) while the next step's
-//   input projections are prefetched, z = Zx + h W_h (MFMA), add the other
-//   waves' partial products in LDS (one round), cell update in the waves that
-//   own complete units (all four gates of 16 units each, lane-local), push
-//   the stack, write h_t (history = exchange) and y_t.
+//   1. every wave polls its k-steps of h_{t-1} (K split over the 8 waves);
+//      the cell threads also fetch the next step's input projections;
+//   2. z = h W_h over the wave's k-steps (MFMA), partial products -> LDS;
+//   3. cell: thread (row, unit) of the first 16*HJ threads adds the 8
+//      partial products of its four gates and the input projection, runs the
+//      cell and stores h_t (the exchange, first), the stack row and y_t.
 // ---------------------------------------------------------------------------
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
-__global__ __launch_bounds__(256, 1) void xfwd_kernel(XLoopArgs a) {
+__global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 4 * NCT;
-  constexpr int NCW = NCT / 4;                 // waves that own complete units
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
+  constexpr int IS = xfwd_is(NCT);
+  static_assert(16 * HJ <= XNT, "one cell thread per (row, unit) of a tile");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
 
@@ -131,14 +156,15 @@ __global__ __launch_bounds__(256, 1) void xfwd_kernel(XLoopArgs a) {
   if (rank >= a.P) return;
   const int H = a.H, B = a.B;
   const long G4 = 4L * H;
+  const long H5 = 5L * H;
   const int j0 = rank * HJ;
   const int KS = H / (4 * KPC);
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
   const T* WT = reinterpret_cast<const T*>(a.W);
   T* HH = reinterpret_cast<T*>(a.X);
 
-  // Weight slice: column tile ct, lane column l16 <-> local gate column
-  // ct*16 + l16 = gate * HJ + u.
+  // weight slice: column tile ct, lane column l16 <-> local gate column
+  // ct*16 + l16 = gate * HJ + u
   uint4 wr[NCT][KSR];
 #pragma unroll
   for (int ct = 0; ct < NCT; ++ct) {
@@ -156,109 +182,91 @@ __global__ __launch_bounds__(256, 1) void xfwd_kernel(XLoopArgs a) {
       lds[((wave * KSL + i) * NCT + ct) * 64 + lane] = ks < ks1 ? ld16(wcol + (ks * 4 + q) * KPC) : zero4();
     }
   }
-  // partial products of the non-owning waves: slot (ct, s), s < 3
-  float* red = reinterpret_cast<float*>(lds + 4 * KSL * NCT * 64);
+  float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCT * 64);   // [XNW][4][IS]
+  int* win = reinterpret_cast<int*>(red + XNW * 4 * IS);               // [2][WIN+1]
+  int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
 
-  // Cell waves: lane (l16, q) owns unit ju and rows 4q + i of every tile.
-  const bool cellw = wave < NCW;
-  const int ju = j0 + 16 * wave + l16;
-  int pr[MRT_MAX][4];
-  float hs[MRT_MAX][4], cs[MRT_MAX][4];
-#pragma unroll
-  for (int mt = 0; mt < MRT_MAX; ++mt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = (grp + 8 * mt) * 16 + 4 * q + i;
-      pr[mt][i] = (mt < a.MRT && r < B) ? a.perm[r] : -1;
-      hs[mt][i] = 0.f;
-      cs[mt][i] = 0.f;
-      if (cellw && pr[mt][i] >= 0) {
-        if (a.h0) hs[mt][i] = a.h0[(long)pr[mt][i] * H + ju];
-        if (a.c0) cs[mt][i] = a.c0[(long)pr[mt][i] * H + ju];
-      }
-    }
+  // cell thread: 16 lanes take 16 consecutive units of one row, a wave four
+  // rows (the four MFMA result elements of one lane group)
+  const bool cellt = tid < 16 * HJ;
+  const int cu = (tid >> 8) * 16 + (tid & 15);    // local unit
+  const int crow = (tid >> 4) & 15;               // row within the tile
+  const int ju = j0 + cu;
+  // LDS slot of this thread's gate-0 partial product of wave 0
+  const float* rp = red + (crow & 3) * IS + (cu >> 4) * 64 + (crow >> 2) * 16 + (cu & 15);
+  float hs[MRT_MAX], cs[MRT_MAX];
+  if (tid < MRT_MAX * 16) {
+    const int r = (grp + 8 * (tid >> 4)) * 16 + (tid & 15);
+    sperm[tid] = ((tid >> 4) < a.MRT && r < B) ? a.perm[r] : -1;
+  }
   __syncthreads();
+#pragma unroll
+  for (int mt = 0; mt < MRT_MAX; ++mt) {
+    const int b = sperm[mt * 16 + crow];
+    hs[mt] = 0.f;
+    cs[mt] = 0.f;
+    if (cellt && b >= 0) {
+      if (a.h0) hs[mt] = a.h0[(long)b * H + ju];
+      if (a.c0) cs[mt] = a.c0[(long)b * H + ju];
+    }
+  }
 
   const int T_eff = a.meta[0];
-  int A_t = a.active[0], off_t = a.off[0], off_p = 0;
-  float zx[MRT_MAX][4][4];
+  int wlo = 0;
+  load_window(a, win, 0);
+  // input projections of the cell thread's (row, unit), one step ahead
+  float zf[MRT_MAX][4];
 #pragma unroll
-  for (int mt = 0; mt < MRT_MAX; ++mt)
+  for (int mt = 0; mt < MRT_MAX; ++mt) {
+    const int r = (grp + 8 * mt) * 16 + crow;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = (grp + 8 * mt) * 16 + 4 * q + i;
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-        zx[mt][i][g] = (cellw && mt < a.MRT && r < A_t && T_eff > 0)
-                           ? a.Zx[(off_t + r) * G4 + (long)g * H + ju] : 0.f;
-    }
+    for (int g = 0; g < 4; ++g)
+      zf[mt][g] = (cellt && T_eff > 0 && mt < a.MRT && r < win[0]) ? a.Zx[(long)r * G4 + (long)g * H + ju] : 0.f;
+  }
 
   for (int t = 0; t < T_eff; ++t) {
-    const int A_n = a.active[t + 1];
-    const int off_n = a.off[t + 1];
-    float zn[MRT_MAX][4][4];
-#pragma unroll
-    for (int mt = 0; mt < MRT_MAX; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) zn[mt][i][g] = 0.f;
-    bool fetched = false;
+    if (t + 1 > wlo + WIN) {
+      wlo = t;
+      load_window(a, win, wlo);
+    }
+    const int A_t = win[t - wlo], A_n = win[t + 1 - wlo];
+    const int off_t = win[WIN + 1 + t - wlo], off_n = win[WIN + 1 + t + 1 - wlo];
+    const int off_p = t > 0 ? (t - 1 >= wlo ? win[WIN + 1 + t - 1 - wlo] : a.off[t - 1]) : 0;
 #pragma unroll
     for (int mt = 0; mt < MRT_MAX; ++mt) {
       if (mt >= a.MRT) continue;
       const int r0 = (grp + 8 * mt) * 16;
       if (r0 >= A_t) {
-        if (cellw && a.y) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (pr[mt][i] >= 0) a.y[((long)t * B + pr[mt][i]) * H + ju] = 0.f;
+        if (a.y && cellt) {   // finished tile: y_t = 0 for its rows
+          const int b = sperm[mt * 16 + crow];
+          if (b >= 0) a.y[((long)t * B + b) * H + ju] = 0.f;
         }
         continue;
       }
-      // 1. issue the loads of h_{t-1} (this wave's k-steps)
+      // 1. h_{t-1} of this wave's k-steps: the history row of step t-1, or
+      //    for t = 0 the row of h0 in length order (written before the loop)
       const int ar = r0 + l16;
       const bool aok = ar < A_t;
-      const T* src[KSW];
-      unsigned long long lo[KSW], hi[KSW];
-#pragma unroll
-      for (int i = 0; i < KSW; ++i) {
-        const int ks = ks0 + i;
-        src[i] = (t > 0 && aok && ks < ks1) ? HH + (long)(off_p + ar) * H + (ks * 4 + q) * KPC : nullptr;
-        lo[i] = src[i] ? ld_u64_agent(src[i]) : 0ull;
-        hi[i] = src[i] ? ld_u64_agent(src[i] + 8 / sizeof(T)) : 0ull;
-      }
-      // 2. prefetch the next step's input projections (issued after step 1)
-      if (!fetched) {
-        fetched = true;
-#pragma unroll
-        for (int m2 = 0; m2 < MRT_MAX; ++m2)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = (grp + 8 * m2) * 16 + 4 * q + i;
-            if (cellw && m2 < a.MRT && r < A_n) {
-#pragma unroll
-              for (int g = 0; g < 4; ++g) zn[m2][i][g] = a.Zx[(off_n + r) * G4 + (long)g * H + ju];
-            }
-          }
-      }
-      // 3. complete h_{t-1}: re-read anything that still holds the fill pattern
+      const int nks = aok ? ks1 - ks0 : 0;                 // chunks this lane reads
+      const T* abase = (t > 0 ? HH + (long)(off_p + ar) * H : reinterpret_cast<const T*>(a.H0) + (long)ar * H) +
+                       (ks0 * 4 + q) * KPC;
       uint4 av[KSW];
+#pragma unroll
+      for (int i = 0; i < KSW; ++i) av[i] = i < nks ? ld_chunk_agent<T>(abase + i * 4 * KPC) : zero4();
+      float zc[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) zc[g] = zf[mt][g];
+      if (cellt) {
+        const int r = r0 + crow;
+        const bool nok = r < A_n;
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          zf[mt][g] = nok ? a.Zx[(long)(off_n + r) * G4 + (long)g * H + ju] : 0.f;
+      }
       unsigned todo = 0;
 #pragma unroll
-      for (int i = 0; i < KSW; ++i) {
-        av[i] = make_uint4((unsigned)lo[i], (unsigned)(lo[i] >> 32), (unsigned)hi[i], (unsigned)(hi[i] >> 32));
-        if (src[i] && (pending<T>(lo[i]) || pending<T>(hi[i]))) todo |= 1u << i;
-      }
-      if (t == 0) {
-#pragma unroll
-        for (int i = 0; i < KSW; ++i) {
-          const int ks = ks0 + i;
-          av[i] = (aok && ks < ks1 && a.h0)
-                      ? xchunk_from_f32<T>(a.h0 + (long)a.perm[ar] * H + (ks * 4 + q) * KPC)
-                      : zero4();
-        }
-      }
+      for (int i = 0; i < KSW; ++i)
+        if (i < nks && pending_chunk<T>(av[i])) todo |= 1u << i;
       if (todo) {
         const unsigned long long t0 = wall_clock64();
         unsigned polls = 0;
@@ -267,10 +275,8 @@ __global__ __launch_bounds__(256, 1) void xfwd_kernel(XLoopArgs a) {
 #pragma unroll
           for (int i = 0; i < KSW; ++i) {
             if (todo & (1u << i)) {
-              const unsigned long long l2 = ld_u64_agent(src[i]);
-              const unsigned long long h2 = ld_u64_agent(src[i] + 8 / sizeof(T));
-              av[i] = make_uint4((unsigned)l2, (unsigned)(l2 >> 32), (unsigned)h2, (unsigned)(h2 >> 32));
-              if (!pending<T>(l2) && !pending<T>(h2)) todo &= ~(1u << i);
+              av[i] = ld_chunk_agent<T>(abase + i * 4 * KPC);
+              if (!pending_chunk<T>(av[i])) todo &= ~(1u << i);
             }
           }
           if ((++polls & 255u) == 0) {
@@ -283,123 +289,109 @@ __global__ __launch_bounds__(256, 1) void xfwd_kernel(XLoopArgs a) {
           }
         }
       }
-      // 4. partial product over this wave's k-steps
-      f32x4 acc[NCT];
+      // 2. partial products over this wave's k-steps, column tiles in two
+      //    halves, into red[wave][i][ct][lane] once the previous tile's cell
+      //    has read them
+      __syncthreads();
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int hf = 0; hf < 2; ++hf) {
+        constexpr int NH = NCT / 2;
+        f32x4 acc[NH];
 #pragma unroll
-      for (int i = 0; i < KSW; ++i) {
-        if (ks0 + i < ks1) {
+        for (int c = 0; c < NH; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int ct = 0; ct < NCT; ++ct) {
-            const uint4 bv = i < KSR ? wr[ct][i < KSR ? i : 0]
-                                     : lds[((wave * KSL + (i - KSR)) * NCT + ct) * 64 + lane];
-            acc[ct] = Mfma<T>::step(av[i], bv, acc[ct]);
+        for (int i = 0; i < KSW; ++i) {
+          if (ks0 + i < ks1) {
+#pragma unroll
+            for (int c = 0; c < NH; ++c) {
+              const int ct = hf * NH + c;
+              const uint4 bv = i < KSR ? wr[ct][i < KSR ? i : 0]
+                                       : lds[((wave * KSL + (i - KSR)) * NCT + ct) * 64 + lane];
+              acc[c] = Mfma<T>::step(av[i], bv, acc[c]);
+            }
           }
         }
-      }
-      // 5. partial products of non-owners -> LDS; owners add them
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
-        const int owner = ct % NCW;
-        if (wave != owner) {
-          const int slot = ct * 3 + (wave - (wave > owner ? 1 : 0));
+        for (int c = 0; c < NH; ++c)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) red[(slot * 4 + e) * 64 + lane] = acc[ct][e];
-        }
+          for (int i = 0; i < 4; ++i) red[(wave * 4 + i) * IS + (hf * NH + c) * 64 + lane] = acc[c][i];
       }
       __syncthreads();
-      if (cellw) {
-        float z[4][4];    // [gate][row slot]
+      // 3. cell of (crow, cu): gate g is local column g*HJ + cu
+      if (cellt) {
+        float z[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int ct = g * NCW + (NCW == 2 ? (wave & 1) : 0);
+          const float* p = rp + g * (HJ / 16) * 64;
+          float v = p[0];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float v = acc[ct][e];
-            v += red[((ct * 3 + 0) * 4 + e) * 64 + lane];
-            v += red[((ct * 3 + 1) * 4 + e) * 64 + lane];
-            v += red[((ct * 3 + 2) * 4 + e) * 64 + lane];
-            z[g][e] = v;
+          for (int w2 = 1; w2 < XNW; ++w2) v += p[w2 * 4 * IS];
+          z[g] = v + zc[g];
+        }
+        const float ig = sigmoidf_(z[0]);
+        const float fg = sigmoidf_(z[1]);
+        const float gg = tanhf_(z[2]);
+        const float og = sigmoidf_(z[3]);
+        const float cn = fg * cs[mt] + ig * gg;
+        const float hn = og * tanhf_(cn);
+        const int r = r0 + crow;
+        const bool act = r < A_t;
+        if (act) {
+          const long cr = off_t + r;
+          HH[cr * H + ju] = to_exchange<T>(hn);
+          cs[mt] = cn;
+          hs[mt] = hn;
+          if (a.stack) {
+            float* st = a.stack + cr * H5 + ju;
+            st[0] = ig;
+            st[H] = fg;
+            st[2 * H] = gg;
+            st[3 * H] = og;
+            st[4 * H] = cn;
           }
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = r0 + 4 * q + i;
-          if (pr[mt][i] < 0) continue;
-          float* yrow = a.y ? a.y + ((long)t * B + pr[mt][i]) * H : nullptr;
-          if (r < A_t) {
-            const long krow = off_t + r;
-            const float ig = sigmoidf_(z[0][i] + zx[mt][i][0]);
-            const float fg = sigmoidf_(z[1][i] + zx[mt][i][1]);
-            const float gg = tanhf_(z[2][i] + zx[mt][i][2]);
-            const float og = sigmoidf_(z[3][i] + zx[mt][i][3]);
-            const float cn = fg * cs[mt][i] + ig * gg;
-            const float hn = og * tanhf_(cn);
-            HH[krow * H + ju] = to_exchange<T>(hn);
-            if (a.stack) {
-              float* st = a.stack + krow * 5 * H;
-              st[ju] = ig;
-              st[H + ju] = fg;
-              st[2 * H + ju] = gg;
-              st[3 * H + ju] = og;
-              st[4 * H + ju] = cn;
-            }
-            cs[mt][i] = cn;
-            hs[mt][i] = hn;
-            if (yrow) yrow[ju] = hn;
-          } else if (yrow) {
-            yrow[ju] = 0.f;
-          }
+        if (a.y) {
+          const int b = sperm[mt * 16 + crow];
+          if (b >= 0) a.y[((long)t * B + b) * H + ju] = act ? hn : 0.f;
         }
       }
-      __syncthreads();
     }
-    off_p = off_t;
-    off_t = off_n;
-    A_t = A_n;
-#pragma unroll
-    for (int mt = 0; mt < MRT_MAX; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) zx[mt][i][g] = zn[mt][i][g];
   }
 
-  if (cellw) {
+  if (cellt) {
 #pragma unroll
-    for (int mt = 0; mt < MRT_MAX; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (pr[mt][i] < 0) continue;
-        const long b = pr[mt][i];
-        a.hT[b * H + ju] = hs[mt][i];
-        a.cT[b * H + ju] = cs[mt][i];
-        if (a.y)
-          for (int t = T_eff; t < a.T_max; ++t) a.y[((long)t * B + b) * H + ju] = 0.f;
-      }
+    for (int mt = 0; mt < MRT_MAX; ++mt) {
+      const int b = sperm[mt * 16 + crow];
+      if (b < 0) continue;
+      a.hT[(long)b * H + ju] = hs[mt];
+      a.cT[(long)b * H + ju] = cs[mt];
+      if (a.y)
+        for (int t = T_eff; t < a.T_max; ++t) a.y[((long)t * B + b) * H + ju] = 0.f;
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
 // Gradient loop, XCD-local.  Member `rank` owns hidden units j0 .. j0+HJ-1
-// (HJ = 16 NCT).  Step t (descending) for a row tile:
-//   phase 1 (own units, from values prefetched during step t+1): dz and dc,
-//     write dz (the exchange array), accumulate db;
+// (HJ = 16 NCT).  In phase 1 each of the first HJ*4 threads handles four
+// consecutive units of one row of the tile.  Step t (descending):
+//   phase 1: from the values popped during step t+1: dh_tot, dz, dc; write
+//     dz (the exchange array); accumulate db;
 //   phase 2: poll the dz rows of the tile (all 4H gate columns, K split
-//     across the 4 waves, two batches) while the stack rows of step t-1 are
-//     prefetched; dh <- dz W_h^T for the own units (MFMA); one LDS round adds
-//     the 4 partial products.
+//     over the 8 waves, in batches; the pops of step t-1 are issued after the
+//     last batch), dh <- dz W_h^T for the own units (MFMA), one LDS round
+//     adds the 8 partial products.
 // ---------------------------------------------------------------------------
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
-__global__ __launch_bounds__(256, 1) void xbwd_kernel(XLoopArgs a) {
+__global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT;                 // units per work-group
-  constexpr int EPT = HJ / 16;                 // elements per thread per tile
+  constexpr int Q4 = HJ / 4;                   // unit quads per row
+  constexpr int NPT = 16 * Q4;                 // phase-1 threads (one quad each)
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
-  constexpr int KB = KSW < 16 ? KSW : 16;      // k-steps per load batch
+  constexpr int KB = KSW < 8 ? KSW : 8;        // k-steps per load batch
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
 
@@ -422,7 +414,6 @@ __global__ __launch_bounds__(256, 1) void xbwd_kernel(XLoopArgs a) {
   const T* W = reinterpret_cast<const T*>(a.W);
   T* DZ = reinterpret_cast<T*>(a.X);
 
-  // W_h row of output column ct*16 + l16 (a hidden unit of this member)
   uint4 wr[NCT][KSR];
 #pragma unroll
   for (int ct = 0; ct < NCT; ++ct) {
@@ -438,72 +429,76 @@ __global__ __launch_bounds__(256, 1) void xbwd_kernel(XLoopArgs a) {
       lds[((wave * KSL + i) * NCT + ct) * 64 + lane] = ks < ks1 ? ld16(wrow + (ks * 4 + q) * KPC) : zero4();
     }
   }
-  float* red = reinterpret_cast<float*>(lds + 4 * KSL * NCT * 64);   // [4 waves][NCT][4][64]
+  float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCT * 64);   // [XNW waves][NCT][4][64]
+  int* win = reinterpret_cast<int*>(red + (XNW * NCT * 256 > 64 * HJ ? XNW * NCT * 256 : 64 * HJ));  // [2][WIN+1]
+  int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
 
-  // element k of a tile for this thread: e = tid + 256 k -> (row e / HJ, unit e % HJ)
-  int pr[MRT_MAX][EPT];
-  float dh[MRT_MAX][EPT], dc[MRT_MAX][EPT];
+  // phase-1 element of this thread: row pr_row, units j0 + pu .. +3
+  const bool p1 = tid < NPT;
+  const int prow = tid / Q4, pu = (tid - (tid / Q4) * Q4) * 4;
+  if (tid < MRT_MAX * 16) {
+    const int r = (grp + 8 * (tid >> 4)) * 16 + (tid & 15);
+    sperm[tid] = ((tid >> 4) < a.MRT && r < B) ? a.perm[r] : -1;
+  }
+  __syncthreads();
+  float4 dh[MRT_MAX], dc[MRT_MAX];
 #pragma unroll
-  for (int mt = 0; mt < MRT_MAX; ++mt)
-#pragma unroll
-    for (int k = 0; k < EPT; ++k) {
-      const int e = tid + 256 * k;
-      const int r = (grp + 8 * mt) * 16 + e / HJ;
-      const int j = j0 + e % HJ;
-      pr[mt][k] = (mt < a.MRT && r < B) ? a.perm[r] : -1;
-      dh[mt][k] = 0.f;
-      dc[mt][k] = 0.f;
-      if (pr[mt][k] >= 0) {
-        if (a.dhT) dh[mt][k] = a.dhT[(long)pr[mt][k] * H + j];
-        if (a.dcT) dc[mt][k] = a.dcT[(long)pr[mt][k] * H + j];
-      }
+  for (int mt = 0; mt < MRT_MAX; ++mt) {
+    dh[mt] = make_float4(0.f, 0.f, 0.f, 0.f);
+    dc[mt] = make_float4(0.f, 0.f, 0.f, 0.f);
+    const int b = p1 ? sperm[mt * 16 + prow] : -1;
+    if (b >= 0) {
+      if (a.dhT) dh[mt] = *reinterpret_cast<const float4*>(a.dhT + (long)b * H + j0 + pu);
+      if (a.dcT) dc[mt] = *reinterpret_cast<const float4*>(a.dcT + (long)b * H + j0 + pu);
     }
-  float dbacc[EPT][4];
+  }
+  float4 dbacc[4];
 #pragma unroll
-  for (int k = 0; k < EPT; ++k)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) dbacc[k][g] = 0.f;
+  for (int g = 0; g < 4; ++g) dbacc[g] = make_float4(0.f, 0.f, 0.f, 0.f);
 
-  // popped values of a (step, tile): i, f, g, o, c_t, c_{t-1}, dy
-  auto fetch = [&](float (&v)[EPT][7], int tt, int mt, int A, int off, int offp) {
+  // pops of (step tt, tile mt) for this thread: i, f, g, o, c_t, c_{t-1}, dy
+  auto fetch = [&](float4 (&v)[7], int tt, int mt, int A, int off, int offp) {
 #pragma unroll
-    for (int k = 0; k < EPT; ++k) {
-      const int e = tid + 256 * k;
-      const int r = (grp + 8 * mt) * 16 + e / HJ;
-      const int j = j0 + e % HJ;
+    for (int c = 0; c < 7; ++c) v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+    const int r = (grp + 8 * mt) * 16 + prow;
+    if (!p1 || tt < 0 || r >= A) return;
+    const int b = sperm[mt * 16 + prow];
+    const float* st = a.stack + (long)(off + r) * H5 + j0 + pu;
 #pragma unroll
-      for (int c = 0; c < 7; ++c) v[k][c] = 0.f;
-      if (tt >= 0 && r < A) {
-        const float* st = a.stack + (off + r) * H5;
-        v[k][0] = st[j];
-        v[k][1] = st[H + j];
-        v[k][2] = st[2 * H + j];
-        v[k][3] = st[3 * H + j];
-        v[k][4] = st[4 * H + j];
-        if (tt > 0) v[k][5] = a.stack[(long)(offp + r) * H5 + 4 * H + j];
-        else if (a.c0) v[k][5] = a.c0[(long)pr[mt][k] * H + j];
-        if (a.dy)
-          v[k][6] = a.dy_compact ? a.dy[(long)(off + r) * H + j]
-                                 : a.dy[((long)tt * B + pr[mt][k]) * H + j];
-      }
-    }
+    for (int c = 0; c < 5; ++c) v[c] = *reinterpret_cast<const float4*>(st + (long)c * H);
+    if (tt > 0)
+      v[5] = *reinterpret_cast<const float4*>(a.stack + (long)(offp + r) * H5 + 4L * H + j0 + pu);
+    else if (a.c0)
+      v[5] = *reinterpret_cast<const float4*>(a.c0 + (long)b * H + j0 + pu);
+    if (a.dy)
+      v[6] = *reinterpret_cast<const float4*>(
+          a.dy_compact ? a.dy + (long)(off + r) * H + j0 + pu : a.dy + ((long)tt * B + b) * H + j0 + pu);
   };
 
   const int T_eff = a.meta[0];
-  int t = T_eff - 1;
-  int A_t = t >= 0 ? a.active[t] : 0;
-  int off_t = t >= 0 ? a.off[t] : 0;
-  int off_p = t >= 1 ? a.off[t - 1] : 0;
-  float pv[MRT_MAX][EPT][7];
+  int wlo = T_eff - 1 - WIN > 0 ? T_eff - 1 - WIN : 0;
+  load_window(a, win, wlo);
+  float4 pv[MRT_MAX][7];
+  {
+    const int t = T_eff - 1;
+    const int A_t = t >= 0 ? win[t - wlo] : 0;
+    const int off_t = t >= 0 ? win[WIN + 1 + t - wlo] : 0;
+    const int off_p = t >= 1 ? win[WIN + 1 + t - 1 - wlo] : 0;
 #pragma unroll
-  for (int mt = 0; mt < MRT_MAX; ++mt)
-    if (mt < a.MRT) fetch(pv[mt], t, mt, A_t, off_t, off_p);
-  __syncthreads();
+    for (int mt = 0; mt < MRT_MAX; ++mt)
+      if (mt < a.MRT) fetch(pv[mt], t, mt, A_t, off_t, off_p);
+  }
 
-  for (; t >= 0; --t) {
-    const int A_n = t >= 1 ? a.active[t - 1] : 0;
-    const int off_n = off_p;
-    const int off_pn = t >= 2 ? a.off[t - 2] : 0;
+  for (int t = T_eff - 1; t >= 0; --t) {
+    if (t - 2 < wlo && wlo > 0) {
+      wlo = t - WIN > 0 ? t - WIN : 0;
+      load_window(a, win, wlo);
+    }
+    const int A_t = win[t - wlo];
+    const int off_t = win[WIN + 1 + t - wlo];
+    const int A_n = t >= 1 ? win[t - 1 - wlo] : 0;
+    const int off_n = t >= 1 ? win[WIN + 1 + t - 1 - wlo] : 0;
+    const int off_pn = t >= 2 ? win[WIN + 1 + t - 2 - wlo] : 0;
 #pragma unroll
     for (int mt = 0; mt < MRT_MAX; ++mt) {
       if (mt >= a.MRT) continue;
@@ -514,59 +509,68 @@ __global__ __launch_bounds__(256, 1) void xbwd_kernel(XLoopArgs a) {
         continue;
       }
       // phase 1
+      if (p1 && r0 + prow < A_t) {
+        const long krow = off_t + r0 + prow;
+        float dzv[4][4];   // [gate][unit]
+        float* dhp = reinterpret_cast<float*>(&dh[mt]);
+        float* dcp = reinterpret_cast<float*>(&dc[mt]);
 #pragma unroll
-      for (int k = 0; k < EPT; ++k) {
-        const int e = tid + 256 * k;
-        const int r = r0 + e / HJ;
-        if (r >= A_t) continue;
-        const int j = j0 + e % HJ;
-        const long krow = off_t + r;
-        const float dht = dh[mt][k] + pv[mt][k][6];
-        const float ig = pv[mt][k][0], fg = pv[mt][k][1], gg = pv[mt][k][2], og = pv[mt][k][3];
-        const float c = pv[mt][k][4], cp = pv[mt][k][5];
-        const float tc = tanhf_(c);
-        const float d_o = dht * tc;
-        const float dct = dc[mt][k] + dht * og * (1.f - tc * tc);
-        const float dz0 = dct * gg * (ig * (1.f - ig));
-        const float dz1 = dct * cp * (fg * (1.f - fg));
-        const float dz2 = dct * ig * (1.f - gg * gg);
-        const float dz3 = d_o * (og * (1.f - og));
-        T* dzr = DZ + krow * G4;
-        dzr[j] = to_exchange<T>(dz0);
-        dzr[H + j] = to_exchange<T>(dz1);
-        dzr[2 * H + j] = to_exchange<T>(dz2);
-        dzr[3 * H + j] = to_exchange<T>(dz3);
-        dbacc[k][0] += dz0;
-        dbacc[k][1] += dz1;
-        dbacc[k][2] += dz2;
-        dbacc[k][3] += dz3;
-        dc[mt][k] = dct * fg;
+        for (int k = 0; k < 4; ++k) {
+          const float dht = dhp[k] + reinterpret_cast<const float*>(&pv[mt][6])[k];
+          const float ig = reinterpret_cast<const float*>(&pv[mt][0])[k];
+          const float fg = reinterpret_cast<const float*>(&pv[mt][1])[k];
+          const float gg = reinterpret_cast<const float*>(&pv[mt][2])[k];
+          const float og = reinterpret_cast<const float*>(&pv[mt][3])[k];
+          const float c = reinterpret_cast<const float*>(&pv[mt][4])[k];
+          const float cp = reinterpret_cast<const float*>(&pv[mt][5])[k];
+          const float tc = tanhf_(c);
+          const float d_o = dht * tc;
+          const float dct = dcp[k] + dht * og * (1.f - tc * tc);
+          dzv[0][k] = dct * gg * (ig * (1.f - ig));
+          dzv[1][k] = dct * cp * (fg * (1.f - fg));
+          dzv[2][k] = dct * ig * (1.f - gg * gg);
+          dzv[3][k] = d_o * (og * (1.f - og));
+          dcp[k] = dct * fg;
+        }
+        T* dzr = DZ + krow * G4 + j0 + pu;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          T tmp[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) tmp[k] = to_exchange<T>(dzv[g][k]);
+          if constexpr (sizeof(T) == 2) {
+            uint2 pk;
+            __builtin_memcpy(&pk, tmp, 8);
+            *reinterpret_cast<uint2*>(dzr + (long)g * H) = pk;
+          } else {
+            uint4 pk;
+            __builtin_memcpy(&pk, tmp, 16);
+            *reinterpret_cast<uint4*>(dzr + (long)g * H) = pk;
+          }
+          dbacc[g].x += dzv[g][0];
+          dbacc[g].y += dzv[g][1];
+          dbacc[g].z += dzv[g][2];
+          dbacc[g].w += dzv[g][3];
+        }
       }
       // phase 2
       const int ar = r0 + l16;
-      const T* arow = ar < A_t ? DZ + (long)(off_t + ar) * G4 : nullptr;
+      const int nks = ar < A_t ? ks1 - ks0 : 0;             // chunks this lane reads
+      const T* abase = DZ + (long)(off_t + ar) * G4 + (ks0 * 4 + q) * KPC;
       f32x4 acc[NCT];
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int b0 = 0; b0 < KSW; b0 += KB) {
-        const T* src[KB];
-        unsigned long long lo[KB], hi[KB];
-#pragma unroll
-        for (int i = 0; i < KB; ++i) {
-          const int ks = ks0 + b0 + i;
-          src[i] = (arow && b0 + i < KSW && ks < ks1) ? arow + (ks * 4 + q) * KPC : nullptr;
-          lo[i] = src[i] ? ld_u64_agent(src[i]) : 0ull;
-          hi[i] = src[i] ? ld_u64_agent(src[i] + 8 / sizeof(T)) : 0ull;
-        }
-        if (b0 == 0) fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);   // next step's pops
         uint4 av[KB];
+#pragma unroll
+        for (int i = 0; i < KB; ++i)
+          av[i] = b0 + i < nks ? ld_chunk_agent<T>(abase + (b0 + i) * 4 * KPC) : zero4();
+        if (b0 + KB >= KSW) fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);   // next step's pops
         unsigned todo = 0;
 #pragma unroll
-        for (int i = 0; i < KB; ++i) {
-          av[i] = make_uint4((unsigned)lo[i], (unsigned)(lo[i] >> 32), (unsigned)hi[i], (unsigned)(hi[i] >> 32));
-          if (src[i] && (pending<T>(lo[i]) || pending<T>(hi[i]))) todo |= 1u << i;
-        }
+        for (int i = 0; i < KB; ++i)
+          if (b0 + i < nks && pending_chunk<T>(av[i])) todo |= 1u << i;
         if (todo) {
           const unsigned long long t0 = wall_clock64();
           unsigned polls = 0;
@@ -575,10 +579,8 @@ __global__ __launch_bounds__(256, 1) void xbwd_kernel(XLoopArgs a) {
 #pragma unroll
             for (int i = 0; i < KB; ++i) {
               if (todo & (1u << i)) {
-                const unsigned long long l2 = ld_u64_agent(src[i]);
-                const unsigned long long h2 = ld_u64_agent(src[i] + 8 / sizeof(T));
-                av[i] = make_uint4((unsigned)l2, (unsigned)(l2 >> 32), (unsigned)h2, (unsigned)(h2 >> 32));
-                if (!pending<T>(l2) && !pending<T>(h2)) todo &= ~(1u << i);
+                av[i] = ld_chunk_agent<T>(abase + (b0 + i) * 4 * KPC);
+                if (!pending_chunk<T>(av[i])) todo &= ~(1u << i);
               }
             }
             if ((++polls & 255u) == 0) {
@@ -609,52 +611,70 @@ __global__ __launch_bounds__(256, 1) void xbwd_kernel(XLoopArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) red[((wave * NCT + ct) * 4 + e) * 64 + lane] = acc[ct][e];
       __syncthreads();
+      if (p1 && r0 + prow < A_t) {
+        float* dhp = reinterpret_cast<float*>(&dh[mt]);
 #pragma unroll
-      for (int k = 0; k < EPT; ++k) {
-        const int e = tid + 256 * k;
-        const int row = e / HJ, u = e - (e / HJ) * HJ;
-        if (r0 + row >= A_t) continue;
-        // element (row, u): column tile u/16, lane (row/4)*16 + u%16, slot row%4
-        const int ct = u >> 4, ln = (row >> 2) * 16 + (u & 15), ee = row & 3;
-        float s = red[((0 * NCT + ct) * 4 + ee) * 64 + ln];
-        s += red[((1 * NCT + ct) * 4 + ee) * 64 + ln];
-        s += red[((2 * NCT + ct) * 4 + ee) * 64 + ln];
-        s += red[((3 * NCT + ct) * 4 + ee) * 64 + ln];
-        dh[mt][k] = s;
+        for (int k = 0; k < 4; ++k) {
+          const int u = pu + k;
+          // element (prow, u): column tile u/16, lane (prow/4)*16 + u%16, slot prow%4
+          const int ct = u >> 4, ln = (prow >> 2) * 16 + (u & 15), ee = prow & 3;
+          float s = red[((0 * NCT + ct) * 4 + ee) * 64 + ln];
+#pragma unroll
+          for (int w2 = 1; w2 < XNW; ++w2) s += red[((w2 * NCT + ct) * 4 + ee) * 64 + ln];
+          dhp[k] = s;
+        }
       }
       __syncthreads();
     }
-    A_t = A_n;
-    off_t = off_n;
-    off_p = off_pn;
   }
 
 #pragma unroll
-  for (int mt = 0; mt < MRT_MAX; ++mt)
-#pragma unroll
-    for (int k = 0; k < EPT; ++k) {
-      if (pr[mt][k] < 0) continue;
-      const long b = pr[mt][k];
-      const int j = j0 + (tid + 256 * k) % HJ;
-      if (a.dh0) a.dh0[b * H + j] = dh[mt][k];
-      if (a.dc0) a.dc0[b * H + j] = dc[mt][k];
-    }
+  for (int mt = 0; mt < MRT_MAX; ++mt) {
+    const int b = p1 ? sperm[mt * 16 + prow] : -1;
+    if (b < 0) continue;
+    if (a.dh0) *reinterpret_cast<float4*>(a.dh0 + (long)b * H + j0 + pu) = dh[mt];
+    if (a.dc0) *reinterpret_cast<float4*>(a.dc0 + (long)b * H + j0 + pu) = dc[mt];
+  }
   // db partial of this work-group (its rows of this XCD), fixed order
   __syncthreads();
+  if (p1) {
 #pragma unroll
-  for (int k = 0; k < EPT; ++k) {
-    const int e = tid + 256 * k;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) red[(e / HJ) * 4 * HJ + g * HJ + e % HJ] = dbacc[k][g];
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<float4*>(red + prow * 4 * HJ + g * HJ + pu) = dbacc[g];
   }
   __syncthreads();
-  for (int c = tid; c < 4 * HJ; c += 256) {
+  for (int c = tid; c < 4 * HJ; c += XNT) {
     float s = 0.f;
     for (int m = 0; m < 16; ++m) s += red[m * 4 * HJ + c];
     const int g = c / HJ, u = c - (c / HJ) * HJ;
     a.db_part[(long)grp * G4 + (long)g * H + j0 + u] = s;
   }
 }
+
+// h0 rows in length order, in operand type: out[r, :] = op(h0[perm[r], :])
+// (zeros when h0 is NULL).  The forward loop reads it as h_{-1}.
+template <typename T>
+__global__ __launch_bounds__(256) void h0_sorted_kernel(const float* __restrict__ h0,
+                                                        const int* __restrict__ perm, int B, int H,
+                                                        T* __restrict__ out) {
+  const long n = (long)B * H;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+    const int r = (int)(i / H), j = (int)(i - (long)r * H);
+    out[i] = Op<T>::from_f32(h0 ? h0[(long)perm[r] * H + j] : 0.f);
+  }
+}
+
+template <typename T>
+hipError_t launch_h0_sorted(const float* h0, const int* perm, int B, int H, void* out,
+                            hipStream_t s) {
+  long blocks = ((long)B * H + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(h0_sorted_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, h0, perm, B, H,
+                     reinterpret_cast<T*>(out));
+  return hipGetLastError();
+}
+template hipError_t launch_h0_sorted<float>(const float*, const int*, int, int, void*, hipStream_t);
+template hipError_t launch_h0_sorted<bf16_t>(const float*, const int*, int, int, void*, hipStream_t);
 
 // Fill rows [0, total) of a compact array of `row_bytes`-byte rows with the
 // all-ones pattern.  row_bytes % 16 == 0.
@@ -671,23 +691,24 @@ namespace {
 }  // namespace
 
 // Kernel for a (dtype, H class, row tiles per XCD) combination.
-//   bf16: HJ = 32 units, forward NCT 8, KSW = H/128; backward NCT 2, KSW = H/32.
-//   f32:  HJ = 16 units, forward NCT 4, KSW = H/64;  backward NCT 1, KSW = H/16.
-// hc in {1, 2, 4, 8} is the forward KSW; mrt <= 4 row tiles per XCD.  The
-// register-resident share of the weight slice (KSR of KSW k-steps per wave)
-// is chosen per instantiation so that nothing spills to scratch.
+//   bf16: HJ = 32 units, forward NCT 8, KSW = H/256; backward NCT 2, KSW = H/64.
+//   f32:  HJ = 16 units, forward NCT 4, KSW = H/128; backward NCT 1, KSW = H/32.
+// hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
+// row tiles per XCD.  The weight slice is held entirely in registers.
 namespace {
 template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT>
 XKernels x_make() {
   XKernels k{};
   k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT>);
   k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, 4 * HC, RB, MRT>);
-  k.lds_fwd = xfwd_lds(HC, RF, NF);
-  k.lds_bwd = xbwd_lds(4 * HC, RB, NB);
+  k.lds_fwd = xfwd_lds(HC, RF, NF, MRT);
+  k.lds_bwd = xbwd_lds(4 * HC, RB, NB, MRT);
   return k;
 }
 }  // namespace
 
+// RF / RB: k-steps per wave whose weights stay in registers (the rest in LDS),
+// chosen so that no instantiation spills.
 template <typename T>
 XKernels x_kernels(int hc, int mrt) {
   constexpr bool bf = sizeof(T) == 2;
@@ -695,22 +716,11 @@ XKernels x_kernels(int hc, int mrt) {
   constexpr int NB = bf ? 2 : 1;
   const bool one = mrt <= 1;
   if (mrt > 4) return XKernels{};
-  if constexpr (bf) {
-    switch (hc) {
-      case 1: return one ? x_make<T, NF, NB, 1, 1, 4, 1>() : x_make<T, NF, NB, 1, 1, 4, 4>();
-      case 2: return one ? x_make<T, NF, NB, 2, 2, 8, 1>() : x_make<T, NF, NB, 2, 2, 8, 4>();
-      case 4: return one ? x_make<T, NF, NB, 4, 4, 16, 1>() : x_make<T, NF, NB, 4, 2, 16, 4>();
-      case 8: return one ? x_make<T, NF, NB, 8, 8, 24, 1>() : x_make<T, NF, NB, 8, 4, 16, 4>();
-      default: return XKernels{};
-    }
-  } else {
   switch (hc) {
-    case 1: return one ? x_make<T, NF, NB, 1, 1, 4, 1>() : x_make<T, NF, NB, 1, 1, 4, 4>();
-    case 2: return one ? x_make<T, NF, NB, 2, 2, 8, 1>() : x_make<T, NF, NB, 2, 2, 8, 4>();
-    case 4: return one ? x_make<T, NF, NB, 4, 4, 16, 1>() : x_make<T, NF, NB, 4, 4, 16, 4>();
-    case 8: return one ? x_make<T, NF, NB, 8, 8, 32, 1>() : x_make<T, NF, NB, 8, 8, 24, 4>();
+    case 1: return one ? x_make<T, NF, NB, 1, 1, 4, 1>() : x_make<T, NF, NB, 1, 1, 2, 4>();
+    case 2: return one ? x_make<T, NF, NB, 2, 2, 8, 1>() : x_make<T, NF, NB, 2, 2, 4, 4>();
+    case 4: return one ? x_make<T, NF, NB, 4, 4, 12, 1>() : x_make<T, NF, NB, 4, 3, 8, 4>();
     default: return XKernels{};
-  }
   }
 }
 
@@ -718,13 +728,13 @@ template XKernels x_kernels<float>(int, int);
 template XKernels x_kernels<bf16_t>(int, int);
 
 hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd) {
-  // a variant that spills registers to scratch memory is not used
+  // a variant that spills more than a few registers to scratch is not used
   hipFuncAttributes fa{}, fb{};
   hipError_t e = hipFuncGetAttributes(&fa, k.fwd);
   if (e != hipSuccess) return e;
   e = hipFuncGetAttributes(&fb, k.bwd);
   if (e != hipSuccess) return e;
-  if (fa.localSizeBytes > 0 || fb.localSizeBytes > 0) {
+  if (fa.localSizeBytes > 32 || fb.localSizeBytes > 32) {
     *occ_fwd = 0;
     *occ_bwd = 0;
     return hipSuccess;
@@ -733,15 +743,15 @@ hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd) {
   if (e != hipSuccess) return e;
   e = hipFuncSetAttribute(k.bwd, hipFuncAttributeMaxDynamicSharedMemorySize, (int)k.lds_bwd);
   if (e != hipSuccess) return e;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(occ_fwd, k.fwd, 256, k.lds_fwd);
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(occ_fwd, k.fwd, XNT, k.lds_fwd);
   if (e != hipSuccess) return e;
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(occ_bwd, k.bwd, 256, k.lds_bwd);
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(occ_bwd, k.bwd, XNT, k.lds_bwd);
 }
 
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s) {
   XLoopArgs copy = a;
   void* kargs[] = {&copy};
-  return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(256), kargs, (unsigned)lds, s);
+  return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(XNT), kargs, (unsigned)lds, s);
 }
 
 hipError_t launch_fill_pending(void* base, long row_bytes, const int* meta, long cap_rows,
