@@ -31,11 +31,6 @@ namespace {
 
 constexpr int kXccIdReg = (3 << 11) | 20;    // s_getreg: HW_REG_XCC_ID, bits [3:0]
 
-__device__ __forceinline__ unsigned long long ld_u64_agent(const void* p) {
-  return __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // True if any element of the 8-byte word still holds the fill pattern.
 template <typename T> __device__ __forceinline__ bool pending(unsigned long long v);
 template <> __device__ __forceinline__ bool pending<bf16_t>(unsigned long long v) {
@@ -47,12 +42,19 @@ template <> __device__ __forceinline__ bool pending<float>(unsigned long long v)
   return ((unsigned)v == 0xffffffffu) || ((unsigned)(v >> 32) == 0xffffffffu);
 }
 
-// 16-byte chunk read with two agent-scope (L1-bypassing) 64-bit loads.
-template <typename T>
-__device__ __forceinline__ uint4 ld_chunk_agent(const T* p) {
-  const unsigned long long lo = ld_u64_agent(p);
-  const unsigned long long hi = ld_u64_agent(p + 8 / sizeof(T));
-  return make_uint4((unsigned)lo, (unsigned)(lo >> 32), (unsigned)hi, (unsigned)(hi >> 32));
+// Raw buffer resource over `bytes` bytes from `base` (stride 0; reads past
+// the end return zeros).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte chunk read with cache policy sc1: it bypasses the CU's L1 and is
+// served by the L2, so it sees the plain stores other CUs of the same XCD
+// made there.  An element is never torn (2- and 4-byte elements are
+// naturally aligned); a chunk may mix old and new elements, which the
+// per-element fill-pattern test catches.
+constexpr int kCpolSc1 = 16;
+__device__ __forceinline__ uint4 ld_chunk_l2(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolSc1));
 }
 template <typename T>
 __device__ __forceinline__ bool pending_chunk(uint4 v) {
@@ -102,13 +104,17 @@ size_t xfwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
   return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)XNW * 4 * xfwd_is(NCT) * 4 +
          (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
 }
+// LDS of the gradient kernel: weight k-steps not in registers, partial
+// products [wave][i][column tile][lane] (reused for the db rows at the end),
+// metadata window, perm rows.
+constexpr int xbwd_is(int NCT) { return NCT * 64 + 16; }
+constexpr int xbwd_red_floats(int NCT) {
+  return XNW * 4 * xbwd_is(NCT) > 16 * 4 * 16 * NCT ? XNW * 4 * xbwd_is(NCT) : 16 * 4 * 16 * NCT;
+}
 size_t xbwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
   const int KSL = KSW > KSR ? KSW - KSR : 0;
-  const size_t HJ = 16 * NCT;
-  size_t red = (size_t)XNW * NCT * 256 * 4;
-  const size_t dbr = 16 * 4 * HJ * 4;
-  if (red < dbr) red = dbr;
-  return (size_t)XNW * KSL * NCT * 64 * 16 + red + (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
+  return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)xbwd_red_floats(NCT) * 4 +
+         (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
 }
 
 __device__ __forceinline__ void load_window(const XLoopArgs& a, int* win, int lo) {
@@ -140,6 +146,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   constexpr int HJ = 4 * NCT;
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
   constexpr int IS = xfwd_is(NCT);
+  constexpr int CB = 4 * KPC * (int)sizeof(T);    // bytes of one k-step of a row
   static_assert(16 * HJ <= XNT, "one cell thread per (row, unit) of a tile");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
@@ -245,14 +252,16 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
       }
       // 1. h_{t-1} of this wave's k-steps: the history row of step t-1, or
       //    for t = 0 the row of h0 in length order (written before the loop)
-      const int ar = r0 + l16;
-      const bool aok = ar < A_t;
-      const int nks = aok ? ks1 - ks0 : 0;                 // chunks this lane reads
-      const T* abase = (t > 0 ? HH + (long)(off_p + ar) * H : reinterpret_cast<const T*>(a.H0) + (long)ar * H) +
-                       (ks0 * 4 + q) * KPC;
+      //    Rows r0 .. r0+nrow-1 of the tile are running; the buffer range
+      //    ends there, so the other lanes read zeros.
+      const int nrow = min(16, A_t - r0);
+      const T* tb = t > 0 ? HH + (long)(off_p + r0) * H : reinterpret_cast<const T*>(a.H0) + (long)r0 * H;
+      const __amdgpu_buffer_rsrc_t rs = make_rsrc(tb, (unsigned)(nrow * H * (int)sizeof(T)));
+      const unsigned aoff = (unsigned)((l16 * H + (ks0 * 4 + q) * KPC) * (int)sizeof(T));
+      const int nks = ks1 - ks0;                             // k-steps of this wave
       uint4 av[KSW];
 #pragma unroll
-      for (int i = 0; i < KSW; ++i) av[i] = i < nks ? ld_chunk_agent<T>(abase + i * 4 * KPC) : zero4();
+      for (int i = 0; i < KSW; ++i) av[i] = i < nks ? ld_chunk_l2(rs, aoff + i * CB) : zero4();
       float zc[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) zc[g] = zf[mt][g];
@@ -275,7 +284,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
 #pragma unroll
           for (int i = 0; i < KSW; ++i) {
             if (todo & (1u << i)) {
-              av[i] = ld_chunk_agent<T>(abase + i * 4 * KPC);
+              av[i] = ld_chunk_l2(rs, aoff + i * CB);
               if (!pending_chunk<T>(av[i])) todo &= ~(1u << i);
             }
           }
@@ -373,14 +382,14 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
 
 // ---------------------------------------------------------------------------
 // Gradient loop, XCD-local.  Member `rank` owns hidden units j0 .. j0+HJ-1
-// (HJ = 16 NCT).  In phase 1 each of the first HJ*4 threads handles four
-// consecutive units of one row of the tile.  Step t (descending):
+// (HJ = 16 NCT); thread (row, unit) of the first 16*HJ threads keeps dh, dc
+// of that row and unit.  Step t (descending), per row tile:
 //   phase 1: from the values popped during step t+1: dh_tot, dz, dc; write
 //     dz (the exchange array); accumulate db;
 //   phase 2: poll the dz rows of the tile (all 4H gate columns, K split
 //     over the 8 waves, in batches; the pops of step t-1 are issued after the
-//     last batch), dh <- dz W_h^T for the own units (MFMA), one LDS round
-//     adds the 8 partial products.
+//     last batch), dh <- dz W_h^T for the own units (MFMA); the thread of
+//     (row, unit) adds the 8 partial products.
 // ---------------------------------------------------------------------------
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
 __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
@@ -388,10 +397,11 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   __shared__ int s_info[2];
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT;                 // units per work-group
-  constexpr int Q4 = HJ / 4;                   // unit quads per row
-  constexpr int NPT = 16 * Q4;                 // phase-1 threads (one quad each)
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
   constexpr int KB = KSW < 8 ? KSW : 8;        // k-steps per load batch
+  constexpr int IS = xbwd_is(NCT);
+  constexpr int CB = 4 * KPC * (int)sizeof(T);    // bytes of one k-step of a row
+  static_assert(16 * HJ <= XNT, "one thread per (row, unit) of a tile");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, l16 = lane & 15;
 
@@ -429,56 +439,56 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
       lds[((wave * KSL + i) * NCT + ct) * 64 + lane] = ks < ks1 ? ld16(wrow + (ks * 4 + q) * KPC) : zero4();
     }
   }
-  float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCT * 64);   // [XNW waves][NCT][4][64]
-  int* win = reinterpret_cast<int*>(red + (XNW * NCT * 256 > 64 * HJ ? XNW * NCT * 256 : 64 * HJ));  // [2][WIN+1]
+  float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCT * 64);   // [XNW][4][IS]
+  int* win = reinterpret_cast<int*>(red + xbwd_red_floats(NCT));       // [2][WIN+1]
   int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
 
-  // phase-1 element of this thread: row pr_row, units j0 + pu .. +3
-  const bool p1 = tid < NPT;
-  const int prow = tid / Q4, pu = (tid - (tid / Q4) * Q4) * 4;
+  // (row, unit) of this thread: 16 lanes take 16 consecutive units of one
+  // row, a wave four rows (the four MFMA result elements of a lane group)
+  const bool cellt = tid < 16 * HJ;
+  const int cu = (tid >> 8) * 16 + (tid & 15);
+  const int crow = (tid >> 4) & 15;
+  const int ju = j0 + cu;
+  const float* rp = red + (crow & 3) * IS + (cu >> 4) * 64 + (crow >> 2) * 16 + (cu & 15);
   if (tid < MRT_MAX * 16) {
     const int r = (grp + 8 * (tid >> 4)) * 16 + (tid & 15);
     sperm[tid] = ((tid >> 4) < a.MRT && r < B) ? a.perm[r] : -1;
   }
   __syncthreads();
-  float4 dh[MRT_MAX], dc[MRT_MAX];
+  float dh[MRT_MAX], dc[MRT_MAX];
 #pragma unroll
   for (int mt = 0; mt < MRT_MAX; ++mt) {
-    dh[mt] = make_float4(0.f, 0.f, 0.f, 0.f);
-    dc[mt] = make_float4(0.f, 0.f, 0.f, 0.f);
-    const int b = p1 ? sperm[mt * 16 + prow] : -1;
+    dh[mt] = 0.f;
+    dc[mt] = 0.f;
+    const int b = cellt ? sperm[mt * 16 + crow] : -1;
     if (b >= 0) {
-      if (a.dhT) dh[mt] = *reinterpret_cast<const float4*>(a.dhT + (long)b * H + j0 + pu);
-      if (a.dcT) dc[mt] = *reinterpret_cast<const float4*>(a.dcT + (long)b * H + j0 + pu);
+      if (a.dhT) dh[mt] = a.dhT[(long)b * H + ju];
+      if (a.dcT) dc[mt] = a.dcT[(long)b * H + ju];
     }
   }
-  float4 dbacc[4];
-#pragma unroll
-  for (int g = 0; g < 4; ++g) dbacc[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+  float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
 
   // pops of (step tt, tile mt) for this thread: i, f, g, o, c_t, c_{t-1}, dy
-  auto fetch = [&](float4 (&v)[7], int tt, int mt, int A, int off, int offp) {
+  auto fetch = [&](float (&v)[7], int tt, int mt, int A, int off, int offp) {
 #pragma unroll
-    for (int c = 0; c < 7; ++c) v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-    const int r = (grp + 8 * mt) * 16 + prow;
-    if (!p1 || tt < 0 || r >= A) return;
-    const int b = sperm[mt * 16 + prow];
-    const float* st = a.stack + (long)(off + r) * H5 + j0 + pu;
+    for (int c = 0; c < 7; ++c) v[c] = 0.f;
+    const int r = (grp + 8 * mt) * 16 + crow;
+    if (!cellt || tt < 0 || r >= A) return;
+    const int b = sperm[mt * 16 + crow];
+    const float* st = a.stack + (long)(off + r) * H5 + ju;
 #pragma unroll
-    for (int c = 0; c < 5; ++c) v[c] = *reinterpret_cast<const float4*>(st + (long)c * H);
+    for (int c = 0; c < 5; ++c) v[c] = st[(long)c * H];
     if (tt > 0)
-      v[5] = *reinterpret_cast<const float4*>(a.stack + (long)(offp + r) * H5 + 4L * H + j0 + pu);
+      v[5] = a.stack[(long)(offp + r) * H5 + 4L * H + ju];
     else if (a.c0)
-      v[5] = *reinterpret_cast<const float4*>(a.c0 + (long)b * H + j0 + pu);
-    if (a.dy)
-      v[6] = *reinterpret_cast<const float4*>(
-          a.dy_compact ? a.dy + (long)(off + r) * H + j0 + pu : a.dy + ((long)tt * B + b) * H + j0 + pu);
+      v[5] = a.c0[(long)b * H + ju];
+    if (a.dy) v[6] = a.dy_compact ? a.dy[(long)(off + r) * H + ju] : a.dy[((long)tt * B + b) * H + ju];
   };
 
   const int T_eff = a.meta[0];
   int wlo = T_eff - 1 - WIN > 0 ? T_eff - 1 - WIN : 0;
   load_window(a, win, wlo);
-  float4 pv[MRT_MAX][7];
+  float pv[MRT_MAX][7];
   {
     const int t = T_eff - 1;
     const int A_t = t >= 0 ? win[t - wlo] : 0;
@@ -508,55 +518,34 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
         fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);
         continue;
       }
+      const bool act = cellt && r0 + crow < A_t;
       // phase 1
-      if (p1 && r0 + prow < A_t) {
-        const long krow = off_t + r0 + prow;
-        float dzv[4][4];   // [gate][unit]
-        float* dhp = reinterpret_cast<float*>(&dh[mt]);
-        float* dcp = reinterpret_cast<float*>(&dc[mt]);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const float dht = dhp[k] + reinterpret_cast<const float*>(&pv[mt][6])[k];
-          const float ig = reinterpret_cast<const float*>(&pv[mt][0])[k];
-          const float fg = reinterpret_cast<const float*>(&pv[mt][1])[k];
-          const float gg = reinterpret_cast<const float*>(&pv[mt][2])[k];
-          const float og = reinterpret_cast<const float*>(&pv[mt][3])[k];
-          const float c = reinterpret_cast<const float*>(&pv[mt][4])[k];
-          const float cp = reinterpret_cast<const float*>(&pv[mt][5])[k];
-          const float tc = tanhf_(c);
-          const float d_o = dht * tc;
-          const float dct = dcp[k] + dht * og * (1.f - tc * tc);
-          dzv[0][k] = dct * gg * (ig * (1.f - ig));
-          dzv[1][k] = dct * cp * (fg * (1.f - fg));
-          dzv[2][k] = dct * ig * (1.f - gg * gg);
-          dzv[3][k] = d_o * (og * (1.f - og));
-          dcp[k] = dct * fg;
-        }
-        T* dzr = DZ + krow * G4 + j0 + pu;
+      if (act) {
+        const float dht = dh[mt] + pv[mt][6];
+        const float ig = pv[mt][0], fg = pv[mt][1], gg = pv[mt][2], og = pv[mt][3];
+        const float c = pv[mt][4], cp = pv[mt][5];
+        const float tc = tanhf_(c);
+        const float d_o = dht * tc;
+        const float dct = dc[mt] + dht * og * (1.f - tc * tc);
+        float dz[4];
+        dz[0] = dct * gg * (ig * (1.f - ig));
+        dz[1] = dct * cp * (fg * (1.f - fg));
+        dz[2] = dct * ig * (1.f - gg * gg);
+        dz[3] = d_o * (og * (1.f - og));
+        dc[mt] = dct * fg;
+        T* dzr = DZ + (long)(off_t + r0 + crow) * G4 + ju;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          T tmp[4];
-#pragma unroll
-          for (int k = 0; k < 4; ++k) tmp[k] = to_exchange<T>(dzv[g][k]);
-          if constexpr (sizeof(T) == 2) {
-            uint2 pk;
-            __builtin_memcpy(&pk, tmp, 8);
-            *reinterpret_cast<uint2*>(dzr + (long)g * H) = pk;
-          } else {
-            uint4 pk;
-            __builtin_memcpy(&pk, tmp, 16);
-            *reinterpret_cast<uint4*>(dzr + (long)g * H) = pk;
-          }
-          dbacc[g].x += dzv[g][0];
-          dbacc[g].y += dzv[g][1];
-          dbacc[g].z += dzv[g][2];
-          dbacc[g].w += dzv[g][3];
+          dzr[(long)g * H] = to_exchange<T>(dz[g]);
+          dbacc[g] += dz[g];
         }
       }
       // phase 2
-      const int ar = r0 + l16;
-      const int nks = ar < A_t ? ks1 - ks0 : 0;             // chunks this lane reads
-      const T* abase = DZ + (long)(off_t + ar) * G4 + (ks0 * 4 + q) * KPC;
+      const int nrow = min(16, A_t - r0);                   // running rows of the tile
+      const __amdgpu_buffer_rsrc_t rs =
+          make_rsrc(DZ + (long)(off_t + r0) * G4, (unsigned)(nrow * G4 * (long)sizeof(T)));
+      const unsigned aoff = (unsigned)((l16 * G4 + (ks0 * 4 + q) * KPC) * (long)sizeof(T));
+      const int nks = ks1 - ks0;                            // k-steps of this wave
       f32x4 acc[NCT];
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -565,7 +554,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
         uint4 av[KB];
 #pragma unroll
         for (int i = 0; i < KB; ++i)
-          av[i] = b0 + i < nks ? ld_chunk_agent<T>(abase + (b0 + i) * 4 * KPC) : zero4();
+          av[i] = b0 + i < nks ? ld_chunk_l2(rs, aoff + (b0 + i) * CB) : zero4();
         if (b0 + KB >= KSW) fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);   // next step's pops
         unsigned todo = 0;
 #pragma unroll
@@ -579,7 +568,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
 #pragma unroll
             for (int i = 0; i < KB; ++i) {
               if (todo & (1u << i)) {
-                av[i] = ld_chunk_agent<T>(abase + (b0 + i) * 4 * KPC);
+                av[i] = ld_chunk_l2(rs, aoff + (b0 + i) * CB);
                 if (!pending_chunk<T>(av[i])) todo &= ~(1u << i);
               }
             }
@@ -606,41 +595,34 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
           }
         }
       }
+      // partial products -> red once the previous tile's sums have been read
+      __syncthreads();
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) red[((wave * NCT + ct) * 4 + e) * 64 + lane] = acc[ct][e];
+        for (int e = 0; e < 4; ++e) red[(wave * 4 + e) * IS + ct * 64 + lane] = acc[ct][e];
       __syncthreads();
-      if (p1 && r0 + prow < A_t) {
-        float* dhp = reinterpret_cast<float*>(&dh[mt]);
+      if (act) {
+        float s = rp[0];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int u = pu + k;
-          // element (prow, u): column tile u/16, lane (prow/4)*16 + u%16, slot prow%4
-          const int ct = u >> 4, ln = (prow >> 2) * 16 + (u & 15), ee = prow & 3;
-          float s = red[((0 * NCT + ct) * 4 + ee) * 64 + ln];
-#pragma unroll
-          for (int w2 = 1; w2 < XNW; ++w2) s += red[((w2 * NCT + ct) * 4 + ee) * 64 + ln];
-          dhp[k] = s;
-        }
+        for (int w2 = 1; w2 < XNW; ++w2) s += rp[w2 * 4 * IS];
+        dh[mt] = s;
       }
-      __syncthreads();
     }
   }
 
 #pragma unroll
   for (int mt = 0; mt < MRT_MAX; ++mt) {
-    const int b = p1 ? sperm[mt * 16 + prow] : -1;
+    const int b = cellt ? sperm[mt * 16 + crow] : -1;
     if (b < 0) continue;
-    if (a.dh0) *reinterpret_cast<float4*>(a.dh0 + (long)b * H + j0 + pu) = dh[mt];
-    if (a.dc0) *reinterpret_cast<float4*>(a.dc0 + (long)b * H + j0 + pu) = dc[mt];
+    if (a.dh0) a.dh0[(long)b * H + ju] = dh[mt];
+    if (a.dc0) a.dc0[(long)b * H + ju] = dc[mt];
   }
   // db partial of this work-group (its rows of this XCD), fixed order
   __syncthreads();
-  if (p1) {
+  if (cellt) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g)
-      *reinterpret_cast<float4*>(red + prow * 4 * HJ + g * HJ + pu) = dbacc[g];
+    for (int g = 0; g < 4; ++g) red[(crow * 4 + g) * HJ + cu] = dbacc[g];
   }
   __syncthreads();
   for (int c = tid; c < 4 * HJ; c += XNT) {
@@ -717,9 +699,9 @@ XKernels x_kernels(int hc, int mrt) {
   const bool one = mrt <= 1;
   if (mrt > 4) return XKernels{};
   switch (hc) {
-    case 1: return one ? x_make<T, NF, NB, 1, 1, 4, 1>() : x_make<T, NF, NB, 1, 1, 2, 4>();
-    case 2: return one ? x_make<T, NF, NB, 2, 2, 8, 1>() : x_make<T, NF, NB, 2, 2, 4, 4>();
-    case 4: return one ? x_make<T, NF, NB, 4, 4, 12, 1>() : x_make<T, NF, NB, 4, 3, 8, 4>();
+    case 1: return one ? x_make<T, NF, NB, 1, 1, 4, 1>() : x_make<T, NF, NB, 1, 1, 4, 4>();
+    case 2: return one ? x_make<T, NF, NB, 2, 2, 8, 1>() : x_make<T, NF, NB, 2, 2, 6, 4>();
+    case 4: return one ? x_make<T, NF, NB, 4, 4, 16, 1>() : x_make<T, NF, NB, 4, 3, 8, 4>();
     default: return XKernels{};
   }
 }
