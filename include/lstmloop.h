@@ -193,7 +193,8 @@ typedef enum {
   LL_STAGE_BWD_OPERANDS = 4,  /* transposed operands of the dW products      */
   LL_STAGE_DW = 5,            /* dW = sum_t [x_t, h_{t-1}]^T dz_t, db        */
   LL_STAGE_DX = 6,            /* dx_t = dz_t W_x^T (and finished-row zeros)  */
-  LL_STAGE_COUNT = 7
+  LL_STAGE_LOOP_SETUP = 7,    /* exchange arrays filled, h0 rows reordered   */
+  LL_STAGE_COUNT = 8
 } ll_stage;
 
 ll_status ll_plan_set_timing(ll_plan* plan, int32_t enable);

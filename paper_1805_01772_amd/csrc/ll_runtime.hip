@@ -490,6 +490,8 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       ev = tbeg(p, s);
       LL_HIP(ll::launch_fill_pending(p->HH[l], (long)H * p->es, p->meta, p->cap, s));
       LL_HIP(ll::launch_h0_sorted<T>(h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->H0s, s));
+      tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+      ev = tbeg(p, s);
       ll::XLoopArgs xa{};
       xa.H0 = p->H0s;
       xa.B = B;
@@ -567,6 +569,8 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     if (p->xmode) {
       ev = tbeg(p, s);
       LL_HIP(ll::launch_fill_pending(p->DZ, 4L * H * p->es, p->meta, p->cap, s));
+      tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+      ev = tbeg(p, s);
       ll::XLoopArgs xa{};
       xa.B = B;
       xa.H = H;

@@ -24,7 +24,7 @@ EXPORTED = ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes",
             "ll_plan_geometry", "lstm_loop_fwd", "lstm_loop_bwd",
             "ll_status_sync", "ll_last_error", "ll_version",
             "ll_plan_set_timing", "ll_plan_read_timing")
-STAGES = ("prep", "input_proj", "fwd_loop", "bwd_loop", "bwd_operands", "dw", "dx")
+STAGES = ("prep", "input_proj", "fwd_loop", "bwd_loop", "bwd_operands", "dw", "dx", "loop_setup")
 
 
 class ll_desc(ctypes.Structure):

@@ -80,3 +80,16 @@ def test_null_arguments_rejected():
     assert lib.lstm_loop_bwd(None, None, None, None, None, None, None, None, None, None) \
         == ll.LL_EINVAL
     assert lib.ll_plan_destroy(None) == ll.LL_OK
+
+
+def test_binding_constants_match_the_header():
+    """Stage names and status codes of the binding follow the header's enums."""
+    text = open(HEADER).read()
+    stages = dict((int(v), k.lower()) for k, v in re.findall(r"LL_STAGE_([A-Z_]+) = (\d+)", text))
+    count = [k for k in stages.values() if k == "count"]
+    assert count and max(stages) == len(ll.STAGES)
+    assert tuple(stages[i] for i in range(len(ll.STAGES))) == ll.STAGES
+    status = dict(re.findall(r"(LL_E[A-Z]+) = (\d+)", text))
+    for name, val in status.items():
+        if hasattr(ll, name):
+            assert getattr(ll, name) == int(val), name

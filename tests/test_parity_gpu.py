@@ -42,9 +42,13 @@ SMALL = [
 ]
 
 
-def run_case(w, inp, save=True, backward=True, with_dy=True):
+def run_case(w, inp, save=True, backward=True, with_dy=True, geometry=None):
     dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
     plan = dc.plan()
+    geom = plan.geometry()
+    say(f"    {w.name}: loops {geom}")
+    if geometry is not None:
+        geometry.update(geom)
     dc.fwd(plan, save=save)
     if backward:
         dc.bwd(plan, with_dy=with_dy)
@@ -268,8 +272,11 @@ def test_backward_without_forward_is_a_state_error():
 def test_full_size_parity(w):
     say(f"[full] {w.name}")
     inp = wl.generate(w)
-    res, err = run_case(w, inp)
+    geom = {}
+    res, err = run_case(w, inp, geometry=geom)
     assert err == 0
+    # the launch configuration the benchmark times: XCD-local loops
+    assert geom["xcd_local"], geom
     say("    oracle running")
     ref = oracle_reference(inp, w.layers, w.dtype)
     errs, bad = compare(res, ref, TOL[w.dtype])
