@@ -122,9 +122,10 @@ struct XLoopArgs {
   const void* W;          // forward: W^T [4H, ldw]; backward: W [rows, 4H]
   int ldw;
   int woff;               // forward: column of the h part in W^T; backward: row of W_h
-  const void* H0;         // forward: h0 rows in length order, operand type [B, H]
-  void* X;                // exchange array: forward h history [cap, H];
-                          // backward dz [cap, 4H] (operand type, pre-filled)
+  void* X;                // forward: h history [cap, H]; backward: dz [cap, 4H] (operand type)
+  void* ring;             // exchange ring [2][8][MRT][ring_ks][1 KB] (forward: slot 1 holds h0)
+  int ring_ks;            // k-step blocks per row tile: H / (4 KPC) forward, 4H / (4 KPC) backward
+  unsigned* flags;        // [8][MRT][32] per-member step flags, zero before the launch
   const float* Zx;        // forward: [cap, 4H]
   const float* h0;
   const float* c0;
@@ -156,11 +157,11 @@ template <typename T>
 XKernels x_kernels(int hc, int mrt);
 hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd);
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s);
-hipError_t launch_fill_pending(void* base, long row_bytes, const int* meta, long cap_rows,
-                               hipStream_t s);
+// h0 rows into ring slot 1 (consumer lane order) and the launch's flags to zero.
 template <typename T>
-hipError_t launch_h0_sorted(const float* h0, const int* perm, int B, int H, void* out,
-                            hipStream_t s);
+hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, int mrt, int ring_ks,
+                                void* ring, unsigned* flags, int nflags, hipStream_t s);
+hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s);
 
 hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
                        int* rowmap, int* meta, int* trip_out, hipStream_t s);

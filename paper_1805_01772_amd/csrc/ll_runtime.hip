@@ -89,7 +89,8 @@ struct ll_plan {
   void* XT = nullptr;
   void* HPT = nullptr;
   float* dyc = nullptr;
-  void* H0s = nullptr;         // h0 rows in length order, operand type [B, H]
+  void* xring = nullptr;       // XCD-local loops: exchange ring
+  unsigned* xflags = nullptr;  // XCD-local loops: per-member step flags [8][MRT][32]
   float* db_part = nullptr;
   float* ws = nullptr;
   long ws_floats = 0;
@@ -168,7 +169,7 @@ void drain_timing(ll_plan* p) {
 void free_plan_memory(ll_plan* p) {
   void* ptrs[] = {p->perm, p->active, p->off, p->rowmap, p->meta, p->WT[0], p->WT[1], p->Zx,
                   p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT, p->HPT,
-                  p->dyc, p->H0s, p->db_part, p->ws};
+                  p->dyc, p->xring, p->xflags, p->db_part, p->ws};
   for (void* q : ptrs)
     if (q) hipFree(q);
 }
@@ -383,7 +384,12 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->XT, es * maxI * p->ldT, "x transposed");
   ALLOC(p->HPT, es * H * p->ldT, "h_prev transposed");
   if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
-  ALLOC(p->H0s, es * B * H, "sorted h0");
+  if (p->xmode) {
+    // two slots x 8 XCDs x row tiles x (4H / k-step) blocks of 1 KB
+    const long ks_b = 4L * H * (long)es / 64;
+    ALLOC(p->xring, 2L * 8 * p->xMRT * ks_b * 1024, "exchange ring");
+    ALLOC(p->xflags, sizeof(unsigned) * 8 * p->xMRT * 32, "exchange flags");
+  }
   ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * 4 * H, "db partials");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
 #undef ALLOC
@@ -488,12 +494,15 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     tend(p, s, LL_STAGE_INPUT_PROJ, ev);
     if (p->xmode) {
       ev = tbeg(p, s);
-      LL_HIP(ll::launch_fill_pending(p->HH[l], (long)H * p->es, p->meta, p->cap, s));
-      LL_HIP(ll::launch_h0_sorted<T>(h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->H0s, s));
+      const int ring_ks = (int)((long)H * p->es / 64);
+      LL_HIP(ll::launch_x_prepare_fwd<T>(h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->xMRT,
+                                         ring_ks, p->xring, p->xflags, 8 * p->xMRT * 32, s));
       tend(p, s, LL_STAGE_LOOP_SETUP, ev);
       ev = tbeg(p, s);
       ll::XLoopArgs xa{};
-      xa.H0 = p->H0s;
+      xa.ring = p->xring;
+      xa.ring_ks = ring_ks;
+      xa.flags = p->xflags;
       xa.B = B;
       xa.H = H;
       xa.T_max = d.T_max;
@@ -568,10 +577,13 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     const int Il = in_width(p, l);
     if (p->xmode) {
       ev = tbeg(p, s);
-      LL_HIP(ll::launch_fill_pending(p->DZ, 4L * H * p->es, p->meta, p->cap, s));
+      LL_HIP(ll::launch_zero_u32(p->xflags, 8 * p->xMRT * 32, s));
       tend(p, s, LL_STAGE_LOOP_SETUP, ev);
       ev = tbeg(p, s);
       ll::XLoopArgs xa{};
+      xa.ring = p->xring;
+      xa.ring_ks = (int)(4L * H * p->es / 64);
+      xa.flags = p->xflags;
       xa.B = B;
       xa.H = H;
       xa.T_max = d.T_max;

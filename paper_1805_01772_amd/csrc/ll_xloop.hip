@@ -4,25 +4,31 @@
 // Here the 32 work-groups resident on one XCD form a group that runs the
 // recurrence of its own batch rows (row tiles x, x+8, ... for XCD x) and
 // splits the hidden units 32 ways, so every value exchanged inside the loop
-// (h_t forward, dz_t backward) moves only through that XCD's L2:
-//   * producers write it with plain stores (the vector L1 writes through to
-//     the L2);
-//   * the arrays it lands in are filled with an all-ones pattern (a NaN
-//     payload no arithmetic result carries: produced NaNs are stored in
-//     canonical form) before the loop starts, and every element is written
-//     exactly once per call;
-//   * consumers read it with agent-scope atomic loads, which bypass the
-//     CU's L1, and re-read any element that still holds the fill pattern.
-// There is no grid barrier and no L2 writeback or invalidate in the loop:
-// the data itself carries the readiness.  A work-group learns its XCD from
-// the XCC_ID hardware register and its rank from a per-XCD counter, so the
+// (h_t forward, dz_t backward) moves only through that XCD's L2.
+//
+// The exchange goes through a ring of two slots per row tile, laid out in the
+// order the consumers' matrix-core operands need it: block ks of a slot holds
+// k-step ks (32 bf16 or 16 fp32 columns) of the tile's 16 rows, lane l's 16
+// bytes being row l % 16, k-chunk l / 16.  Every block has exactly one
+// producer (its columns are the producer's own hidden units), and a consumer
+// wave reads each of its k-steps as one contiguous 1 KB load.
+//   * A producer stores its blocks with plain stores (the vector L1 writes
+//     through to the L2), waits until they are acknowledged
+//     (s_waitcnt vmcnt(0)), meets its work-group at a barrier, and one thread
+//     stores the step number into the producer's flag.
+//   * A consumer wave polls, one lane per producer, the flags of the blocks it
+//     needs with L1-bypassing loads, then reads the blocks with L1-bypassing
+//     (cache policy sc1) loads: they are in the shared L2 by then.
+// Slot t % 2 is rewritten at step t + 2 (t - 2 in the gradient loop) only
+// after every member has published step t + 1, which each does after reading
+// slot t % 2, so two slots suffice.  There is no grid barrier and no L2
+// writeback or invalidate in the loop.  A work-group learns its XCD from the
+// XCC_ID hardware register and its rank from a per-XCD counter, so the
 // mapping does not depend on the dispatch order.
 //
 // Each work-group keeps its recurrent weight slice on chip for the whole
 // loop, in registers (the first KSR k-steps of each wave's share; any rest in
 // LDS).
-#include <type_traits>
-
 #include "ll_kernels.h"
 
 namespace ll {
@@ -31,45 +37,35 @@ namespace {
 
 constexpr int kXccIdReg = (3 << 11) | 20;    // s_getreg: HW_REG_XCC_ID, bits [3:0]
 
-// True if any element of the 8-byte word still holds the fill pattern.
-template <typename T> __device__ __forceinline__ bool pending(unsigned long long v);
-template <> __device__ __forceinline__ bool pending<bf16_t>(unsigned long long v) {
-  // an element is all ones iff its 16 bits of ~v are zero (zero-lane test)
-  const unsigned long long x = ~v;
-  return ((x - 0x0001000100010001ull) & ~x & 0x8000800080008000ull) != 0;
-}
-template <> __device__ __forceinline__ bool pending<float>(unsigned long long v) {
-  return ((unsigned)v == 0xffffffffu) || ((unsigned)(v >> 32) == 0xffffffffu);
-}
+// Wave-uniform copy of a value every lane holds (keeps it in a scalar
+// register, so buffer descriptors built from it stay scalar).
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // Raw buffer resource over `bytes` bytes from `base` (stride 0; reads past
-// the end return zeros).
+// the end return zeros).  Both arguments must be the same on every lane; they
+// are read from the first lane so that the descriptor lives in scalar
+// registers.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+  const unsigned long long p = reinterpret_cast<unsigned long long>(base);
+  const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)p);
+  const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(p >> 32));
+  void* pb = reinterpret_cast<void*>(((unsigned long long)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(pb, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes),
+                                           0x00020000);
 }
-// 16-byte chunk read with cache policy sc1: it bypasses the CU's L1 and is
-// served by the L2, so it sees the plain stores other CUs of the same XCD
-// made there.  An element is never torn (2- and 4-byte elements are
-// naturally aligned); a chunk may mix old and new elements, which the
-// per-element fill-pattern test catches.
+// 16-byte read with cache policy sc1: it bypasses the CU's L1 and is served
+// by the L2, so it sees what other CUs of the same XCD stored there.
 constexpr int kCpolSc1 = 16;
 __device__ __forceinline__ uint4 ld_chunk_l2(__amdgpu_buffer_rsrc_t r, unsigned off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolSc1));
 }
-template <typename T>
-__device__ __forceinline__ bool pending_chunk(uint4 v) {
-  return pending<T>((unsigned long long)v.x | ((unsigned long long)v.y << 32)) ||
-         pending<T>((unsigned long long)v.z | ((unsigned long long)v.w << 32));
+// Plain 4-byte read through a buffer descriptor.
+__device__ __forceinline__ float ld_f32(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
-
-// Store forms of an exchanged value: NaN in canonical form (never all ones).
-template <typename T> __device__ __forceinline__ T to_exchange(float v);
-template <> __device__ __forceinline__ float to_exchange<float>(float v) {
-  return v != v ? __uint_as_float(0x7fc00000u) : v;
-}
-template <> __device__ __forceinline__ bf16_t to_exchange<bf16_t>(float v) {
-  return v != v ? (bf16_t)0x7fc0 : f32_to_bf16(v);
-}
+// Offset past every buffer range used here: a lane with nothing to read
+// loads from it and gets zeros, so no load needs a per-lane branch.
+constexpr unsigned kOOB = 0x80000000u;
 
 // Group of this work-group: (XCD, rank within the XCD).
 __device__ __forceinline__ void join_group(unsigned* rank_ctr, int* s_info) {
@@ -79,6 +75,38 @@ __device__ __forceinline__ void join_group(unsigned* rank_ctr, int* s_info) {
     s_info[1] = (int)atomicAdd(rank_ctr + (x & 7), 1u);
   }
   __syncthreads();
+}
+
+// Publish: every wave waits until its stores are acknowledged by the L2, the
+// work-group meets, and thread 0 stores `value` into the flag.
+__device__ __forceinline__ void publish(unsigned* flag, unsigned value) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_store(flag, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Wait until flags[p(l)] >= need for the lanes l < n (p(l) = (p0 + l) % P),
+// with the loop's wall-clock limit and abort flag.
+__device__ __forceinline__ void wait_flags(const XLoopArgs& a, const unsigned* flags, int p0, int n,
+                                           int P, unsigned need) {
+  const int lane = threadIdx.x & 63;
+  const unsigned* fp = flags + (p0 + (lane < n ? lane : 0)) % P;
+  unsigned long long t0 = 0;
+  unsigned polls = 0;
+  while (true) {
+    const unsigned f = __hip_atomic_load(fp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (__builtin_amdgcn_ballot_w64(lane < n && f < need) == 0) return;
+    if (polls == 0) t0 = wall_clock64();
+    __builtin_amdgcn_s_sleep(1);
+    if ((++polls & 255u) == 0) {
+      if (__hip_atomic_load(a.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+      if (wall_clock64() - t0 > a.limit) {
+        __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(a.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+      }
+    }
+  }
 }
 
 }  // namespace
@@ -91,11 +119,15 @@ constexpr int XNT = 64 * XNW;
 // lo .. lo+WIN, kept in LDS so that no step waits on a global load for it.
 constexpr int WIN = 256;
 
-// Forward partial products in LDS: [wave][element i of the MFMA result]
-// [column tile][lane], one slice of xfwd_is floats per (wave, i).  The pad of
-// 16 floats puts the four rows a 16-lane group of the cell reads in distinct
+// Partial products in LDS: [wave][element i of the MFMA result][column
+// tile][lane], one slice of NCT*64 + 16 floats per (wave, i).  The pad of 16
+// floats puts the four rows a 16-lane group of the cell reads in distinct
 // LDS banks.
 constexpr int xfwd_is(int NCT) { return NCT * 64 + 16; }
+constexpr int xbwd_is(int NCT) { return NCT * 64 + 16; }
+constexpr int xbwd_red_floats(int NCT) {
+  return XNW * 4 * xbwd_is(NCT) > 16 * 4 * 16 * NCT ? XNW * 4 * xbwd_is(NCT) : 16 * 4 * 16 * NCT;
+}
 
 // LDS of the forward kernel: weight k-steps not in registers, partial
 // products, metadata window, perm rows.
@@ -105,12 +137,7 @@ size_t xfwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
          (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
 }
 // LDS of the gradient kernel: weight k-steps not in registers, partial
-// products [wave][i][column tile][lane] (reused for the db rows at the end),
-// metadata window, perm rows.
-constexpr int xbwd_is(int NCT) { return NCT * 64 + 16; }
-constexpr int xbwd_red_floats(int NCT) {
-  return XNW * 4 * xbwd_is(NCT) > 16 * 4 * 16 * NCT ? XNW * 4 * xbwd_is(NCT) : 16 * 4 * 16 * NCT;
-}
+// products (reused for the db rows at the end), metadata window, perm rows.
 size_t xbwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
   const int KSL = KSW > KSR ? KSW - KSR : 0;
   return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)xbwd_red_floats(NCT) * 4 +
@@ -127,16 +154,24 @@ __device__ __forceinline__ void load_window(const XLoopArgs& a, int* win, int lo
   __syncthreads();
 }
 
+// Ring slot of row tile mt: ring_ks blocks of 1 KB.
+__device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp, int mt) {
+  return reinterpret_cast<char*>(a.ring) + ((long)((slot * 8 + grp) * a.MRT + mt) * a.ring_ks << 10);
+}
+
 // ---------------------------------------------------------------------------
 // Forward loop, XCD-local.  Member `rank` of XCD x owns hidden units
 // j0 .. j0+HJ-1 (HJ = 4 NCT: all four gates of each unit, NCT column tiles of
-// 16 gate columns) of the rows in tiles x, x+8, ...  Step t for a row tile:
-//   1. every wave polls its k-steps of h_{t-1} (K split over the 8 waves);
-//      the cell threads also fetch the next step's input projections;
+// 16 gate columns) of the rows in tiles x, x+8, ...; HJ units are one k-step
+// of the recurrent product, ring block `rank`.  Step t for a row tile:
+//   1. every wave waits for the producers of its k-steps of h_{t-1} (K split
+//      over the 8 waves) and reads them from the ring; the cell threads also
+//      fetch the next step's input projections;
 //   2. z = h W_h over the wave's k-steps (MFMA), partial products -> LDS;
 //   3. cell: thread (row, unit) of the first 16*HJ threads adds the 8
 //      partial products of its four gates and the input projection, runs the
-//      cell and stores h_t (the exchange, first), the stack row and y_t.
+//      cell, stores h_t into the ring and publishes it; then the h history,
+//      the stack row and y_t.
 // ---------------------------------------------------------------------------
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
 __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
@@ -146,13 +181,13 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   constexpr int HJ = 4 * NCT;
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
   constexpr int IS = xfwd_is(NCT);
-  constexpr int CB = 4 * KPC * (int)sizeof(T);    // bytes of one k-step of a row
   static_assert(16 * HJ <= XNT, "one cell thread per (row, unit) of a tile");
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  static_assert(HJ == 4 * KPC, "a member's units are one k-step");
+  const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
 
   join_group(a.rank_ctr, s_info);
-  const int grp = s_info[0], rank = s_info[1];
+  const int grp = uni(s_info[0]), rank = uni(s_info[1]);
   if (grp >= 8 || rank >= 32) {
     if (tid == 0) {
       __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -167,6 +202,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   const int j0 = rank * HJ;
   const int KS = H / (4 * KPC);
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
+  const int nks = ks1 - ks0;                             // k-steps of this wave
   const T* WT = reinterpret_cast<const T*>(a.W);
   T* HH = reinterpret_cast<T*>(a.X);
 
@@ -201,6 +237,8 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   const int ju = j0 + cu;
   // LDS slot of this thread's gate-0 partial product of wave 0
   const float* rp = red + (crow & 3) * IS + (cu >> 4) * 64 + (crow >> 2) * 16 + (cu & 15);
+  // byte offset of (crow, cu) in a ring block
+  const int rbo = ((crow + 16 * (cu / KPC)) * KPC + cu % KPC) * (int)sizeof(T);
   float hs[MRT_MAX], cs[MRT_MAX];
   if (tid < MRT_MAX * 16) {
     const int r = (grp + 8 * (tid >> 4)) * 16 + (tid & 15);
@@ -218,7 +256,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
     }
   }
 
-  const int T_eff = a.meta[0];
+  const int T_eff = uni(a.meta[0]);
   int wlo = 0;
   load_window(a, win, 0);
   // input projections of the cell thread's (row, unit), one step ahead
@@ -232,13 +270,12 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   }
 
   for (int t = 0; t < T_eff; ++t) {
-    if (t + 1 > wlo + WIN) {
-      wlo = t;
+    if (t + 1 > wlo + WIN) {   // the window keeps step t-1 as well
+      wlo = t - 1;
       load_window(a, win, wlo);
     }
-    const int A_t = win[t - wlo], A_n = win[t + 1 - wlo];
-    const int off_t = win[WIN + 1 + t - wlo], off_n = win[WIN + 1 + t + 1 - wlo];
-    const int off_p = t > 0 ? (t - 1 >= wlo ? win[WIN + 1 + t - 1 - wlo] : a.off[t - 1]) : 0;
+    const int A_t = uni(win[t - wlo]), A_n = uni(win[t + 1 - wlo]);
+    const int off_t = uni(win[WIN + 1 + t - wlo]), off_n = uni(win[WIN + 1 + t + 1 - wlo]);
 #pragma unroll
     for (int mt = 0; mt < MRT_MAX; ++mt) {
       if (mt >= a.MRT) continue;
@@ -250,58 +287,26 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
         }
         continue;
       }
-      // 1. h_{t-1} of this wave's k-steps: the history row of step t-1, or
-      //    for t = 0 the row of h0 in length order (written before the loop)
-      //    Rows r0 .. r0+nrow-1 of the tile are running; the buffer range
-      //    ends there, so the other lanes read zeros.
-      const int nrow = min(16, A_t - r0);
-      const T* tb = t > 0 ? HH + (long)(off_p + r0) * H : reinterpret_cast<const T*>(a.H0) + (long)r0 * H;
-      const __amdgpu_buffer_rsrc_t rs = make_rsrc(tb, (unsigned)(nrow * H * (int)sizeof(T)));
-      const unsigned aoff = (unsigned)((l16 * H + (ks0 * 4 + q) * KPC) * (int)sizeof(T));
-      const int nks = ks1 - ks0;                             // k-steps of this wave
+      unsigned* flags = a.flags + (grp * a.MRT + mt) * 32;
+      // 1. h_{t-1} of this wave's k-steps (for t = 0 the ring holds h0)
+      if (t > 0) wait_flags(a, flags, ks0, nks, a.P, (unsigned)(t + 1));
+      const __amdgpu_buffer_rsrc_t rs = make_rsrc(ring_tile(a, (t + 1) & 1, grp, mt), (unsigned)(a.ring_ks << 10));
       uint4 av[KSW];
 #pragma unroll
-      for (int i = 0; i < KSW; ++i) av[i] = i < nks ? ld_chunk_l2(rs, aoff + i * CB) : zero4();
+      for (int i = 0; i < KSW; ++i) av[i] = ld_chunk_l2(rs, i < nks ? (unsigned)(((ks0 + i) << 10) + lane * 16) : kOOB);
       float zc[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) zc[g] = zf[mt][g];
-      if (cellt) {
-        const int r = r0 + crow;
-        const bool nok = r < A_n;
+      {  // input projections of step t+1 (rows past A_n read zeros)
+        const int nr = max(0, min(16, A_n - r0));
+        const __amdgpu_buffer_rsrc_t rz = make_rsrc(a.Zx + (long)(off_n + r0) * G4, (unsigned)(nr * G4 * 4));
+        const unsigned zo = cellt ? (unsigned)((crow * G4 + ju) * 4) : kOOB;
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
-          zf[mt][g] = nok ? a.Zx[(long)(off_n + r) * G4 + (long)g * H + ju] : 0.f;
-      }
-      unsigned todo = 0;
-#pragma unroll
-      for (int i = 0; i < KSW; ++i)
-        if (i < nks && pending_chunk<T>(av[i])) todo |= 1u << i;
-      if (todo) {
-        const unsigned long long t0 = wall_clock64();
-        unsigned polls = 0;
-        while (todo) {
-          __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-          for (int i = 0; i < KSW; ++i) {
-            if (todo & (1u << i)) {
-              av[i] = ld_chunk_l2(rs, aoff + i * CB);
-              if (!pending_chunk<T>(av[i])) todo &= ~(1u << i);
-            }
-          }
-          if ((++polls & 255u) == 0) {
-            if (__hip_atomic_load(a.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
-            if (wall_clock64() - t0 > a.limit) {
-              __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              __hip_atomic_store(a.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              break;
-            }
-          }
-        }
+        for (int g = 0; g < 4; ++g) zf[mt][g] = ld_f32(rz, zo + g * H * 4);
       }
       // 2. partial products over this wave's k-steps, column tiles in two
-      //    halves, into red[wave][i][ct][lane] once the previous tile's cell
-      //    has read them
-      __syncthreads();
+      //    halves, into red[wave][i][ct][lane] (the previous tile's cell has
+      //    read them: it ended at a barrier)
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         constexpr int NH = NCT / 2;
@@ -310,7 +315,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
         for (int c = 0; c < NH; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < KSW; ++i) {
-          if (ks0 + i < ks1) {
+          if (i < nks) {
 #pragma unroll
             for (int c = 0; c < NH; ++c) {
               const int ct = hf * NH + c;
@@ -327,6 +332,9 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
       }
       __syncthreads();
       // 3. cell of (crow, cu): gate g is local column g*HJ + cu
+      float ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cn = 0.f, hn = 0.f;
+      const int r = r0 + crow;
+      const bool act = cellt && r < A_t;
       if (cellt) {
         float z[4];
 #pragma unroll
@@ -337,32 +345,34 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
           for (int w2 = 1; w2 < XNW; ++w2) v += p[w2 * 4 * IS];
           z[g] = v + zc[g];
         }
-        const float ig = sigmoidf_(z[0]);
-        const float fg = sigmoidf_(z[1]);
-        const float gg = tanhf_(z[2]);
-        const float og = sigmoidf_(z[3]);
-        const float cn = fg * cs[mt] + ig * gg;
-        const float hn = og * tanhf_(cn);
-        const int r = r0 + crow;
-        const bool act = r < A_t;
+        ig = sigmoidf_(z[0]);
+        fg = sigmoidf_(z[1]);
+        gg = tanhf_(z[2]);
+        og = sigmoidf_(z[3]);
+        cn = fg * cs[mt] + ig * gg;
+        hn = og * tanhf_(cn);
         if (act) {
-          const long cr = off_t + r;
-          HH[cr * H + ju] = to_exchange<T>(hn);
+          *reinterpret_cast<T*>(ring_tile(a, t & 1, grp, mt) + (rank << 10) + rbo) = Op<T>::from_f32(hn);
           cs[mt] = cn;
           hs[mt] = hn;
-          if (a.stack) {
-            float* st = a.stack + cr * H5 + ju;
-            st[0] = ig;
-            st[H] = fg;
-            st[2 * H] = gg;
-            st[3 * H] = og;
-            st[4 * H] = cn;
-          }
         }
-        if (a.y) {
-          const int b = sperm[mt * 16 + crow];
-          if (b >= 0) a.y[((long)t * B + b) * H + ju] = act ? hn : 0.f;
+      }
+      publish(flags + rank, (unsigned)(t + 2));
+      if (act) {
+        const long cr = off_t + r;
+        HH[cr * H + ju] = Op<T>::from_f32(hn);
+        if (a.stack) {
+          float* st = a.stack + cr * H5 + ju;
+          st[0] = ig;
+          st[H] = fg;
+          st[2 * H] = gg;
+          st[3 * H] = og;
+          st[4 * H] = cn;
         }
+      }
+      if (a.y && cellt) {
+        const int b = sperm[mt * 16 + crow];
+        if (b >= 0) a.y[((long)t * B + b) * H + ju] = act ? hn : 0.f;
       }
     }
   }
@@ -383,13 +393,17 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
 // ---------------------------------------------------------------------------
 // Gradient loop, XCD-local.  Member `rank` owns hidden units j0 .. j0+HJ-1
 // (HJ = 16 NCT); thread (row, unit) of the first 16*HJ threads keeps dh, dc
-// of that row and unit.  Step t (descending), per row tile:
-//   phase 1: from the values popped during step t+1: dh_tot, dz, dc; write
-//     dz (the exchange array); accumulate db;
-//   phase 2: poll the dz rows of the tile (all 4H gate columns, K split
-//     over the 8 waves, in batches; the pops of step t-1 are issued after the
-//     last batch), dh <- dz W_h^T for the own units (MFMA); the thread of
-//     (row, unit) adds the 8 partial products.
+// of that row and unit.  The dz columns of gate g of the member's units are
+// k-step g*P + rank of the product dz W_h^T.  Step t (descending), per row
+// tile:
+//   phase 1: from the values popped during step t+1: dh_tot, dz, dc; store
+//     dz into the ring and publish it; then the dz rows for the dW and dx
+//     products; accumulate db;
+//   phase 2: wait for the producers of the wave's k-steps (all 4H gate
+//     columns, K split over the 8 waves), read them in two batches (the pops
+//     of step t-1 are issued after the last batch), dh <- dz W_h^T for the
+//     own units (MFMA); the thread of (row, unit) adds the 8 partial
+//     products.
 // ---------------------------------------------------------------------------
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
 __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
@@ -400,13 +414,13 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
   constexpr int KB = KSW < 8 ? KSW : 8;        // k-steps per load batch
   constexpr int IS = xbwd_is(NCT);
-  constexpr int CB = 4 * KPC * (int)sizeof(T);    // bytes of one k-step of a row
   static_assert(16 * HJ <= XNT, "one thread per (row, unit) of a tile");
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  static_assert(HJ == 4 * KPC, "a member's units of one gate are one k-step");
+  const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
 
   join_group(a.rank_ctr, s_info);
-  const int grp = s_info[0], rank = s_info[1];
+  const int grp = uni(s_info[0]), rank = uni(s_info[1]);
   if (grp >= 8 || rank >= 32) {
     if (tid == 0) {
       __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -415,12 +429,13 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  const int H = a.H, B = a.B;
+  const int H = a.H, B = a.B, P = a.P;
   const long G4 = 4L * H;
   const long H5 = 5L * H;
   const int j0 = rank * HJ;
   const int KS = (int)(G4 / (4 * KPC));
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
+  const int nks = ks1 - ks0;                            // k-steps of this wave
   const T* W = reinterpret_cast<const T*>(a.W);
   T* DZ = reinterpret_cast<T*>(a.X);
 
@@ -450,6 +465,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   const int crow = (tid >> 4) & 15;
   const int ju = j0 + cu;
   const float* rp = red + (crow & 3) * IS + (cu >> 4) * 64 + (crow >> 2) * 16 + (cu & 15);
+  const int rbo = ((crow + 16 * (cu / KPC)) * KPC + cu % KPC) * (int)sizeof(T);
   if (tid < MRT_MAX * 16) {
     const int r = (grp + 8 * (tid >> 4)) * 16 + (tid & 15);
     sperm[tid] = ((tid >> 4) < a.MRT && r < B) ? a.perm[r] : -1;
@@ -468,24 +484,36 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   }
   float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
 
-  // pops of (step tt, tile mt) for this thread: i, f, g, o, c_t, c_{t-1}, dy
+  // pops of (step tt, tile mt) for this thread: i, f, g, o, c_t, c_{t-1}, dy;
+  // zeros for rows not running at tt (every read is issued, out of range)
   auto fetch = [&](float (&v)[7], int tt, int mt, int A, int off, int offp) {
-#pragma unroll
-    for (int c = 0; c < 7; ++c) v[c] = 0.f;
-    const int r = (grp + 8 * mt) * 16 + crow;
-    if (!cellt || tt < 0 || r >= A) return;
+    const int r0 = (grp + 8 * mt) * 16;
+    const int nr = tt >= 0 ? max(0, min(16, A - r0)) : 0;
+    const bool ok = cellt && crow < nr;
     const int b = sperm[mt * 16 + crow];
-    const float* st = a.stack + (long)(off + r) * H5 + ju;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.stack + (long)(off + r0) * H5, (unsigned)(nr * H5 * 4));
+    const unsigned so = ok ? (unsigned)((crow * H5 + ju) * 4) : kOOB;
 #pragma unroll
-    for (int c = 0; c < 5; ++c) v[c] = st[(long)c * H];
-    if (tt > 0)
-      v[5] = a.stack[(long)(offp + r) * H5 + 4L * H + ju];
-    else if (a.c0)
-      v[5] = a.c0[(long)b * H + ju];
-    if (a.dy) v[6] = a.dy_compact ? a.dy[(long)(off + r) * H + ju] : a.dy[((long)tt * B + b) * H + ju];
+    for (int c = 0; c < 5; ++c) v[c] = ld_f32(rs, so + c * H * 4);
+    if (tt > 0) {
+      const __amdgpu_buffer_rsrc_t rp2 =
+          make_rsrc(a.stack + (long)(offp + r0) * H5 + 4L * H, (unsigned)(nr * H5 * 4));
+      v[5] = ld_f32(rp2, so);
+    } else {
+      const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.c0, a.c0 ? (unsigned)(B * H * 4) : 0u);
+      v[5] = ld_f32(rc, ok ? (unsigned)((b * H + ju) * 4) : kOOB);
+    }
+    if (a.dy_compact) {
+      const __amdgpu_buffer_rsrc_t rd = make_rsrc(a.dy + (long)(off + r0) * H, (unsigned)(nr * H * 4));
+      v[6] = ld_f32(rd, ok ? (unsigned)((crow * H + ju) * 4) : kOOB);
+    } else {
+      const __amdgpu_buffer_rsrc_t rd =
+          make_rsrc(a.dy ? a.dy + (long)max(tt, 0) * B * H : nullptr, a.dy ? (unsigned)(B * H * 4) : 0u);
+      v[6] = ld_f32(rd, ok ? (unsigned)((b * H + ju) * 4) : kOOB);
+    }
   };
 
-  const int T_eff = a.meta[0];
+  const int T_eff = uni(a.meta[0]);
   int wlo = T_eff - 1 - WIN > 0 ? T_eff - 1 - WIN : 0;
   load_window(a, win, wlo);
   float pv[MRT_MAX][7];
@@ -504,11 +532,11 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
       wlo = t - WIN > 0 ? t - WIN : 0;
       load_window(a, win, wlo);
     }
-    const int A_t = win[t - wlo];
-    const int off_t = win[WIN + 1 + t - wlo];
-    const int A_n = t >= 1 ? win[t - 1 - wlo] : 0;
-    const int off_n = t >= 1 ? win[WIN + 1 + t - 1 - wlo] : 0;
-    const int off_pn = t >= 2 ? win[WIN + 1 + t - 2 - wlo] : 0;
+    const int A_t = uni(win[t - wlo]);
+    const int off_t = uni(win[WIN + 1 + t - wlo]);
+    const int A_n = uni(t >= 1 ? win[t - 1 - wlo] : 0);
+    const int off_n = uni(t >= 1 ? win[WIN + 1 + t - 1 - wlo] : 0);
+    const int off_pn = uni(t >= 2 ? win[WIN + 1 + t - 2 - wlo] : 0);
 #pragma unroll
     for (int mt = 0; mt < MRT_MAX; ++mt) {
       if (mt >= a.MRT) continue;
@@ -518,8 +546,11 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
         fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);
         continue;
       }
+      unsigned* flags = a.flags + (grp * a.MRT + mt) * 32;
+      char* slot = ring_tile(a, t & 1, grp, mt);
       const bool act = cellt && r0 + crow < A_t;
       // phase 1
+      float dz[4] = {0.f, 0.f, 0.f, 0.f};
       if (act) {
         const float dht = dh[mt] + pv[mt][6];
         const float ig = pv[mt][0], fg = pv[mt][1], gg = pv[mt][2], og = pv[mt][3];
@@ -527,25 +558,27 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
         const float tc = tanhf_(c);
         const float d_o = dht * tc;
         const float dct = dc[mt] + dht * og * (1.f - tc * tc);
-        float dz[4];
         dz[0] = dct * gg * (ig * (1.f - ig));
         dz[1] = dct * cp * (fg * (1.f - fg));
         dz[2] = dct * ig * (1.f - gg * gg);
         dz[3] = d_o * (og * (1.f - og));
         dc[mt] = dct * fg;
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *reinterpret_cast<T*>(slot + ((g * P + rank) << 10) + rbo) = Op<T>::from_f32(dz[g]);
+      }
+      publish(flags + rank, (unsigned)(T_eff - t));
+      if (act) {
         T* dzr = DZ + (long)(off_t + r0 + crow) * G4 + ju;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          dzr[(long)g * H] = to_exchange<T>(dz[g]);
+          dzr[(long)g * H] = Op<T>::from_f32(dz[g]);
           dbacc[g] += dz[g];
         }
       }
       // phase 2
-      const int nrow = min(16, A_t - r0);                   // running rows of the tile
-      const __amdgpu_buffer_rsrc_t rs =
-          make_rsrc(DZ + (long)(off_t + r0) * G4, (unsigned)(nrow * G4 * (long)sizeof(T)));
-      const unsigned aoff = (unsigned)((l16 * G4 + (ks0 * 4 + q) * KPC) * (long)sizeof(T));
-      const int nks = ks1 - ks0;                            // k-steps of this wave
+      wait_flags(a, flags, ks0, nks < 64 ? nks : 64, P, (unsigned)(T_eff - t));
+      const __amdgpu_buffer_rsrc_t rs = make_rsrc(slot, (unsigned)(a.ring_ks << 10));
       f32x4 acc[NCT];
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -554,38 +587,12 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
         uint4 av[KB];
 #pragma unroll
         for (int i = 0; i < KB; ++i)
-          av[i] = b0 + i < nks ? ld_chunk_l2(rs, aoff + (b0 + i) * CB) : zero4();
+          av[i] = ld_chunk_l2(rs, b0 + i < nks ? (unsigned)(((ks0 + b0 + i) << 10) + lane * 16) : kOOB);
         if (b0 + KB >= KSW) fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);   // next step's pops
-        unsigned todo = 0;
-#pragma unroll
-        for (int i = 0; i < KB; ++i)
-          if (b0 + i < nks && pending_chunk<T>(av[i])) todo |= 1u << i;
-        if (todo) {
-          const unsigned long long t0 = wall_clock64();
-          unsigned polls = 0;
-          while (todo) {
-            __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-            for (int i = 0; i < KB; ++i) {
-              if (todo & (1u << i)) {
-                av[i] = ld_chunk_l2(rs, aoff + (b0 + i) * CB);
-                if (!pending_chunk<T>(av[i])) todo &= ~(1u << i);
-              }
-            }
-            if ((++polls & 255u) == 0) {
-              if (__hip_atomic_load(a.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
-              if (wall_clock64() - t0 > a.limit) {
-                __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(a.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                break;
-              }
-            }
-          }
-        }
 #pragma unroll
         for (int i = 0; i < KB; ++i) {
           const int ii = b0 + i;
-          if (ii < KSW && ks0 + ii < ks1) {
+          if (ii < KSW && ii < nks) {
 #pragma unroll
             for (int ct = 0; ct < NCT; ++ct) {
               const uint4 bv = ii < KSR ? wr[ct][ii < KSR ? ii : 0]
@@ -595,8 +602,8 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
           }
         }
       }
-      // partial products -> red once the previous tile's sums have been read
-      __syncthreads();
+      // partial products -> red (the previous tile's sums were read before
+      // this step's publish barrier)
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
@@ -633,50 +640,71 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   }
 }
 
-// h0 rows in length order, in operand type: out[r, :] = op(h0[perm[r], :])
-// (zeros when h0 is NULL).  The forward loop reads it as h_{-1}.
+// Forward loop set-up: h0 rows (length order, operand type) into ring slot 1
+// of every row tile in the consumers' lane order (the loop reads it as
+// h_{-1}), and the launch's flags to zero.  One element per thread:
+//   f = (((x * MRT + mt) * KS + ks) * 64 + l) * KPC + e
+//   row r = (x + 8 mt) * 16 + l % 16, unit u = ks * 4 KPC + (l / 16) * KPC + e.
 template <typename T>
-__global__ __launch_bounds__(256) void h0_sorted_kernel(const float* __restrict__ h0,
-                                                        const int* __restrict__ perm, int B, int H,
-                                                        T* __restrict__ out) {
-  const long n = (long)B * H;
-  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
-    const int r = (int)(i / H), j = (int)(i - (long)r * H);
-    out[i] = Op<T>::from_f32(h0 ? h0[(long)perm[r] * H + j] : 0.f);
+__global__ __launch_bounds__(256) void x_prepare_fwd_kernel(const float* __restrict__ h0,
+                                                            const int* __restrict__ perm, int B, int H,
+                                                            int MRT, int ring_ks, void* ring,
+                                                            unsigned* flags, int nflags) {
+  constexpr int KPC = Op<T>::kPerChunk;
+  const int KS = H / (4 * KPC);
+  const long n = 8L * MRT * KS * 64 * KPC;
+  T* slot1 = reinterpret_cast<T*>(reinterpret_cast<char*>(ring) + ((long)8 * MRT * ring_ks << 10));
+  for (long f = blockIdx.x * 256L + threadIdx.x; f < n; f += gridDim.x * 256L) {
+    const int e = (int)(f % KPC);
+    const int l = (int)((f / KPC) % 64);
+    const int ks = (int)((f / (64 * KPC)) % KS);
+    const int tile = (int)(f / (64L * KPC * KS));
+    const int x = tile / MRT, mt = tile - x * MRT;
+    const int r = (x + 8 * mt) * 16 + (l & 15);
+    const int u = ks * 4 * KPC + (l >> 4) * KPC + e;
+    const float v = (h0 && r < B) ? h0[(long)perm[r] * H + u] : 0.f;
+    // block ks of tile `tile` in slot 1 (tiles are ring_ks blocks apart)
+    slot1[(((long)tile * ring_ks + ks) * 64 + l) * KPC + e] = Op<T>::from_f32(v);
   }
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < nflags; i += gridDim.x * 256L) flags[i] = 0u;
+}
+
+__global__ __launch_bounds__(256) void zero_u32_kernel(unsigned* p, int n) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
 }
 
 template <typename T>
-hipError_t launch_h0_sorted(const float* h0, const int* perm, int B, int H, void* out,
-                            hipStream_t s) {
-  long blocks = ((long)B * H + 255) / 256;
+hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, int mrt, int ring_ks,
+                                void* ring, unsigned* flags, int nflags, hipStream_t s) {
+  constexpr int KPC = Op<T>::kPerChunk;
+  const long n = 8L * mrt * (H / (4 * KPC)) * 64 * KPC;
+  long blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(h0_sorted_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, h0, perm, B, H,
-                     reinterpret_cast<T*>(out));
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(x_prepare_fwd_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, h0, perm, B, H, mrt,
+                     ring_ks, ring, flags, nflags);
   return hipGetLastError();
 }
-template hipError_t launch_h0_sorted<float>(const float*, const int*, int, int, void*, hipStream_t);
-template hipError_t launch_h0_sorted<bf16_t>(const float*, const int*, int, int, void*, hipStream_t);
+template hipError_t launch_x_prepare_fwd<float>(const float*, const int*, int, int, int, int, void*,
+                                                unsigned*, int, hipStream_t);
+template hipError_t launch_x_prepare_fwd<bf16_t>(const float*, const int*, int, int, int, int, void*,
+                                                 unsigned*, int, hipStream_t);
 
-// Fill rows [0, total) of a compact array of `row_bytes`-byte rows with the
-// all-ones pattern.  row_bytes % 16 == 0.
-__global__ __launch_bounds__(256) void fill_pending_kernel(uint4* base, long row_chunks,
-                                                           const int* meta) {
-  const long n = (long)meta[1] * row_chunks;
-  const uint4 ones = make_uint4(~0u, ~0u, ~0u, ~0u);
-  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) base[i] = ones;
+hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s) {
+  int blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(zero_u32_kernel, dim3(blocks), dim3(256), 0, s, p, n);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------ launchers
-namespace {
-
-}  // namespace
 
 // Kernel for a (dtype, H class, row tiles per XCD) combination.
 //   bf16: HJ = 32 units, forward NCT 8, KSW = H/256; backward NCT 2, KSW = H/64.
 //   f32:  HJ = 16 units, forward NCT 4, KSW = H/128; backward NCT 1, KSW = H/32.
 // hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
-// row tiles per XCD.  The weight slice is held entirely in registers.
+// row tiles per XCD.
 namespace {
 template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT>
 XKernels x_make() {
@@ -734,17 +762,6 @@ hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hip
   XLoopArgs copy = a;
   void* kargs[] = {&copy};
   return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(XNT), kargs, (unsigned)lds, s);
-}
-
-hipError_t launch_fill_pending(void* base, long row_bytes, const int* meta, long cap_rows,
-                               hipStream_t s) {
-  const long chunks = cap_rows * (row_bytes / 16);
-  long blocks = (chunks + 255) / 256;
-  if (blocks > 8192) blocks = 8192;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(fill_pending_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
-                     reinterpret_cast<uint4*>(base), row_bytes / 16, meta);
-  return hipGetLastError();
 }
 
 }  // namespace ll
