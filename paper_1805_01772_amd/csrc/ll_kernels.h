@@ -144,6 +144,15 @@ struct XLoopArgs {
   int* abort_flag;
   int* err;
   unsigned long long limit;
+  // steps of this launch: [t_begin, min(t_end, T_eff)) (the gradient loop runs
+  // them in descending order); the loop state enters through h0/c0 (dhT/dcT)
+  // and leaves through hT/cT (dh0/dc0)
+  int t_begin, t_end;
+  // stack ring: row of (step t, compact index r) is
+  //   (((t / chunk_steps) % nslots) * chunk_steps + t % chunk_steps) * B + r
+  int chunk_steps, nslots;
+  float* db_state;        // backward: per-thread db sums carried between launches (NULL: none)
+  int db_resume;          // backward: 1 = start from db_state
 };
 
 struct XKernels {
@@ -160,7 +169,7 @@ hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hip
 // h0 rows into ring slot 1 (consumer lane order) and the launch's flags to zero.
 template <typename T>
 hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, int mrt, int ring_ks,
-                                void* ring, unsigned* flags, int nflags, hipStream_t s);
+                                int slot, void* ring, unsigned* flags, int nflags, hipStream_t s);
 hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s);
 
 hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,

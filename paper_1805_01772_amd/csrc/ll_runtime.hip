@@ -90,7 +90,19 @@ struct ll_plan {
   void* HPT = nullptr;
   float* dyc = nullptr;
   void* xring = nullptr;       // XCD-local loops: exchange ring
-  unsigned* xflags = nullptr;  // XCD-local loops: per-member step flags [8][MRT][32]
+  unsigned* xflags = nullptr;  // XCD-local loops: [8] rank counters, then step flags [8][MRT][32]
+  int xflag_words = 0;
+  // stack spill (XCD-local loops only): device ring of nslots chunks of
+  // chunk_steps steps per layer, pinned host copy of every chunk
+  bool spill = false;
+  int chunk_steps = 0, nslots = 1, nchunks = 1;
+  long slot_floats = 0;
+  float* host_stack[2] = {nullptr, nullptr};
+  hipStream_t cstream = nullptr;
+  hipEvent_t ev_compute = nullptr;
+  std::vector<hipEvent_t> ev_d2h, ev_h2d;   // per (layer, slot)
+  float* carry = nullptr;      // [4][B, H]: h, c (forward) / dh, dc (backward) between chunks
+  float* db_state = nullptr;   // per-thread db sums between backward chunks
   float* db_part = nullptr;
   float* ws = nullptr;
   long ws_floats = 0;
@@ -169,9 +181,17 @@ void drain_timing(ll_plan* p) {
 void free_plan_memory(ll_plan* p) {
   void* ptrs[] = {p->perm, p->active, p->off, p->rowmap, p->meta, p->WT[0], p->WT[1], p->Zx,
                   p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT, p->HPT,
-                  p->dyc, p->xring, p->xflags, p->db_part, p->ws};
+                  p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state};
   for (void* q : ptrs)
-    if (q) hipFree(q);
+    if (q) (void)hipFree(q);
+  for (float* h : p->host_stack)
+    if (h) (void)hipHostFree(h);
+  for (hipEvent_t e : p->ev_d2h)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : p->ev_h2d)
+    if (e) (void)hipEventDestroy(e);
+  if (p->ev_compute) (void)hipEventDestroy(p->ev_compute);
+  if (p->cstream) (void)hipStreamDestroy(p->cstream);
 }
 
 ll_status dalloc(void** out, size_t bytes, const char* what) {
@@ -234,7 +254,6 @@ ll_status validate_desc(const ll_desc* d) {
   if (d->I % ialign)
     return fail(LL_EUNSUPPORTED, "I = %d must be a multiple of %d for this dtype", d->I, ialign);
   if (d->B > 4096) return fail(LL_EUNSUPPORTED, "B = %d exceeds 4096", d->B);
-  if (d->spill) return fail(LL_EUNSUPPORTED, "spill is not available in this build");
   return LL_OK;
 }
 
@@ -338,6 +357,24 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     }
   }
 
+  // Stack spill (swapping of the saved values to host memory while the loop
+  // runs): the XCD-local loops run one launch per chunk of steps, and the
+  // stack becomes a device ring of nslots chunks.
+  if (desc->spill) {
+    if (!p->xmode) {
+      delete p;
+      return fail(LL_EUNSUPPORTED, "spill needs the XCD-local loops (H = %d, B = %d do not fit them)",
+                  H, B);
+    }
+    p->spill = true;
+    p->chunk_steps = std::min(desc->T_max, desc->spill_chunk_steps > 0 ? desc->spill_chunk_steps : 32);
+    p->nchunks = (desc->T_max + p->chunk_steps - 1) / p->chunk_steps;
+    p->slot_floats = (long)p->chunk_steps * B * 5 * H;
+    const long slot_bytes = p->slot_floats * (long)sizeof(float);
+    long r = desc->device_stack_budget_bytes > 0 ? desc->device_stack_budget_bytes / slot_bytes : 4;
+    p->nslots = (int)std::max(3L, std::min(r, (long)p->nchunks));
+  }
+
   // dW split-K: enough work-groups to cover the chip.
   for (int w = 0; w < 2; ++w) {
     const int M = w == 0 ? desc->I : H;
@@ -375,7 +412,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->meta, sizeof(int) * ll::META_INTS, "meta");
   for (int l = 0; l < L; ++l) {
     ALLOC(p->WT[l], es * 4 * H * (in_width(p, l) + H), "transposed W");
-    ALLOC(p->stack[l], sizeof(float) * cap * 5 * H, "stack");
+    ALLOC(p->stack[l], sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * 5 * H), "stack");
     ALLOC(p->HH[l], es * cap * H, "h history");
   }
   ALLOC(p->Zx, sizeof(float) * cap * 4 * H, "input projection");
@@ -388,7 +425,12 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     // two slots x 8 XCDs x row tiles x (4H / k-step) blocks of 1 KB
     const long ks_b = 4L * H * (long)es / 64;
     ALLOC(p->xring, 2L * 8 * p->xMRT * ks_b * 1024, "exchange ring");
-    ALLOC(p->xflags, sizeof(unsigned) * 8 * p->xMRT * 32, "exchange flags");
+    p->xflag_words = 8 + 8 * p->xMRT * 32;
+    ALLOC(p->xflags, sizeof(unsigned) * p->xflag_words, "exchange flags");
+  }
+  if (p->spill) {
+    ALLOC(p->carry, sizeof(float) * 4 * B * H, "chunk carry");
+    ALLOC(p->db_state, sizeof(float) * 8 * 32 * 512 * 4, "db state");
   }
   ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * 4 * H, "db partials");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
@@ -398,8 +440,33 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     delete p;
     return fail(LL_EHIP, "hipMemset of the plan's meta words failed");
   }
-  p->stack_device_bytes = (int64_t)L * (int64_t)(sizeof(float) * cap * 5 * H + es * cap * H);
-  p->stack_host_bytes = 0;
+  if (p->spill) {
+    const size_t hbytes = sizeof(float) * (size_t)p->nchunks * (size_t)p->slot_floats;
+    for (int l = 0; l < L; ++l) {
+      if (hipHostMalloc(reinterpret_cast<void**>(&p->host_stack[l]), hbytes, hipHostMallocDefault) !=
+          hipSuccess) {
+        free_plan_memory(p);
+        delete p;
+        return fail(LL_ENOMEM, "pinned host allocation of %zu bytes for the spilled stack failed", hbytes);
+      }
+    }
+    bool ok = hipStreamCreateWithFlags(&p->cstream, hipStreamNonBlocking) == hipSuccess &&
+              hipEventCreateWithFlags(&p->ev_compute, hipEventDisableTiming) == hipSuccess;
+    p->ev_d2h.assign((size_t)L * p->nslots, nullptr);
+    p->ev_h2d.assign((size_t)L * p->nslots, nullptr);
+    for (size_t i = 0; ok && i < p->ev_d2h.size(); ++i)
+      ok = hipEventCreateWithFlags(&p->ev_d2h[i], hipEventDisableTiming) == hipSuccess &&
+           hipEventCreateWithFlags(&p->ev_h2d[i], hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
+      free_plan_memory(p);
+      delete p;
+      return fail(LL_EHIP, "creating the spill copy stream and events failed");
+    }
+  }
+  const int64_t stack_dev = p->spill ? (int64_t)sizeof(float) * p->nslots * p->slot_floats
+                                     : (int64_t)sizeof(float) * cap * 5 * H;
+  p->stack_device_bytes = (int64_t)L * (stack_dev + (int64_t)es * cap * H);
+  p->stack_host_bytes = p->spill ? (int64_t)L * (int64_t)sizeof(float) * p->nchunks * p->slot_floats : 0;
   *out = p;
   return LL_OK;
 }
@@ -493,16 +560,12 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     LL_HIP(ll::launch_gemm_nt<T>(g, s));
     tend(p, s, LL_STAGE_INPUT_PROJ, ev);
     if (p->xmode) {
-      ev = tbeg(p, s);
       const int ring_ks = (int)((long)H * p->es / 64);
-      LL_HIP(ll::launch_x_prepare_fwd<T>(h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->xMRT,
-                                         ring_ks, p->xring, p->xflags, 8 * p->xMRT * 32, s));
-      tend(p, s, LL_STAGE_LOOP_SETUP, ev);
-      ev = tbeg(p, s);
       ll::XLoopArgs xa{};
       xa.ring = p->xring;
       xa.ring_ks = ring_ks;
-      xa.flags = p->xflags;
+      xa.rank_ctr = p->xflags;
+      xa.flags = p->xflags + 8;
       xa.B = B;
       xa.H = H;
       xa.T_max = d.T_max;
@@ -517,18 +580,50 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       xa.woff = Il;
       xa.X = p->HH[l];
       xa.Zx = p->Zx;
-      xa.h0 = h0 ? h0 + (long)l * B * H : nullptr;
-      xa.c0 = c0 ? c0 + (long)l * B * H : nullptr;
       xa.stack = save ? p->stack[l] : nullptr;
       xa.y = (l == L - 1) ? y : nullptr;
-      xa.hT = hT + (long)l * B * H;
-      xa.cT = cT + (long)l * B * H;
-      xa.rank_ctr = reinterpret_cast<unsigned*>(p->meta + ll::META_RANK0 + 8 * l);
       xa.abort_flag = p->meta + 3;
       xa.err = p->meta + 2;
       xa.limit = p->barrier_ticks;
-      LL_HIP(ll::x_launch(p->xk.fwd, xa, 256, p->xk.lds_fwd, s));
-      tend(p, s, LL_STAGE_FWD_LOOP, ev);
+      const float* hin = h0 ? h0 + (long)l * B * H : nullptr;
+      const float* cin = c0 ? c0 + (long)l * B * H : nullptr;
+      float* hout = hT + (long)l * B * H;
+      float* cout = cT + (long)l * B * H;
+      // one launch per chunk of steps when the stack spills, else one launch
+      const int C = p->spill ? p->chunk_steps : d.T_max;
+      const int nch = p->spill ? p->nchunks : 1;
+      xa.chunk_steps = C;
+      xa.nslots = p->spill ? p->nslots : 1;
+      for (int k = 0; k < nch; ++k) {
+        const int t0 = k * C, t1 = std::min(d.T_max, t0 + C);
+        const int slot = k % xa.nslots;
+        const bool last = k == nch - 1;
+        ev = tbeg(p, s);
+        // the chunk that used this ring slot before has reached host memory
+        if (p->spill && save && k >= p->nslots) LL_HIP(hipStreamWaitEvent(s, p->ev_d2h[l * p->nslots + slot], 0));
+        LL_HIP(ll::launch_x_prepare_fwd<T>(hin, p->perm, B, H, p->xMRT, ring_ks, (t0 + 1) & 1, p->xring,
+                                           p->xflags, p->xflag_words, s));
+        tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+        ev = tbeg(p, s);
+        xa.t_begin = t0;
+        xa.t_end = t1;
+        xa.h0 = hin;
+        xa.c0 = cin;
+        xa.hT = last ? hout : p->carry;
+        xa.cT = last ? cout : p->carry + (long)B * H;
+        LL_HIP(ll::x_launch(p->xk.fwd, xa, 256, p->xk.lds_fwd, s));
+        tend(p, s, LL_STAGE_FWD_LOOP, ev);
+        if (p->spill && save) {   // swap the chunk out on the copy stream
+          LL_HIP(hipEventRecord(p->ev_compute, s));
+          LL_HIP(hipStreamWaitEvent(p->cstream, p->ev_compute, 0));
+          LL_HIP(hipMemcpyAsync(p->host_stack[l] + (long)k * p->slot_floats,
+                                p->stack[l] + (long)slot * p->slot_floats, sizeof(float) * p->slot_floats,
+                                hipMemcpyDeviceToHost, p->cstream));
+          LL_HIP(hipEventRecord(p->ev_d2h[l * p->nslots + slot], p->cstream));
+        }
+        hin = p->carry;
+        cin = p->carry + (long)B * H;
+      }
       continue;
     }
     ll::FwdLoopArgs a{};
@@ -576,14 +671,11 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
   for (int l = L - 1; l >= 0; --l) {
     const int Il = in_width(p, l);
     if (p->xmode) {
-      ev = tbeg(p, s);
-      LL_HIP(ll::launch_zero_u32(p->xflags, 8 * p->xMRT * 32, s));
-      tend(p, s, LL_STAGE_LOOP_SETUP, ev);
-      ev = tbeg(p, s);
       ll::XLoopArgs xa{};
       xa.ring = p->xring;
       xa.ring_ks = (int)(4L * H * p->es / 64);
-      xa.flags = p->xflags;
+      xa.rank_ctr = p->xflags;
+      xa.flags = p->xflags + 8;
       xa.B = B;
       xa.H = H;
       xa.T_max = d.T_max;
@@ -605,17 +697,56 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
         xa.dy = p->dyc;
         xa.dy_compact = 1;
       }
-      xa.dhT = dhT ? dhT + (long)l * B * H : nullptr;
-      xa.dcT = dcT ? dcT + (long)l * B * H : nullptr;
       xa.db_part = p->db_part;
-      xa.dh0 = dh0 ? dh0 + (long)l * B * H : nullptr;
-      xa.dc0 = dc0 ? dc0 + (long)l * B * H : nullptr;
-      xa.rank_ctr = reinterpret_cast<unsigned*>(p->meta + ll::META_RANK0 + 8 * (2 + l));
       xa.abort_flag = p->meta + 3;
       xa.err = p->meta + 2;
       xa.limit = p->barrier_ticks;
-      LL_HIP(ll::x_launch(p->xk.bwd, xa, 256, p->xk.lds_bwd, s));
-      tend(p, s, LL_STAGE_BWD_LOOP, ev);
+      const float* dhin = dhT ? dhT + (long)l * B * H : nullptr;
+      const float* dcin = dcT ? dcT + (long)l * B * H : nullptr;
+      float* dhout = dh0 ? dh0 + (long)l * B * H : nullptr;
+      float* dcout = dc0 ? dc0 + (long)l * B * H : nullptr;
+      const int C = p->spill ? p->chunk_steps : d.T_max;
+      const int nch = p->spill ? p->nchunks : 1;
+      const int R = p->spill ? p->nslots : 1;
+      xa.chunk_steps = C;
+      xa.nslots = R;
+      xa.db_state = p->spill ? p->db_state : nullptr;
+      // chunks at or above nch - R are still in the ring after the forward; a
+      // chunk j below is swapped in after the launch of chunk j + R (the last
+      // use of its slot) and waited for before the launches of j + 1 (which
+      // reads c_{t-1} from it) and j
+      auto wait_loaded = [&](int j) -> hipError_t {
+        if (!p->spill || j < 0 || j >= nch - R) return hipSuccess;
+        return hipStreamWaitEvent(s, p->ev_h2d[l * R + j % R], 0);
+      };
+      for (int k = nch - 1; k >= 0; --k) {
+        const int t0 = k * C, t1 = std::min(d.T_max, t0 + C);
+        const bool first = k == nch - 1, last = k == 0;
+        ev = tbeg(p, s);
+        LL_HIP(wait_loaded(k));
+        LL_HIP(wait_loaded(k - 1));
+        LL_HIP(ll::launch_zero_u32(p->xflags, p->xflag_words, s));
+        tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+        ev = tbeg(p, s);
+        xa.t_begin = t0;
+        xa.t_end = t1;
+        xa.db_resume = first ? 0 : 1;
+        xa.dhT = first ? dhin : p->carry + 2L * B * H;
+        xa.dcT = first ? dcin : p->carry + 3L * B * H;
+        xa.dh0 = last ? dhout : p->carry + 2L * B * H;
+        xa.dc0 = last ? dcout : p->carry + 3L * B * H;
+        LL_HIP(ll::x_launch(p->xk.bwd, xa, 256, p->xk.lds_bwd, s));
+        tend(p, s, LL_STAGE_BWD_LOOP, ev);
+        const int j = k - R;   // swap chunk j into the slot chunk k leaves
+        if (p->spill && j >= 0) {
+          LL_HIP(hipEventRecord(p->ev_compute, s));
+          LL_HIP(hipStreamWaitEvent(p->cstream, p->ev_compute, 0));
+          LL_HIP(hipMemcpyAsync(p->stack[l] + (long)(j % R) * p->slot_floats,
+                                p->host_stack[l] + (long)j * p->slot_floats, sizeof(float) * p->slot_floats,
+                                hipMemcpyHostToDevice, p->cstream));
+          LL_HIP(hipEventRecord(p->ev_h2d[l * R + j % R], p->cstream));
+        }
+      }
     }
     ll::BwdLoopArgs a{};
     a.B = B;

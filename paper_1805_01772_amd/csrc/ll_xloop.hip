@@ -154,6 +154,12 @@ __device__ __forceinline__ void load_window(const XLoopArgs& a, int* win, int lo
   __syncthreads();
 }
 
+// Stack row of (step t, compact index r) in the stack ring.
+__device__ __forceinline__ long stack_row(const XLoopArgs& a, int t, int r) {
+  const int k = t / a.chunk_steps;
+  return ((long)((k % a.nslots) * a.chunk_steps + (t - k * a.chunk_steps)) * a.B + r);
+}
+
 // Ring slot of row tile mt: ring_ks blocks of 1 KB.
 __device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp, int mt) {
   return reinterpret_cast<char*>(a.ring) + ((long)((slot * 8 + grp) * a.MRT + mt) * a.ring_ks << 10);
@@ -257,19 +263,23 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   }
 
   const int T_eff = uni(a.meta[0]);
-  int wlo = 0;
-  load_window(a, win, 0);
+  const int t0 = a.t_begin, t1 = min(a.t_end, T_eff);
+  int wlo = t0 > 0 ? t0 - 1 : 0;
+  load_window(a, win, wlo);
   // input projections of the cell thread's (row, unit), one step ahead
   float zf[MRT_MAX][4];
+  {
+    const int A0 = t0 < t1 ? win[t0 - wlo] : 0, off0 = win[WIN + 1 + t0 - wlo];
 #pragma unroll
-  for (int mt = 0; mt < MRT_MAX; ++mt) {
-    const int r = (grp + 8 * mt) * 16 + crow;
+    for (int mt = 0; mt < MRT_MAX; ++mt) {
+      const int r = (grp + 8 * mt) * 16 + crow;
 #pragma unroll
-    for (int g = 0; g < 4; ++g)
-      zf[mt][g] = (cellt && T_eff > 0 && mt < a.MRT && r < win[0]) ? a.Zx[(long)r * G4 + (long)g * H + ju] : 0.f;
+      for (int g = 0; g < 4; ++g)
+        zf[mt][g] = (cellt && mt < a.MRT && r < A0) ? a.Zx[(long)(off0 + r) * G4 + (long)g * H + ju] : 0.f;
+    }
   }
 
-  for (int t = 0; t < T_eff; ++t) {
+  for (int t = t0; t < t1; ++t) {
     if (t + 1 > wlo + WIN) {   // the window keeps step t-1 as well
       wlo = t - 1;
       load_window(a, win, wlo);
@@ -288,8 +298,9 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
         continue;
       }
       unsigned* flags = a.flags + (grp * a.MRT + mt) * 32;
-      // 1. h_{t-1} of this wave's k-steps (for t = 0 the ring holds h0)
-      if (t > 0) wait_flags(a, flags, ks0, nks, a.P, (unsigned)(t + 1));
+      // 1. h_{t-1} of this wave's k-steps (for the launch's first step the
+      //    ring holds the entering state)
+      if (t > t0) wait_flags(a, flags, ks0, nks, a.P, (unsigned)(t + 1));
       const __amdgpu_buffer_rsrc_t rs = make_rsrc(ring_tile(a, (t + 1) & 1, grp, mt), (unsigned)(a.ring_ks << 10));
       uint4 av[KSW];
 #pragma unroll
@@ -362,7 +373,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
         const long cr = off_t + r;
         HH[cr * H + ju] = Op<T>::from_f32(hn);
         if (a.stack) {
-          float* st = a.stack + cr * H5 + ju;
+          float* st = a.stack + stack_row(a, t, r) * H5 + ju;
           st[0] = ig;
           st[H] = fg;
           st[2 * H] = gg;
@@ -385,7 +396,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
       a.hT[(long)b * H + ju] = hs[mt];
       a.cT[(long)b * H + ju] = cs[mt];
       if (a.y)
-        for (int t = T_eff; t < a.T_max; ++t) a.y[((long)t * B + b) * H + ju] = 0.f;
+        for (int t = max(T_eff, t0); t < a.t_end; ++t) a.y[((long)t * B + b) * H + ju] = 0.f;
     }
   }
 }
@@ -483,6 +494,11 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     }
   }
   float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
+  float* dbst = a.db_state ? a.db_state + ((long)(grp * 32 + rank) * XNT + tid) * 4 : nullptr;
+  if (dbst && a.db_resume) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) dbacc[g] = dbst[g];
+  }
 
   // pops of (step tt, tile mt) for this thread: i, f, g, o, c_t, c_{t-1}, dy;
   // zeros for rows not running at tt (every read is issued, out of range)
@@ -491,13 +507,14 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     const int nr = tt >= 0 ? max(0, min(16, A - r0)) : 0;
     const bool ok = cellt && crow < nr;
     const int b = sperm[mt * 16 + crow];
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.stack + (long)(off + r0) * H5, (unsigned)(nr * H5 * 4));
+    const int ts = max(tt, 0);
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.stack + stack_row(a, ts, r0) * H5, (unsigned)(nr * H5 * 4));
     const unsigned so = ok ? (unsigned)((crow * H5 + ju) * 4) : kOOB;
 #pragma unroll
     for (int c = 0; c < 5; ++c) v[c] = ld_f32(rs, so + c * H * 4);
     if (tt > 0) {
       const __amdgpu_buffer_rsrc_t rp2 =
-          make_rsrc(a.stack + (long)(offp + r0) * H5 + 4L * H, (unsigned)(nr * H5 * 4));
+          make_rsrc(a.stack + stack_row(a, tt - 1, r0) * H5 + 4L * H, (unsigned)(nr * H5 * 4));
       v[5] = ld_f32(rp2, so);
     } else {
       const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.c0, a.c0 ? (unsigned)(B * H * 4) : 0u);
@@ -508,17 +525,19 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
       v[6] = ld_f32(rd, ok ? (unsigned)((crow * H + ju) * 4) : kOOB);
     } else {
       const __amdgpu_buffer_rsrc_t rd =
-          make_rsrc(a.dy ? a.dy + (long)max(tt, 0) * B * H : nullptr, a.dy ? (unsigned)(B * H * 4) : 0u);
+          make_rsrc(a.dy ? a.dy + (long)ts * B * H : nullptr, a.dy ? (unsigned)(B * H * 4) : 0u);
       v[6] = ld_f32(rd, ok ? (unsigned)((b * H + ju) * 4) : kOOB);
     }
+    (void)offp;
   };
 
   const int T_eff = uni(a.meta[0]);
-  int wlo = T_eff - 1 - WIN > 0 ? T_eff - 1 - WIN : 0;
+  const int t0 = a.t_begin, t1 = min(a.t_end, T_eff);
+  int wlo = t1 - 1 - WIN > 0 ? t1 - 1 - WIN : 0;
   load_window(a, win, wlo);
   float pv[MRT_MAX][7];
   {
-    const int t = T_eff - 1;
+    const int t = t1 - 1;
     const int A_t = t >= 0 ? win[t - wlo] : 0;
     const int off_t = t >= 0 ? win[WIN + 1 + t - wlo] : 0;
     const int off_p = t >= 1 ? win[WIN + 1 + t - 1 - wlo] : 0;
@@ -527,7 +546,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
       if (mt < a.MRT) fetch(pv[mt], t, mt, A_t, off_t, off_p);
   }
 
-  for (int t = T_eff - 1; t >= 0; --t) {
+  for (int t = t1 - 1; t >= t0; --t) {
     if (t - 2 < wlo && wlo > 0) {
       wlo = t - WIN > 0 ? t - WIN : 0;
       load_window(a, win, wlo);
@@ -625,6 +644,10 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     if (a.dh0) a.dh0[(long)b * H + ju] = dh[mt];
     if (a.dc0) a.dc0[(long)b * H + ju] = dc[mt];
   }
+  if (dbst) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) dbst[g] = dbacc[g];
+  }
   // db partial of this work-group (its rows of this XCD), fixed order
   __syncthreads();
   if (cellt) {
@@ -640,20 +663,21 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   }
 }
 
-// Forward loop set-up: h0 rows (length order, operand type) into ring slot 1
-// of every row tile in the consumers' lane order (the loop reads it as
-// h_{-1}), and the launch's flags to zero.  One element per thread:
+// Forward loop set-up: the entering h rows (length order, operand type) into
+// ring slot `slot` of every row tile in the consumers' lane order (the
+// launch's first step t0 reads it as h_{t0-1}: slot (t0 + 1) % 2), and the
+// launch's flags to zero.  One element per thread:
 //   f = (((x * MRT + mt) * KS + ks) * 64 + l) * KPC + e
 //   row r = (x + 8 mt) * 16 + l % 16, unit u = ks * 4 KPC + (l / 16) * KPC + e.
 template <typename T>
 __global__ __launch_bounds__(256) void x_prepare_fwd_kernel(const float* __restrict__ h0,
                                                             const int* __restrict__ perm, int B, int H,
-                                                            int MRT, int ring_ks, void* ring,
+                                                            int MRT, int ring_ks, int slot, void* ring,
                                                             unsigned* flags, int nflags) {
   constexpr int KPC = Op<T>::kPerChunk;
   const int KS = H / (4 * KPC);
   const long n = 8L * MRT * KS * 64 * KPC;
-  T* slot1 = reinterpret_cast<T*>(reinterpret_cast<char*>(ring) + ((long)8 * MRT * ring_ks << 10));
+  T* slot1 = reinterpret_cast<T*>(reinterpret_cast<char*>(ring) + ((long)slot * 8 * MRT * ring_ks << 10));
   for (long f = blockIdx.x * 256L + threadIdx.x; f < n; f += gridDim.x * 256L) {
     const int e = (int)(f % KPC);
     const int l = (int)((f / KPC) % 64);
@@ -675,19 +699,19 @@ __global__ __launch_bounds__(256) void zero_u32_kernel(unsigned* p, int n) {
 
 template <typename T>
 hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, int mrt, int ring_ks,
-                                void* ring, unsigned* flags, int nflags, hipStream_t s) {
+                                int slot, void* ring, unsigned* flags, int nflags, hipStream_t s) {
   constexpr int KPC = Op<T>::kPerChunk;
   const long n = 8L * mrt * (H / (4 * KPC)) * 64 * KPC;
   long blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(x_prepare_fwd_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, h0, perm, B, H, mrt,
-                     ring_ks, ring, flags, nflags);
+                     ring_ks, slot, ring, flags, nflags);
   return hipGetLastError();
 }
-template hipError_t launch_x_prepare_fwd<float>(const float*, const int*, int, int, int, int, void*,
+template hipError_t launch_x_prepare_fwd<float>(const float*, const int*, int, int, int, int, int, void*,
                                                 unsigned*, int, hipStream_t);
-template hipError_t launch_x_prepare_fwd<bf16_t>(const float*, const int*, int, int, int, int, void*,
+template hipError_t launch_x_prepare_fwd<bf16_t>(const float*, const int*, int, int, int, int, int, void*,
                                                  unsigned*, int, hipStream_t);
 
 hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s) {

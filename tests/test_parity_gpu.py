@@ -299,3 +299,80 @@ def test_two_layer_full_size_sampled_rows():
     errs, bad = compare(got, ref, TOL[w.dtype], keys=("y", "hT", "cT", "dx", "dh0", "dc0"))
     say(f"    errors {errs}")
     assert not bad, bad
+
+
+# ----------------------------------------------------------- stack spill
+def _run_plan(w, inp, **plan_kw):
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
+    plan = dc.plan(**plan_kw)
+    dev_bytes, host_bytes = plan.stack_bytes()
+    dc.fwd(plan)
+    dc.bwd(plan)
+    err = plan.status_sync()
+    res = dc.results()
+    plan.close()
+    return res, err, dev_bytes, host_bytes
+
+
+SPILL_CASES = [
+    # (workload, chunk steps, ring slots)
+    (W("spill_f32_b20_i24_h64_t50", B=20, I=24, H=64, T_max=50, dtype="f32", len_lo=0, len_hi=50,
+       w_scale=0.3, random_state=True, seed=21), 8, 3),
+    (W("spill_bf16_b40_i32_h128_t37", B=40, I=32, H=128, T_max=37, dtype="bf16", len_lo=1, len_hi=37,
+       w_scale=0.3, random_state=True, seed=22), 5, 4),
+    (W("spill_f32_2layer_b17_i16_h32_t29", B=17, I=16, H=32, T_max=29, dtype="f32", layers=2,
+       len_lo=0, len_hi=29, w_scale=0.3, random_state=True, seed=23), 4, 3),
+    (W("spill_f32_resident_b9_i8_h32_t12", B=9, I=8, H=32, T_max=12, dtype="f32", len_lo=0,
+       len_hi=12, w_scale=0.3, random_state=True, seed=24), 6, 3),
+]
+
+
+@pytest.mark.parametrize("w,C,R", SPILL_CASES, ids=[c[0].name for c in SPILL_CASES])
+def test_spill_matches_resident_stack_bitwise(w, C, R):
+    """Swapping the stack to host memory in chunks changes no result bit."""
+    say(f"[spill] {w.name} C={C} R={R}")
+    inp = wl.generate(w)
+    ref, err0, dev0, host0 = _run_plan(w, inp)
+    slot_bytes = C * w.B * 5 * w.H * 4
+    got, err1, dev1, host1 = _run_plan(w, inp, spill=1, spill_chunk_steps=C,
+                                       device_stack_budget_bytes=R * slot_bytes)
+    assert err0 == 0 and err1 == 0
+    assert host0 == 0 and host1 > 0
+    nch = -(-w.T_max // C)
+    assert host1 == w.layers * nch * slot_bytes
+    for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+        assert np.array_equal(got[k], ref[k]), k
+    for a, b in zip(got["dW"] + got["dbias"], ref["dW"] + ref["dbias"]):
+        assert np.array_equal(a, b)
+    # and the resident run is right
+    errs, bad = compare(ref, oracle_reference(inp, w.layers, w.dtype), TOL[w.dtype])
+    assert not bad, bad
+
+
+def test_spill_long_sequences():
+    """2000-step sequences, the stack swapped through a ring of 4 chunks."""
+    w = wl.LONG_SPILL
+    say(f"[spill] {w.name}")
+    inp = wl.generate(w)
+    C = 32
+    slot_bytes = C * w.B * 5 * w.H * 4
+    got, err1, dev1, host1 = _run_plan(w, inp, spill=1, spill_chunk_steps=C,
+                                       device_stack_budget_bytes=4 * slot_bytes)
+    assert err1 == 0
+    ref, err0, dev0, _ = _run_plan(w, inp)
+    assert err0 == 0
+    say(f"    device stack bytes {dev1} (resident {dev0}), host {host1}")
+    assert dev1 < dev0 and host1 >= w.T_max * w.B * 5 * w.H * 4
+    for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+        assert np.array_equal(got[k], ref[k]), k
+    assert all(np.array_equal(a, b) for a, b in zip(got["dW"], ref["dW"]))
+    # sampled rows against the oracle
+    rows = [0, 31, 63]
+    sub = {k: (v[:, rows].copy() if k in ("x", "dy", "h0", "c0", "dhT", "dcT") else v)
+           for k, v in inp.items()}
+    sub["seq_len"] = inp["seq_len"][rows].copy()
+    ref_o = oracle_reference(sub, w.layers, w.dtype)
+    gsub = {k: got[k][:, rows] for k in ("y", "hT", "cT", "dx", "dh0", "dc0")}
+    errs, bad = compare(gsub, ref_o, TOL[w.dtype], keys=("y", "hT", "cT", "dx", "dh0", "dc0"))
+    say(f"    errors {errs}")
+    assert not bad, bad
