@@ -162,33 +162,51 @@ def main():
     sum_len = int(inp["seq_len"].sum())
     T_eff = int(inp["seq_len"].max())
     dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, device="cuda:0")
-    plan = dc.plan()
-    for _ in range(args.warmup):
-        dc.fwd(plan)
-        dc.bwd(plan)
-    torch.cuda.synchronize()
-    if plan.status_sync() != 0:
-        raise RuntimeError("device error during warmup")
-    plan.set_timing(True)
-    stream = torch.cuda.current_stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        dc.fwd(plan)
-        dc.bwd(plan)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_ms = ev0.elapsed_time(ev1)
-    stages = plan.read_timing()
-    plan.set_timing(False)
-    err = plan.status_sync()
-    if err:
-        raise RuntimeError(f"device error word {err}")
-    geom = plan.geometry()
-    plan.close()
+    plan_kw = {}
+    if w.spill:   # stack swapped to pinned host memory through a ring of 4 chunks of 32 steps
+        C = 32
+        plan_kw = dict(spill=1, spill_chunk_steps=C,
+                       device_stack_budget_bytes=4 * C * w.B * 5 * w.H * 4)
+
+    def timed(kw, timing):
+        plan = dc.plan(**kw)
+        for _ in range(args.warmup):
+            dc.fwd(plan)
+            dc.bwd(plan)
+        torch.cuda.synchronize()
+        if plan.status_sync() != 0:
+            raise RuntimeError("device error during warmup")
+        plan.set_timing(timing)
+        stream = torch.cuda.current_stream()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            dc.fwd(plan)
+            dc.bwd(plan)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        stages = plan.read_timing()
+        plan.set_timing(False)
+        err = plan.status_sync()
+        if err:
+            raise RuntimeError(f"device error word {err}")
+        geom, sbytes = plan.geometry(), plan.stack_bytes()
+        plan.close()
+        return ev0.elapsed_time(ev1), wall, stages, geom, sbytes
+
+    gpu_ms, wall, stages, geom, sbytes = timed(plan_kw, True)
+    spill = None
+    if w.spill:
+        res_ms = timed({}, False)[0]
+        nch = -(-w.T_max // C)
+        moved = sbytes[1] + sbytes[1] * max(nch - 4, 0) / nch   # out: every chunk, in: all but the resident ones
+        spill = {"chunk_steps": C, "ring_slots": 4, "device_stack_bytes": sbytes[0],
+                 "host_stack_bytes": sbytes[1], "ms_per_step_resident": res_ms / args.steps,
+                 "overlap_efficiency": (res_ms / args.steps) / (gpu_ms / args.steps),
+                 "host_link_GBps": moved / (gpu_ms / args.steps / 1e3) / 1e9}
 
     ms_per_step = gpu_ms / args.steps
     value = sum_len / (ms_per_step / 1e3)
@@ -227,6 +245,8 @@ def main():
                      "per_launch_ms": per_launch[dom],
                      "algorithmic_flops_per_launch": sflops[dom]},
     }
+    if spill:
+        out["spill"] = spill
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -68,7 +68,8 @@ typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
 
 /* Device error word bits (ll_status_sync). */
 #define LL_DEVERR_SEQ_LEN 1      /* some seq_len[b] < 0 or > T_max          */
-#define LL_DEVERR_BARRIER 2      /* a grid-barrier wait exceeded its bound  */
+/* a loop wait (grid barrier or exchange flag) exceeded its bound */
+#define LL_DEVERR_BARRIER 2
 
 /*
  * Problem description.
@@ -76,12 +77,17 @@ typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
  *   Supported tiling: H % 32 == 0, I % 8 == 0 (bf16) or I % 4 == 0 (f32),
  *   B <= 4096; otherwise ll_plan_create returns LL_EUNSUPPORTED.
  *   spill = 0: the stack lives in device memory (T_max*B rows capacity).
- *   spill = 1: the stack is swapped to pinned host memory in chunks of
- *     spill_chunk_steps time steps (0 = library default) on a device-to-host
- *     copy stream while the forward runs, and prefetched back on a
- *     host-to-device stream ahead of the gradient loop (Section 5.3).
- *     device_stack_budget_bytes bounds the device ring that stages the
- *     chunks (0 = the smallest ring that still overlaps, 3 chunks).
+ *   spill = 1: the stack is swapped to pinned host memory (Section 5.3):
+ *     the loops run one launch per chunk of spill_chunk_steps time steps
+ *     (0 = 32; the loop state passes exactly from one launch to the next),
+ *     the stack is a device ring of R chunk slots, each chunk is copied to
+ *     host memory on the plan's copy stream after the forward launch that
+ *     filled it, and copied back ahead of the gradient launches that read
+ *     it.  R = device_stack_budget_bytes / (chunk_steps * B * 5H * 4),
+ *     at least 3 (0 = 4); the results are bitwise those of spill = 0.
+ *     Needs the XCD-local loops (see ll_plan_geometry); otherwise
+ *     ll_plan_create returns LL_EUNSUPPORTED.  The h history, the input
+ *     projections and dz stay in device memory.
  *   reserved must be 0.
  */
 typedef struct {
