@@ -153,6 +153,17 @@ struct XLoopArgs {
   int chunk_steps, nslots;
   float* db_state;        // backward: per-thread db sums carried between launches (NULL: none)
   int db_resume;          // backward: 1 = start from db_state
+  // two-layer wavefront (one launch runs both layers, the upper one a step
+  // behind in the forward direction, ahead in the gradient direction):
+  const void* in_ring;    // upper layer, forward: the lower layer's ring (its h_t is y1_t)
+  const unsigned* in_flags;
+  int in_ks;              // k-steps of the recurrent product taken from in_ring
+  const float* zbias;     // upper layer, forward: bias (there is no hoisted input projection)
+  const unsigned* out_flags;  // lower layer, forward: the upper layer's flags (ring reuse)
+  void* dyx_ring;         // gradient: dy of the lower layer's output, [2][8][MRT][16][H] float
+  unsigned* dyx_flags;    // gradient: per-member flags of dyx_ring ([8][MRT][32])
+  const unsigned* peer_flags;  // gradient: the other layer's step flags
+  const void* Wx;         // upper layer, gradient: W rows of the input part [I_l, 4H]
 };
 
 struct XKernels {
@@ -166,6 +177,12 @@ template <typename T>
 XKernels x_kernels(int hc, int mrt);
 hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd);
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s);
+// Two-layer wavefront: one launch runs both layers (a0 lower, a1 upper);
+// needs 2 H / HJ <= 32 members per XCD.
+template <typename T>
+XKernels x_kernels2(int hc, int mrt);
+hipError_t x_launch2(const void* fn, const XLoopArgs& a0, const XLoopArgs& a1, int nwg, size_t lds,
+                     hipStream_t s);
 // h0 rows into ring slot 1 (consumer lane order) and the launch's flags to zero.
 template <typename T>
 hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, int mrt, int ring_ks,

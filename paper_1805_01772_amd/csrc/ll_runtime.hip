@@ -38,6 +38,12 @@ ll_status fail(ll_status s, const char* fmt, ...) {
       return fail(LL_EHIP, "%s failed: %s", #call, hipGetErrorString(e_));        \
   } while (0)
 
+#define LL_STATUS(call)         \
+  do {                          \
+    ll_status st_ = (call);     \
+    if (st_ != LL_OK) return st_; \
+  } while (0)
+
 enum PlanState { ST_EMPTY = 0, ST_FWD_DONE = 1 };
 
 class DeviceGuard {
@@ -74,6 +80,10 @@ struct ll_plan {
   ll::XKernels xk{};
   int xP = 0;                  // unit blocks per XCD
   int xMRT = 0;                // row tiles per XCD
+  int xhc = 0;                 // forward k-steps per wave
+  // two-layer wavefront: one launch per direction runs both layers
+  bool wave = false;
+  ll::XKernels xk2{};
   // device memory
   int* perm = nullptr;
   int* active = nullptr;
@@ -90,8 +100,14 @@ struct ll_plan {
   void* HPT = nullptr;
   float* dyc = nullptr;
   void* xring = nullptr;       // XCD-local loops: exchange ring
-  unsigned* xflags = nullptr;  // XCD-local loops: [8] rank counters, then step flags [8][MRT][32]
+  // XCD-local loops: [8] rank counters, then step flags [8][MRT][32] (the
+  // wavefront: lower layer, upper layer, dy exchange)
+  unsigned* xflags = nullptr;
   int xflag_words = 0;
+  void* xring2 = nullptr;      // wavefront: the upper layer's exchange ring
+  void* DZ2 = nullptr;         // wavefront: dz of the upper layer
+  float* dyx = nullptr;        // wavefront: dy exchange [2][8][MRT][16][H]
+  float* db_part2 = nullptr;   // wavefront: db partials of the upper layer
   // stack spill (XCD-local loops only): device ring of nslots chunks of
   // chunk_steps steps per layer, pinned host copy of every chunk
   bool spill = false;
@@ -181,7 +197,8 @@ void drain_timing(ll_plan* p) {
 void free_plan_memory(ll_plan* p) {
   void* ptrs[] = {p->perm, p->active, p->off, p->rowmap, p->meta, p->WT[0], p->WT[1], p->Zx,
                   p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT, p->HPT,
-                  p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state};
+                  p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
+                  p->xring2, p->DZ2, p->dyx, p->db_part2};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -349,6 +366,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
             p->xk = xk;
             p->xP = P;
             p->xMRT = mrt;
+            p->xhc = hc;
           } else {
             (void)hipGetLastError();
           }
@@ -373,6 +391,27 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     const long slot_bytes = p->slot_floats * (long)sizeof(float);
     long r = desc->device_stack_budget_bytes > 0 ? desc->device_stack_budget_bytes / slot_bytes : 4;
     p->nslots = (int)std::max(3L, std::min(r, (long)p->nchunks));
+  }
+
+  // Two-layer wavefront: on every XCD, members 0..P-1 run the lower layer
+  // and P..2P-1 the upper one, so both layers' steps overlap in one launch.
+  // LSTMLOOP_WAVEFRONT=off at plan creation runs the layers one after the
+  // other.
+  if (L == 2 && p->xmode && !p->spill && 2 * p->xP <= 32 && p->xhc <= 2) {
+    const char* wf = getenv("LSTMLOOP_WAVEFRONT");
+    if (!(wf && strcmp(wf, "off") == 0)) {
+      ll::XKernels xk2 = p->bf16 ? ll::x_kernels2<bf16_t>(p->xhc, p->xMRT)
+                                 : ll::x_kernels2<float>(p->xhc, p->xMRT);
+      if (xk2.fwd && xk2.bwd && xk2.lds_fwd <= lds_limit && xk2.lds_bwd <= lds_limit) {
+        int of = 0, ob = 0;
+        if (ll::x_setup(xk2, &of, &ob) == hipSuccess && of >= 1 && ob >= 1) {
+          p->wave = true;
+          p->xk2 = xk2;
+        } else {
+          (void)hipGetLastError();
+        }
+      }
+    }
   }
 
   // dW split-K: enough work-groups to cover the chip.
@@ -425,8 +464,14 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     // two slots x 8 XCDs x row tiles x (4H / k-step) blocks of 1 KB
     const long ks_b = 4L * H * (long)es / 64;
     ALLOC(p->xring, 2L * 8 * p->xMRT * ks_b * 1024, "exchange ring");
-    p->xflag_words = 8 + 8 * p->xMRT * 32;
+    p->xflag_words = 8 + (p->wave ? 3 : 1) * 8 * p->xMRT * 32;
     ALLOC(p->xflags, sizeof(unsigned) * p->xflag_words, "exchange flags");
+    if (p->wave) {
+      ALLOC(p->xring2, 2L * 8 * p->xMRT * ks_b * 1024, "exchange ring");
+      ALLOC(p->DZ2, es * cap * 4 * H, "dz");
+      ALLOC(p->dyx, sizeof(float) * 2L * 8 * p->xMRT * 16 * H, "dy exchange");
+      ALLOC(p->db_part2, sizeof(float) * 8 * 4 * H, "db partials");
+    }
   }
   if (p->spill) {
     ALLOC(p->carry, sizeof(float) * 4 * B * H, "chunk carry");
@@ -512,18 +557,124 @@ ll_status ll_plan_stack_bytes(const ll_plan* p, int64_t* dev, int64_t* host) {
 }
 
 ll_status ll_plan_geometry(const ll_plan* p, int32_t* nwg, int32_t* hj, int32_t* rg,
-                           int32_t* xcd_local) {
+                           int32_t* xcd_local, int32_t* wavefront) {
   if (!p) return fail(LL_EINVAL, "plan is NULL");
   if (nwg) *nwg = p->xmode ? 256 : p->geom.nwg;
   if (hj) *hj = p->xmode ? (p->bf16 ? 32 : 16) : p->geom.HJ;
   if (rg) *rg = p->xmode ? 8 : p->geom.RG;
   if (xcd_local) *xcd_local = p->xmode ? 1 : 0;
+  if (wavefront) *wavefront = p->wave ? 1 : 0;
   return LL_OK;
 }
 
 }  // extern "C"
 
 namespace {
+
+// Fields shared by both layers' argument blocks of an XCD-local launch.
+ll::XLoopArgs x_common(const ll_plan* p) {
+  ll::XLoopArgs a{};
+  a.B = p->d.B;
+  a.H = p->d.H;
+  a.T_max = p->d.T_max;
+  a.P = p->xP;
+  a.MRT = p->xMRT;
+  a.meta = p->meta;
+  a.active = p->active;
+  a.off = p->off;
+  a.perm = p->perm;
+  a.rank_ctr = p->xflags;
+  a.abort_flag = p->meta + 3;
+  a.err = p->meta + 2;
+  a.limit = p->barrier_ticks;
+  a.t_begin = 0;
+  a.t_end = p->d.T_max;
+  a.chunk_steps = p->d.T_max;
+  a.nslots = 1;
+  return a;
+}
+
+// Two-layer wavefront, forward: the input projection of layer 0 only (the
+// upper layer multiplies y1_t inside the loop), then one launch in which the
+// upper layer's step t follows the lower layer's step t on every XCD.
+template <typename T>
+ll_status enqueue_fwd_wave(ll_plan* p, hipStream_t s, const void* x, const void* const* W,
+                           const float* const* bias, const float* h0, const float* c0, float* y,
+                           float* hT, float* cT, bool save) {
+  const ll_desc& d = p->d;
+  const int H = d.H, B = d.B, I = d.I;
+  const long BH = (long)B * H;
+  hipEvent_t ev = tbeg(p, s);
+  for (int l = 0; l < 2; ++l) {
+    const int Il = in_width(p, l);
+    LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, 4 * H, 4 * H,
+                                   reinterpret_cast<T*>(p->WT[l]), Il + H, s));
+  }
+  ll::GemmArgs g{};
+  g.A = x;
+  g.lda = I;
+  g.a_rowmap = p->rowmap;
+  g.Bm = p->WT[0];
+  g.ldb = I + H;
+  g.C = p->Zx;
+  g.ldc = 4L * H;
+  g.bias = bias[0];
+  g.M = (int)p->cap;
+  g.M_dev = p->meta + 1;
+  g.N = 4 * H;
+  g.K = I;
+  g.splits = 1;
+  LL_HIP(ll::launch_gemm_nt<T>(g, s));
+  tend(p, s, LL_STAGE_INPUT_PROJ, ev);
+
+  const int ring_ks = (int)((long)H * p->es / 64);
+  unsigned* F0 = p->xflags + 8;
+  unsigned* F1 = F0 + 8L * p->xMRT * 32;
+  ev = tbeg(p, s);
+  LL_HIP(ll::launch_x_prepare_fwd<T>(h0, p->perm, B, H, p->xMRT, ring_ks, 1, p->xring, p->xflags,
+                                     p->xflag_words, s));
+  LL_HIP(ll::launch_x_prepare_fwd<T>(h0 ? h0 + BH : nullptr, p->perm, B, H, p->xMRT, ring_ks, 1,
+                                     p->xring2, nullptr, 0, s));
+  tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+
+  ll::XLoopArgs a0 = x_common(p), a1 = x_common(p);
+  a0.ring = p->xring;
+  a0.ring_ks = ring_ks;
+  a0.flags = F0;
+  a0.W = p->WT[0];
+  a0.ldw = I + H;
+  a0.woff = I;
+  a0.X = p->HH[0];
+  a0.Zx = p->Zx;
+  a0.stack = save ? p->stack[0] : nullptr;
+  a0.h0 = h0;
+  a0.c0 = c0;
+  a0.hT = hT;
+  a0.cT = cT;
+  a0.out_flags = F1;
+
+  a1.ring = p->xring2;
+  a1.ring_ks = ring_ks;
+  a1.flags = F1;
+  a1.W = p->WT[1];
+  a1.ldw = 2 * H;
+  a1.woff = 0;
+  a1.X = p->HH[1];
+  a1.zbias = bias[1];
+  a1.stack = save ? p->stack[1] : nullptr;
+  a1.y = y;
+  a1.h0 = h0 ? h0 + BH : nullptr;
+  a1.c0 = c0 ? c0 + BH : nullptr;
+  a1.hT = hT + BH;
+  a1.cT = cT + BH;
+  a1.in_ring = p->xring;
+  a1.in_flags = F0;
+  a1.in_ks = ring_ks;
+  ev = tbeg(p, s);
+  LL_HIP(ll::x_launch2(p->xk2.fwd, a0, a1, 256, p->xk2.lds_fwd, s));
+  tend(p, s, LL_STAGE_FWD_LOOP, ev);
+  return LL_OK;
+}
 
 template <typename T>
 ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* seq_len,
@@ -536,6 +687,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
   LL_HIP(ll::launch_prep(seq_len, B, d.T_max, p->perm, p->active, p->off, p->rowmap, p->meta,
                          trip, s));
   tend(p, s, LL_STAGE_PREP, ev);
+  if (p->wave) return enqueue_fwd_wave<T>(p, s, x, W, bias, h0, c0, y, hT, cT, save);
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
     ev = tbeg(p, s);
@@ -659,6 +811,164 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
   return LL_OK;
 }
 
+// Products after the gradient loop of layer l: db from the loop's row-group
+// partials, dW = [x_t, h_{t-1}]^T dz_t summed over steps, and, if dx is not
+// NULL, dx_t = dz_t W_x^T (layer 0: time-major [T_max, B, I]; layer 1:
+// compact rows, the gradient of the layer below).  dz: [cap, 4H] compact rows.
+template <typename T>
+ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const float* db_part,
+                       float* dx, float* const* dW, float* const* dbias) {
+  const ll_desc& d = p->d;
+  const int H = d.H, B = d.B;
+  const int Il = in_width(p, l);
+  hipEvent_t ev = nullptr;
+  // db = sum of the row-group partials
+  ev = tbeg(p, s);
+  LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->geom.RG, 4L * H, 4L * H, dbias[l], s));
+  tend(p, s, LL_STAGE_DW, ev);
+  ev = tbeg(p, s);
+  // transposed operands of the dW products (reduction over compact rows)
+  ll::GatherTArgs gt{};
+  gt.B = B;
+  gt.meta = p->meta;
+  gt.rowmap = p->rowmap;
+  gt.off = p->off;
+  gt.perm = p->perm;
+  gt.ldo = (int)p->ldT;
+  gt.in = dz;
+  gt.out = p->DZT;
+  gt.C = 4 * H;
+  gt.mode = 1;
+  LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+  gt.in = l == 0 ? p->x : p->HH[0];
+  gt.out = p->XT;
+  gt.C = Il;
+  gt.mode = l == 0 ? 0 : 1;
+  LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+  gt.in = p->HH[l];
+  gt.out = p->HPT;
+  gt.C = H;
+  gt.mode = 2;
+  gt.h0f = p->h0 ? p->h0 + (long)l * B * H : nullptr;
+  LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+  tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
+  // dW_x = X^T DZ, dW_h = Hprev^T DZ
+  ev = tbeg(p, s);
+  for (int part = 0; part < 2; ++part) {
+    const int M = part == 0 ? Il : H;
+    ll::GemmArgs g{};
+    g.A = part == 0 ? p->XT : p->HPT;
+    g.lda = p->ldT;
+    g.Bm = p->DZT;
+    g.ldb = p->ldT;
+    g.M = M;
+    g.N = 4 * H;
+    g.K = (int)p->cap;
+    g.K_dev = p->meta + 1;
+    g.splits = p->dw_splits[part];
+    float* dst = dW[l] + (part == 0 ? 0L : (long)Il * 4 * H);
+    if (g.splits > 1) {
+      g.C = p->ws;
+      g.ldc = 4L * H;
+      g.split_stride = (long)M * 4 * H;
+      LL_HIP(ll::launch_gemm_nt<T>(g, s));
+      LL_HIP(ll::launch_sum_slices(p->ws, g.splits, g.split_stride, g.split_stride, dst, s));
+    } else {
+      g.C = dst;
+      g.ldc = 4L * H;
+      LL_HIP(ll::launch_gemm_nt<T>(g, s));
+    }
+  }
+  tend(p, s, LL_STAGE_DW, ev);
+  // dx_t = dz_t W_x^T: scattered to time-major dx (layer 0) or kept compact
+  // as the gradient of the layer below (layer 1)
+  if (!dx) return LL_OK;
+  ev = tbeg(p, s);
+  ll::GemmArgs g{};
+  g.A = dz;
+  g.lda = 4L * H;
+  g.Bm = p->W[l];
+  g.ldb = 4L * H;
+  g.M = (int)p->cap;
+  g.M_dev = p->meta + 1;
+  g.N = Il;
+  g.K = 4 * H;
+  g.splits = 1;
+  g.C = dx;
+  if (l == 0) {
+    g.ldc = d.I;
+    g.c_rowmap = p->rowmap;
+  } else {
+    g.ldc = H;
+  }
+  LL_HIP(ll::launch_gemm_nt<T>(g, s));
+  tend(p, s, LL_STAGE_DX, ev);
+  return LL_OK;
+}
+
+// Two-layer wavefront, gradient: one launch in which the upper layer's step t
+// runs beside the lower layer's step t+1 on every XCD; the upper layer hands
+// dy of the lower layer's output over per step (dz W_x^T of its own units),
+// so no dx product of layer 1 is needed.  Then the dW and db products of both
+// layers and dx of layer 0.
+template <typename T>
+ll_status enqueue_bwd_wave(ll_plan* p, hipStream_t s, const float* dy, const float* dhT,
+                           const float* dcT, float* dx, float* const* dW, float* const* dbias,
+                           float* dh0, float* dc0) {
+  const ll_desc& d = p->d;
+  const int H = d.H, B = d.B;
+  const long BH = (long)B * H;
+  const long fw = 8L * p->xMRT * 32;
+  unsigned* F0 = p->xflags + 8;
+  unsigned* F1 = F0 + fw;
+  unsigned* FY = F1 + fw;
+  hipEvent_t ev = tbeg(p, s);
+  LL_HIP(ll::launch_zero_u32(p->xflags, p->xflag_words, s));
+  tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+  const int ring_ks = (int)(4L * H * p->es / 64);
+  ll::XLoopArgs a0 = x_common(p), a1 = x_common(p);
+  a0.ring = p->xring;
+  a0.ring_ks = ring_ks;
+  a0.flags = F0;
+  a0.W = p->W[0];
+  a0.woff = d.I;
+  a0.X = p->DZ;
+  a0.c0 = p->c0;
+  a0.stack = p->stack[0];
+  a0.dhT = dhT;
+  a0.dcT = dcT;
+  a0.db_part = p->db_part;
+  a0.dh0 = dh0;
+  a0.dc0 = dc0;
+  a0.dyx_ring = p->dyx;
+  a0.dyx_flags = FY;
+
+  a1.ring = p->xring2;
+  a1.ring_ks = ring_ks;
+  a1.flags = F1;
+  a1.W = p->W[1];
+  a1.woff = H;
+  a1.Wx = p->W[1];
+  a1.X = p->DZ2;
+  a1.c0 = p->c0 ? p->c0 + BH : nullptr;
+  a1.stack = p->stack[1];
+  a1.dy = dy;
+  a1.dy_compact = 0;
+  a1.dhT = dhT ? dhT + BH : nullptr;
+  a1.dcT = dcT ? dcT + BH : nullptr;
+  a1.db_part = p->db_part2;
+  a1.dh0 = dh0 ? dh0 + BH : nullptr;
+  a1.dc0 = dc0 ? dc0 + BH : nullptr;
+  a1.dyx_ring = p->dyx;
+  a1.dyx_flags = FY;
+  a1.peer_flags = F0;
+  ev = tbeg(p, s);
+  LL_HIP(ll::x_launch2(p->xk2.bwd, a0, a1, 256, p->xk2.lds_bwd, s));
+  tend(p, s, LL_STAGE_BWD_LOOP, ev);
+  LL_STATUS(bwd_products<T>(p, s, 1, p->DZ2, p->db_part2, nullptr, dW, dbias));
+  return bwd_products<T>(p, s, 0, p->DZ, p->db_part, dx, dW, dbias);
+}
+
 template <typename T>
 ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* dhT,
                       const float* dcT, float* dx, float* const* dW, float* const* dbias,
@@ -668,6 +978,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
   hipEvent_t ev = tbeg(p, s);
   if (dx) LL_HIP(ll::launch_zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta, s));
   tend(p, s, LL_STAGE_DX, ev);
+  if (p->wave) return enqueue_bwd_wave<T>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
   for (int l = L - 1; l >= 0; --l) {
     const int Il = in_width(p, l);
     if (p->xmode) {
@@ -785,89 +1096,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       LL_HIP(ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s));
       tend(p, s, LL_STAGE_BWD_LOOP, ev);
     }
-    // db = sum of the row-group partials
-    ev = tbeg(p, s);
-    LL_HIP(ll::launch_sum_slices(p->db_part, p->xmode ? 8 : p->geom.RG, 4L * H, 4L * H,
-                                 dbias[l], s));
-    tend(p, s, LL_STAGE_DW, ev);
-    ev = tbeg(p, s);
-    // transposed operands of the dW products (reduction over compact rows)
-    ll::GatherTArgs gt{};
-    gt.B = B;
-    gt.meta = p->meta;
-    gt.rowmap = p->rowmap;
-    gt.off = p->off;
-    gt.perm = p->perm;
-    gt.ldo = (int)p->ldT;
-    gt.in = p->DZ;
-    gt.out = p->DZT;
-    gt.C = 4 * H;
-    gt.mode = 1;
-    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
-    gt.in = l == 0 ? p->x : p->HH[0];
-    gt.out = p->XT;
-    gt.C = Il;
-    gt.mode = l == 0 ? 0 : 1;
-    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
-    gt.in = p->HH[l];
-    gt.out = p->HPT;
-    gt.C = H;
-    gt.mode = 2;
-    gt.h0f = p->h0 ? p->h0 + (long)l * B * H : nullptr;
-    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
-    tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
-    // dW_x = X^T DZ, dW_h = Hprev^T DZ
-    ev = tbeg(p, s);
-    for (int part = 0; part < 2; ++part) {
-      const int M = part == 0 ? Il : H;
-      ll::GemmArgs g{};
-      g.A = part == 0 ? p->XT : p->HPT;
-      g.lda = p->ldT;
-      g.Bm = p->DZT;
-      g.ldb = p->ldT;
-      g.M = M;
-      g.N = 4 * H;
-      g.K = (int)p->cap;
-      g.K_dev = p->meta + 1;
-      g.splits = p->dw_splits[part];
-      float* dst = dW[l] + (part == 0 ? 0L : (long)Il * 4 * H);
-      if (g.splits > 1) {
-        g.C = p->ws;
-        g.ldc = 4L * H;
-        g.split_stride = (long)M * 4 * H;
-        LL_HIP(ll::launch_gemm_nt<T>(g, s));
-        LL_HIP(ll::launch_sum_slices(p->ws, g.splits, g.split_stride, g.split_stride, dst, s));
-      } else {
-        g.C = dst;
-        g.ldc = 4L * H;
-        LL_HIP(ll::launch_gemm_nt<T>(g, s));
-      }
-    }
-    tend(p, s, LL_STAGE_DW, ev);
-    // dx_t = dz_t W_x^T: scattered to time-major dx (layer 0) or kept compact
-    // as the gradient of the layer below (layer 1)
-    if (l == 0 && !dx) continue;
-    ev = tbeg(p, s);
-    ll::GemmArgs g{};
-    g.A = p->DZ;
-    g.lda = 4L * H;
-    g.Bm = p->W[l];
-    g.ldb = 4L * H;
-    g.M = (int)p->cap;
-    g.M_dev = p->meta + 1;
-    g.N = Il;
-    g.K = 4 * H;
-    g.splits = 1;
-    if (l == 0) {
-      g.C = dx;
-      g.ldc = d.I;
-      g.c_rowmap = p->rowmap;
-    } else {
-      g.C = p->dyc;
-      g.ldc = H;
-    }
-    LL_HIP(ll::launch_gemm_nt<T>(g, s));
-    tend(p, s, LL_STAGE_DX, ev);
+    LL_STATUS(bwd_products<T>(p, s, l, p->DZ, p->db_part, l == 0 ? dx : p->dyc, dW, dbias));
   }
   return LL_OK;
 }

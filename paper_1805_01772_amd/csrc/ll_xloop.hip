@@ -59,6 +59,10 @@ constexpr int kCpolSc1 = 16;
 __device__ __forceinline__ uint4 ld_chunk_l2(__amdgpu_buffer_rsrc_t r, unsigned off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolSc1));
 }
+// 4-byte read with cache policy sc1 (served by the L2, like ld_chunk_l2).
+__device__ __forceinline__ float ld_f32_l2(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCpolSc1));
+}
 // Plain 4-byte read through a buffer descriptor.
 __device__ __forceinline__ float ld_f32(__amdgpu_buffer_rsrc_t r, unsigned off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
@@ -179,10 +183,13 @@ __device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp
 //      cell, stores h_t into the ring and publishes it; then the h history,
 //      the stack row and y_t.
 // ---------------------------------------------------------------------------
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
-__global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
-  extern __shared__ uint4 lds[];
-  __shared__ int s_info[2];
+// TOP: the upper layer of the two-layer wavefront.  Its recurrent product
+// runs over K = I_l + H = 2H: the first in_ks k-steps are y1_t, read from the
+// lower layer's ring for step t (bf16(y1_t) in the bf16 contract: the ring
+// holds the operand-type h_t), the rest h_{t-1} from its own ring; the bias
+// replaces the hoisted input projection.
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP>
+__device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 4 * NCT;
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
@@ -191,22 +198,12 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   static_assert(HJ == 4 * KPC, "a member's units are one k-step");
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
-
-  join_group(a.rank_ctr, s_info);
-  const int grp = uni(s_info[0]), rank = uni(s_info[1]);
-  if (grp >= 8 || rank >= 32) {
-    if (tid == 0) {
-      __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(a.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    return;
-  }
-  if (rank >= a.P) return;
   const int H = a.H, B = a.B;
   const long G4 = 4L * H;
   const long H5 = 5L * H;
   const int j0 = rank * HJ;
-  const int KS = H / (4 * KPC);
+  const int KX = TOP ? a.in_ks : 0;                      // k-steps from the lower layer
+  const int KS = KX + H / (4 * KPC);
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
   const int nks = ks1 - ks0;                             // k-steps of this wave
   const T* WT = reinterpret_cast<const T*>(a.W);
@@ -266,9 +263,15 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   const int t0 = a.t_begin, t1 = min(a.t_end, T_eff);
   int wlo = t0 > 0 ? t0 - 1 : 0;
   load_window(a, win, wlo);
-  // input projections of the cell thread's (row, unit), one step ahead
+  // input projections of the cell thread's (row, unit), one step ahead (the
+  // upper wavefront layer: its bias)
   float zf[MRT_MAX][4];
-  {
+  if constexpr (TOP) {
+#pragma unroll
+    for (int mt = 0; mt < MRT_MAX; ++mt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) zf[mt][g] = cellt ? a.zbias[(long)g * H + ju] : 0.f;
+  } else {
     const int A0 = t0 < t1 ? win[t0 - wlo] : 0, off0 = win[WIN + 1 + t0 - wlo];
 #pragma unroll
     for (int mt = 0; mt < MRT_MAX; ++mt) {
@@ -299,16 +302,30 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
       }
       unsigned* flags = a.flags + (grp * a.MRT + mt) * 32;
       // 1. h_{t-1} of this wave's k-steps (for the launch's first step the
-      //    ring holds the entering state)
-      if (t > t0) wait_flags(a, flags, ks0, nks, a.P, (unsigned)(t + 1));
+      //    ring holds the entering state); the upper wavefront layer first
+      //    takes y1_t from the lower layer's ring
+      const int kx1 = min(ks1, KX);                        // [ks0, kx1): lower layer's k-steps
+      if (TOP && ks0 < kx1)
+        wait_flags(a, a.in_flags + (grp * a.MRT + mt) * 32, ks0, kx1 - ks0, a.in_ks, (unsigned)(t + 2));
+      if (t > t0 && max(ks0, KX) < ks1)
+        wait_flags(a, flags, max(ks0, KX) - KX, ks1 - max(ks0, KX), a.P, (unsigned)(t + 1));
       const __amdgpu_buffer_rsrc_t rs = make_rsrc(ring_tile(a, (t + 1) & 1, grp, mt), (unsigned)(a.ring_ks << 10));
+      __amdgpu_buffer_rsrc_t rsx = rs;
+      if constexpr (TOP)
+        rsx = make_rsrc(reinterpret_cast<const char*>(a.in_ring) +
+                            ((long)(((t & 1) * 8 + grp) * a.MRT + mt) * a.in_ks << 10),
+                        (unsigned)(a.in_ks << 10));
       uint4 av[KSW];
 #pragma unroll
-      for (int i = 0; i < KSW; ++i) av[i] = ld_chunk_l2(rs, i < nks ? (unsigned)(((ks0 + i) << 10) + lane * 16) : kOOB);
+      for (int i = 0; i < KSW; ++i) {
+        const int ks = ks0 + i;
+        av[i] = ks < KX ? ld_chunk_l2(rsx, i < nks ? (unsigned)((ks << 10) + lane * 16) : kOOB)
+                        : ld_chunk_l2(rs, i < nks ? (unsigned)(((ks - KX) << 10) + lane * 16) : kOOB);
+      }
       float zc[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) zc[g] = zf[mt][g];
-      {  // input projections of step t+1 (rows past A_n read zeros)
+      if constexpr (!TOP) {  // input projections of step t+1 (rows past A_n read zeros)
         const int nr = max(0, min(16, A_n - r0));
         const __amdgpu_buffer_rsrc_t rz = make_rsrc(a.Zx + (long)(off_n + r0) * G4, (unsigned)(nr * G4 * 4));
         const unsigned zo = cellt ? (unsigned)((crow * G4 + ju) * 4) : kOOB;
@@ -342,6 +359,10 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
           for (int i = 0; i < 4; ++i) red[(wave * 4 + i) * IS + (hf * NH + c) * 64 + lane] = acc[c][i];
       }
       __syncthreads();
+      // the lower wavefront layer rewrites ring slot t % 2 only after the
+      // upper layer has published step t - 2, its last read of that slot
+      if (a.out_flags && t >= 2)
+        wait_flags(a, a.out_flags + (grp * a.MRT + mt) * 32, 0, a.P, a.P, (unsigned)t);
       // 3. cell of (crow, cu): gate g is local column g*HJ + cu
       float ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cn = 0.f, hn = 0.f;
       const int r = r0 + crow;
@@ -401,6 +422,44 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   }
 }
 
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
+__global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
+  extern __shared__ uint4 lds[];
+  __shared__ int s_info[2];
+  join_group(a.rank_ctr, s_info);
+  const int grp = uni(s_info[0]), rank = uni(s_info[1]);
+  if (grp >= 8 || rank >= 32) {
+    if (threadIdx.x == 0) {
+      __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
+  }
+  if (rank >= a.P) return;
+  xfwd_body<T, NCT, KSW, KSR, MRT_MAX, false>(a, grp, rank, lds);
+}
+
+// Two-layer wavefront, forward: members 0 .. P-1 of every XCD run the lower
+// layer (a0), members P .. 2P-1 the upper layer (a1), one step behind.
+template <typename T, int NCT, int KSWB, int KSRB, int KSWT, int KSRT, int MRT_MAX>
+__global__ __launch_bounds__(XNT, 1) void xfwd2_kernel(XLoopArgs a0, XLoopArgs a1) {
+  extern __shared__ uint4 lds[];
+  __shared__ int s_info[2];
+  join_group(a0.rank_ctr, s_info);
+  const int grp = uni(s_info[0]), rank = uni(s_info[1]);
+  if (grp >= 8 || rank >= 32) {
+    if (threadIdx.x == 0) {
+      __hip_atomic_fetch_or(a0.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a0.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
+  }
+  if (rank < a0.P)
+    xfwd_body<T, NCT, KSWB, KSRB, MRT_MAX, false>(a0, grp, rank, lds);
+  else if (rank < a0.P + a1.P)
+    xfwd_body<T, NCT, KSWT, KSRT, MRT_MAX, true>(a1, grp, rank - a0.P, lds);
+}
+
 // ---------------------------------------------------------------------------
 // Gradient loop, XCD-local.  Member `rank` owns hidden units j0 .. j0+HJ-1
 // (HJ = 16 NCT); thread (row, unit) of the first 16*HJ threads keeps dh, dc
@@ -416,30 +475,22 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
 //     own units (MFMA); the thread of (row, unit) adds the 8 partial
 //     products.
 // ---------------------------------------------------------------------------
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
-__global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
-  extern __shared__ uint4 lds[];
-  __shared__ int s_info[2];
+// ROLE 0: a single layer; 1: the lower layer of the two-layer wavefront
+// (its dy comes from the upper layer's dyx ring, one step later); 2: the upper
+// layer, which also computes dy_{lower} = dz W_x^T for its units (NCO = 2 NCT
+// output column tiles: W_h rows, then W_x rows) and publishes it per step.
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE>
+__device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT;                 // units per work-group
+  constexpr int NCO = ROLE == 2 ? 2 * NCT : NCT;   // output column tiles
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
   constexpr int KB = KSW < 8 ? KSW : 8;        // k-steps per load batch
-  constexpr int IS = xbwd_is(NCT);
+  constexpr int IS = xbwd_is(NCO);
   static_assert(16 * HJ <= XNT, "one thread per (row, unit) of a tile");
   static_assert(HJ == 4 * KPC, "a member's units of one gate are one k-step");
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
-
-  join_group(a.rank_ctr, s_info);
-  const int grp = uni(s_info[0]), rank = uni(s_info[1]);
-  if (grp >= 8 || rank >= 32) {
-    if (tid == 0) {
-      __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(a.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    return;
-  }
-  if (rank >= a.P) return;
   const int H = a.H, B = a.B, P = a.P;
   const long G4 = 4L * H;
   const long H5 = 5L * H;
@@ -450,10 +501,11 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   const T* W = reinterpret_cast<const T*>(a.W);
   T* DZ = reinterpret_cast<T*>(a.X);
 
-  uint4 wr[NCT][KSR];
+  uint4 wr[NCO][KSR];
 #pragma unroll
-  for (int ct = 0; ct < NCT; ++ct) {
-    const T* wrow = W + (long)(a.woff + j0 + ct * 16 + l16) * G4;
+  for (int ct = 0; ct < NCO; ++ct) {
+    const T* wrow = ct < NCT ? W + (long)(a.woff + j0 + ct * 16 + l16) * G4
+                             : reinterpret_cast<const T*>(a.Wx) + (long)(j0 + (ct - NCT) * 16 + l16) * G4;
 #pragma unroll
     for (int i = 0; i < KSR; ++i) {
       const int ks = ks0 + i;
@@ -462,11 +514,11 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
 #pragma unroll
     for (int i = 0; i < KSL; ++i) {
       const int ks = ks0 + KSR + i;
-      lds[((wave * KSL + i) * NCT + ct) * 64 + lane] = ks < ks1 ? ld16(wrow + (ks * 4 + q) * KPC) : zero4();
+      lds[((wave * KSL + i) * NCO + ct) * 64 + lane] = ks < ks1 ? ld16(wrow + (ks * 4 + q) * KPC) : zero4();
     }
   }
-  float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCT * 64);   // [XNW][4][IS]
-  int* win = reinterpret_cast<int*>(red + xbwd_red_floats(NCT));       // [2][WIN+1]
+  float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCO * 64);   // [XNW][4][IS]
+  int* win = reinterpret_cast<int*>(red + xbwd_red_floats(NCO));       // [2][WIN+1]
   int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
 
   // (row, unit) of this thread: 16 lanes take 16 consecutive units of one
@@ -533,7 +585,8 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
 
   const int T_eff = uni(a.meta[0]);
   const int t0 = a.t_begin, t1 = min(a.t_end, T_eff);
-  int wlo = t1 - 1 - WIN > 0 ? t1 - 1 - WIN : 0;
+  // the window covers steps t-2 .. t+2 of every step t of the loop
+  int wlo = t1 + 1 - WIN > 0 ? t1 + 1 - WIN : 0;
   load_window(a, win, wlo);
   float pv[MRT_MAX][7];
   {
@@ -548,7 +601,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
 
   for (int t = t1 - 1; t >= t0; --t) {
     if (t - 2 < wlo && wlo > 0) {
-      wlo = t - WIN > 0 ? t - WIN : 0;
+      wlo = t + 2 - WIN > 0 ? t + 2 - WIN : 0;
       load_window(a, win, wlo);
     }
     const int A_t = uni(win[t - wlo]);
@@ -568,10 +621,19 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
       unsigned* flags = a.flags + (grp * a.MRT + mt) * 32;
       char* slot = ring_tile(a, t & 1, grp, mt);
       const bool act = cellt && r0 + crow < A_t;
+      // dyx ring slot of this tile for step t: [16 rows][H] floats
+      const long dyx_off = ((long)(((t & 1) * 8 + grp) * a.MRT + mt) * 16) * H;
+      float dyl = 0.f;   // lower wavefront layer: dy of its output from the upper layer
+      if constexpr (ROLE == 1) {
+        wait_flags(a, a.dyx_flags + (grp * a.MRT + mt) * 32, rank, 1, 32, (unsigned)(T_eff - t));
+        const __amdgpu_buffer_rsrc_t ry =
+            make_rsrc(reinterpret_cast<const float*>(a.dyx_ring) + dyx_off, (unsigned)(16 * H * 4));
+        dyl = ld_f32_l2(ry, act ? (unsigned)((crow * H + ju) * 4) : kOOB);
+      }
       // phase 1
       float dz[4] = {0.f, 0.f, 0.f, 0.f};
       if (act) {
-        const float dht = dh[mt] + pv[mt][6];
+        const float dht = dh[mt] + pv[mt][6] + dyl;
         const float ig = pv[mt][0], fg = pv[mt][1], gg = pv[mt][2], og = pv[mt][3];
         const float c = pv[mt][4], cp = pv[mt][5];
         const float tc = tanhf_(c);
@@ -598,9 +660,9 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
       // phase 2
       wait_flags(a, flags, ks0, nks < 64 ? nks : 64, P, (unsigned)(T_eff - t));
       const __amdgpu_buffer_rsrc_t rs = make_rsrc(slot, (unsigned)(a.ring_ks << 10));
-      f32x4 acc[NCT];
+      f32x4 acc[NCO];
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int ct = 0; ct < NCO; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int b0 = 0; b0 < KSW; b0 += KB) {
         uint4 av[KB];
@@ -613,9 +675,9 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
           const int ii = b0 + i;
           if (ii < KSW && ii < nks) {
 #pragma unroll
-            for (int ct = 0; ct < NCT; ++ct) {
+            for (int ct = 0; ct < NCO; ++ct) {
               const uint4 bv = ii < KSR ? wr[ct][ii < KSR ? ii : 0]
-                                        : lds[((wave * KSL + (ii - KSR)) * NCT + ct) * 64 + lane];
+                                        : lds[((wave * KSL + (ii - KSR)) * NCO + ct) * 64 + lane];
               acc[ct] = Mfma<T>::step(av[i], bv, acc[ct]);
             }
           }
@@ -624,7 +686,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
       // partial products -> red (the previous tile's sums were read before
       // this step's publish barrier)
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct)
+      for (int ct = 0; ct < NCO; ++ct)
 #pragma unroll
         for (int e = 0; e < 4; ++e) red[(wave * 4 + e) * IS + ct * 64 + lane] = acc[ct][e];
       __syncthreads();
@@ -633,6 +695,21 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
 #pragma unroll
         for (int w2 = 1; w2 < XNW; ++w2) s += rp[w2 * 4 * IS];
         dh[mt] = s;
+      }
+      if constexpr (ROLE == 2) {
+        // dy of the lower layer's output at step t for the own units; the
+        // slot held step t+2, which the lower partner has read once it has
+        // published that step (if the tile ran at t+2)
+        if (r0 < win[t + 2 - wlo])
+          wait_flags(a, a.peer_flags + (grp * a.MRT + mt) * 32, rank, 1, 32, (unsigned)(T_eff - (t + 2)));
+        if (act) {
+          const float* rx = rp + NCT * 64;
+          float s = rx[0];
+#pragma unroll
+          for (int w2 = 1; w2 < XNW; ++w2) s += rx[w2 * 4 * IS];
+          reinterpret_cast<float*>(a.dyx_ring)[dyx_off + crow * H + ju] = s;
+        }
+        publish(a.dyx_flags + (grp * a.MRT + mt) * 32 + rank, (unsigned)(T_eff - t));
       }
     }
   }
@@ -661,6 +738,44 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     const int g = c / HJ, u = c - (c / HJ) * HJ;
     a.db_part[(long)grp * G4 + (long)g * H + j0 + u] = s;
   }
+}
+
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
+__global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
+  extern __shared__ uint4 lds[];
+  __shared__ int s_info[2];
+  join_group(a.rank_ctr, s_info);
+  const int grp = uni(s_info[0]), rank = uni(s_info[1]);
+  if (grp >= 8 || rank >= 32) {
+    if (threadIdx.x == 0) {
+      __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
+  }
+  if (rank >= a.P) return;
+  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0>(a, grp, rank, lds);
+}
+
+// Two-layer wavefront, gradient: members 0 .. P-1 of every XCD run the lower
+// layer (a0) one step behind the upper layer (a1, members P .. 2P-1).
+template <typename T, int NCT, int KSW, int KSRB, int KSRT, int MRT_MAX>
+__global__ __launch_bounds__(XNT, 1) void xbwd2_kernel(XLoopArgs a0, XLoopArgs a1) {
+  extern __shared__ uint4 lds[];
+  __shared__ int s_info[2];
+  join_group(a0.rank_ctr, s_info);
+  const int grp = uni(s_info[0]), rank = uni(s_info[1]);
+  if (grp >= 8 || rank >= 32) {
+    if (threadIdx.x == 0) {
+      __hip_atomic_fetch_or(a0.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a0.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
+  }
+  if (rank < a0.P)
+    xbwd_body<T, NCT, KSW, KSRB, MRT_MAX, 1>(a0, grp, rank, lds);
+  else if (rank < a0.P + a1.P)
+    xbwd_body<T, NCT, KSW, KSRT, MRT_MAX, 2>(a1, grp, rank - a0.P, lds);
 }
 
 // Forward loop set-up: the entering h rows (length order, operand type) into
@@ -761,6 +876,41 @@ XKernels x_kernels(int hc, int mrt) {
 template XKernels x_kernels<float>(int, int);
 template XKernels x_kernels<bf16_t>(int, int);
 
+// Two-layer wavefront kernels: the lower layer as in x_kernels, the upper one
+// with twice the forward k-steps (K = I_l + H = 2H) and, in the gradient, twice
+// the output column tiles (W_h and W_x rows).  RFT / RBT: register k-steps of
+// the upper layer's role.
+namespace {
+template <typename T, int NF, int NB, int HC, int RFB, int RFT, int RBB, int RBT, int MRT>
+XKernels x_make2() {
+  XKernels k{};
+  k.fwd = reinterpret_cast<const void*>(&xfwd2_kernel<T, NF, HC, RFB, 2 * HC, RFT, MRT>);
+  k.bwd = reinterpret_cast<const void*>(&xbwd2_kernel<T, NB, 4 * HC, RBB, RBT, MRT>);
+  const size_t fb = xfwd_lds(HC, RFB, NF, MRT), ft = xfwd_lds(2 * HC, RFT, NF, MRT);
+  const size_t bb = xbwd_lds(4 * HC, RBB, NB, MRT), bt = xbwd_lds(4 * HC, RBT, 2 * NB, MRT);
+  k.lds_fwd = fb > ft ? fb : ft;
+  k.lds_bwd = bb > bt ? bb : bt;
+  return k;
+}
+}  // namespace
+
+template <typename T>
+XKernels x_kernels2(int hc, int mrt) {
+  constexpr bool bf = sizeof(T) == 2;
+  constexpr int NF = bf ? 8 : 4;
+  constexpr int NB = bf ? 2 : 1;
+  const bool one = mrt <= 1;
+  if (mrt > 4) return XKernels{};
+  switch (hc) {
+    case 1: return one ? x_make2<T, NF, NB, 1, 1, 2, 4, 4, 1>() : x_make2<T, NF, NB, 1, 1, 2, 4, 4, 4>();
+    case 2: return one ? x_make2<T, NF, NB, 2, 2, 4, 8, 6, 1>() : x_make2<T, NF, NB, 2, 2, 3, 6, 5, 4>();
+    default: return XKernels{};
+  }
+}
+
+template XKernels x_kernels2<float>(int, int);
+template XKernels x_kernels2<bf16_t>(int, int);
+
 hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd) {
   // a variant that spills more than a few registers to scratch is not used
   hipFuncAttributes fa{}, fb{};
@@ -785,6 +935,13 @@ hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd) {
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s) {
   XLoopArgs copy = a;
   void* kargs[] = {&copy};
+  return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(XNT), kargs, (unsigned)lds, s);
+}
+
+hipError_t x_launch2(const void* fn, const XLoopArgs& a0, const XLoopArgs& a1, int nwg, size_t lds,
+                     hipStream_t s) {
+  XLoopArgs c0 = a0, c1 = a1;
+  void* kargs[] = {&c0, &c1};
   return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(XNT), kargs, (unsigned)lds, s);
 }
 

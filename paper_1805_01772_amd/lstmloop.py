@@ -64,7 +64,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ll_plan_destroy.argtypes = [vp]
     lib.ll_plan_stack_bytes.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.ll_plan_geometry.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32),
-                                     ctypes.POINTER(i32), ctypes.POINTER(i32)]
+                                     ctypes.POINTER(i32), ctypes.POINTER(i32),
+                                     ctypes.POINTER(i32)]
     lib.lstm_loop_fwd.argtypes = [vp, vp, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp),
                                   vp, vp, vp, vp, vp, vp, i32]
     lib.lstm_loop_bwd.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.POINTER(vp),
@@ -163,11 +164,11 @@ class Plan:
         return d.value, h.value
 
     def geometry(self):
-        n, hj, rg, xl = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        n, hj, rg, xl, wf = (ctypes.c_int32() for _ in range(5))
         _check(self._lib.ll_plan_geometry(self._h, ctypes.byref(n), ctypes.byref(hj),
-                                          ctypes.byref(rg), ctypes.byref(xl)))
+                                          ctypes.byref(rg), ctypes.byref(xl), ctypes.byref(wf)))
         return dict(workgroups=n.value, units_per_workgroup=hj.value, row_groups=rg.value,
-                    xcd_local=bool(xl.value))
+                    xcd_local=bool(xl.value), wavefront=bool(wf.value))
 
     def fwd(self, x, seq_len, W: Sequence, bias: Sequence, h0, c0, y, hT, cT,
             trip_count=None, save_for_backward: bool = True, stream=None) -> None:

@@ -197,12 +197,16 @@ def test_repeat_calls_are_deterministic():
             np.testing.assert_array_equal(u, v)
 
 
-def test_two_layers_equal_two_single_layer_calls():
+def test_two_layers_equal_two_single_layer_calls(monkeypatch):
+    # layer by layer, the two-layer plan makes the same calls as two plans
+    monkeypatch.setenv("LSTMLOOP_WAVEFRONT", "off")
     w = W("stack2", B=45, I=64, H=64, T_max=10, dtype="bf16", layers=2, len_lo=0, len_hi=10,
           random_state=True, seed=26)
     inp = wl.generate(w)
     say("[edge] two layers vs two calls")
-    both, _ = run_case(w, inp)
+    geom = {}
+    both, _ = run_case(w, inp, geometry=geom)
+    assert not geom["wavefront"]
     w1 = w.with_(layers=1)
     l1 = dict(inp, W=[inp["W"][0]], bias=[inp["bias"][0]], h0=inp["h0"][:1], c0=inp["c0"][:1],
               dhT=inp["dhT"][:1], dcT=inp["dcT"][:1])
@@ -232,6 +236,74 @@ def test_two_layers_equal_two_single_layer_calls():
     np.testing.assert_array_equal(both["dW"][0], r1["dW"][0])
     np.testing.assert_array_equal(both["dW"][1], r2["dW"][0])
     np.testing.assert_array_equal(both["dbias"][1], r2["dbias"][0])
+
+
+# ------------------------------------------------ two-layer wavefront
+# Shapes where one launch runs both layers (2 H / units per work-group <= 32),
+# covering one and several row tiles per XCD, both forward k-step classes and
+# tiles that start or finish at different steps.
+TWO_LAYER_WAVE = [
+    W("wave_bf16_b150_i64_h512_t12", B=150, I=64, H=512, T_max=12, dtype="bf16", layers=2,
+      len_lo=0, len_hi=12, random_state=True, seed=31),
+    W("wave_f32_b40_i24_h256_t15", B=40, I=24, H=256, T_max=15, dtype="f32", layers=2,
+      len_lo=1, len_hi=15, random_state=True, seed=32),
+    W("wave_bf16_b300_i32_h128_t10_mrt3", B=300, I=32, H=128, T_max=10, dtype="bf16",
+      layers=2, len_lo=0, len_hi=10, w_scale=0.3, random_state=True, seed=33),
+    W("wave_f32_b9_i8_h96_t20", B=9, I=8, H=96, T_max=20, dtype="f32", layers=2, len_lo=0,
+      len_hi=20, w_scale=0.3, random_state=True, seed=34),
+]
+
+
+@pytest.fixture(params=["wavefront", "layerwise"])
+def layer_schedule(request, monkeypatch):
+    """wavefront: the library's choice for these shapes; layerwise: one launch
+    per layer, forced through LSTMLOOP_WAVEFRONT."""
+    if request.param == "layerwise":
+        monkeypatch.setenv("LSTMLOOP_WAVEFRONT", "off")
+    else:
+        monkeypatch.delenv("LSTMLOOP_WAVEFRONT", raising=False)
+    monkeypatch.delenv("LSTMLOOP_LOOPS", raising=False)
+    return request.param
+
+
+@pytest.mark.parametrize("w", TWO_LAYER_WAVE, ids=[w.name for w in TWO_LAYER_WAVE])
+def test_two_layer_wavefront_parity(w, layer_schedule):
+    say(f"[wave] {w.name} {layer_schedule}")
+    inp = wl.generate(w)
+    geom = {}
+    res, err = run_case(w, inp, geometry=geom)
+    assert geom["xcd_local"] and geom["wavefront"] == (layer_schedule == "wavefront"), geom
+    assert err == 0
+    ref = oracle_reference(inp, w.layers, w.dtype)
+    assert res["T_eff"] == ref["T_eff"]
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
+
+
+def test_two_layer_wavefront_zero_trip_and_finished_rows():
+    w = TWO_LAYER_WAVE[3]
+    inp = wl.generate(w)
+    say("[wave] all lengths zero")
+    zero = dict(inp, seq_len=np.zeros_like(inp["seq_len"]))
+    geom = {}
+    res, err = run_case(w, zero, geometry=geom)
+    assert geom["wavefront"] and err == 0 and res["T_eff"] == 0
+    assert (res["y"] == 0).all() and (res["dx"] == 0).all()
+    np.testing.assert_array_equal(res["hT"], inp["h0"])
+    np.testing.assert_array_equal(res["cT"], inp["c0"])
+    np.testing.assert_array_equal(res["dh0"], inp["dhT"])
+    np.testing.assert_array_equal(res["dc0"], inp["dcT"])
+    assert all((d == 0).all() for d in res["dW"]) and all((d == 0).all() for d in res["dbias"])
+    say("[wave] finished rows")
+    res, err = run_case(w, inp)
+    L = inp["seq_len"]
+    for b in range(w.B):
+        assert (res["y"][L[b]:, b] == 0).all() and (res["dx"][L[b]:, b] == 0).all()
+        if L[b] > 0:
+            np.testing.assert_array_equal(res["hT"][1, b], res["y"][L[b] - 1, b])
+        else:
+            np.testing.assert_array_equal(res["hT"][:, b], inp["h0"][:, b])
 
 
 def test_invalid_lengths_raise_device_error_and_recover():
@@ -328,8 +400,11 @@ SPILL_CASES = [
 
 
 @pytest.mark.parametrize("w,C,R", SPILL_CASES, ids=[c[0].name for c in SPILL_CASES])
-def test_spill_matches_resident_stack_bitwise(w, C, R):
-    """Swapping the stack to host memory in chunks changes no result bit."""
+def test_spill_matches_resident_stack_bitwise(w, C, R, monkeypatch):
+    """Swapping the stack to host memory in chunks changes no result bit
+    (against the resident stack with the same layer-by-layer schedule: a
+    spilling plan runs its layers one after the other)."""
+    monkeypatch.setenv("LSTMLOOP_WAVEFRONT", "off")
     say(f"[spill] {w.name} C={C} R={R}")
     inp = wl.generate(w)
     ref, err0, dev0, host0 = _run_plan(w, inp)
