@@ -121,22 +121,28 @@ ll_status ll_plan_destroy(ll_plan* plan);
 ll_status ll_plan_stack_bytes(const ll_plan* plan, int64_t* device_bytes,
                               int64_t* host_bytes);
 
+/* Forms of the recurrent loops (ll_plan_geometry). */
+#define LL_LOOPS_GRID 0   /* one grid-wide barrier per step                   */
+#define LL_LOOPS_XCD 1    /* each XCD runs its own rows through its own L2    */
+#define LL_LOOPS_CHIP 2   /* weights split over all XCDs, per-tile flags      */
+
 /* Launch geometry the plan chose for the recurrent loops (for reports):
- * work-groups per loop launch, hidden units per work-group, row groups
- * (independent recurrences), whether the XCD-local loops are used (1: each
- * of the 8 XCDs runs the rows of its own group through its own L2; 0: one
- * grid-wide barrier per step), and whether a two-layer plan runs its layers
+ * work-groups per loop launch, hidden units per work-group (the cell units
+ * of a work-group in the chip-wide form), row groups (independent
+ * recurrences), the loop form (LL_LOOPS_*: XCD-local where one XCD holds the
+ * recurrent weights, chip-wide where it cannot (bf16 H = 2048, f32
+ * H = 1024, B <= 256), grid-barrier otherwise), and whether a two-layer plan runs its layers
  * as a wavefront (1: one launch per direction runs both layers, the upper
  * layer's step t beside the lower layer's step t+1 (forward) or t-1
  * (gradient); 0: one launch per layer).  Any output may be NULL.
  * Environment variables read at plan creation: LSTMLOOP_LOOPS=grid forces
- * the grid-barrier loops; LSTMLOOP_WAVEFRONT=off runs the layers one after
+ * the grid-barrier form; LSTMLOOP_WAVEFRONT=off runs the layers one after
  * the other.  The wavefront needs the XCD-local loops, no spill and
  * 2H / units_per_workgroup <= 32; its results equal the layer-by-layer
  * ones up to the order of floating-point sums. */
 ll_status ll_plan_geometry(const ll_plan* plan, int32_t* loop_workgroups,
                            int32_t* units_per_workgroup,
-                           int32_t* row_groups, int32_t* xcd_local,
+                           int32_t* row_groups, int32_t* loop_form,
                            int32_t* wavefront);
 
 /*

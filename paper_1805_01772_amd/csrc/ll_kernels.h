@@ -166,6 +166,63 @@ struct XLoopArgs {
   const void* Wx;         // upper layer, gradient: W rows of the input part [I_l, 4H]
 };
 
+// Chip-wide loops (ll_cloop.hip), for shapes whose recurrent weights need
+// more than one XCD: XCD x owns hidden units [x H/8, (x+1) H/8); its 32
+// work-groups split the reduction (K) and the units (N) of the recurrent
+// product.  Every row tile of the batch runs on every work-group.
+struct CLoopArgs {
+  int B, H, T_max;
+  int MRT;                // row tiles of the batch = ceil(B / 16)
+  const int* meta;
+  const int* active;
+  const int* off;
+  const int* perm;
+  const void* W;          // forward: W^T [4H, ldw]; backward: W [rows, 4H]
+  int ldw;
+  int woff;               // forward: column of the h part in W^T; backward: row of W_h
+  void* X;                // forward: h history [cap, H]; backward: dz [cap, 4H] (operand type)
+  void* ring;             // exchange ring [2][MRT][ring_ks][1 KB] (forward: slot 1 holds h0)
+  int ring_ks;            // blocks per row tile: H / (4 KPC) forward, 4H / (4 KPC) backward
+  float* part;            // partial products [2][8][MRT][32][pw]
+  unsigned* xflags;       // exchange flags [MRT][256] (one per work-group and row tile)
+  unsigned* pflags;       // partial-product flags [8][MRT][32]
+  unsigned* rank_ctr;     // [8]
+  const float* Zx;        // forward: [cap, 4H]
+  const float* h0;
+  const float* c0;
+  float* stack;           // [cap, 5H] compact rows: forward push (NULL = inference), backward pop
+  float* y;
+  float* hT;
+  float* cT;
+  const float* dy;
+  int dy_compact;
+  const float* dhT;
+  const float* dcT;
+  float* db;              // backward: [4H]
+  float* dh0;
+  float* dc0;
+  int* abort_flag;
+  int* err;
+  unsigned long long limit;
+};
+
+struct CKernels {
+  const void* fwd;
+  const void* bwd;
+  size_t lds_fwd;
+  size_t lds_bwd;
+  int pw;                 // partial floats per (work-group, row tile)
+};
+template <typename T>
+CKernels c_kernels(int H, int mrt);
+hipError_t c_setup(const CKernels& k, int* occ_fwd, int* occ_bwd);
+hipError_t c_launch(const void* fn, const CLoopArgs& a, size_t lds, hipStream_t s);
+// h0 rows (length order, operand type) into ring slot 1 and every flag and
+// rank counter of the launch to zero.
+template <typename T>
+hipError_t launch_c_prepare(const float* h0, const int* perm, int B, int H, int mrt, void* ring,
+                            unsigned* flags, int nflags, hipStream_t s);
+
 struct XKernels {
   const void* fwd;
   const void* bwd;

@@ -81,6 +81,14 @@ struct ll_plan {
   int xP = 0;                  // unit blocks per XCD
   int xMRT = 0;                // row tiles per XCD
   int xhc = 0;                 // forward k-steps per wave
+  // chip-wide loops (ll_cloop.hip): weights split over all XCDs
+  bool cmode = false;
+  ll::CKernels ck{};
+  int cMRT = 0;
+  void* cring = nullptr;
+  float* cpart = nullptr;
+  unsigned* cflags = nullptr;  // [8] rank counters, exchange flags [MRT][256], partial flags [8][MRT][32]
+  int cflag_words = 0;
   // two-layer wavefront: one launch per direction runs both layers
   bool wave = false;
   ll::XKernels xk2{};
@@ -198,7 +206,7 @@ void free_plan_memory(ll_plan* p) {
   void* ptrs[] = {p->perm, p->active, p->off, p->rowmap, p->meta, p->WT[0], p->WT[1], p->Zx,
                   p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT, p->HPT,
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
-                  p->xring2, p->DZ2, p->dyx, p->db_part2};
+                  p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -346,9 +354,9 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
 
   // XCD-local loops: 8 XCDs x 32 CUs, every exchanged row 128-byte aligned,
   // H split 32 ways (bf16: 32 units per work-group, f32: 16).
+  const char* loops_env = getenv("LSTMLOOP_LOOPS");
+  const bool allow = !(loops_env && strcmp(loops_env, "grid") == 0);
   {
-    const char* mode = getenv("LSTMLOOP_LOOPS");
-    const bool allow = !(mode && strcmp(mode, "grid") == 0);
     const int HJx = p->bf16 ? 32 : 16;
     const int P = H / HJx;
     if (allow && p->n_cu == 256 && H % HJx == 0 && P >= 1 && P <= 32 &&
@@ -371,6 +379,23 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
             (void)hipGetLastError();
           }
         }
+      }
+    }
+  }
+
+  // Chip-wide loops where one XCD cannot hold the recurrent weights (bf16
+  // H = 2048, f32 H = 1024, B <= 256).
+  if (!p->xmode && allow && p->n_cu == 256) {
+    const int mrt = (B + 15) / 16;
+    ll::CKernels ck = p->bf16 ? ll::c_kernels<bf16_t>(H, mrt) : ll::c_kernels<float>(H, mrt);
+    if (ck.fwd && ck.bwd) {
+      int of = 0, ob = 0;
+      if (ll::c_setup(ck, &of, &ob) == hipSuccess && of >= 1 && ob >= 1) {
+        p->cmode = true;
+        p->ck = ck;
+        p->cMRT = mrt;
+      } else {
+        (void)hipGetLastError();
       }
     }
   }
@@ -473,6 +498,13 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
       ALLOC(p->db_part2, sizeof(float) * 8 * 4 * H, "db partials");
     }
   }
+  if (p->cmode) {
+    // two slots x row tiles x (4H / k-step) blocks of 1 KB; partial products
+    ALLOC(p->cring, 2L * p->cMRT * (4L * H * (long)es / 64) * 1024, "exchange ring");
+    ALLOC(p->cpart, sizeof(float) * 2L * 8 * p->cMRT * 32 * p->ck.pw, "partial products");
+    p->cflag_words = 8 + p->cMRT * 256 + 8 * p->cMRT * 32;
+    ALLOC(p->cflags, sizeof(unsigned) * p->cflag_words, "exchange flags");
+  }
   if (p->spill) {
     ALLOC(p->carry, sizeof(float) * 4 * B * H, "chunk carry");
     ALLOC(p->db_state, sizeof(float) * 8 * 32 * 512 * 4, "db state");
@@ -557,12 +589,12 @@ ll_status ll_plan_stack_bytes(const ll_plan* p, int64_t* dev, int64_t* host) {
 }
 
 ll_status ll_plan_geometry(const ll_plan* p, int32_t* nwg, int32_t* hj, int32_t* rg,
-                           int32_t* xcd_local, int32_t* wavefront) {
+                           int32_t* loop_form, int32_t* wavefront) {
   if (!p) return fail(LL_EINVAL, "plan is NULL");
-  if (nwg) *nwg = p->xmode ? 256 : p->geom.nwg;
-  if (hj) *hj = p->xmode ? (p->bf16 ? 32 : 16) : p->geom.HJ;
-  if (rg) *rg = p->xmode ? 8 : p->geom.RG;
-  if (xcd_local) *xcd_local = p->xmode ? 1 : 0;
+  if (nwg) *nwg = (p->xmode || p->cmode) ? 256 : p->geom.nwg;
+  if (hj) *hj = p->xmode ? (p->bf16 ? 32 : 16) : p->cmode ? p->d.H / 256 : p->geom.HJ;
+  if (rg) *rg = p->xmode ? 8 : p->cmode ? 1 : p->geom.RG;
+  if (loop_form) *loop_form = p->xmode ? LL_LOOPS_XCD : p->cmode ? LL_LOOPS_CHIP : LL_LOOPS_GRID;
   if (wavefront) *wavefront = p->wave ? 1 : 0;
   return LL_OK;
 }
@@ -570,6 +602,28 @@ ll_status ll_plan_geometry(const ll_plan* p, int32_t* nwg, int32_t* hj, int32_t*
 }  // extern "C"
 
 namespace {
+
+// Fields shared by every argument block of a chip-wide launch.
+ll::CLoopArgs c_common(const ll_plan* p) {
+  ll::CLoopArgs a{};
+  a.B = p->d.B;
+  a.H = p->d.H;
+  a.T_max = p->d.T_max;
+  a.MRT = p->cMRT;
+  a.meta = p->meta;
+  a.active = p->active;
+  a.off = p->off;
+  a.perm = p->perm;
+  a.ring = p->cring;
+  a.part = p->cpart;
+  a.rank_ctr = p->cflags;
+  a.xflags = p->cflags + 8;
+  a.pflags = p->cflags + 8 + p->cMRT * 256;
+  a.abort_flag = p->meta + 3;
+  a.err = p->meta + 2;
+  a.limit = p->barrier_ticks;
+  return a;
+}
 
 // Fields shared by both layers' argument blocks of an XCD-local launch.
 ll::XLoopArgs x_common(const ll_plan* p) {
@@ -778,6 +832,29 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       }
       continue;
     }
+    if (p->cmode) {
+      const float* hin = h0 ? h0 + (long)l * B * H : nullptr;
+      ev = tbeg(p, s);
+      LL_HIP(ll::launch_c_prepare<T>(hin, p->perm, B, H, p->cMRT, p->cring, p->cflags, p->cflag_words, s));
+      tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+      ll::CLoopArgs ca = c_common(p);
+      ca.W = p->WT[l];
+      ca.ldw = Il + H;
+      ca.woff = Il;
+      ca.X = p->HH[l];
+      ca.ring_ks = (int)((long)H * p->es / 64);
+      ca.Zx = p->Zx;
+      ca.h0 = hin;
+      ca.c0 = c0 ? c0 + (long)l * B * H : nullptr;
+      ca.stack = save ? p->stack[l] : nullptr;
+      ca.y = (l == L - 1) ? y : nullptr;
+      ca.hT = hT + (long)l * B * H;
+      ca.cT = cT + (long)l * B * H;
+      ev = tbeg(p, s);
+      LL_HIP(ll::c_launch(p->ck.fwd, ca, p->ck.lds_fwd, s));
+      tend(p, s, LL_STAGE_FWD_LOOP, ev);
+      continue;
+    }
     ll::FwdLoopArgs a{};
     a.B = B;
     a.H = H;
@@ -824,7 +901,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   hipEvent_t ev = nullptr;
   // db = sum of the row-group partials
   ev = tbeg(p, s);
-  LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->geom.RG, 4L * H, 4L * H, dbias[l], s));
+  LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, 4L * H, 4L * H, dbias[l], s));
   tend(p, s, LL_STAGE_DW, ev);
   ev = tbeg(p, s);
   // transposed operands of the dW products (reduction over compact rows)
@@ -1059,6 +1136,28 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
         }
       }
     }
+    if (p->cmode) {
+      ev = tbeg(p, s);
+      LL_HIP(ll::launch_zero_u32(p->cflags, p->cflag_words, s));
+      tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+      ll::CLoopArgs ca = c_common(p);
+      ca.W = p->W[l];
+      ca.woff = Il;
+      ca.X = p->DZ;
+      ca.ring_ks = (int)(4L * H * p->es / 64);
+      ca.c0 = p->c0 ? p->c0 + (long)l * B * H : nullptr;
+      ca.stack = p->stack[l];
+      ca.dy = l == L - 1 ? dy : p->dyc;
+      ca.dy_compact = l == L - 1 ? 0 : 1;
+      ca.dhT = dhT ? dhT + (long)l * B * H : nullptr;
+      ca.dcT = dcT ? dcT + (long)l * B * H : nullptr;
+      ca.db = p->db_part;
+      ca.dh0 = dh0 ? dh0 + (long)l * B * H : nullptr;
+      ca.dc0 = dc0 ? dc0 + (long)l * B * H : nullptr;
+      ev = tbeg(p, s);
+      LL_HIP(ll::c_launch(p->ck.bwd, ca, p->ck.lds_bwd, s));
+      tend(p, s, LL_STAGE_BWD_LOOP, ev);
+    }
     ll::BwdLoopArgs a{};
     a.B = B;
     a.H = H;
@@ -1091,7 +1190,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     a.abort_flag = p->meta + 3;
     a.err = p->meta + 2;
     a.limit = p->barrier_ticks;
-    if (!p->xmode) {
+    if (!p->xmode && !p->cmode) {
       ev = tbeg(p, s);
       LL_HIP(ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s));
       tend(p, s, LL_STAGE_BWD_LOOP, ev);

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_PKG, "liblstmloop.so")
 LL_OK, LL_EINVAL, LL_ENOMEM, LL_EHIP, LL_ESTATE, LL_EUNSUPPORTED = range(6)
 LL_F32, LL_BF16 = 0, 1
 LL_DEVERR_SEQ_LEN, LL_DEVERR_BARRIER = 1, 2
+LL_LOOPS_GRID, LL_LOOPS_XCD, LL_LOOPS_CHIP = 0, 1, 2
 STATUS_NAMES = {0: "LL_OK", 1: "LL_EINVAL", 2: "LL_ENOMEM", 3: "LL_EHIP",
                 4: "LL_ESTATE", 5: "LL_EUNSUPPORTED"}
 
@@ -167,8 +168,9 @@ class Plan:
         n, hj, rg, xl, wf = (ctypes.c_int32() for _ in range(5))
         _check(self._lib.ll_plan_geometry(self._h, ctypes.byref(n), ctypes.byref(hj),
                                           ctypes.byref(rg), ctypes.byref(xl), ctypes.byref(wf)))
+        form = {LL_LOOPS_GRID: "grid", LL_LOOPS_XCD: "xcd", LL_LOOPS_CHIP: "chip"}[xl.value]
         return dict(workgroups=n.value, units_per_workgroup=hj.value, row_groups=rg.value,
-                    xcd_local=bool(xl.value), wavefront=bool(wf.value))
+                    loops=form, xcd_local=form == "xcd", wavefront=bool(wf.value))
 
     def fwd(self, x, seq_len, W: Sequence, bias: Sequence, h0, c0, y, hT, cT,
             trip_count=None, save_for_backward: bool = True, stream=None) -> None:

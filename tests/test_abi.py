@@ -93,3 +93,7 @@ def test_binding_constants_match_the_header():
     for name, val in status.items():
         if hasattr(ll, name):
             assert getattr(ll, name) == int(val), name
+    forms = dict(re.findall(r"#define (LL_LOOPS_[A-Z]+) (\d+)", text))
+    assert len(forms) == 3
+    for name, val in forms.items():
+        assert getattr(ll, name) == int(val), name

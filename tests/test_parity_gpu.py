@@ -88,6 +88,38 @@ def test_small_parity(w, loop_mode):
     assert not bad, bad
 
 
+# Shapes whose recurrent weights need more than one XCD: the chip-wide form
+# (bf16 H = 2048, f32 H = 1024), one row tile to all 16, ragged lengths, two
+# layers; against the oracle in that form and in the grid-barrier form.
+CHIP = [
+    W("chip_bf16_b37_i64_h2048_t7", B=37, I=64, H=2048, T_max=7, dtype="bf16", len_lo=0,
+      len_hi=7, random_state=True, seed=41),
+    W("chip_f32_b50_i32_h1024_t9", B=50, I=32, H=1024, T_max=9, dtype="f32", len_lo=1,
+      len_hi=9, random_state=True, seed=42),
+    W("chip_bf16_b256_i32_h2048_t4_mrt16", B=256, I=32, H=2048, T_max=4, dtype="bf16",
+      len_lo=0, len_hi=4, random_state=True, seed=43),
+    W("chip_f32_b9_i8_h1024_t12", B=9, I=8, H=1024, T_max=12, dtype="f32", len_lo=0,
+      len_hi=12, random_state=True, seed=44),
+    W("chip_f32_2layer_b20_i16_h1024_t6", B=20, I=16, H=1024, T_max=6, dtype="f32", layers=2,
+      len_lo=0, len_hi=6, random_state=True, seed=45),
+]
+
+
+@pytest.mark.parametrize("w", CHIP, ids=[w.name for w in CHIP])
+def test_chip_loops_parity(w, loop_mode):
+    say(f"[chip] {w.name} mode={loop_mode}")
+    inp = wl.generate(w)
+    geom = {}
+    res, err = run_case(w, inp, geometry=geom)
+    assert geom["loops"] == ("grid" if loop_mode == "grid" else "chip"), geom
+    assert err == 0
+    ref = oracle_reference(inp, w.layers, w.dtype)
+    assert res["T_eff"] == ref["T_eff"]
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
+
+
 def test_zero_trip_loop_returns_inits_bitwise():
     w = wl.TINY.with_(name="all_zero", random_state=True, with_dy=True, seed=21)
     inp = wl.generate(w)
