@@ -19,9 +19,10 @@
 // One step (forward; the gradient loop is the same with its cell first):
 //   phase A: for every running row tile, wait until the producers of the
 //     wave's k-steps of h_{t-1} have published them, load them from the
-//     exchange ring (device-scope loads), multiply, reduce the 8 waves'
-//     partials in LDS and store the work-group's partial product (16 rows x
-//     16 NCT columns); then publish all tiles' partials at once.
+//     exchange ring (device-scope loads, two tiles ahead), multiply, reduce
+//     the 8 waves' partials in LDS (two buffers, one barrier per tile) and
+//     store the work-group's partial product (16 rows x 16 NCT columns);
+//     then publish all tiles' partials at once.
 //   phase B: wait for the KG partial products of the own N-group, sum them,
 //     add the input projection, run the cell for CW units of every row, store
 //     h_t into the ring with device-scope stores (written through to where
@@ -49,7 +50,9 @@ struct CShape {
   static constexpr int CT = 16 * CW;       // cell threads per row tile
   static constexpr int TPP = CNT / CT;     // row tiles per cell pass
   static constexpr int PW = 16 * 16 * NCT; // partial floats per (work-group, row tile)
-  static constexpr int IS = NCT * 64 + 16; // LDS slice of one wave's partials (padded)
+  static constexpr int RB = CNW * NCT * 256;  // floats of one LDS partial buffer
+  static constexpr int EPT = NCT / 2;          // partial floats each thread reduces
+  static_assert(EPT == 1 || EPT == 2, "reduction split");
   static constexpr int NPROD = KSW * 4 * KPC / CW;   // producers of one wave's k-steps
   static_assert(KSW * KPC == 8 * NCT, "H = 64 KSW KPC = 512 NCT");
   static_assert(CW % KPC == 0 && CT % 64 == 0 && TPP * CT == CNT, "cell layout");
@@ -83,6 +86,66 @@ __device__ __forceinline__ int producer_of(int j) {
   return (j / UX) * 32 + ((v % UN) / CW) * NG + v / UN;
 }
 
+// Wait until every flag this lane names is >= need: flag (tile m, producer
+// pr) for the pairs i = lane + 64 j < n_pairs, m = i / NPROD, pr = i % NPROD;
+// flag index m * 256 + prod[pr] where prod is the lane's producer table.
+template <int NPROD, int NJ>
+__device__ __forceinline__ void wait_tiles(const CLoopArgs& a, const unsigned* flags, int nt, int my_prod,
+                                           unsigned need) {
+  const int lane = threadIdx.x & 63;
+  const unsigned* fp[NJ];
+  bool mine[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int i = lane + 64 * j;
+    const int m = i / NPROD, pr = i % NPROD;
+    // the producer of pair i is the one lane pr names
+    const int id = __shfl(my_prod, pr, 64);
+    mine[j] = m < nt;
+    fp[j] = flags + (mine[j] ? m * 256 + id : 0);
+  }
+  unsigned long long t0 = 0;
+  unsigned polls = 0;
+  while (true) {
+    bool pend = false;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      pend |= mine[j] && __hip_atomic_load(fp[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need;
+    if (__builtin_amdgcn_ballot_w64(pend) == 0) return;
+    if (polls == 0) t0 = wall_clock64();
+    __builtin_amdgcn_s_sleep(1);
+    if ((++polls & 255u) == 0) {
+      if (__hip_atomic_load(a.abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+      if (wall_clock64() - t0 > a.limit) {
+        __hip_atomic_fetch_or(a.err, LL_DEVERR_BARRIER_BIT, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(a.abort_flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+      }
+    }
+  }
+}
+
+// The 8 waves' partial products of one row tile, summed: thread tid takes
+// EPT of the 4 rows of item (column tile, lane) it = tid / (4 / EPT), the
+// LDS buffer being [wave][item] float4.  out(c, rq, e, v) receives column
+// c = ct*16 + lane % 16, row 4 rq + e.
+template <int NCT, int EPT, typename Out>
+__device__ __forceinline__ void reduce_waves(const float4* rb, Out out) {
+  const int tid = threadIdx.x;
+  const int it = tid / (4 / EPT), e0 = (tid % (4 / EPT)) * EPT;
+  const float* rf = reinterpret_cast<const float*>(rb) + it * 4 + e0;
+  float v[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) v[i] = rf[i];
+#pragma unroll
+  for (int w2 = 1; w2 < CNW; ++w2)
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) v[i] += rf[w2 * NCT * 256 + i];
+  const int c = (it >> 6) * 16 + (it & 15), rq = (it >> 4) & 3;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) out(c, rq, e0 + i, v[i]);
+}
+
 // Byte offset of element (row, column n) of row tile m in ring slot sl:
 // blocks of 4 KPC columns, lane l of a block holding row l % 16, columns
 // (l / 16) KPC .. + KPC.
@@ -102,13 +165,13 @@ template <typename T, int KSW, int NCT, int MRT_MAX>
 __global__ __launch_bounds__(CNT, 1) void cfwd_kernel(CLoopArgs a) {
   using S = CShape<T, KSW, NCT>;
   constexpr int KPC = S::KPC, H = S::H, UX = S::UX, KC = S::KC, CW = S::CW, CT = S::CT;
-  constexpr int TPP = S::TPP, PW = S::PW, IS = S::IS, NPROD = S::NPROD;
+  constexpr int TPP = S::TPP, PW = S::PW, RB = S::RB, NPROD = S::NPROD, EPT = S::EPT;
   constexpr int KG = 2, NG = 16, UN = 4 * NCT;
   constexpr int KS = H / (4 * KPC);
   constexpr int NPASS = (MRT_MAX + TPP - 1) / TPP;
   static_assert(NPASS * KG <= 64, "one lane per partial flag");
   constexpr long G4 = 4L * H, H5 = 5L * H;
-  __shared__ float red[CNW * 4 * IS];
+  __shared__ float4 red[2 * RB / 4];
   __shared__ int win[2 * (CWIN + 1)];
   __shared__ int sperm[MRT_MAX * 16];
   __shared__ int s_info[2];
@@ -173,6 +236,30 @@ __global__ __launch_bounds__(CNT, 1) void cfwd_kernel(CLoopArgs a) {
       for (int g = 0; g < 4; ++g) zx[p][g] = ld_f32(rz, zo + g * H * 4);
     }
   };
+  // h history, stack row and y of step tt (A rows running from compact
+  // offset off), from the cell registers, after h_tt is published
+  float gv[NPASS][5];
+  auto flush = [&](int tt, int A, int off) {
+#pragma unroll
+    for (int p = 0; p < NPASS; ++p) {
+      const int m = p * TPP + tp, r = m * 16 + crow;
+      const bool act = r < A;
+      if (act) {
+        const long cr = off + r;
+        HH[cr * H + jc] = Op<T>::from_f32(hs[p]);
+        if (a.stack) {
+          float* st = a.stack + cr * H5 + jc;
+#pragma unroll
+          for (int c = 0; c < 5; ++c) st[(long)c * H] = gv[p][c];
+        }
+      }
+      if (a.y && m < MRT) {
+        const int b = sperm[r];
+        if (b >= 0) a.y[((long)tt * B + b) * H + jc] = act ? hs[p] : 0.f;
+      }
+    }
+  };
+
   for (int t = 0; t < t1; ++t) {
     if (t + 1 > wlo + CWIN) {
       wlo = t;
@@ -183,21 +270,21 @@ __global__ __launch_bounds__(CNT, 1) void cfwd_kernel(CLoopArgs a) {
     const int sl = t & 1;
 
     // ---- phase A: partial products of every running tile
-    auto fetch_a = [&](int m, uint4 (&v)[KSW]) {
-      if (t > 0) {
-        const int u = kb0 * 4 * KPC + lane * CW;
-        wait_each(a, a.xflags + m * 256, producer_of<UX, UN, CW, NG>(u), lane < NPROD, (unsigned)(t + 1));
-      }
+    // every producer of this wave's k-steps has published h_{t-1} of every
+    // running tile (one wait for all tiles: they are published together)
+    if (t > 0)
+      wait_tiles<NPROD, (MRT_MAX * NPROD + 63) / 64>(
+          a, a.xflags, nt, producer_of<UX, UN, CW, NG>(kb0 * 4 * KPC + (lane % NPROD) * CW), (unsigned)(t + 1));
+    auto load_a = [&](int m, uint4 (&v)[KSW]) {
       const __amdgpu_buffer_rsrc_t rs =
           make_rsrc(reinterpret_cast<char*>(a.ring) + ((long)((sl ^ 1) * MRT + m) * KS << 10), (unsigned)KS << 10);
 #pragma unroll
       for (int i = 0; i < KSW; ++i) v[i] = ld_chunk_l2(rs, (unsigned)(((kb0 + i) << 10) + lane * 16));
     };
-    uint4 av[KSW], an[KSW];
-    fetch_a(0, av);
-    for (int m = 0; m < nt; ++m) {
-      if (m + 1 < nt) fetch_a(m + 1, an);
-      // the input projections of this step, issued after the next tile's
+    // tile m: operands in cur; the operands of tile m+2 go to nxt2
+    auto tile = [&](int m, uint4 (&cur)[KSW], uint4 (&nxt2)[KSW]) {
+      if (m + 2 < nt) load_a(m + 2, nxt2);
+      // the input projections of this step, issued after the next tiles'
       // operands so that the first products do not wait for them
       if (m == 0) load_zx(t);
       f32x4 acc[NCT];
@@ -206,26 +293,31 @@ __global__ __launch_bounds__(CNT, 1) void cfwd_kernel(CLoopArgs a) {
 #pragma unroll
       for (int i = 0; i < KSW; ++i)
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) acc[ct] = Mfma<T>::step(av[i], wr[ct][i], acc[ct]);
+        for (int ct = 0; ct < NCT; ++ct) acc[ct] = Mfma<T>::step(cur[i], wr[ct][i], acc[ct]);
+      // LDS buffer m % 2: [wave][ct][lane] float4 (the lane's 4 result rows)
+      float4* rb = red + (m & 1) * (RB / 4);
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) red[(wave * 4 + e) * IS + ct * 64 + lane] = acc[ct][e];
+        rb[(wave * NCT + ct) * 64 + lane] = make_float4(acc[ct][0], acc[ct][1], acc[ct][2], acc[ct][3]);
       __syncthreads();
-      // partial layout: [gate][owner kc][row][CW units], owner kc = u / CW
+      // column c = gate * UN + kc * CW + uu; partial layout
+      // [kc][row / 4][uu][row % 4][gate], so that a cell reads its 4 gates
+      // as one 16-byte load
       float* pd = a.part + ((long)((sl * 8 + x) * MRT + m) * 32 + rank) * PW;
-      for (int o = tid; o < PW; o += CNT) {
-        const int ou = o % CW, orow = (o / CW) & 15, kc = (o / (16 * CW)) % KG, g = o / (16 * CW * KG);
-        const int c = g * UN + kc * CW + ou;
-        const float* rp = red + (orow & 3) * IS + (c >> 4) * 64 + (orow >> 2) * 16 + (c & 15);
-        float s = rp[0];
-#pragma unroll
-        for (int w2 = 1; w2 < CNW; ++w2) s += rp[w2 * 4 * IS];
-        pd[o] = s;
-      }
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < KSW; ++i) av[i] = an[i];
+      reduce_waves<NCT, EPT>(rb, [&](int c, int rq, int e, float v) {
+        const int g = c / UN, u = c - g * UN, kc = u / CW, ou = u - kc * CW;
+        pd[(((kc * 4 + rq) * CW + ou) * 4 + e) * 4 + g] = v;
+      });
+    };
+    // three operand buffers with fixed roles per unrolled tile, so that no
+    // register copy waits for a load in flight
+    uint4 a0[KSW], a1[KSW], a2[KSW];
+    load_a(0, a0);
+    if (nt > 1) load_a(1, a1);
+    for (int m = 0; m < nt; m += 3) {
+      tile(m, a0, a2);
+      if (m + 1 < nt) tile(m + 1, a1, a0);
+      if (m + 2 < nt) tile(m + 2, a2, a1);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -248,14 +340,17 @@ __global__ __launch_bounds__(CNT, 1) void cfwd_kernel(CLoopArgs a) {
       if (m < nt) {
         const long base = (long)((sl * 8 + x) * MRT + m) * 32 * PW;
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
-#pragma unroll
-          for (int k = 0; k < KG; ++k)
-            zs[p][g] += ld_f32_l2(rpart, (unsigned)((base + (long)(k * NG + nq) * PW +
-                                                     (g * KG + kq) * 16 * CW + crow * CW + uu) * 4));
+        for (int k = 0; k < KG; ++k) {
+          const uint4 v = ld_chunk_l2(rpart, (unsigned)((base + (long)(k * NG + nq) * PW +
+                                                         (((kq * 4 + (crow >> 2)) * CW + uu) * 4 + (crow & 3)) * 4) *
+                                                        4));
+          zs[p][0] += __uint_as_float(v.x);
+          zs[p][1] += __uint_as_float(v.y);
+          zs[p][2] += __uint_as_float(v.z);
+          zs[p][3] += __uint_as_float(v.w);
+        }
       }
     }
-    float gv[NPASS][5];
 #pragma unroll
     for (int p = 0; p < NPASS; ++p) {
       const int m = p * TPP + tp, r = m * 16 + crow;
@@ -275,25 +370,7 @@ __global__ __launch_bounds__(CNT, 1) void cfwd_kernel(CLoopArgs a) {
     if (tid < nt)
       __hip_atomic_store(a.xflags + tid * 256 + x * 32 + rank, (unsigned)(t + 2), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
-    // h history, stack, y
-#pragma unroll
-    for (int p = 0; p < NPASS; ++p) {
-      const int m = p * TPP + tp, r = m * 16 + crow;
-      const bool act = m < nt && r < A_t;
-      if (act) {
-        const long cr = off_t + r;
-        HH[cr * H + jc] = Op<T>::from_f32(hs[p]);
-        if (a.stack) {
-          float* st = a.stack + cr * H5 + jc;
-#pragma unroll
-          for (int c = 0; c < 5; ++c) st[(long)c * H] = gv[p][c];
-        }
-      }
-      if (a.y && m < MRT) {
-        const int b = sperm[r];
-        if (b >= 0) a.y[((long)t * B + b) * H + jc] = act ? hs[p] : 0.f;
-      }
-    }
+    flush(t, A_t, off_t);
   }
 
 #pragma unroll
@@ -323,13 +400,13 @@ template <typename T, int KSW, int NCT, int MRT_MAX>
 __global__ __launch_bounds__(CNT, 1) void cbwd_kernel(CLoopArgs a) {
   using S = CShape<T, KSW, NCT>;
   constexpr int KPC = S::KPC, H = S::H, UX = S::UX, KC = S::KC, CW = S::CW, CT = S::CT;
-  constexpr int TPP = S::TPP, PW = S::PW, IS = S::IS, NPROD = S::NPROD;
+  constexpr int TPP = S::TPP, PW = S::PW, RB = S::RB, NPROD = S::NPROD, EPT = S::EPT;
   constexpr int KG = 8, NG = 4, UN = 16 * NCT;
   constexpr int KS = 4 * H / (4 * KPC);
   constexpr int NPASS = (MRT_MAX + TPP - 1) / TPP;
   static_assert(NPASS * KG <= 64, "one lane per partial flag");
   constexpr long G4 = 4L * H, H5 = 5L * H;
-  __shared__ float red[CNW * 4 * IS];
+  __shared__ float4 red[2 * RB / 4];
   __shared__ int win[2 * (CWIN + 1)];
   __shared__ int sperm[MRT_MAX * 16];
   __shared__ int s_info[2];
@@ -422,7 +499,8 @@ __global__ __launch_bounds__(CNT, 1) void cbwd_kernel(CLoopArgs a) {
         float s = 0.f;
 #pragma unroll
         for (int k = 0; k < KG; ++k)
-          s += ld_f32_l2(rpart, (unsigned)((base + (long)(k * NG + nq) * PW + (kq * 16 + crow) * CW + uu) * 4));
+          s += ld_f32_l2(rpart, (unsigned)((base + (long)(k * NG + nq) * PW +
+                                            ((kq * 4 + (crow >> 2)) * CW + uu) * 4 + (crow & 3)) * 4));
         if (r < A_tt) dh[p] = s;
       }
     }
@@ -482,20 +560,20 @@ __global__ __launch_bounds__(CNT, 1) void cbwd_kernel(CLoopArgs a) {
     }
 
     // ---- phase A': partial products of dh_{t-1}
-    auto fetch_a = [&](int m, uint4 (&v)[KSW]) {
-      const int n = kb0 * 4 * KPC + lane * CW;   // dz column of this lane's producer
-      wait_each(a, a.xflags + m * 256, producer_of<UX, UN, CW, NG>(n % H), lane < NPROD,
-                (unsigned)(T_eff - t));
+    // every producer of this wave's dz columns has published dz_t of every
+    // running tile (the wave's columns lie in one gate block)
+    wait_tiles<NPROD, (MRT_MAX * NPROD + 63) / 64>(
+        a, a.xflags, nt, producer_of<UX, UN, CW, NG>((kb0 * 4 * KPC + (lane % NPROD) * CW) % H),
+        (unsigned)(T_eff - t));
+    auto load_a = [&](int m, uint4 (&v)[KSW]) {
       const __amdgpu_buffer_rsrc_t rs =
           make_rsrc(reinterpret_cast<char*>(a.ring) + ((long)(sl * MRT + m) * KS << 10), (unsigned)KS << 10);
 #pragma unroll
       for (int i = 0; i < KSW; ++i) v[i] = ld_chunk_l2(rs, (unsigned)(((kb0 + i) << 10) + lane * 16));
     };
-    uint4 av[KSW], an[KSW];
-    fetch_a(0, av);
-    for (int m = 0; m < nt; ++m) {
-      if (m + 1 < nt) fetch_a(m + 1, an);
-      // pops of step t-1, issued after the next tile's operands
+    auto tile = [&](int m, uint4 (&cur)[KSW], uint4 (&nxt2)[KSW]) {
+      if (m + 2 < nt) load_a(m + 2, nxt2);
+      // pops of step t-1, issued after the next tiles' operands
       if (m == 0 && t >= 1) fetch(t - 1);
       f32x4 acc[NCT];
 #pragma unroll
@@ -503,26 +581,26 @@ __global__ __launch_bounds__(CNT, 1) void cbwd_kernel(CLoopArgs a) {
 #pragma unroll
       for (int i = 0; i < KSW; ++i)
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) acc[ct] = Mfma<T>::step(av[i], wr[ct][i], acc[ct]);
+        for (int ct = 0; ct < NCT; ++ct) acc[ct] = Mfma<T>::step(cur[i], wr[ct][i], acc[ct]);
+      float4* rb = red + (m & 1) * (RB / 4);
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) red[(wave * 4 + e) * IS + ct * 64 + lane] = acc[ct][e];
+        rb[(wave * NCT + ct) * 64 + lane] = make_float4(acc[ct][0], acc[ct][1], acc[ct][2], acc[ct][3]);
       __syncthreads();
-      // partial layout: [owner kc][row][CW units], owner kc = u / CW
+      // local unit c = kc * CW + uu; partial layout [kc][row / 4][uu][row % 4]
       float* pd = a.part + ((long)((sl * 8 + x) * MRT + m) * 32 + rank) * PW;
-      for (int o = tid; o < PW; o += CNT) {
-        const int ou = o % CW, orow = (o / CW) & 15, kc = o / (16 * CW);
-        const int c = kc * CW + ou;
-        const float* rp = red + (orow & 3) * IS + (c >> 4) * 64 + (orow >> 2) * 16 + (c & 15);
-        float s = rp[0];
-#pragma unroll
-        for (int w2 = 1; w2 < CNW; ++w2) s += rp[w2 * 4 * IS];
-        pd[o] = s;
-      }
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < KSW; ++i) av[i] = an[i];
+      reduce_waves<NCT, EPT>(rb, [&](int c, int rq, int e, float v) {
+        const int kc = c / CW, ou = c - kc * CW;
+        pd[((kc * 4 + rq) * CW + ou) * 4 + e] = v;
+      });
+    };
+    uint4 a0[KSW], a1[KSW], a2[KSW];
+    load_a(0, a0);
+    if (nt > 1) load_a(1, a1);
+    for (int m = 0; m < nt; m += 3) {
+      tile(m, a0, a2);
+      if (m + 1 < nt) tile(m + 1, a1, a0);
+      if (m + 2 < nt) tile(m + 2, a2, a1);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -543,13 +621,14 @@ __global__ __launch_bounds__(CNT, 1) void cbwd_kernel(CLoopArgs a) {
   // db of the work-group's CW units (each unit's cell runs on exactly one
   // work-group): sum over the cell threads of the unit, fixed order
   __syncthreads();
+  float* rf = reinterpret_cast<float*>(red);
 #pragma unroll
-  for (int g = 0; g < 4; ++g) red[g * CNT + tid] = dbacc[g];
+  for (int g = 0; g < 4; ++g) rf[g * CNT + tid] = dbacc[g];
   __syncthreads();
   if (tid < 4 * CW) {
     const int g = tid / CW, u = tid % CW;
     float s = 0.f;
-    for (int i = u; i < CNT; i += CW) s += red[g * CNT + i];
+    for (int i = u; i < CNT; i += CW) s += rf[g * CNT + i];
     a.db[(long)g * H + x * UX + nq * UN + kq * CW + u] = s;
   }
 }
