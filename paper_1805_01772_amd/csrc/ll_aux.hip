@@ -131,40 +131,59 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in
 //   mode 2: h_{t-1} of that row: t = rowmap[k] / B, r = k - off[t];
 //           t > 0: in + (off[t-1] + r) * C (compact history of h);
 //           t = 0: bf/fp conversion of h0f[perm[r] * C] (float, NULL = 0).
+// A 64 x 64 tile per work-group, moved in 16-byte chunks both ways: thread
+// (row k, chunk) loads KPC consecutive columns of one source row, the tile
+// goes through LDS (row pitch padded by one chunk), and thread (column c,
+// chunk) stores KPC consecutive k of one output row.  C is a multiple of KPC
+// (the plan checks I and H), so no chunk straddles the end of a row; chunks
+// of k past the sum of lengths are written as zeros.
 template <typename T>
 __global__ __launch_bounds__(256) void gather_transpose_kernel(GatherTArgs g) {
-  __shared__ T tile[64][65];
+  constexpr int KPC = Op<T>::kPerChunk;
+  constexpr int CPR = 64 / KPC;              // chunks per 64-element tile row
+  __shared__ T tile[64][64 + KPC];
   const int total = g.meta[1];
   const int k0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
   if (k0 >= total) return;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
   const T* in = reinterpret_cast<const T*>(g.in);
-  for (int i = ty; i < 64; i += 4) {
-    const int k = k0 + i, c = c0 + tx;
+  for (int i = tid; i < 64 * CPR; i += 256) {
+    const int kr = i / CPR, ch = i % CPR;
+    const int k = k0 + kr, c = c0 + ch * KPC;
+    uint4 v = zero4();
     if (k < total && c < g.C) {
-      T v;
       if (g.mode == 0) {
-        v = in[(long)g.rowmap[k] * g.C + c];
+        v = ld16(in + (long)g.rowmap[k] * g.C + c);
       } else if (g.mode == 1) {
-        v = in[(long)k * g.C + c];
+        v = ld16(in + (long)k * g.C + c);
       } else {
         const int t = g.rowmap[k] / g.B;
         const int r = k - g.off[t];
         if (t > 0) {
-          v = in[(long)(g.off[t - 1] + r) * g.C + c];
-        } else {
-          const float f = g.h0f ? g.h0f[(long)g.perm[r] * g.C + c] : 0.0f;
-          v = Op<T>::from_f32(f);
+          v = ld16(in + (long)(g.off[t - 1] + r) * g.C + c);
+        } else if (g.h0f) {
+          const float* f = g.h0f + (long)g.perm[r] * g.C + c;
+          T tmp[KPC];
+#pragma unroll
+          for (int e = 0; e < KPC; ++e) tmp[e] = Op<T>::from_f32(f[e]);
+          __builtin_memcpy(&v, tmp, 16);
         }
       }
-      tile[i][tx] = v;
     }
+    __builtin_memcpy(&tile[kr][ch * KPC], &v, 16);
   }
   __syncthreads();
   T* out = reinterpret_cast<T*>(g.out);
-  for (int i = ty; i < 64; i += 4) {
-    const int c = c0 + i, k = k0 + tx;
-    if (c < g.C && k < total) out[(long)c * g.ldo + k] = tile[tx][i];
+  for (int i = tid; i < 64 * CPR; i += 256) {
+    const int cr = i / CPR, ch = i % CPR;
+    const int c = c0 + cr, k = k0 + ch * KPC;
+    if (c >= g.C) continue;
+    T tmp[KPC];
+#pragma unroll
+    for (int e = 0; e < KPC; ++e) tmp[e] = tile[ch * KPC + e][cr];
+    uint4 v;
+    __builtin_memcpy(&v, tmp, 16);
+    *reinterpret_cast<uint4*>(out + (long)c * g.ldo + k) = v;
   }
 }
 
