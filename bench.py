@@ -105,19 +105,22 @@ def cpu_baseline(w, inp, target_s):
 # figures are used only while the kernel source they were taken on is
 # unchanged.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.md")
-KERNEL_SOURCES = {"fwd_loop": "paper_1805_01772_amd/csrc/ll_xloop.hip",
-                  "bwd_loop": "paper_1805_01772_amd/csrc/ll_xloop.hip"}
+LOOP_STAGES = ("fwd_loop", "bwd_loop")
 
 
-def source_hash(rel):
+def source_hash(rels):
+    """Hash of the kernel sources (a list of repository-relative paths)."""
     import hashlib
-    with open(os.path.join(ROOT, rel), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for rel in rels:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def recorded_traffic(kernel, workload):
     """Bytes per launch recorded for (kernel, workload), or None."""
-    if kernel not in KERNEL_SOURCES or not os.path.exists(TRAFFIC_FILE):
+    if kernel not in LOOP_STAGES or not os.path.exists(TRAFFIC_FILE):
         return None
     text = open(TRAFFIC_FILE).read()
     if "```json" not in text:
@@ -128,7 +131,7 @@ def recorded_traffic(kernel, workload):
     except ValueError:
         return None
     ent = rec.get("entries", {}).get(f"{kernel}/{workload}")
-    if not ent or ent.get("source_sha256_16") != source_hash(KERNEL_SOURCES[kernel]):
+    if not ent or not ent.get("sources") or ent.get("source_sha256_16") != source_hash(ent["sources"]):
         return None
     return float(ent["bytes_per_launch"])
 
