@@ -157,7 +157,7 @@ def main():
               "(the data-parallel split over GPUs is described, not run)", file=sys.stderr)
         sys.exit(2)
     import torch
-    from paper_1805_01772_amd import workloads as wl
+    from paper_1805_01772_amd import lstmloop, workloads as wl
     from paper_1805_01772_amd.runner import DeviceCase
 
     w = wl.BY_NAME[args.workload]
@@ -181,16 +181,17 @@ def main():
             raise RuntimeError("device error during warmup")
         plan.set_timing(timing)
         stream = torch.cuda.current_stream()
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        ev0.record(stream)
-        for _ in range(args.steps):
+        evs[0].record(stream)
+        for k in range(args.steps):
             dc.fwd(plan)
             dc.bwd(plan)
-        ev1.record(stream)
+            evs[k + 1].record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        per_step = [evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)]
         stages = plan.read_timing()
         plan.set_timing(False)
         err = plan.status_sync()
@@ -198,9 +199,9 @@ def main():
             raise RuntimeError(f"device error word {err}")
         geom, sbytes = plan.geometry(), plan.stack_bytes()
         plan.close()
-        return ev0.elapsed_time(ev1), wall, stages, geom, sbytes
+        return evs[0].elapsed_time(evs[-1]), wall, stages, geom, sbytes, per_step
 
-    gpu_ms, wall, stages, geom, sbytes = timed(plan_kw, True)
+    gpu_ms, wall, stages, geom, sbytes, per_step = timed(plan_kw, True)
     spill = None
     if w.spill:
         res_ms = timed({}, False)[0]
@@ -220,6 +221,12 @@ def main():
     dom = max(("fwd_loop", "bwd_loop", "input_proj", "dw", "dx"), key=lambda k: stages[k][0])
     achieved = sflops[dom] / (per_launch[dom] / 1e3) / 1e12
     peak_tf = PEAK[w.dtype] / 1e12
+    measured_peak = lstmloop.ll_measure_mfma_peak(w.dtype)
+    # what a loop over T_eff (or T_max) padded steps would execute: every
+    # sequence runs every step (a static unroll to the longest sequence)
+    padded = {f"T_{n}": sum(24.0 * w.H * ((w.I if l == 0 else w.H) + w.H) * w.B * T
+                            for l in range(w.layers)) for n, T in (("eff", T_eff), ("max", w.T_max))}
+    q = np.percentile(per_step, [5, 50, 95])
     out = {
         "metric": METRIC,
         "value": value,
@@ -238,12 +245,18 @@ def main():
                    "sum_len": sum_len, "T_eff": T_eff, "loop_workgroups": geom["workgroups"],
                    "units_per_workgroup": geom["units_per_workgroup"]},
         "mfma_util": mfma_util,
+        "mfma_util_of_measured_peak": flops / (ms_per_step / 1e3) / (measured_peak * 1e12),
+        "measured_mfma_peak_tflops": measured_peak,
+        "step_ms": {"median": q[1], "p5": q[0], "p95": q[2]},
+        "padded_flops_per_step": padded,
+        "flops_skipped_vs_padded_T_eff": 1.0 - flops / padded["T_eff"],
         "per_iteration_us": ms_per_step * 1e3 / T_eff if T_eff else None,
         "algorithmic_tflops": flops / (ms_per_step / 1e3) / 1e12,
         "host_wall_ms_per_step": wall * 1e3 / args.steps,
         "stage_ms_per_step": {k: ms / args.steps for k, (ms, n) in stages.items()},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak_tf,
                      "unit": "TFLOP/s", "frac": achieved / peak_tf,
+                     "frac_of_measured_peak": achieved / measured_peak,
                      "traffic": recorded_traffic(dom, w.name),
                      "per_launch_ms": per_launch[dom],
                      "algorithmic_flops_per_launch": sflops[dom]},

@@ -220,6 +220,13 @@ ll_status ll_plan_set_timing(ll_plan* plan, int32_t enable);
 ll_status ll_plan_read_timing(ll_plan* plan, int32_t stage, double* total_ms,
                               int64_t* instances);
 
+/* Diagnostic for reports: the sustained dense matrix-core rate of `device`
+ * for `dtype` (LL_BF16: 16x16x32 bfloat16 MFMA; LL_F32: 16x16x4 float MFMA)
+ * in TFLOP/s, measured with a kernel in which every wave runs independent
+ * MFMA chains on every CU (about 10 ms; synchronous).  Kernels of the loops
+ * can be compared with it as well as with the datasheet peak. */
+ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, double* tflops);
+
 /* Library version string. */
 const char* ll_version(void);
 

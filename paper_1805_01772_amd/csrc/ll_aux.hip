@@ -239,6 +239,58 @@ hipError_t launch_transpose(const T* in, int R, int C, int ldi, T* out, int ldo,
   return hipGetLastError();
 }
 
+// Sustained matrix-core rate: every wave runs 8 independent accumulator
+// chains of the operand type's k-step (Mfma<T>::step) for `iters` rounds.
+template <typename T>
+__global__ __launch_bounds__(256) void mfma_peak_kernel(int iters, float* sink) {
+  const uint4 a = make_uint4(0x3f803f80u + threadIdx.x, 0x3f803f80u, 0x3c003c00u, 0x3f803f80u);
+  const uint4 b = make_uint4(0x3f803f80u, 0x3f803f80u + blockIdx.x, 0x3f803f80u, 0x3c003c00u);
+  f32x4 acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = Mfma<T>::step(a, b, acc[c]);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) s += acc[c][0] + acc[c][1] + acc[c][2] + acc[c][3];
+  if (s == 1234.5f) sink[threadIdx.x] = s;
+}
+
+template <typename T>
+hipError_t measure_mfma_peak(int n_cu, double* tflops) {
+  constexpr double flop_per_step = sizeof(T) == 2 ? 16.0 * 16 * 32 * 2 : 4.0 * 16 * 16 * 4 * 2;
+  const int iters = sizeof(T) == 2 ? 20000 : 2000;
+  const int blocks = n_cu * 8;
+  float* sink = nullptr;
+  hipStream_t st = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  hipError_t e = hipMalloc(&sink, 256 * sizeof(float));
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  float ms = 0.f;
+  for (int rep = 0; rep < 2 && e == hipSuccess; ++rep) {   // the first launch warms up
+    hipLaunchKernelGGL(mfma_peak_kernel<T>, dim3(blocks), dim3(256), 0, st, iters, sink);
+    e = hipEventRecord(e0, st);
+    if (e == hipSuccess) hipLaunchKernelGGL(mfma_peak_kernel<T>, dim3(blocks), dim3(256), 0, st, iters, sink);
+    if (e == hipSuccess) e = hipGetLastError();
+    if (e == hipSuccess) e = hipEventRecord(e1, st);
+    if (e == hipSuccess) e = hipEventSynchronize(e1);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  }
+  if (e == hipSuccess && ms > 0.f)
+    *tflops = (double)blocks * 4 * 8 * iters * flop_per_step / (ms * 1e-3) / 1e12;
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (st) (void)hipStreamDestroy(st);
+  if (sink) (void)hipFree(sink);
+  return e;
+}
+template hipError_t measure_mfma_peak<float>(int, double*);
+template hipError_t measure_mfma_peak<bf16_t>(int, double*);
+
 template <typename T>
 hipError_t launch_gather_transpose(const GatherTArgs& g, int cap_rows, hipStream_t s) {
   dim3 grid((cap_rows + 63) / 64, (g.C + 63) / 64);

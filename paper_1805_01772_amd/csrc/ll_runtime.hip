@@ -290,6 +290,21 @@ const char* ll_last_error(void) { return g_last_error.c_str(); }
 
 const char* ll_version(void) { return "lstmloop 0.1 (gfx950)"; }
 
+ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, double* tflops) {
+  if (!tflops) return fail(LL_EINVAL, "tflops is NULL");
+  if (dtype != LL_F32 && dtype != LL_BF16) return fail(LL_EINVAL, "dtype must be LL_F32 or LL_BF16");
+  int ndev = 0;
+  LL_HIP(hipGetDeviceCount(&ndev));
+  if (device < 0 || device >= ndev) return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
+  DeviceGuard guard(device);
+  hipDeviceProp_t prop;
+  LL_HIP(hipGetDeviceProperties(&prop, device));
+  *tflops = 0.0;
+  LL_HIP(dtype == LL_BF16 ? ll::measure_mfma_peak<bf16_t>(prop.multiProcessorCount, tflops)
+                          : ll::measure_mfma_peak<float>(prop.multiProcessorCount, tflops));
+  return LL_OK;
+}
+
 ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   if (!out) return fail(LL_EINVAL, "out is NULL");
   *out = nullptr;

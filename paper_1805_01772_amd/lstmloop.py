@@ -24,7 +24,7 @@ STATUS_NAMES = {0: "LL_OK", 1: "LL_EINVAL", 2: "LL_ENOMEM", 3: "LL_EHIP",
 EXPORTED = ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes",
             "ll_plan_geometry", "lstm_loop_fwd", "lstm_loop_bwd",
             "ll_status_sync", "ll_last_error", "ll_version",
-            "ll_plan_set_timing", "ll_plan_read_timing")
+            "ll_plan_set_timing", "ll_plan_read_timing", "ll_measure_mfma_peak")
 STAGES = ("prep", "input_proj", "fwd_loop", "bwd_loop", "bwd_operands", "dw", "dx", "loop_setup")
 
 
@@ -75,11 +75,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ll_plan_set_timing.argtypes = [vp, i32]
     lib.ll_plan_read_timing.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(i64)]
+    lib.ll_measure_mfma_peak.argtypes = [ctypes.c_int, i32, ctypes.POINTER(ctypes.c_double)]
     lib.ll_last_error.restype = ctypes.c_char_p
     lib.ll_version.restype = ctypes.c_char_p
     for name in ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes", "ll_plan_geometry",
                  "lstm_loop_fwd", "lstm_loop_bwd", "ll_status_sync", "ll_plan_set_timing",
-                 "ll_plan_read_timing"):
+                 "ll_plan_read_timing", "ll_measure_mfma_peak"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -87,6 +88,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
 
 def ll_last_error() -> str:
     return load_library().ll_last_error().decode()
+
+
+def ll_measure_mfma_peak(dtype: str, device: int = 0) -> float:
+    """Sustained dense matrix-core rate of the device in TFLOP/s
+    (dtype "bf16" or "f32")."""
+    v = ctypes.c_double()
+    _check(load_library().ll_measure_mfma_peak(device, LL_BF16 if dtype == "bf16" else LL_F32,
+                                               ctypes.byref(v)))
+    return v.value
 
 
 def ll_version() -> str:
