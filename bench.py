@@ -221,7 +221,8 @@ def main():
     dom = max(("fwd_loop", "bwd_loop", "input_proj", "dw", "dx"), key=lambda k: stages[k][0])
     achieved = sflops[dom] / (per_launch[dom] / 1e3) / 1e12
     peak_tf = PEAK[w.dtype] / 1e12
-    measured_peak = lstmloop.ll_measure_mfma_peak(w.dtype)
+    measured_peak = lstmloop.ll_measure_mfma_peak(w.dtype, 32)
+    measured_16 = lstmloop.ll_measure_mfma_peak(w.dtype, 16)
     # what a loop over T_eff (or T_max) padded steps would execute: every
     # sequence runs every step (a static unroll to the longest sequence)
     padded = {f"T_{n}": sum(24.0 * w.H * ((w.I if l == 0 else w.H) + w.H) * w.B * T
@@ -247,6 +248,7 @@ def main():
         "mfma_util": mfma_util,
         "mfma_util_of_measured_peak": flops / (ms_per_step / 1e3) / (measured_peak * 1e12),
         "measured_mfma_peak_tflops": measured_peak,
+        "measured_mfma_rate_16x16_tflops": measured_16,
         "step_ms": {"median": q[1], "p5": q[0], "p95": q[2]},
         "padded_flops_per_step": padded,
         "flops_skipped_vs_padded_T_eff": 1.0 - flops / padded["T_eff"],

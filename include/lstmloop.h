@@ -221,11 +221,14 @@ ll_status ll_plan_read_timing(ll_plan* plan, int32_t stage, double* total_ms,
                               int64_t* instances);
 
 /* Diagnostic for reports: the sustained dense matrix-core rate of `device`
- * for `dtype` (LL_BF16: 16x16x32 bfloat16 MFMA; LL_F32: 16x16x4 float MFMA)
- * in TFLOP/s, measured with a kernel in which every wave runs independent
- * MFMA chains on every CU (about 10 ms; synchronous).  Kernels of the loops
- * can be compared with it as well as with the datasheet peak. */
-ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, double* tflops);
+ * for `dtype` in TFLOP/s, measured with a kernel in which every wave runs
+ * independent MFMA chains on every CU (about 10 ms; synchronous).
+ *   shape = 16: the 16x16 k-step the loops use (16x16x32 bfloat16, or four
+ *               16x16x4 float instructions);
+ *   shape = 32: the 32x32 shape (32x32x16 bfloat16, 32x32x2 float), which on
+ *               gfx950 runs at the datasheet rate.
+ * Other shape values give LL_EINVAL. */
+ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, int32_t shape, double* tflops);
 
 /* Library version string. */
 const char* ll_version(void);

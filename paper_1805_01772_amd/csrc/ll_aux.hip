@@ -240,27 +240,52 @@ hipError_t launch_transpose(const T* in, int R, int C, int ldi, T* out, int ldo,
 }
 
 // Sustained matrix-core rate: every wave runs 8 independent accumulator
-// chains of the operand type's k-step (Mfma<T>::step) for `iters` rounds.
-template <typename T>
+// chains for `iters` rounds, of the 16x16 k-step the loops use
+// (SHAPE32 = false: 16x16x32 bf16 / four 16x16x4 f32) or of the 32x32 shape
+// (true: 32x32x16 bf16 / 32x32x2 f32).
+template <typename T, bool SHAPE32>
 __global__ __launch_bounds__(256) void mfma_peak_kernel(int iters, float* sink) {
   const uint4 a = make_uint4(0x3f803f80u + threadIdx.x, 0x3f803f80u, 0x3c003c00u, 0x3f803f80u);
   const uint4 b = make_uint4(0x3f803f80u, 0x3f803f80u + blockIdx.x, 0x3f803f80u, 0x3c003c00u);
-  f32x4 acc[8];
-#pragma unroll
-  for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int i = 0; i < iters; ++i) {
-#pragma unroll
-    for (int c = 0; c < 8; ++c) acc[c] = Mfma<T>::step(a, b, acc[c]);
-  }
   float s = 0.f;
+  if constexpr (SHAPE32) {
+    typedef __attribute__((ext_vector_type(16))) float f32x16;
+    f32x16 acc[8];
 #pragma unroll
-  for (int c = 0; c < 8; ++c) s += acc[c][0] + acc[c][1] + acc[c][2] + acc[c][3];
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        if constexpr (sizeof(T) == 2)
+          acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                          __builtin_bit_cast(bf16x8_t, b), acc[c], 0, 0, 0);
+        else
+          acc[c] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.y), acc[c], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) s += acc[c][0] + acc[c][15];
+  } else {
+    f32x4 acc[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < iters; ++i) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[c] = Mfma<T>::step(a, b, acc[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) s += acc[c][0] + acc[c][1] + acc[c][2] + acc[c][3];
+  }
   if (s == 1234.5f) sink[threadIdx.x] = s;
 }
 
 template <typename T>
-hipError_t measure_mfma_peak(int n_cu, double* tflops) {
-  constexpr double flop_per_step = sizeof(T) == 2 ? 16.0 * 16 * 32 * 2 : 4.0 * 16 * 16 * 4 * 2;
+hipError_t measure_mfma_peak(int n_cu, bool shape32, double* tflops) {
+  // flops of one chain round: 16x16x32 bf16, four 16x16x4 f32, 32x32x16 bf16, one 32x32x2 f32
+  const double flop_per_step = shape32 ? (sizeof(T) == 2 ? 32.0 * 32 * 16 * 2 : 32.0 * 32 * 2 * 2)
+                                       : (sizeof(T) == 2 ? 16.0 * 16 * 32 * 2 : 4.0 * 16 * 16 * 4 * 2);
   const int iters = sizeof(T) == 2 ? 20000 : 2000;
   const int blocks = n_cu * 8;
   float* sink = nullptr;
@@ -270,12 +295,16 @@ hipError_t measure_mfma_peak(int n_cu, double* tflops) {
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreate(&e0);
   if (e == hipSuccess) e = hipEventCreate(&e1);
+  const void* fn = shape32 ? reinterpret_cast<const void*>(&mfma_peak_kernel<T, true>)
+                           : reinterpret_cast<const void*>(&mfma_peak_kernel<T, false>);
   float ms = 0.f;
+  int it = iters;
+  float* sk = sink;
+  void* kargs[] = {&it, &sk};
   for (int rep = 0; rep < 2 && e == hipSuccess; ++rep) {   // the first launch warms up
-    hipLaunchKernelGGL(mfma_peak_kernel<T>, dim3(blocks), dim3(256), 0, st, iters, sink);
-    e = hipEventRecord(e0, st);
-    if (e == hipSuccess) hipLaunchKernelGGL(mfma_peak_kernel<T>, dim3(blocks), dim3(256), 0, st, iters, sink);
-    if (e == hipSuccess) e = hipGetLastError();
+    e = hipLaunchKernel(fn, dim3(blocks), dim3(256), kargs, 0, st);
+    if (e == hipSuccess) e = hipEventRecord(e0, st);
+    if (e == hipSuccess) e = hipLaunchKernel(fn, dim3(blocks), dim3(256), kargs, 0, st);
     if (e == hipSuccess) e = hipEventRecord(e1, st);
     if (e == hipSuccess) e = hipEventSynchronize(e1);
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
@@ -288,8 +317,8 @@ hipError_t measure_mfma_peak(int n_cu, double* tflops) {
   if (sink) (void)hipFree(sink);
   return e;
 }
-template hipError_t measure_mfma_peak<float>(int, double*);
-template hipError_t measure_mfma_peak<bf16_t>(int, double*);
+template hipError_t measure_mfma_peak<float>(int, bool, double*);
+template hipError_t measure_mfma_peak<bf16_t>(int, bool, double*);
 
 template <typename T>
 hipError_t launch_gather_transpose(const GatherTArgs& g, int cap_rows, hipStream_t s) {

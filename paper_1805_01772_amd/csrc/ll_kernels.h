@@ -246,9 +246,10 @@ hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, 
                                 int slot, void* ring, unsigned* flags, int nflags, hipStream_t s);
 hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s);
 
-// Sustained matrix-core rate of the device (TFLOP/s), for reports.
+// Sustained matrix-core rate of the device (TFLOP/s), for reports: the 16x16
+// k-step the loops use, or the 32x32 shape.
 template <typename T>
-hipError_t measure_mfma_peak(int n_cu, double* tflops);
+hipError_t measure_mfma_peak(int n_cu, bool shape32, double* tflops);
 
 hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
                        int* rowmap, int* meta, int* trip_out, hipStream_t s);

@@ -290,9 +290,10 @@ const char* ll_last_error(void) { return g_last_error.c_str(); }
 
 const char* ll_version(void) { return "lstmloop 0.1 (gfx950)"; }
 
-ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, double* tflops) {
+ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, int32_t shape, double* tflops) {
   if (!tflops) return fail(LL_EINVAL, "tflops is NULL");
   if (dtype != LL_F32 && dtype != LL_BF16) return fail(LL_EINVAL, "dtype must be LL_F32 or LL_BF16");
+  if (shape != 16 && shape != 32) return fail(LL_EINVAL, "shape must be 16 or 32 (got %d)", shape);
   int ndev = 0;
   LL_HIP(hipGetDeviceCount(&ndev));
   if (device < 0 || device >= ndev) return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
@@ -300,8 +301,8 @@ ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, double* tflops) {
   hipDeviceProp_t prop;
   LL_HIP(hipGetDeviceProperties(&prop, device));
   *tflops = 0.0;
-  LL_HIP(dtype == LL_BF16 ? ll::measure_mfma_peak<bf16_t>(prop.multiProcessorCount, tflops)
-                          : ll::measure_mfma_peak<float>(prop.multiProcessorCount, tflops));
+  LL_HIP(dtype == LL_BF16 ? ll::measure_mfma_peak<bf16_t>(prop.multiProcessorCount, shape == 32, tflops)
+                          : ll::measure_mfma_peak<float>(prop.multiProcessorCount, shape == 32, tflops));
   return LL_OK;
 }
 

@@ -75,7 +75,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ll_plan_set_timing.argtypes = [vp, i32]
     lib.ll_plan_read_timing.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(i64)]
-    lib.ll_measure_mfma_peak.argtypes = [ctypes.c_int, i32, ctypes.POINTER(ctypes.c_double)]
+    lib.ll_measure_mfma_peak.argtypes = [ctypes.c_int, i32, i32, ctypes.POINTER(ctypes.c_double)]
     lib.ll_last_error.restype = ctypes.c_char_p
     lib.ll_version.restype = ctypes.c_char_p
     for name in ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes", "ll_plan_geometry",
@@ -90,11 +90,11 @@ def ll_last_error() -> str:
     return load_library().ll_last_error().decode()
 
 
-def ll_measure_mfma_peak(dtype: str, device: int = 0) -> float:
+def ll_measure_mfma_peak(dtype: str, shape: int = 32, device: int = 0) -> float:
     """Sustained dense matrix-core rate of the device in TFLOP/s
-    (dtype "bf16" or "f32")."""
+    (dtype "bf16" or "f32"; shape 16: the loops' 16x16 k-step, 32: 32x32)."""
     v = ctypes.c_double()
-    _check(load_library().ll_measure_mfma_peak(device, LL_BF16 if dtype == "bf16" else LL_F32,
+    _check(load_library().ll_measure_mfma_peak(device, LL_BF16 if dtype == "bf16" else LL_F32, shape,
                                                ctypes.byref(v)))
     return v.value
 
