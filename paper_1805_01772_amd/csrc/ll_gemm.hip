@@ -148,6 +148,8 @@ __global__ __launch_bounds__(256, 2) void gemm_nt_kernel(GemmArgs g) {
   }
 }
 
+long gemm_groups(long M, long N) { return ((N + 127) / 128) * ((M + 127) / 128); }
+
 template <typename T>
 hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s) {
   dim3 grid((g.N + 127) / 128, (g.M + 127) / 128, g.splits);

@@ -266,6 +266,8 @@ hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s);
 
 template <typename T>
 hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s);
+// Work-groups of a GEMM launch with M x N outputs (one split).
+long gemm_groups(long M, long N);
 
 // Recurrent loops (cooperative launches).
 template <typename T>

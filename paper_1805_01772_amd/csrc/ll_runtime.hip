@@ -123,6 +123,10 @@ struct ll_plan {
   long slot_floats = 0;
   float* host_stack[2] = {nullptr, nullptr};
   hipStream_t cstream = nullptr;
+  // side stream for the dx product, which runs beside the dW products after
+  // the gradient loop (forked from and joined back into the call's stream)
+  hipStream_t gstream = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   hipEvent_t ev_compute = nullptr;
   std::vector<hipEvent_t> ev_d2h, ev_h2d;   // per (layer, slot)
   float* carry = nullptr;      // [4][B, H]: h, c (forward) / dh, dc (backward) between chunks
@@ -217,6 +221,9 @@ void free_plan_memory(ll_plan* p) {
     if (e) (void)hipEventDestroy(e);
   if (p->ev_compute) (void)hipEventDestroy(p->ev_compute);
   if (p->cstream) (void)hipStreamDestroy(p->cstream);
+  if (p->ev_fork) (void)hipEventDestroy(p->ev_fork);
+  if (p->ev_join) (void)hipEventDestroy(p->ev_join);
+  if (p->gstream) (void)hipStreamDestroy(p->gstream);
 }
 
 ll_status dalloc(void** out, size_t bytes, const char* what) {
@@ -532,6 +539,13 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     free_plan_memory(p);
     delete p;
     return fail(LL_EHIP, "hipMemset of the plan's meta words failed");
+  }
+  if (hipStreamCreateWithFlags(&p->gstream, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&p->ev_fork, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&p->ev_join, hipEventDisableTiming) != hipSuccess) {
+    free_plan_memory(p);
+    delete p;
+    return fail(LL_EHIP, "creating the plan's side stream failed");
   }
   if (p->spill) {
     const size_t hbytes = sizeof(float) * (size_t)p->nchunks * (size_t)p->slot_floats;
@@ -915,6 +929,44 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   const int H = d.H, B = d.B;
   const int Il = in_width(p, l);
   hipEvent_t ev = nullptr;
+  // dx_t = dz_t W_x^T: scattered to time-major dx (layer 0) or kept compact
+  // as the gradient of the layer below (layer 1).  A product whose grid fills
+  // the chip at most a few times runs on the side stream beside the dW
+  // products (both only read dz) and is joined back before returning; a
+  // larger one runs after them on the call's stream (measured: two large
+  // products side by side only slow each other).
+  auto dx_product = [&](hipStream_t st) -> ll_status {
+    hipEvent_t evx = tbeg(p, st);
+    ll::GemmArgs g{};
+    g.A = dz;
+    g.lda = 4L * H;
+    g.Bm = p->W[l];
+    g.ldb = 4L * H;
+    g.M = (int)p->cap;
+    g.M_dev = p->meta + 1;
+    g.N = Il;
+    g.K = 4 * H;
+    g.splits = 1;
+    g.C = dx;
+    if (l == 0) {
+      g.ldc = d.I;
+      g.c_rowmap = p->rowmap;
+    } else {
+      g.ldc = H;
+    }
+    LL_HIP(ll::launch_gemm_nt<T>(g, st));
+    tend(p, st, LL_STAGE_DX, evx);
+    return LL_OK;
+  };
+  // (the grid covers the row capacity T_max * B; groups past the running
+  // rows return at once)
+  const bool side = dx && ll::gemm_groups(p->cap, Il) <= 8L * p->n_cu;
+  if (side) {
+    LL_HIP(hipEventRecord(p->ev_fork, s));
+    LL_HIP(hipStreamWaitEvent(p->gstream, p->ev_fork, 0));
+    LL_STATUS(dx_product(p->gstream));
+    LL_HIP(hipEventRecord(p->ev_join, p->gstream));
+  }
   // db = sum of the row-group partials
   ev = tbeg(p, s);
   LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, 4L * H, 4L * H, dbias[l], s));
@@ -973,29 +1025,8 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
     }
   }
   tend(p, s, LL_STAGE_DW, ev);
-  // dx_t = dz_t W_x^T: scattered to time-major dx (layer 0) or kept compact
-  // as the gradient of the layer below (layer 1)
-  if (!dx) return LL_OK;
-  ev = tbeg(p, s);
-  ll::GemmArgs g{};
-  g.A = dz;
-  g.lda = 4L * H;
-  g.Bm = p->W[l];
-  g.ldb = 4L * H;
-  g.M = (int)p->cap;
-  g.M_dev = p->meta + 1;
-  g.N = Il;
-  g.K = 4 * H;
-  g.splits = 1;
-  g.C = dx;
-  if (l == 0) {
-    g.ldc = d.I;
-    g.c_rowmap = p->rowmap;
-  } else {
-    g.ldc = H;
-  }
-  LL_HIP(ll::launch_gemm_nt<T>(g, s));
-  tend(p, s, LL_STAGE_DX, ev);
+  if (side) LL_HIP(hipStreamWaitEvent(s, p->ev_join, 0));
+  else if (dx) LL_STATUS(dx_product(s));
   return LL_OK;
 }
 
