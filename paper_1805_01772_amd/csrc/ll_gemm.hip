@@ -9,11 +9,18 @@
 //   * dW = sum over iterations of [x_t, h_{t-1}]^T dz_t (the loop-constant
 //     gradient, a sum over iterations), with the reduction running over the
 //     compact rows of all steps.
-// 256 threads = 4 waves in a 2x2 arrangement, 128x128 output tile; each wave
-// owns 64x64 = 4x4 MFMA tiles of 16x16.  A k-tile is 128 bytes of every row
-// (8 chunks of 16 bytes), staged through LDS with a 16-byte row pad; the next
-// k-tile is fetched into registers while the current one is multiplied.
-#include "ll_kernels.h"
+// Two kernels:
+//   * gemm_nt_kernel (any element type, any shape): 256 threads = 4 waves in
+//     a 2x2 arrangement, 128x128 output tile; each wave owns 64x64 = 4x4 MFMA
+//     tiles of 16x16.  A k-tile is 128 bytes of every row (8 chunks of 16
+//     bytes), staged through LDS with a 16-byte row pad; the next k-tile is
+//     fetched into registers while the current one is multiplied.
+//   * gemm_nt_bf16_lds_kernel (bf16 operands with 16-byte aligned rows): a
+//     256x256 output tile on 8 waves, operands loaded straight into LDS
+//     (buffer loads with the LDS-destination form), two LDS stages, 32x32x16
+//     MFMAs.  Per k-tile of 64 a work-group moves 64 KB into LDS for 8.4
+//     MFLOP, half the bytes per flop of the 128x128 tile.
+#include "ll_exchange.h"
 
 namespace ll {
 
@@ -148,10 +155,222 @@ __global__ __launch_bounds__(256, 2) void gemm_nt_kernel(GemmArgs g) {
   }
 }
 
-long gemm_groups(long M, long N) { return ((N + 127) / 128) * ((M + 127) / 128); }
+// ---------------------------------------------------------------------------
+// Large-tile bf16 kernel.
+//
+// Work-groups: 512 threads = 8 waves, 4 (rows) x 2 (columns); a wave owns a
+// 64x128 block of the 256x256 tile = 2x4 MFMA tiles of 32x32 (128
+// accumulator registers, so two waves share each SIMD).
+//
+// LDS: per stage, the A and B k-tiles (256 rows x 64 elements, 32 KB each) as
+// 8 chunks of 16 bytes per row.  Chunk c of row r sits in slot c ^ swz(r),
+// swz(r) = (r & 7) ^ ((r >> 3) & 1): the 16 rows read by 16 consecutive
+// lanes hit 16 different 16-byte bank groups, and so do 8 consecutive rows.
+// A load instruction (64 lanes x 16 bytes) fills 8 rows: lane l writes slot
+// l % 8 of row l / 8 (the hardware places lane l's data at base + 16 l), so it
+// reads k-chunk (l % 8) ^ swz(row) of that row.
+//
+// Pipeline: the loads of k-tile kt + 1 go into the other stage while k-tile
+// kt is multiplied; one barrier per k-tile.  The stage being read and the
+// stage being filled are different arrays, so the compiler does not wait for
+// the fills before each LDS read.
+//
+// Rows past M or N and k-chunks past the end of the reduction read as zero
+// (buffer loads past the descriptor's range return zero); a chunk that
+// straddles the end of K is read whole, which needs K % 8 == 0 or zeros in
+// the operands up to the next multiple of 8 (GemmArgs::k_zero_tail).
+//
+// Tile order: work-group id L runs on XCD L % 8 (round-robin dispatch); XCD x
+// takes a contiguous share of the tiles that exist for the M rows actually
+// present, ordered in groups of 4 row tiles, so the work-groups running
+// together on one XCD read 4 A panels and about 8 B panels through its L2.
+// ---------------------------------------------------------------------------
+namespace {
+
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr int kBigTile = 256;
+constexpr int kBigThreads = 512;
+constexpr int kBigGroupRows = 4;
+
+__device__ __forceinline__ int big_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+}  // namespace
+
+__global__ __launch_bounds__(kBigThreads, 1) void gemm_nt_bf16_lds_kernel(GemmArgs g, unsigned a_bytes,
+                                                                         unsigned b_bytes) {
+  constexpr int BM = kBigTile, BN = kBigTile;
+  constexpr int NW = kBigThreads / 64;       // 8 waves
+  constexpr int WGN = 2;                     // waves across the columns
+  constexpr int WM = BM / (NW / WGN), WN = BN / WGN;   // 64 x 128 per wave
+  constexpr int MI = WM / 32, NI = WN / 32;  // 2 x 4 MFMA tiles
+  constexpr int KT = 64;                     // elements per k-tile
+  constexpr int CH = BM * 8;                 // chunks per operand and stage
+  constexpr int LI = BM / 8 / NW;            // load instructions per wave and operand
+  __shared__ uint4 sA0[CH], sA1[CH], sB0[CH], sB1[CH];
+
+  const int M = g.M_dev ? min(*g.M_dev, g.M) : g.M;
+  const int K = g.K_dev ? *g.K_dev : g.K;
+  const int nmt = (M + BM - 1) / BM, nnt = (g.N + BN - 1) / BN;
+  const int per_split = nmt * nnt;
+  const int ntiles = per_split * g.splits;
+  const int share = (ntiles + 7) / 8;
+  const int L = blockIdx.x;
+  const int t = (L & 7) * share + (L >> 3);
+  if ((L >> 3) >= share || t >= ntiles) return;
+  const int z = t / per_split;
+  const int tt = t - z * per_split;
+  const int grp = tt / (kBigGroupRows * nnt);
+  const int fm = grp * kBigGroupRows;
+  const int gsz = min(nmt - fm, kBigGroupRows);
+  const int within = tt - grp * kBigGroupRows * nnt;
+  const int m0 = (fm + within % gsz) * BM, n0 = (within / gsz) * BN;
+
+  const int kper = ((K + g.splits - 1) / g.splits + KT - 1) / KT * KT;
+  const int kb = min(K, z * kper);
+  const int ke = min(K, kb + kper);
+  const int nkt = (ke - kb + KT - 1) / KT;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int l32 = lane & 31, kc = lane >> 5;
+
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(g.A, a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.Bm, b_bytes);
+  // this lane's source in load instruction i: row (i NW + wave) 8 + lane / 8,
+  // k-chunk ach / bch of the k-tile (byte offset without the k-tile base)
+  unsigned aoff[LI], boff[LI];
+  int ach[LI], bch[LI];
+#pragma unroll
+  for (int i = 0; i < LI; ++i) {
+    const int row = (i * NW + wave) * 8 + (lane >> 3);
+    const int m = m0 + row, n = n0 + row;
+    ach[i] = bch[i] = (lane & 7) ^ big_swz(row);
+    aoff[i] = m < M ? (unsigned)((g.a_rowmap ? g.a_rowmap[m] : m) * (long)g.lda * 2 + ach[i] * 16) : kOOB;
+    boff[i] = n < g.N ? (unsigned)(n * (long)g.ldb * 2 + bch[i] * 16) : kOOB;
+  }
+  auto fill = [&](int kt, uint4* a_dst, uint4* b_dst) {
+    const int k0 = kb + kt * KT;
+    const bool full = k0 + KT <= ke;
+    const unsigned kbytes = (unsigned)k0 * 2u;
+#pragma unroll
+    for (int i = 0; i < LI; ++i) {
+      const bool past = !full & (k0 + ach[i] * 8 >= ke);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(a_dst + (i * NW + wave) * 64), 16,
+                                               past ? kOOB : aoff[i] + kbytes, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < LI; ++i) {
+      const bool past = !full & (k0 + bch[i] * 8 >= ke);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(b_dst + (i * NW + wave) * 64), 16,
+                                               past ? kOOB : boff[i] + kbytes, 0, 0, 0);
+    }
+  };
+
+  f32x16 acc[MI][NI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{};
+
+  // MFMA operand lanes: lane l supplies row (A) / column (B) l % 32 and the
+  // 8 consecutive k of chunk 2 ks + l / 32 of k-step ks
+  const int sw = big_swz(l32);
+  const int arow = (wm * WM + l32) * 8, brow = (wn * WN + l32) * 8;
+  auto step = [&](int kt, const uint4* a, const uint4* b, uint4* a_next, uint4* b_next) {
+    // this wave's fills of k-tile kt have landed; the barrier makes every
+    // wave's visible and ends every wave's reads of the other stage
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (kt + 1 < nkt) fill(kt + 1, a_next, b_next);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int c = (2 * ks + kc) ^ sw;
+      uint4 av[MI], bv[NI];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) av[i] = a[arow + i * 256 + c];
+#pragma unroll
+      for (int j = 0; j < NI; ++j) bv[j] = b[brow + j * 256 + c];
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, av[i]), __builtin_bit_cast(bf16x8_t, bv[j]), acc[i][j], 0, 0, 0);
+    }
+  };
+  if (nkt > 0) fill(0, sA0, sB0);
+  for (int kt = 0; kt < nkt; kt += 2) {
+    step(kt, sA0, sB0, sA1, sB1);
+    if (kt + 1 < nkt) step(kt + 1, sA1, sB1, sA0, sB0);
+  }
+
+  // result register r of lane l: row (r % 4) + 8 (r / 4) + 4 (l / 32), column l % 32
+  const bool split = g.splits > 1;
+  float* Cb = g.C + (split ? (long)z * g.split_stride : 0L);
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + wm * WM + i * 32 + (r & 3) + 8 * (r >> 2) + 4 * kc;
+      if (m >= M) continue;
+      const long crow = (!split && g.c_rowmap) ? (long)g.c_rowmap[m] : (long)m;
+      float* cr = Cb + crow * g.ldc;
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int n = n0 + wn * WN + j * 32 + l32;
+        if (n < g.N) {
+          float v = acc[i][j][r];
+          if (g.bias && (!split || z == 0)) v += g.bias[n];
+          cr[n] = v;
+        }
+      }
+    }
+  }
+}
+
+namespace {
+
+// Bytes of A and B the products of g may address (0 if past a 31-bit range).
+void big_ranges(const GemmArgs& g, long* a_bytes, long* b_bytes) {
+  *a_bytes = (long)(g.a_rows > 0 ? g.a_rows : g.M) * g.lda * 2;
+  *b_bytes = (long)g.N * g.ldb * 2;
+}
+
+}  // namespace
+
+bool gemm_big_applies(const GemmArgs& g, int elem_bytes) {
+  if (elem_bytes != 2 || g.splits < 1) return false;
+  if (g.lda % 8 != 0 || g.ldb % 8 != 0) return false;
+  if ((reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.Bm)) & 15) return false;
+  if (!g.k_zero_tail && (g.K_dev || g.K % 8 != 0)) return false;
+  long ab, bb;
+  big_ranges(g, &ab, &bb);
+  return ab < (long)kOOB && bb < (long)kOOB;
+}
+
+long gemm_rounds(const GemmArgs& g, int elem_bytes, int n_cu) {
+  if (gemm_big_applies(g, elem_bytes)) {
+    const long tiles = (long)((g.M + kBigTile - 1) / kBigTile) * ((g.N + kBigTile - 1) / kBigTile) * g.splits;
+    return (tiles + n_cu - 1) / n_cu;
+  }
+  const long groups = (long)((g.M + 127) / 128) * ((g.N + 127) / 128) * g.splits;
+  return (groups + 2L * n_cu - 1) / (2L * n_cu);
+}
 
 template <typename T>
 hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s) {
+  if (gemm_big_applies(g, (int)sizeof(T))) {
+    long ab, bb;
+    big_ranges(g, &ab, &bb);
+    const long tiles = (long)((g.M + kBigTile - 1) / kBigTile) * ((g.N + kBigTile - 1) / kBigTile) * g.splits;
+    const long share = (tiles + 7) / 8;
+    hipLaunchKernelGGL(gemm_nt_bf16_lds_kernel, dim3((unsigned)(share * 8)), dim3(kBigThreads), 0, s, g,
+                       (unsigned)ab, (unsigned)bb);
+    return hipGetLastError();
+  }
   dim3 grid((g.N + 127) / 128, (g.M + 127) / 128, g.splits);
   hipLaunchKernelGGL(gemm_nt_kernel<T>, grid, dim3(256), 0, s, g);
   return hipGetLastError();

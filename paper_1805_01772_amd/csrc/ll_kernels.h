@@ -49,6 +49,8 @@ struct GemmArgs {
   const int* K_dev;      // NULL or device scalar: reduction length
   int splits;            // > 1: split-K; slice z written to C + z * split_stride
   long split_stride;
+  int a_rows;            // rows of A the row map addresses (0: M)
+  int k_zero_tail;       // 1: both operands hold zeros from K up to the next multiple of 8
 };
 
 struct LoopGeom {
@@ -266,8 +268,11 @@ hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s);
 
 template <typename T>
 hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s);
-// Work-groups of a GEMM launch with M x N outputs (one split).
-long gemm_groups(long M, long N);
+// Whether launch_gemm_nt takes the large-tile bf16 kernel for g, and how
+// many times the launch fills n_cu compute units (row capacity g.M).
+bool gemm_big_applies(const GemmArgs& g, int elem_bytes);
+long gemm_rounds(const GemmArgs& g, int elem_bytes, int n_cu);
+constexpr int kGemmBigTile = 256;
 
 // Recurrent loops (cooperative launches).
 template <typename T>

@@ -462,11 +462,22 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     }
   }
 
-  // dW split-K: enough work-groups to cover the chip.
+  // dW split-K: enough work-groups to cover the chip (one 256x256 tile per
+  // compute unit for the large-tile bf16 kernel, two 128x128 tiles else).
   for (int w = 0; w < 2; ++w) {
     const int M = w == 0 ? desc->I : H;
-    const long tiles = (long)((M + 127) / 128) * ((4 * H + 127) / 128);
-    long s = (2L * p->n_cu + tiles - 1) / tiles;
+    ll::GemmArgs g{};
+    g.lda = g.ldb = p->ldT;
+    g.M = M;
+    g.N = 4 * H;
+    g.K = (int)p->cap;
+    g.splits = 1;
+    g.k_zero_tail = 1;
+    const bool big = ll::gemm_big_applies(g, (int)p->es);
+    const long tile = big ? ll::kGemmBigTile : 128;
+    const long tiles = (long)((M + tile - 1) / tile) * ((4 * H + tile - 1) / tile);
+    const long want = big ? p->n_cu : 2L * p->n_cu;
+    long s = (want + tiles - 1) / tiles;
     s = std::max(1L, std::min(16L, s));
     const long max_by_k = std::max(1L, p->cap / 256);
     p->dw_splits[w] = (int)std::min(s, max_by_k);
@@ -935,32 +946,32 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   // products (both only read dz) and is joined back before returning; a
   // larger one runs after them on the call's stream (measured: two large
   // products side by side only slow each other).
+  ll::GemmArgs gx{};
+  gx.A = dz;
+  gx.lda = 4L * H;
+  gx.Bm = p->W[l];
+  gx.ldb = 4L * H;
+  gx.M = (int)p->cap;
+  gx.M_dev = p->meta + 1;
+  gx.N = Il;
+  gx.K = 4 * H;
+  gx.splits = 1;
+  gx.C = dx;
+  if (l == 0) {
+    gx.ldc = d.I;
+    gx.c_rowmap = p->rowmap;
+  } else {
+    gx.ldc = H;
+  }
   auto dx_product = [&](hipStream_t st) -> ll_status {
     hipEvent_t evx = tbeg(p, st);
-    ll::GemmArgs g{};
-    g.A = dz;
-    g.lda = 4L * H;
-    g.Bm = p->W[l];
-    g.ldb = 4L * H;
-    g.M = (int)p->cap;
-    g.M_dev = p->meta + 1;
-    g.N = Il;
-    g.K = 4 * H;
-    g.splits = 1;
-    g.C = dx;
-    if (l == 0) {
-      g.ldc = d.I;
-      g.c_rowmap = p->rowmap;
-    } else {
-      g.ldc = H;
-    }
-    LL_HIP(ll::launch_gemm_nt<T>(g, st));
+    LL_HIP(ll::launch_gemm_nt<T>(gx, st));
     tend(p, st, LL_STAGE_DX, evx);
     return LL_OK;
   };
   // (the grid covers the row capacity T_max * B; groups past the running
   // rows return at once)
-  const bool side = dx && ll::gemm_groups(p->cap, Il) <= 8L * p->n_cu;
+  const bool side = dx && ll::gemm_rounds(gx, (int)sizeof(T), p->n_cu) <= 2;
   if (side) {
     LL_HIP(hipEventRecord(p->ev_fork, s));
     LL_HIP(hipStreamWaitEvent(p->gstream, p->ev_fork, 0));
@@ -1010,6 +1021,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
     g.N = 4 * H;
     g.K = (int)p->cap;
     g.K_dev = p->meta + 1;
+    g.k_zero_tail = 1;   // the transposes write zeros past the last row, up to a multiple of 64
     g.splits = p->dw_splits[part];
     float* dst = dW[l] + (part == 0 ? 0L : (long)Il * 4 * H);
     if (g.splits > 1) {
