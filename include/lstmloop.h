@@ -199,10 +199,14 @@ const char* ll_last_error(void);
  * Stage timing, for benchmarks.  While enabled, the plan records a pair of
  * HIP events around every stage it enqueues, on the call's stream, so each
  * pair brackets that stage's kernels exactly as the stream runs them.
- * ll_plan_set_timing(plan, 1) clears the accumulators and starts recording;
- * 0 stops.  ll_plan_read_timing waits for the recorded events, then returns
- * the accumulated milliseconds and the number of recorded instances of
- * `stage` (an ll_stage).  Outputs may be NULL.
+ * ll_plan_set_timing(plan, 1) clears the accumulators and starts recording
+ * every stage; 0 stops.  ll_plan_set_timing_stages records only the stages
+ * whose bit (1 << stage) is set in stage_mask (each event pair costs a few
+ * microseconds of stream time, so a benchmark times few stages in its timed
+ * region); a mask naming no ll_stage is LL_EINVAL.  ll_plan_read_timing waits
+ * for the recorded events, then returns the accumulated milliseconds and the
+ * number of recorded instances of `stage` (an ll_stage).  Outputs may be
+ * NULL.
  */
 typedef enum {
   LL_STAGE_PREP = 0,          /* trip count, length order, compact offsets   */
@@ -217,6 +221,7 @@ typedef enum {
 } ll_stage;
 
 ll_status ll_plan_set_timing(ll_plan* plan, int32_t enable);
+ll_status ll_plan_set_timing_stages(ll_plan* plan, uint32_t stage_mask);
 ll_status ll_plan_read_timing(ll_plan* plan, int32_t stage, double* total_ms,
                               int64_t* instances);
 

@@ -711,7 +711,7 @@ hipError_t c_setup(const CKernels& k, int* occ_fwd, int* occ_bwd) {
 hipError_t c_launch(const void* fn, const CLoopArgs& a, size_t lds, hipStream_t s) {
   CLoopArgs copy = a;
   void* kargs[] = {&copy};
-  return hipLaunchCooperativeKernel(fn, dim3(256), dim3(CNT), kargs, (unsigned)lds, s);
+  return hipLaunchKernel(fn, dim3(256), dim3(CNT), kargs, lds, s);
 }
 
 }  // namespace ll

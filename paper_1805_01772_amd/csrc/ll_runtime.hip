@@ -144,8 +144,8 @@ struct ll_plan {
   const float* h0 = nullptr;
   const float* c0 = nullptr;
   hipStream_t last_stream = nullptr;
-  // stage timing
-  bool timing = false;
+  // stage timing: bit s set = stage s recorded
+  uint32_t timing_mask = 0;
   struct Rec {
     int stage;
     hipEvent_t a, b;
@@ -171,9 +171,10 @@ hipEvent_t take_event(ll_plan* p) {
   return e;
 }
 
-// Stage bracket: tbeg records the opening event, tend the closing one.
-hipEvent_t tbeg(ll_plan* p, hipStream_t s) {
-  if (!p->timing) return nullptr;
+// Stage bracket: tbeg records the opening event, tend the closing one (only
+// for the stages the plan times).
+hipEvent_t tbeg(ll_plan* p, hipStream_t s, int stage) {
+  if (!(p->timing_mask & (1u << stage))) return nullptr;
   hipEvent_t a = take_event(p);
   if (a && hipEventRecord(a, s) != hipSuccess) {
     p->ev_pool.push_back(a);
@@ -183,7 +184,7 @@ hipEvent_t tbeg(ll_plan* p, hipStream_t s) {
 }
 
 void tend(ll_plan* p, hipStream_t s, int stage, hipEvent_t a) {
-  if (!p->timing || !a) return;
+  if (!a) return;
   hipEvent_t b = take_event(p);
   if (!b || hipEventRecord(b, s) != hipSuccess) {
     p->ev_pool.push_back(a);
@@ -600,16 +601,21 @@ ll_status ll_plan_destroy(ll_plan* p) {
   return LL_OK;
 }
 
-ll_status ll_plan_set_timing(ll_plan* p, int32_t enable) {
+ll_status ll_plan_set_timing_stages(ll_plan* p, uint32_t stage_mask) {
   if (!p) return fail(LL_EINVAL, "plan is NULL");
+  if (stage_mask >> LL_STAGE_COUNT) return fail(LL_EINVAL, "stage mask 0x%x names no stage", stage_mask);
   DeviceGuard guard(p->device);
   drain_timing(p);
   for (int i = 0; i < LL_STAGE_COUNT; ++i) {
     p->t_ms[i] = 0.0;
     p->t_n[i] = 0;
   }
-  p->timing = enable != 0;
+  p->timing_mask = stage_mask;
   return LL_OK;
+}
+
+ll_status ll_plan_set_timing(ll_plan* p, int32_t enable) {
+  return ll_plan_set_timing_stages(p, enable ? (1u << LL_STAGE_COUNT) - 1u : 0u);
 }
 
 ll_status ll_plan_read_timing(ll_plan* p, int32_t stage, double* total_ms, int64_t* n) {
@@ -699,7 +705,7 @@ ll_status enqueue_fwd_wave(ll_plan* p, hipStream_t s, const void* x, const void*
   const ll_desc& d = p->d;
   const int H = d.H, B = d.B, I = d.I;
   const long BH = (long)B * H;
-  hipEvent_t ev = tbeg(p, s);
+  hipEvent_t ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
   for (int l = 0; l < 2; ++l) {
     const int Il = in_width(p, l);
     LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, 4 * H, 4 * H,
@@ -725,7 +731,7 @@ ll_status enqueue_fwd_wave(ll_plan* p, hipStream_t s, const void* x, const void*
   const int ring_ks = (int)((long)H * p->es / 64);
   unsigned* F0 = p->xflags + 8;
   unsigned* F1 = F0 + 8L * p->xMRT * 32;
-  ev = tbeg(p, s);
+  ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
   LL_HIP(ll::launch_x_prepare_fwd<T>(h0, p->perm, B, H, p->xMRT, ring_ks, 1, p->xring, p->xflags,
                                      p->xflag_words, s));
   LL_HIP(ll::launch_x_prepare_fwd<T>(h0 ? h0 + BH : nullptr, p->perm, B, H, p->xMRT, ring_ks, 1,
@@ -765,7 +771,7 @@ ll_status enqueue_fwd_wave(ll_plan* p, hipStream_t s, const void* x, const void*
   a1.in_ring = p->xring;
   a1.in_flags = F0;
   a1.in_ks = ring_ks;
-  ev = tbeg(p, s);
+  ev = tbeg(p, s, LL_STAGE_FWD_LOOP);
   LL_HIP(ll::x_launch2(p->xk2.fwd, a0, a1, 256, p->xk2.lds_fwd, s));
   tend(p, s, LL_STAGE_FWD_LOOP, ev);
   return LL_OK;
@@ -778,14 +784,14 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
                       bool save) {
   const ll_desc& d = p->d;
   const int H = d.H, B = d.B, L = d.layers;
-  hipEvent_t ev = tbeg(p, s);
+  hipEvent_t ev = tbeg(p, s, LL_STAGE_PREP);
   LL_HIP(ll::launch_prep(seq_len, B, d.T_max, p->perm, p->active, p->off, p->rowmap, p->meta,
                          trip, s));
   tend(p, s, LL_STAGE_PREP, ev);
   if (p->wave) return enqueue_fwd_wave<T>(p, s, x, W, bias, h0, c0, y, hT, cT, save);
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
-    ev = tbeg(p, s);
+    ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
     // W^T: row n = gate column n, K-contiguous operand of both products
     LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, 4 * H, 4 * H,
                                    reinterpret_cast<T*>(p->WT[l]), Il + H, s));
@@ -845,13 +851,13 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
         const int t0 = k * C, t1 = std::min(d.T_max, t0 + C);
         const int slot = k % xa.nslots;
         const bool last = k == nch - 1;
-        ev = tbeg(p, s);
+        ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
         // the chunk that used this ring slot before has reached host memory
         if (p->spill && save && k >= p->nslots) LL_HIP(hipStreamWaitEvent(s, p->ev_d2h[l * p->nslots + slot], 0));
         LL_HIP(ll::launch_x_prepare_fwd<T>(hin, p->perm, B, H, p->xMRT, ring_ks, (t0 + 1) & 1, p->xring,
                                            p->xflags, p->xflag_words, s));
         tend(p, s, LL_STAGE_LOOP_SETUP, ev);
-        ev = tbeg(p, s);
+        ev = tbeg(p, s, LL_STAGE_FWD_LOOP);
         xa.t_begin = t0;
         xa.t_end = t1;
         xa.h0 = hin;
@@ -875,7 +881,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     }
     if (p->cmode) {
       const float* hin = h0 ? h0 + (long)l * B * H : nullptr;
-      ev = tbeg(p, s);
+      ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
       LL_HIP(ll::launch_c_prepare<T>(hin, p->perm, B, H, p->cMRT, p->cring, p->cflags, p->cflag_words, s));
       tend(p, s, LL_STAGE_LOOP_SETUP, ev);
       ll::CLoopArgs ca = c_common(p);
@@ -891,7 +897,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       ca.y = (l == L - 1) ? y : nullptr;
       ca.hT = hT + (long)l * B * H;
       ca.cT = cT + (long)l * B * H;
-      ev = tbeg(p, s);
+      ev = tbeg(p, s, LL_STAGE_FWD_LOOP);
       LL_HIP(ll::c_launch(p->ck.fwd, ca, p->ck.lds_fwd, s));
       tend(p, s, LL_STAGE_FWD_LOOP, ev);
       continue;
@@ -922,7 +928,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     a.abort_flag = p->meta + 3;
     a.err = p->meta + 2;
     a.limit = p->barrier_ticks;
-    ev = tbeg(p, s);
+    ev = tbeg(p, s, LL_STAGE_FWD_LOOP);
     LL_HIP(ll::launch_fwd_loop<T>(a, p->geom.nwg, p->geom.lds_fwd, s));
     tend(p, s, LL_STAGE_FWD_LOOP, ev);
   }
@@ -964,7 +970,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
     gx.ldc = H;
   }
   auto dx_product = [&](hipStream_t st) -> ll_status {
-    hipEvent_t evx = tbeg(p, st);
+    hipEvent_t evx = tbeg(p, st, LL_STAGE_DX);
     LL_HIP(ll::launch_gemm_nt<T>(gx, st));
     tend(p, st, LL_STAGE_DX, evx);
     return LL_OK;
@@ -979,10 +985,10 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
     LL_HIP(hipEventRecord(p->ev_join, p->gstream));
   }
   // db = sum of the row-group partials
-  ev = tbeg(p, s);
+  ev = tbeg(p, s, LL_STAGE_DW);
   LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, 4L * H, 4L * H, dbias[l], s));
   tend(p, s, LL_STAGE_DW, ev);
-  ev = tbeg(p, s);
+  ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
   // transposed operands of the dW products (reduction over compact rows)
   ll::GatherTArgs gt{};
   gt.B = B;
@@ -1009,7 +1015,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
   tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
   // dW_x = X^T DZ, dW_h = Hprev^T DZ
-  ev = tbeg(p, s);
+  ev = tbeg(p, s, LL_STAGE_DW);
   for (int part = 0; part < 2; ++part) {
     const int M = part == 0 ? Il : H;
     ll::GemmArgs g{};
@@ -1058,7 +1064,7 @@ ll_status enqueue_bwd_wave(ll_plan* p, hipStream_t s, const float* dy, const flo
   unsigned* F0 = p->xflags + 8;
   unsigned* F1 = F0 + fw;
   unsigned* FY = F1 + fw;
-  hipEvent_t ev = tbeg(p, s);
+  hipEvent_t ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
   LL_HIP(ll::launch_zero_u32(p->xflags, p->xflag_words, s));
   tend(p, s, LL_STAGE_LOOP_SETUP, ev);
   const int ring_ks = (int)(4L * H * p->es / 64);
@@ -1098,7 +1104,7 @@ ll_status enqueue_bwd_wave(ll_plan* p, hipStream_t s, const float* dy, const flo
   a1.dyx_ring = p->dyx;
   a1.dyx_flags = FY;
   a1.peer_flags = F0;
-  ev = tbeg(p, s);
+  ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
   LL_HIP(ll::x_launch2(p->xk2.bwd, a0, a1, 256, p->xk2.lds_bwd, s));
   tend(p, s, LL_STAGE_BWD_LOOP, ev);
   LL_STATUS(bwd_products<T>(p, s, 1, p->DZ2, p->db_part2, nullptr, dW, dbias));
@@ -1111,7 +1117,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
                       float* dh0, float* dc0) {
   const ll_desc& d = p->d;
   const int H = d.H, B = d.B, L = d.layers;
-  hipEvent_t ev = tbeg(p, s);
+  hipEvent_t ev = tbeg(p, s, LL_STAGE_DX);
   if (dx) LL_HIP(ll::launch_zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta, s));
   tend(p, s, LL_STAGE_DX, ev);
   if (p->wave) return enqueue_bwd_wave<T>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
@@ -1169,12 +1175,12 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       for (int k = nch - 1; k >= 0; --k) {
         const int t0 = k * C, t1 = std::min(d.T_max, t0 + C);
         const bool first = k == nch - 1, last = k == 0;
-        ev = tbeg(p, s);
+        ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
         LL_HIP(wait_loaded(k));
         LL_HIP(wait_loaded(k - 1));
         LL_HIP(ll::launch_zero_u32(p->xflags, p->xflag_words, s));
         tend(p, s, LL_STAGE_LOOP_SETUP, ev);
-        ev = tbeg(p, s);
+        ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
         xa.t_begin = t0;
         xa.t_end = t1;
         xa.db_resume = first ? 0 : 1;
@@ -1196,7 +1202,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       }
     }
     if (p->cmode) {
-      ev = tbeg(p, s);
+      ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
       LL_HIP(ll::launch_zero_u32(p->cflags, p->cflag_words, s));
       tend(p, s, LL_STAGE_LOOP_SETUP, ev);
       ll::CLoopArgs ca = c_common(p);
@@ -1213,7 +1219,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       ca.db = p->db_part;
       ca.dh0 = dh0 ? dh0 + (long)l * B * H : nullptr;
       ca.dc0 = dc0 ? dc0 + (long)l * B * H : nullptr;
-      ev = tbeg(p, s);
+      ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
       LL_HIP(ll::c_launch(p->ck.bwd, ca, p->ck.lds_bwd, s));
       tend(p, s, LL_STAGE_BWD_LOOP, ev);
     }
@@ -1250,7 +1256,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     a.err = p->meta + 2;
     a.limit = p->barrier_ticks;
     if (!p->xmode && !p->cmode) {
-      ev = tbeg(p, s);
+      ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
       LL_HIP(ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s));
       tend(p, s, LL_STAGE_BWD_LOOP, ev);
     }

@@ -855,14 +855,14 @@ hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd) {
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s) {
   XLoopArgs copy = a;
   void* kargs[] = {&copy};
-  return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(XNT), kargs, (unsigned)lds, s);
+  return hipLaunchKernel(fn, dim3(nwg), dim3(XNT), kargs, lds, s);
 }
 
 hipError_t x_launch2(const void* fn, const XLoopArgs& a0, const XLoopArgs& a1, int nwg, size_t lds,
                      hipStream_t s) {
   XLoopArgs c0 = a0, c1 = a1;
   void* kargs[] = {&c0, &c1};
-  return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(XNT), kargs, (unsigned)lds, s);
+  return hipLaunchKernel(fn, dim3(nwg), dim3(XNT), kargs, lds, s);
 }
 
 }  // namespace ll

@@ -24,7 +24,8 @@ STATUS_NAMES = {0: "LL_OK", 1: "LL_EINVAL", 2: "LL_ENOMEM", 3: "LL_EHIP",
 EXPORTED = ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes",
             "ll_plan_geometry", "lstm_loop_fwd", "lstm_loop_bwd",
             "ll_status_sync", "ll_last_error", "ll_version",
-            "ll_plan_set_timing", "ll_plan_read_timing", "ll_measure_mfma_peak")
+            "ll_plan_set_timing", "ll_plan_set_timing_stages", "ll_plan_read_timing",
+            "ll_measure_mfma_peak")
 STAGES = ("prep", "input_proj", "fwd_loop", "bwd_loop", "bwd_operands", "dw", "dx", "loop_setup")
 
 
@@ -73,6 +74,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                   ctypes.POINTER(vp), vp, vp]
     lib.ll_status_sync.argtypes = [vp, ctypes.POINTER(i32)]
     lib.ll_plan_set_timing.argtypes = [vp, i32]
+    lib.ll_plan_set_timing_stages.argtypes = [vp, ctypes.c_uint32]
     lib.ll_plan_read_timing.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(i64)]
     lib.ll_measure_mfma_peak.argtypes = [ctypes.c_int, i32, i32, ctypes.POINTER(ctypes.c_double)]
@@ -80,7 +82,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ll_version.restype = ctypes.c_char_p
     for name in ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes", "ll_plan_geometry",
                  "lstm_loop_fwd", "lstm_loop_bwd", "ll_status_sync", "ll_plan_set_timing",
-                 "ll_plan_read_timing", "ll_measure_mfma_peak"):
+                 "ll_plan_set_timing_stages", "ll_plan_read_timing", "ll_measure_mfma_peak"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -197,9 +199,17 @@ class Plan:
             self._h, _stream(stream), _ptr(dy), _ptr(dhT), _ptr(dcT), _ptr(dx),
             _ptr_array(dW), _ptr_array(dbias), _ptr(dh0), _ptr(dc0)))
 
-    def set_timing(self, enable: bool) -> None:
-        """ll_plan_set_timing: clear the stage accumulators, start/stop recording."""
-        _check(self._lib.ll_plan_set_timing(self._h, 1 if enable else 0))
+    def set_timing(self, enable) -> None:
+        """ll_plan_set_timing: clear the stage accumulators, start/stop recording
+        every stage; a collection of stage names records only those
+        (ll_plan_set_timing_stages)."""
+        if isinstance(enable, (bool, int)):
+            _check(self._lib.ll_plan_set_timing(self._h, 1 if enable else 0))
+            return
+        mask = 0
+        for name in enable:
+            mask |= 1 << STAGES.index(name)
+        _check(self._lib.ll_plan_set_timing_stages(self._h, mask))
 
     def read_timing(self) -> dict:
         """ll_plan_read_timing for every stage: {name: (total_ms, instances)}."""
