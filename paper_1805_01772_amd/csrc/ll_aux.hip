@@ -23,10 +23,13 @@ __global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_
                                                     int T_max, int* __restrict__ perm,
                                                     int* __restrict__ active, int* __restrict__ off,
                                                     int* __restrict__ rowmap, int* __restrict__ meta,
-                                                    int* __restrict__ trip_out) {
+                                                    int* __restrict__ trip_out, int t_in_lds) {
   extern __shared__ int smem[];
-  int* s_len = smem;          // [B]
-  int* s_sorted = smem + B;   // [B] lengths in perm order
+  int* s_len = smem;              // [B]
+  int* s_sorted = smem + B;       // [B] lengths in perm order
+  int* s_perm = smem + 2 * B;     // [B]
+  int* s_act = smem + 3 * B;      // [T_max + 1] when t_in_lds
+  int* s_off = s_act + T_max + 1; // [T_max + 1] when t_in_lds
   __shared__ int s_bad;
   __shared__ int s_wsum[16];
   __shared__ int s_carry;
@@ -49,6 +52,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_
       rank += (Lo > L) || (Lo == L && o < b);
     }
     perm[rank] = b;
+    s_perm[rank] = b;
     s_sorted[rank] = bad ? 0 : L;
   }
   __syncthreads();
@@ -61,12 +65,13 @@ __global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_
       if (s_sorted[mid] > t) lo = mid + 1; else hi = mid;
     }
     active[t] = lo;
+    if (t_in_lds) s_act[t] = lo;
   }
   __syncthreads();
   // exclusive prefix sum of active[0..T_max) into off[0..T_max]
   for (int base = 0; base <= T_max; base += nt) {
     const int t = base + tid;
-    const int v = (t < T_max) ? active[t] : 0;
+    const int v = (t < T_max) ? (t_in_lds ? s_act[t] : active[t]) : 0;
     int incl = v;
     for (int d = 1; d < 64; d <<= 1) {
       const int u = __shfl_up(incl, d, 64);
@@ -81,20 +86,20 @@ __global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_
       tot += s;
     }
     const int carry = s_carry;
-    if (t <= T_max) off[t] = carry + wpre + incl - v;
+    if (t <= T_max) {
+      off[t] = carry + wpre + incl - v;
+      if (t_in_lds) s_off[t] = carry + wpre + incl - v;
+    }
     __syncthreads();
     if (tid == 0) s_carry = carry + tot;
     __syncthreads();
   }
-  const int total = off[T_max];
-  // rowmap: compact row -> t * B + b
-  for (int k = tid; k < total; k += nt) {
-    int lo = 0, hi = T_eff;          // largest t with off[t] <= k
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (off[mid] <= k) lo = mid; else hi = mid;
-    }
-    rowmap[k] = lo * B + perm[k - off[lo]];
+  const int total = s_carry;
+  // rowmap: compact row off[t] + r -> t * B + perm[r]; one wave per step
+  for (int t = wave; t < T_eff; t += nwaves) {
+    const int n = t_in_lds ? s_act[t] : active[t];
+    const int o = t_in_lds ? s_off[t] : off[t];
+    for (int r = lane; r < n; r += 64) rowmap[o + r] = t * B + s_perm[r];
   }
   if (tid == 0) {
     meta[0] = T_eff;
@@ -226,9 +231,11 @@ __global__ __launch_bounds__(256) void convert_kernel(const float* __restrict__ 
 // ------------------------------------------------------------ launchers
 hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
                        int* rowmap, int* meta, int* trip_out, hipStream_t s) {
-  const size_t smem = 2 * sizeof(int) * (size_t)B;
+  // per-step counts and offsets stay in LDS when all fits in 64 KB
+  const int t_in_lds = (3 * (size_t)B + 2 * ((size_t)T_max + 1)) * sizeof(int) <= 64 * 1024;
+  const size_t smem = sizeof(int) * (3 * (size_t)B + (t_in_lds ? 2 * ((size_t)T_max + 1) : 0));
   hipLaunchKernelGGL(prep_kernel, dim3(1), dim3(1024), smem, s, seq_len, B, T_max, perm, active,
-                     off, rowmap, meta, trip_out);
+                     off, rowmap, meta, trip_out, t_in_lds);
   return hipGetLastError();
 }
 

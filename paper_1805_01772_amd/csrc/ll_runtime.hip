@@ -75,7 +75,7 @@ struct ll_plan {
   ll::LoopGeom geom{};
   int n_cu = 0;
   unsigned long long barrier_ticks = 0;
-  int dw_splits[2] = {1, 1};   // split-K of the dW_x / dW_h products
+  int dw_splits[2] = {1, 1};   // split-K of the dW product of layer 0 / 1
   bool xmode = false;          // XCD-local loops (ll_xloop.hip)
   ll::XKernels xk{};
   int xP = 0;                  // unit blocks per XCD
@@ -104,8 +104,8 @@ struct ll_plan {
   void* HH[2] = {nullptr, nullptr};
   void* DZ = nullptr;
   void* DZT = nullptr;
-  void* XT = nullptr;
-  void* HPT = nullptr;
+  void* XT = nullptr;           // [I_l + H, ldT]: x (or y of the layer below) transposed, then h_prev
+                                //   transposed (rows I_l ..), the A operand of one dW product
   float* dyc = nullptr;
   void* xring = nullptr;       // XCD-local loops: exchange ring
   // XCD-local loops: [8] rank counters, then step flags [8][MRT][32] (the
@@ -209,7 +209,7 @@ void drain_timing(ll_plan* p) {
 
 void free_plan_memory(ll_plan* p) {
   void* ptrs[] = {p->perm, p->active, p->off, p->rowmap, p->meta, p->WT[0], p->WT[1], p->Zx,
-                  p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT, p->HPT,
+                  p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT,
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
                   p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags};
   for (void* q : ptrs)
@@ -465,8 +465,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
 
   // dW split-K: enough work-groups to cover the chip (one 256x256 tile per
   // compute unit for the large-tile bf16 kernel, two 128x128 tiles else).
-  for (int w = 0; w < 2; ++w) {
-    const int M = w == 0 ? desc->I : H;
+  for (int l = 0; l < L; ++l) {
+    const int M = (l == 0 ? desc->I : H) + H;
     ll::GemmArgs g{};
     g.lda = g.ldb = p->ldT;
     g.M = M;
@@ -481,14 +481,13 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     long s = (want + tiles - 1) / tiles;
     s = std::max(1L, std::min(16L, s));
     const long max_by_k = std::max(1L, p->cap / 256);
-    p->dw_splits[w] = (int)std::min(s, max_by_k);
+    p->dw_splits[l] = (int)std::min(s, max_by_k);
   }
   const int maxI = std::max(desc->I, H);
   p->ws_floats = 0;
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
-    if (p->dw_splits[0] > 1) p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[0] * Il * 4 * H);
-    if (p->dw_splits[1] > 1) p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[1] * H * 4 * H);
+    if (p->dw_splits[l] > 1) p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[l] * (Il + H) * 4 * H);
   }
 
   const size_t es = p->es;
@@ -517,8 +516,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->Zx, sizeof(float) * cap * 4 * H, "input projection");
   ALLOC(p->DZ, es * cap * 4 * H, "dz");
   ALLOC(p->DZT, es * 4 * H * p->ldT, "dz transposed");
-  ALLOC(p->XT, es * maxI * p->ldT, "x transposed");
-  ALLOC(p->HPT, es * H * p->ldT, "h_prev transposed");
+  ALLOC(p->XT, es * (maxI + H) * p->ldT, "x and h_prev transposed");
   if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
   if (p->xmode) {
     // two slots x 8 XCDs x row tiles x (4H / k-step) blocks of 1 KB
@@ -1008,18 +1006,18 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   gt.mode = l == 0 ? 0 : 1;
   LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
   gt.in = p->HH[l];
-  gt.out = p->HPT;
+  gt.out = static_cast<char*>(p->XT) + p->es * Il * p->ldT;
   gt.C = H;
   gt.mode = 2;
   gt.h0f = p->h0 ? p->h0 + (long)l * B * H : nullptr;
   LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
   tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
-  // dW_x = X^T DZ, dW_h = Hprev^T DZ
+  // [dW_x; dW_h] = [X^T; Hprev^T] DZ: one product over the stacked operand
   ev = tbeg(p, s, LL_STAGE_DW);
-  for (int part = 0; part < 2; ++part) {
-    const int M = part == 0 ? Il : H;
+  {
+    const int M = Il + H;
     ll::GemmArgs g{};
-    g.A = part == 0 ? p->XT : p->HPT;
+    g.A = p->XT;
     g.lda = p->ldT;
     g.Bm = p->DZT;
     g.ldb = p->ldT;
@@ -1028,16 +1026,15 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
     g.K = (int)p->cap;
     g.K_dev = p->meta + 1;
     g.k_zero_tail = 1;   // the transposes write zeros past the last row, up to a multiple of 64
-    g.splits = p->dw_splits[part];
-    float* dst = dW[l] + (part == 0 ? 0L : (long)Il * 4 * H);
+    g.splits = p->dw_splits[l];
     if (g.splits > 1) {
       g.C = p->ws;
       g.ldc = 4L * H;
       g.split_stride = (long)M * 4 * H;
       LL_HIP(ll::launch_gemm_nt<T>(g, s));
-      LL_HIP(ll::launch_sum_slices(p->ws, g.splits, g.split_stride, g.split_stride, dst, s));
+      LL_HIP(ll::launch_sum_slices(p->ws, g.splits, g.split_stride, g.split_stride, dW[l], s));
     } else {
-      g.C = dst;
+      g.C = dW[l];
       g.ldc = 4L * H;
       LL_HIP(ll::launch_gemm_nt<T>(g, s));
     }
