@@ -213,7 +213,7 @@ def main():
     if w.spill:
         res_ms = timed({}, False)[0]
         nch = -(-w.T_max // C)
-        moved = sbytes[1] + sbytes[1] * max(nch - 4, 0) / nch   # out: every chunk, in: all but the resident ones
+        moved = 2 * sbytes[1]   # the chunks evicted from the device ring go out once and come back once
         spill = {"chunk_steps": C, "ring_slots": 4, "device_stack_bytes": sbytes[0],
                  "host_stack_bytes": sbytes[1], "ms_per_step_resident": res_ms / args.steps,
                  "overlap_efficiency": (res_ms / args.steps) / (gpu_ms / args.steps),

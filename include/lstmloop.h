@@ -80,11 +80,15 @@ typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
  *   spill = 1: the stack is swapped to pinned host memory (Section 5.3):
  *     the loops run one launch per chunk of spill_chunk_steps time steps
  *     (0 = 32; the loop state passes exactly from one launch to the next),
- *     the stack is a device ring of R chunk slots, each chunk is copied to
- *     host memory on the plan's copy stream after the forward launch that
- *     filled it, and copied back ahead of the gradient launches that read
- *     it.  R = device_stack_budget_bytes / (chunk_steps * B * 5H * 4),
- *     at least 3 (0 = 4); the results are bitwise those of spill = 0.
+ *     the stack is a device ring of R chunk slots.  Swapping starts only
+ *     when the ring is full and nothing is swapped twice: a chunk that a
+ *     later chunk evicts from its slot is copied to host memory on the
+ *     plan's copy stream after the forward launch that filled it, and
+ *     copied back once, ahead of the gradient launches that read it; the
+ *     last R chunks never leave the device, so a budget that holds every
+ *     chunk moves nothing.  R = device_stack_budget_bytes /
+ *     (chunk_steps * B * 5H * 4), at least 3 (0 = 4); the results are
+ *     bitwise those of spill = 0.
  *     Needs the XCD-local loops (see ll_plan_geometry); otherwise
  *     ll_plan_create returns LL_EUNSUPPORTED.  The h history, the input
  *     projections and dz stay in device memory.

@@ -558,8 +558,10 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     return fail(LL_EHIP, "creating the plan's side stream failed");
   }
   if (p->spill) {
-    const size_t hbytes = sizeof(float) * (size_t)p->nchunks * (size_t)p->slot_floats;
-    for (int l = 0; l < L; ++l) {
+    // only the chunks a later chunk evicts from the ring are swapped out (and
+    // back in); the last nslots chunks stay on the device
+    const size_t hbytes = sizeof(float) * (size_t)std::max(0, p->nchunks - p->nslots) * (size_t)p->slot_floats;
+    for (int l = 0; l < L && hbytes > 0; ++l) {
       if (hipHostMalloc(reinterpret_cast<void**>(&p->host_stack[l]), hbytes, hipHostMallocDefault) !=
           hipSuccess) {
         free_plan_memory(p);
@@ -583,7 +585,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   const int64_t stack_dev = p->spill ? (int64_t)sizeof(float) * p->nslots * p->slot_floats
                                      : (int64_t)sizeof(float) * cap * 5 * H;
   p->stack_device_bytes = (int64_t)L * (stack_dev + (int64_t)es * cap * H);
-  p->stack_host_bytes = p->spill ? (int64_t)L * (int64_t)sizeof(float) * p->nchunks * p->slot_floats : 0;
+  p->stack_host_bytes =
+      p->spill ? (int64_t)L * (int64_t)sizeof(float) * std::max(0, p->nchunks - p->nslots) * p->slot_floats : 0;
   *out = p;
   return LL_OK;
 }
@@ -864,7 +867,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
         xa.cT = last ? cout : p->carry + (long)B * H;
         LL_HIP(ll::x_launch(p->xk.fwd, xa, 256, p->xk.lds_fwd, s));
         tend(p, s, LL_STAGE_FWD_LOOP, ev);
-        if (p->spill && save) {   // swap the chunk out on the copy stream
+        if (p->spill && save && k < nch - p->nslots) {   // evicted later: swap it out on the copy stream
           LL_HIP(hipEventRecord(p->ev_compute, s));
           LL_HIP(hipStreamWaitEvent(p->cstream, p->ev_compute, 0));
           LL_HIP(hipMemcpyAsync(p->host_stack[l] + (long)k * p->slot_floats,
