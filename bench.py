@@ -214,8 +214,12 @@ def main():
         res_ms = timed({}, False)[0]
         nch = -(-w.T_max // C)
         moved = 2 * sbytes[1]   # the chunks evicted from the device ring go out once and come back once
+        # the alternative to swapping: push c_t only, recompute each chunk's
+        # gates in the gradient pass (two products over the chunk's rows)
+        rc = timed({"recompute": 1, "spill_chunk_steps": C}, False)
         spill = {"chunk_steps": C, "ring_slots": 4, "device_stack_bytes": sbytes[0],
                  "host_stack_bytes": sbytes[1], "ms_per_step_resident": res_ms / args.steps,
+                 "ms_per_step_recompute": rc[0] / args.steps, "device_stack_bytes_recompute": rc[4][0],
                  "overlap_efficiency": (res_ms / args.steps) / (gpu_ms / args.steps),
                  "host_link_GBps": moved / (gpu_ms / args.steps / 1e3) / 1e9}
 

@@ -92,6 +92,20 @@ typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
  *     Needs the XCD-local loops (see ll_plan_geometry); otherwise
  *     ll_plan_create returns LL_EUNSUPPORTED.  The h history, the input
  *     projections and dz stay in device memory.
+ *   recompute = 1 (the alternative to spilling; recomputation is the line
+ *     of work the paper's related-work section places swapping in): the
+ *     forward pushes only
+ *     c_t (4 bytes per unit instead of 20); the gradient pass runs one
+ *     launch per chunk of spill_chunk_steps steps (0 = 32) and, just before
+ *     each, recomputes that chunk's gates i, f, g, o into a device buffer
+ *     of one chunk: z = x_t W_x + b + h_{t-1} W_h as two matrix products
+ *     over the chunk's rows (h_{t-1} from the h history the dW products use
+ *     anyway), then the activations.  The values popped equal the saved ones
+ *     up to the summation order of z, so results stay within the parity
+ *     tolerance but are not bitwise those of recompute = 0.  Needs the
+ *     XCD-local loops and spill = 0 (else LL_EUNSUPPORTED); the two layers
+ *     then run one after the other.  The bias passed to lstm_loop_fwd is
+ *     copied into the plan for the gradient pass.
  *   reserved must be 0.
  */
 typedef struct {
@@ -104,7 +118,8 @@ typedef struct {
   int32_t spill;
   int32_t spill_chunk_steps;
   int64_t device_stack_budget_bytes;
-  int64_t reserved;
+  int32_t recompute;
+  int32_t reserved;
 } ll_desc;
 
 typedef struct ll_plan ll_plan;   /* opaque: owns the stack, scratch arrays,
@@ -221,7 +236,8 @@ typedef enum {
   LL_STAGE_DW = 5,            /* dW = sum_t [x_t, h_{t-1}]^T dz_t, db        */
   LL_STAGE_DX = 6,            /* dx_t = dz_t W_x^T (and finished-row zeros)  */
   LL_STAGE_LOOP_SETUP = 7,    /* exchange arrays filled, h0 rows reordered   */
-  LL_STAGE_COUNT = 8
+  LL_STAGE_RECOMPUTE = 8,     /* recompute = 1: gates of a chunk recomputed  */
+  LL_STAGE_COUNT = 9
 } ll_stage;
 
 ll_status ll_plan_set_timing(ll_plan* plan, int32_t enable);

@@ -209,6 +209,33 @@ __global__ __launch_bounds__(256) void zero_finished_rows_kernel(float* __restri
   }
 }
 
+// Row maps of the gate recomputation (one thread per padded row (t, r)).
+__global__ __launch_bounds__(256) void rc_maps_kernel(const int* __restrict__ active,
+                                                      const int* __restrict__ off,
+                                                      const int* __restrict__ perm, int B, int T_max,
+                                                      long cap, int* __restrict__ xmap,
+                                                      int* __restrict__ cmap, int* __restrict__ prevmap) {
+  const long n = (long)T_max * B;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+    const int t = (int)(i / B), r = (int)(i % B);
+    const bool run = r < active[t];
+    xmap[i] = run ? t * B + perm[r] : 0;
+    cmap[i] = run ? off[t] + r : 0;
+    prevmap[i] = run ? (t > 0 ? (int)(off[t - 1] + r) : (int)(cap + r)) : (int)cap;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void h0_rows_kernel(const float* __restrict__ h0,
+                                                      const int* __restrict__ perm, int B, int H,
+                                                      T* __restrict__ dst) {
+  const long n = (long)B * H;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+    const int r = (int)(i / H), j = (int)(i % H);
+    dst[i] = Op<T>::from_f32(h0 ? h0[(long)perm[r] * H + j] : 0.f);
+  }
+}
+
 // out[i] = sum_{s < S} ws[s * stride + i], fixed order.
 __global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict__ ws, int S,
                                                          long stride, long n,
@@ -344,6 +371,23 @@ hipError_t launch_zero_finished_rows(float* dst, int T_max, int B, int C, const 
   return hipGetLastError();
 }
 
+hipError_t launch_rc_maps(const int* active, const int* off, const int* perm, int B, int T_max,
+                          long cap, int* xmap, int* cmap, int* prevmap, hipStream_t s) {
+  long blocks = ((long)T_max * B + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(rc_maps_kernel, dim3((unsigned)blocks), dim3(256), 0, s, active, off, perm, B,
+                     T_max, cap, xmap, cmap, prevmap);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_h0_rows(const float* h0, const int* perm, int B, int H, T* dst, hipStream_t s) {
+  long blocks = ((long)B * H + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(h0_rows_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, h0, perm, B, H, dst);
+  return hipGetLastError();
+}
+
 hipError_t launch_sum_slices(const float* ws, int S, long stride, long n, float* out,
                              hipStream_t s) {
   long blocks = (n + 255) / 256;
@@ -368,6 +412,8 @@ template hipError_t launch_transpose<bf16_t>(const bf16_t*, int, int, int, bf16_
                                              hipStream_t);
 template hipError_t launch_gather_transpose<float>(const GatherTArgs&, int, hipStream_t);
 template hipError_t launch_gather_transpose<bf16_t>(const GatherTArgs&, int, hipStream_t);
+template hipError_t launch_h0_rows<float>(const float*, const int*, int, int, float*, hipStream_t);
+template hipError_t launch_h0_rows<bf16_t>(const float*, const int*, int, int, bf16_t*, hipStream_t);
 template hipError_t launch_convert<float>(const float*, long, float*, hipStream_t);
 template hipError_t launch_convert<bf16_t>(const float*, long, bf16_t*, hipStream_t);
 

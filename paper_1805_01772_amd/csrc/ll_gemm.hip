@@ -39,6 +39,12 @@ __device__ __forceinline__ uint4 load_chunk(const T* row, int kk, int kend) {
   return v;
 }
 
+// Gate activation of column block blk (i, f, g, o): tanh for g, the
+// logistic function for the others (the recomputation of saved gates).
+__device__ __forceinline__ float lstm_gate_act(float u, int blk) {
+  return blk == 2 ? tanhf_(u) : sigmoidf_(u);
+}
+
 }  // namespace
 
 template <typename T>
@@ -148,6 +154,10 @@ __global__ __launch_bounds__(256, 2) void gemm_nt_kernel(GemmArgs g) {
         if (n < g.N) {
           float v = acc[i][j][e];
           if (g.bias && (!split || z == 0)) v += g.bias[n];
+          if (g.act_h) {
+            const float zin = g.addend ? g.addend[(long)g.add_rowmap[m] * g.ld_add + n] : cr[n];
+            v = lstm_gate_act(v + zin, n / g.act_h);
+          }
           cr[n] = v;
         }
       }
@@ -324,6 +334,10 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_nt_bf16_lds_kernel(GemmAr
         if (n < g.N) {
           float v = acc[i][j][r];
           if (g.bias && (!split || z == 0)) v += g.bias[n];
+          if (g.act_h) {
+            const float zin = g.addend ? g.addend[(long)g.add_rowmap[m] * g.ld_add + n] : cr[n];
+            v = lstm_gate_act(v + zin, n / g.act_h);
+          }
           cr[n] = v;
         }
       }
@@ -362,6 +376,7 @@ long gemm_rounds(const GemmArgs& g, int elem_bytes, int n_cu) {
 
 template <typename T>
 hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s) {
+  if (g.act_h > 0 && (g.splits != 1 || g.bias)) return hipErrorInvalidValue;
   if (gemm_big_applies(g, (int)sizeof(T))) {
     long ab, bb;
     big_ranges(g, &ab, &bb);

@@ -51,6 +51,14 @@ struct GemmArgs {
   long split_stride;
   int a_rows;            // rows of A the row map addresses (0: M)
   int k_zero_tail;       // 1: both operands hold zeros from K up to the next multiple of 8
+  // > 0: LSTM gate epilogue with H = act_h: C = act(Z + A B^T), Z = C
+  // (addend NULL) or addend[add_rowmap[m] * ld_add + n], act the logistic
+  // function on columns [0, 2H) and [3H, 4H), tanh on [2H, 3H) (needs
+  // splits == 1 and no bias)
+  int act_h;
+  const float* addend;
+  const int* add_rowmap;
+  long ld_add;
 };
 
 struct LoopGeom {
@@ -166,6 +174,14 @@ struct XLoopArgs {
   unsigned* dyx_flags;    // gradient: per-member flags of dyx_ring ([8][MRT][32])
   const unsigned* peer_flags;  // gradient: the other layer's step flags
   const void* Wx;         // upper layer, gradient: W rows of the input part [I_l, 4H]
+  // saved values: the c field of row (t, r) at stack + stack_row(t, r) * sld
+  // + scoff; i, f, g, o at gstk + grow(t, r) * gld + {0, H, 2H, 3H}, where
+  // grow maps like stack_row with gchunk / gslots (gstk NULL: the gates sit
+  // in the stack rows, at offsets 0 .. 3H)
+  int sld, scoff;
+  int sgates;             // forward: 1 = push i, f, g, o with c (0: c only)
+  const float* gstk;
+  int gld, gchunk, gslots;
 };
 
 // Chip-wide loops (ll_cloop.hip), for shapes whose recurrent weights need
@@ -261,6 +277,16 @@ template <typename T>
 hipError_t launch_gather_transpose(const GatherTArgs& g, int cap_rows, hipStream_t s);
 hipError_t launch_zero_finished_rows(float* dst, int T_max, int B, int C, const int* seq_len,
                                      const int* meta, hipStream_t s);
+// Row maps of the gate recomputation over padded rows (t, r), r < B:
+//   xmap[t B + r] = t B + perm[r] (time-major input row),
+//   cmap[t B + r] = off[t] + r (compact row), prevmap[t B + r] = off[t-1] + r
+//   for t > 0 and cap + r for t = 0 (where the h0 rows follow the history);
+// rows not running at t map to row 0 (x, compact) and cap (h_{t-1}).
+hipError_t launch_rc_maps(const int* active, const int* off, const int* perm, int B, int T_max,
+                          long cap, int* xmap, int* cmap, int* prevmap, hipStream_t s);
+// dst[r * H + j] = h0[perm[r] * H + j] in the operand type (0 if h0 is NULL).
+template <typename T>
+hipError_t launch_h0_rows(const float* h0, const int* perm, int B, int H, T* dst, hipStream_t s);
 hipError_t launch_sum_slices(const float* ws, int S, long stride, long n, float* out,
                              hipStream_t s);
 template <typename T>

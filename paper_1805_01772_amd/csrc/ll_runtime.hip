@@ -123,6 +123,16 @@ struct ll_plan {
   long slot_floats = 0;
   float* host_stack[2] = {nullptr, nullptr};
   hipStream_t cstream = nullptr;
+  // recomputation instead of saved gates (XCD-local loops only): the forward
+  // pushes only c_t ([T_max*B, H] per layer); the gradient pass recomputes
+  // i, f, g, o of each chunk of rc_steps steps into gslot just before the
+  // chunk's launch, from x_t (or y_t of the layer below), the h history and W
+  bool recompute = false;
+  int rc_steps = 0, rc_chunks = 1;
+  float* gslot = nullptr;       // [rc_steps * B, 4H]
+  int* rc_inmap = nullptr;      // [2][T_max * B]: input row of (t, r): x (time-major), compact
+  int* rc_prevmap = nullptr;    // [T_max * B]: h history row of h_{t-1} (rows cap.. hold h0)
+  float* rc_bias = nullptr;     // [layers, 4H]: the forward's bias, kept for the recomputation
   // side stream for the dx product, which runs beside the dW products after
   // the gradient loop (forked from and joined back into the call's stream)
   hipStream_t gstream = nullptr;
@@ -211,7 +221,8 @@ void free_plan_memory(ll_plan* p) {
   void* ptrs[] = {p->perm, p->active, p->off, p->rowmap, p->meta, p->WT[0], p->WT[1], p->Zx,
                   p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT,
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
-                  p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags};
+                  p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags,
+                  p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -279,6 +290,9 @@ ll_status validate_desc(const ll_desc* d) {
   if (d->spill != 0 && d->spill != 1) return fail(LL_EINVAL, "spill must be 0 or 1");
   if (d->spill_chunk_steps < 0 || d->device_stack_budget_bytes < 0)
     return fail(LL_EINVAL, "spill_chunk_steps and device_stack_budget_bytes must be >= 0");
+  if (d->recompute != 0 && d->recompute != 1) return fail(LL_EINVAL, "recompute must be 0 or 1");
+  if (d->recompute && d->spill)
+    return fail(LL_EUNSUPPORTED, "recompute and spill are alternatives; choose one");
   if (d->reserved != 0) return fail(LL_EINVAL, "reserved must be 0");
   if ((long)d->T_max * d->B > (1L << 30))
     return fail(LL_EUNSUPPORTED, "T_max * B = %ld exceeds 2^30 rows", (long)d->T_max * d->B);
@@ -441,12 +455,22 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     long r = desc->device_stack_budget_bytes > 0 ? desc->device_stack_budget_bytes / slot_bytes : 4;
     p->nslots = (int)std::max(3L, std::min(r, (long)p->nchunks));
   }
+  if (desc->recompute) {
+    if (!p->xmode) {
+      delete p;
+      return fail(LL_EUNSUPPORTED,
+                  "recompute needs the XCD-local loops (H = %d, B = %d do not fit them)", H, B);
+    }
+    p->recompute = true;
+    p->rc_steps = std::min(desc->T_max, desc->spill_chunk_steps > 0 ? desc->spill_chunk_steps : 32);
+    p->rc_chunks = (desc->T_max + p->rc_steps - 1) / p->rc_steps;
+  }
 
   // Two-layer wavefront: on every XCD, members 0..P-1 run the lower layer
   // and P..2P-1 the upper one, so both layers' steps overlap in one launch.
   // LSTMLOOP_WAVEFRONT=off at plan creation runs the layers one after the
   // other.
-  if (L == 2 && p->xmode && !p->spill && 2 * p->xP <= 32 && p->xhc <= 2) {
+  if (L == 2 && p->xmode && !p->spill && !p->recompute && 2 * p->xP <= 32 && p->xhc <= 2) {
     const char* wf = getenv("LSTMLOOP_WAVEFRONT");
     if (!(wf && strcmp(wf, "off") == 0)) {
       ll::XKernels xk2 = p->bf16 ? ll::x_kernels2<bf16_t>(p->xhc, p->xMRT)
@@ -510,8 +534,11 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->meta, sizeof(int) * ll::META_INTS, "meta");
   for (int l = 0; l < L; ++l) {
     ALLOC(p->WT[l], es * 4 * H * (in_width(p, l) + H), "transposed W");
-    ALLOC(p->stack[l], sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * 5 * H), "stack");
-    ALLOC(p->HH[l], es * cap * H, "h history");
+    ALLOC(p->stack[l],
+          sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * (p->recompute ? 1 : 5) * H),
+          "stack");
+    // (recompute: B more rows hold h0 in the operand type, the h_{t-1} of step 0)
+    ALLOC(p->HH[l], es * (cap + (p->recompute ? B : 0)) * H, "h history");
   }
   ALLOC(p->Zx, sizeof(float) * cap * 4 * H, "input projection");
   ALLOC(p->DZ, es * cap * 4 * H, "dz");
@@ -538,7 +565,13 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     p->cflag_words = 8 + p->cMRT * 256 + 8 * p->cMRT * 32;
     ALLOC(p->cflags, sizeof(unsigned) * p->cflag_words, "exchange flags");
   }
-  if (p->spill) {
+  if (p->recompute) {
+    ALLOC(p->gslot, sizeof(float) * (long)p->rc_steps * B * 4 * H, "recomputed gates");
+    ALLOC(p->rc_inmap, sizeof(int) * 2 * cap, "recomputation row maps");
+    ALLOC(p->rc_prevmap, sizeof(int) * cap, "recomputation row maps");
+    ALLOC(p->rc_bias, sizeof(float) * L * 4 * H, "saved bias");
+  }
+  if (p->spill || p->recompute) {
     ALLOC(p->carry, sizeof(float) * 4 * B * H, "chunk carry");
     ALLOC(p->db_state, sizeof(float) * 8 * 32 * 512 * 4, "db state");
   }
@@ -583,8 +616,9 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     }
   }
   const int64_t stack_dev = p->spill ? (int64_t)sizeof(float) * p->nslots * p->slot_floats
-                                     : (int64_t)sizeof(float) * cap * 5 * H;
-  p->stack_device_bytes = (int64_t)L * (stack_dev + (int64_t)es * cap * H);
+                                     : (int64_t)sizeof(float) * cap * (p->recompute ? 1 : 5) * H;
+  p->stack_device_bytes = (int64_t)L * (stack_dev + (int64_t)es * (cap + (p->recompute ? B : 0)) * H);
+  if (p->recompute) p->stack_device_bytes += (int64_t)sizeof(float) * p->rc_steps * B * 4 * H;
   p->stack_host_bytes =
       p->spill ? (int64_t)L * (int64_t)sizeof(float) * std::max(0, p->nchunks - p->nslots) * p->slot_floats : 0;
   *out = p;
@@ -693,6 +727,9 @@ ll::XLoopArgs x_common(const ll_plan* p) {
   a.t_end = p->d.T_max;
   a.chunk_steps = p->d.T_max;
   a.nslots = 1;
+  a.sld = 5 * p->d.H;
+  a.scoff = 4 * p->d.H;
+  a.sgates = 1;
   return a;
 }
 
@@ -815,7 +852,15 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     tend(p, s, LL_STAGE_INPUT_PROJ, ev);
     if (p->xmode) {
       const int ring_ks = (int)((long)H * p->es / 64);
-      ll::XLoopArgs xa{};
+      ll::XLoopArgs xa = x_common(p);
+      if (p->recompute) {   // push c_t only; keep the bias for the gate recomputation
+        xa.sld = H;
+        xa.scoff = 0;
+        xa.sgates = 0;
+        if (save)
+          LL_HIP(hipMemcpyAsync(p->rc_bias + (long)l * 4 * H, bias[l], sizeof(float) * 4 * H,
+                                hipMemcpyDeviceToDevice, s));
+      }
       xa.ring = p->xring;
       xa.ring_ks = ring_ks;
       xa.rank_ctr = p->xflags;
@@ -1111,6 +1156,75 @@ ll_status enqueue_bwd_wave(ll_plan* p, hipStream_t s, const float* dy, const flo
   return bwd_products<T>(p, s, 0, p->DZ, p->db_part, dx, dW, dbias);
 }
 
+// Gate recomputation (recompute = 1): row maps over padded rows (t, r) and
+// the h0 rows after every layer's h history, once per gradient pass.
+template <typename T>
+ll_status recompute_setup(ll_plan* p, hipStream_t s) {
+  const ll_desc& d = p->d;
+  const int H = d.H, B = d.B;
+  hipEvent_t ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
+  LL_HIP(ll::launch_rc_maps(p->active, p->off, p->perm, B, d.T_max, p->cap, p->rc_inmap,
+                            p->rc_inmap + p->cap, p->rc_prevmap, s));
+  for (int l = 0; l < d.layers; ++l)
+    LL_HIP(ll::launch_h0_rows<T>(p->h0 ? p->h0 + (long)l * B * H : nullptr, p->perm, B, H,
+                                 reinterpret_cast<T*>(p->HH[l]) + p->cap * H, s));
+  tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+  return LL_OK;
+}
+
+// i, f, g, o of steps [t0, t1) of layer l into gslot (row (t - t0) B + r):
+// z = x_t W_x + b (the top layer reuses its input projection, still in Zx),
+// then act(z + h_{t-1} W_h) in the second product's epilogue.
+template <typename T>
+ll_status recompute_gates(ll_plan* p, hipStream_t s, int l, int t0, int t1) {
+  const ll_desc& d = p->d;
+  const int H = d.H, B = d.B, Il = in_width(p, l);
+  const long M = (long)(t1 - t0) * B;
+  const int* xmap = p->rc_inmap;
+  const int* cmap = p->rc_inmap + p->cap;
+  hipEvent_t ev = tbeg(p, s, LL_STAGE_RECOMPUTE);
+  const bool zx_live = l == d.layers - 1;   // Zx holds this layer's projections
+  if (!zx_live) {
+    ll::GemmArgs g{};
+    g.A = l == 0 ? p->x : p->HH[0];
+    g.lda = Il;
+    g.a_rowmap = (l == 0 ? xmap : cmap) + (long)t0 * B;
+    g.a_rows = (int)p->cap;
+    g.Bm = p->WT[l];
+    g.ldb = Il + H;
+    g.K = Il;
+    g.N = 4 * H;
+    g.M = (int)M;
+    g.bias = p->rc_bias + (long)l * 4 * H;
+    g.C = p->gslot;
+    g.ldc = 4L * H;
+    g.splits = 1;
+    LL_HIP(ll::launch_gemm_nt<T>(g, s));
+  }
+  ll::GemmArgs h{};
+  h.A = p->HH[l];
+  h.lda = H;
+  h.a_rowmap = p->rc_prevmap + (long)t0 * B;
+  h.a_rows = (int)(p->cap + B);
+  h.Bm = reinterpret_cast<const T*>(p->WT[l]) + Il;
+  h.ldb = Il + H;
+  h.K = H;
+  h.N = 4 * H;
+  h.M = (int)M;
+  h.C = p->gslot;
+  h.ldc = 4L * H;
+  h.splits = 1;
+  h.act_h = H;
+  if (zx_live) {
+    h.addend = p->Zx;
+    h.add_rowmap = cmap + (long)t0 * B;
+    h.ld_add = 4L * H;
+  }
+  LL_HIP(ll::launch_gemm_nt<T>(h, s));
+  tend(p, s, LL_STAGE_RECOMPUTE, ev);
+  return LL_OK;
+}
+
 template <typename T>
 ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* dhT,
                       const float* dcT, float* dx, float* const* dW, float* const* dbias,
@@ -1124,7 +1238,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
   for (int l = L - 1; l >= 0; --l) {
     const int Il = in_width(p, l);
     if (p->xmode) {
-      ll::XLoopArgs xa{};
+      ll::XLoopArgs xa = x_common(p);
       xa.ring = p->xring;
       xa.ring_ks = (int)(4L * H * p->es / 64);
       xa.rank_ctr = p->xflags;
@@ -1158,12 +1272,21 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       const float* dcin = dcT ? dcT + (long)l * B * H : nullptr;
       float* dhout = dh0 ? dh0 + (long)l * B * H : nullptr;
       float* dcout = dc0 ? dc0 + (long)l * B * H : nullptr;
-      const int C = p->spill ? p->chunk_steps : d.T_max;
-      const int nch = p->spill ? p->nchunks : 1;
+      const int C = p->spill ? p->chunk_steps : p->recompute ? p->rc_steps : d.T_max;
+      const int nch = p->spill ? p->nchunks : p->recompute ? p->rc_chunks : 1;
       const int R = p->spill ? p->nslots : 1;
-      xa.chunk_steps = C;
+      xa.chunk_steps = p->spill ? C : d.T_max;
       xa.nslots = R;
-      xa.db_state = p->spill ? p->db_state : nullptr;
+      xa.db_state = (p->spill || p->recompute) ? p->db_state : nullptr;
+      if (p->recompute) {   // c_t from the c-only stack, the gates from the chunk buffer
+        xa.sld = H;
+        xa.scoff = 0;
+        xa.gstk = p->gslot;
+        xa.gld = 4 * H;
+        xa.gchunk = C;
+        xa.gslots = 1;
+        if (l == L - 1) LL_STATUS(recompute_setup<T>(p, s));
+      }
       // chunks at or above nch - R are still in the ring after the forward; a
       // chunk j below is swapped in after the launch of chunk j + R (the last
       // use of its slot) and waited for before the launches of j + 1 (which
@@ -1180,6 +1303,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
         LL_HIP(wait_loaded(k - 1));
         LL_HIP(ll::launch_zero_u32(p->xflags, p->xflag_words, s));
         tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+        if (p->recompute) LL_STATUS(recompute_gates<T>(p, s, l, t0, t1));
         ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
         xa.t_begin = t0;
         xa.t_end = t1;

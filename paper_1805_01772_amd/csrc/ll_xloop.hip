@@ -83,6 +83,12 @@ __device__ __forceinline__ long stack_row(const XLoopArgs& a, int t, int r) {
   const int k = t / a.chunk_steps;
   return ((long)((k % a.nslots) * a.chunk_steps + (t - k * a.chunk_steps)) * a.B + r);
 }
+// Row of (step t, compact index r) where the gates i, f, g, o are popped.
+__device__ __forceinline__ long gate_row(const XLoopArgs& a, int t, int r) {
+  if (!a.gstk) return stack_row(a, t, r);
+  const int k = t / a.gchunk;
+  return ((long)((k % a.gslots) * a.gchunk + (t - k * a.gchunk)) * a.B + r);
+}
 
 // Ring slot of row tile mt: ring_ks blocks of 1 KB.
 __device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp, int mt) {
@@ -120,7 +126,6 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   const int q = lane >> 4, l16 = lane & 15;
   const int H = a.H, B = a.B;
   const long G4 = 4L * H;
-  const long H5 = 5L * H;
   const int j0 = rank * HJ;
   const int KX = TOP ? a.in_ks : 0;                      // k-steps from the lower layer
   const int KS = KX + H / (4 * KPC);
@@ -314,12 +319,14 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         const long cr = off_t + r;
         HH[cr * H + ju] = Op<T>::from_f32(hn);
         if (a.stack) {
-          float* st = a.stack + stack_row(a, t, r) * H5 + ju;
-          st[0] = ig;
-          st[H] = fg;
-          st[2 * H] = gg;
-          st[3 * H] = og;
-          st[4 * H] = cn;
+          float* st = a.stack + stack_row(a, t, r) * a.sld + ju;
+          if (a.sgates) {
+            st[0] = ig;
+            st[H] = fg;
+            st[2 * H] = gg;
+            st[3 * H] = og;
+          }
+          st[a.scoff] = cn;
         }
       }
       if (a.y && cellt) {
@@ -413,7 +420,6 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   const int q = lane >> 4, l16 = lane & 15;
   const int H = a.H, B = a.B, P = a.P;
   const long G4 = 4L * H;
-  const long H5 = 5L * H;
   const int j0 = rank * HJ;
   const int KS = (int)(G4 / (4 * KPC));
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
@@ -480,13 +486,19 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
     const bool ok = cellt && crow < nr;
     const int b = sperm[mt * 16 + crow];
     const int ts = max(tt, 0);
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.stack + stack_row(a, ts, r0) * H5, (unsigned)(nr * H5 * 4));
-    const unsigned so = ok ? (unsigned)((crow * H5 + ju) * 4) : kOOB;
+    const long SL = a.sld, GL = a.gstk ? a.gld : a.sld;
+    const float* gbase = a.gstk ? a.gstk : a.stack;
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(gbase + gate_row(a, ts, r0) * GL, (unsigned)(nr * GL * 4));
+    const unsigned go = ok ? (unsigned)((crow * GL + ju) * 4) : kOOB;
 #pragma unroll
-    for (int c = 0; c < 5; ++c) v[c] = ld_f32(rs, so + c * H * 4);
+    for (int c = 0; c < 4; ++c) v[c] = ld_f32(rg, go + c * H * 4);
+    const unsigned so = ok ? (unsigned)((crow * SL + ju) * 4) : kOOB;
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc(a.stack + stack_row(a, ts, r0) * SL + a.scoff, (unsigned)(nr * SL * 4));
+    v[4] = ld_f32(rs, so);
     if (tt > 0) {
       const __amdgpu_buffer_rsrc_t rp2 =
-          make_rsrc(a.stack + stack_row(a, tt - 1, r0) * H5 + 4L * H, (unsigned)(nr * H5 * 4));
+          make_rsrc(a.stack + stack_row(a, tt - 1, r0) * SL + a.scoff, (unsigned)(nr * SL * 4));
       v[5] = ld_f32(rp2, so);
     } else {
       const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.c0, a.c0 ? (unsigned)(B * H * 4) : 0u);

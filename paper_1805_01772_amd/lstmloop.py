@@ -26,7 +26,8 @@ EXPORTED = ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes",
             "ll_status_sync", "ll_last_error", "ll_version",
             "ll_plan_set_timing", "ll_plan_set_timing_stages", "ll_plan_read_timing",
             "ll_measure_mfma_peak")
-STAGES = ("prep", "input_proj", "fwd_loop", "bwd_loop", "bwd_operands", "dw", "dx", "loop_setup")
+STAGES = ("prep", "input_proj", "fwd_loop", "bwd_loop", "bwd_operands", "dw", "dx", "loop_setup",
+          "recompute")
 
 
 class ll_desc(ctypes.Structure):
@@ -35,7 +36,7 @@ class ll_desc(ctypes.Structure):
                 ("layers", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("spill", ctypes.c_int32), ("spill_chunk_steps", ctypes.c_int32),
                 ("device_stack_budget_bytes", ctypes.c_int64),
-                ("reserved", ctypes.c_int64)]
+                ("recompute", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class LoopError(RuntimeError):
@@ -138,12 +139,13 @@ class Plan:
 
     def __init__(self, T_max: int, B: int, I: int, H: int, layers: int = 1,
                  dtype: str = "f32", spill: int = 0, spill_chunk_steps: int = 0,
-                 device_stack_budget_bytes: int = 0, device: int = 0, reserved: int = 0):
+                 device_stack_budget_bytes: int = 0, device: int = 0, recompute: int = 0,
+                 reserved: int = 0):
         lib = load_library()
         self._lib = lib
         self.desc = ll_desc(T_max, B, I, H, layers,
                             LL_BF16 if dtype == "bf16" else LL_F32 if dtype == "f32" else int(dtype),
-                            spill, spill_chunk_steps, device_stack_budget_bytes, reserved)
+                            spill, spill_chunk_steps, device_stack_budget_bytes, recompute, reserved)
         self.dtype = dtype
         self.device = device
         h = ctypes.c_void_p()

@@ -487,3 +487,50 @@ def test_spill_long_sequences():
     errs, bad = compare(gsub, ref_o, TOL[w.dtype], keys=("y", "hT", "cT", "dx", "dh0", "dc0"))
     say(f"    errors {errs}")
     assert not bad, bad
+
+
+RECOMPUTE_CASES = [
+    # (workload, chunk steps)
+    (W("rc_f32_b20_i24_h64_t50", B=20, I=24, H=64, T_max=50, dtype="f32", len_lo=0, len_hi=50,
+       w_scale=0.3, random_state=True, seed=31), 8),
+    (W("rc_bf16_b40_i32_h128_t37", B=40, I=32, H=128, T_max=37, dtype="bf16", len_lo=1, len_hi=37,
+       w_scale=0.3, random_state=True, seed=32), 5),
+    (W("rc_f32_2layer_b17_i16_h32_t29", B=17, I=16, H=32, T_max=29, dtype="f32", layers=2,
+       len_lo=0, len_hi=29, w_scale=0.3, random_state=True, seed=33), 4),
+    (W("rc_bf16_2layer_b70_i64_h128_t21", B=70, I=64, H=128, T_max=21, dtype="bf16", layers=2,
+       len_lo=0, len_hi=21, w_scale=0.3, random_state=True, seed=34), 32),
+    (W("rc_f32_b9_i8_h32_t12_short", B=9, I=8, H=32, T_max=12, dtype="f32", len_lo=0, len_hi=5,
+       w_scale=0.3, random_state=True, seed=35), 3),
+]
+
+
+@pytest.mark.parametrize("w,C", RECOMPUTE_CASES, ids=[c[0].name for c in RECOMPUTE_CASES])
+def test_recompute_parity(w, C):
+    """Gates recomputed per chunk in the gradient pass (only c_t pushed):
+    every output within the tolerance of the oracle, and of the plan that
+    saves the gates; the device stack is smaller."""
+    say(f"[recompute] {w.name} C={C}")
+    inp = wl.generate(w)
+    got, err1, dev1, host1 = _run_plan(w, inp, recompute=1, spill_chunk_steps=C)
+    ref, err0, dev0, _ = _run_plan(w, inp)
+    assert err0 == 0 and err1 == 0
+    assert host1 == 0 and dev1 < dev0
+    errs, bad = compare(got, oracle_reference(inp, w.layers, w.dtype), TOL[w.dtype])
+    say(f"    errors vs oracle {errs}")
+    assert not bad, bad
+    errs, bad = compare(got, ref, TOL[w.dtype])
+    say(f"    errors vs saved gates {errs}")
+    assert not bad, bad
+
+
+def test_recompute_zero_trip():
+    """All lengths zero: no iteration, no recomputation; outputs are the
+    initial state and the incoming gradients."""
+    w = W("rc_zero_b6_i8_h32_t9", B=6, I=8, H=32, T_max=9, dtype="f32", len_lo=0, len_hi=0,
+          w_scale=0.3, random_state=True, seed=36)
+    inp = wl.generate(w)
+    got, err, _, _ = _run_plan(w, inp, recompute=1, spill_chunk_steps=4)
+    assert err == 0
+    assert np.array_equal(got["hT"][0], inp["h0"][0]) and np.array_equal(got["cT"][0], inp["c0"][0])
+    assert np.array_equal(got["dh0"][0], inp["dhT"][0]) and np.array_equal(got["dc0"][0], inp["dcT"][0])
+    assert not np.any(got["dW"][0]) and not np.any(got["dx"])
