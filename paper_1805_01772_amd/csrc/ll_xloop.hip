@@ -48,8 +48,8 @@ constexpr int WIN = 256;
 // floats puts the four rows a 16-lane group of the cell reads in distinct
 // LDS banks.
 constexpr int xfwd_is(int NCT) { return NCT * 64 + 16; }
-constexpr int xbwd_is(int NCT) { return NCT * 64 + 16; }
-constexpr int xbwd_red_floats(int NCT) {
+__host__ __device__ constexpr int xbwd_is(int NCT) { return NCT * 64 + 16; }
+__host__ __device__ constexpr int xbwd_red_floats(int NCT) {
   return XNW * 4 * xbwd_is(NCT) > 16 * 4 * 16 * NCT ? XNW * 4 * xbwd_is(NCT) : 16 * 4 * 16 * NCT;
 }
 
@@ -61,11 +61,15 @@ size_t xfwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
          (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
 }
 // LDS of the gradient kernel: weight k-steps not in registers, partial
-// products (reused for the db rows at the end), metadata window, perm rows.
-size_t xbwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
+// products (reused for the db rows at the end), metadata window, perm rows,
+// and with DMA the dz tile (KSW k-steps of 1 KB per wave).
+__host__ __device__ constexpr int xbwd_tail_chunks(int NCT, int mrt_max) {
+  return (xbwd_red_floats(NCT) * 4 + 2 * (WIN + 1) * 4 + mrt_max * 16 * 4 + 15) / 16;
+}
+size_t xbwd_lds(int KSW, int KSR, int NCT, int mrt_max, bool dma = false) {
   const int KSL = KSW > KSR ? KSW - KSR : 0;
-  return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)xbwd_red_floats(NCT) * 4 +
-         (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
+  return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)xbwd_tail_chunks(NCT, mrt_max) * 16 +
+         (dma ? (size_t)XNW * KSW * 1024 : 0);
 }
 
 __device__ __forceinline__ void load_window(const XLoopArgs& a, int* win, int lo) {
@@ -406,7 +410,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd2_kernel(XLoopArgs a0, XLoopArgs a
 // (its dy comes from the upper layer's dyx ring, one step later); 2: the upper
 // layer, which also computes dy_{lower} = dz W_x^T for its units (NCO = 2 NCT
 // output column tiles: W_h rows, then W_x rows) and publishes it per step.
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE, bool DMA = false>
 __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT;                 // units per work-group
@@ -446,6 +450,8 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCO * 64);   // [XNW][4][IS]
   int* win = reinterpret_cast<int*>(red + xbwd_red_floats(NCO));       // [2][WIN+1]
   int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
+  // DMA: this wave's KSW k-steps of the dz tile, loaded straight into LDS
+  uint4* dzl = lds + XNW * KSL * NCO * 64 + xbwd_tail_chunks(NCO, MRT_MAX) + wave * KSW * 64;
 
   // (row, unit) of this thread: 16 lanes take 16 consecutive units of one
   // row, a wave four rows (the four MFMA result elements of a lane group)
@@ -595,13 +601,34 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       f32x4 acc[NCO];
 #pragma unroll
       for (int ct = 0; ct < NCO; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if constexpr (DMA) {
+        // every k-step of the wave in flight at once (no registers held):
+        // KSW loads into LDS, then the 7 pops of the next step behind them
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int i = 0; i < KSW; ++i)
+          ld_chunk_to_lds(rs, i < nks ? (unsigned)(((ks0 + i) << 10) + lane * 16) : kOOB, dzl + i * 64);
+        asm volatile("" ::: "memory");
+        fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);
+        asm volatile("" ::: "memory");
+      }
+      const unsigned dza = lds_addr(dzl) + lane * 16;
 #pragma unroll
       for (int b0 = 0; b0 < KSW; b0 += KB) {
         uint4 av[KB];
+        if constexpr (DMA) {
+          wait_vm_n(7 + KSW - (b0 + KB < KSW ? b0 + KB : KSW));   // this batch has landed
 #pragma unroll
-        for (int i = 0; i < KB; ++i)
-          av[i] = ld_chunk_l2(rs, b0 + i < nks ? (unsigned)(((ks0 + b0 + i) << 10) + lane * 16) : kOOB);
-        if (b0 + KB >= KSW) fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);   // next step's pops
+          for (int i = 0; i < KB; ++i) av[i] = b0 + i < KSW ? ds_rd(dza + (b0 + i) * 1024) : zero4();
+          wait_lgkm<0>();
+#pragma unroll
+          for (int i = 0; i < KB; ++i) touch(av[i]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < KB; ++i)
+            av[i] = ld_chunk_l2(rs, b0 + i < nks ? (unsigned)(((ks0 + b0 + i) << 10) + lane * 16) : kOOB);
+          if (b0 + KB >= KSW) fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);   // next step's pops
+        }
 #pragma unroll
         for (int i = 0; i < KB; ++i) {
           const int ii = b0 + i;
@@ -672,7 +699,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   }
 }
 
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool DMA>
 __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
@@ -686,7 +713,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0>(a, grp, rank, lds);
+  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, DMA>(a, grp, rank, lds);
 }
 
 // Two-layer wavefront, gradient: members 0 .. P-1 of every XCD run the lower
@@ -781,9 +808,16 @@ template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT>
 XKernels x_make() {
   XKernels k{};
   k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT>);
-  k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, 4 * HC, RB, MRT>);
   k.lds_fwd = xfwd_lds(HC, RF, NF, MRT);
-  k.lds_bwd = xbwd_lds(4 * HC, RB, NB, MRT);
+  // the gradient loop loads its dz k-steps straight into LDS when they fit
+  const size_t dma_lds = xbwd_lds(4 * HC, RB, NB, MRT, true);
+  if (dma_lds <= 160 * 1024) {
+    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, 4 * HC, RB, MRT, true>);
+    k.lds_bwd = dma_lds;
+  } else {
+    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, 4 * HC, RB, MRT, false>);
+    k.lds_bwd = xbwd_lds(4 * HC, RB, NB, MRT);
+  }
   return k;
 }
 }  // namespace
