@@ -323,13 +323,14 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         const long cr = off_t + r;
         HH[cr * H + ju] = Op<T>::from_f32(hn);
         if (a.stack) {
+          // (c only: the gate stores all land on the c field, which the last
+          // store overwrites; no branch on the common path)
           float* st = a.stack + stack_row(a, t, r) * a.sld + ju;
-          if (a.sgates) {
-            st[0] = ig;
-            st[H] = fg;
-            st[2 * H] = gg;
-            st[3 * H] = og;
-          }
+          const int gs = a.sgates ? H : 0;
+          st[0] = ig;
+          st[gs] = fg;
+          st[2 * gs] = gg;
+          st[3 * gs] = og;
           st[a.scoff] = cn;
         }
       }
