@@ -5,7 +5,10 @@ Only tests, the smoke check and the benchmark's CPU-baseline leg use it.
 from .lstm import (bf16_round, sigmoid, lstm_forward_literal, lstm_forward,
                    lstm_backward, stacked_forward, stacked_backward,
                    matmul_chain_grad)
+from .rnn import (rnn_forward_literal, rnn_forward, rnn_backward,
+                  stacked_rnn_forward, stacked_rnn_backward)
 
 __all__ = ["bf16_round", "sigmoid", "lstm_forward_literal", "lstm_forward",
            "lstm_backward", "stacked_forward", "stacked_backward",
-           "matmul_chain_grad"]
+           "matmul_chain_grad", "rnn_forward_literal", "rnn_forward", "rnn_backward",
+           "stacked_rnn_forward", "stacked_rnn_backward"]
