@@ -43,15 +43,15 @@ def parse():
 
 def stage_flops(w, sum_len):
     """Algorithmic flops per launch of each stage (per layer)."""
-    H = w.H
+    H, G2 = w.H, 2.0 * w.gates     # 2 flops per multiply-add, G gate blocks
     out = {}
     for l in range(w.layers):
         I = w.I if l == 0 else w.H
-        out.setdefault("fwd_loop", []).append(8.0 * H * H * sum_len)
-        out.setdefault("bwd_loop", []).append(8.0 * H * H * sum_len)
-        out.setdefault("input_proj", []).append(8.0 * H * I * sum_len)
-        out.setdefault("dw", []).append(8.0 * H * (I + H) * sum_len)
-        out.setdefault("dx", []).append(8.0 * H * I * sum_len)
+        out.setdefault("fwd_loop", []).append(G2 * H * H * sum_len)
+        out.setdefault("bwd_loop", []).append(G2 * H * H * sum_len)
+        out.setdefault("input_proj", []).append(G2 * H * I * sum_len)
+        out.setdefault("dw", []).append(G2 * H * (I + H) * sum_len)
+        out.setdefault("dx", []).append(G2 * H * I * sum_len)
     return {k: float(np.mean(v)) for k, v in out.items()}
 
 
@@ -75,10 +75,15 @@ def cpu_baseline(w, inp, target_s):
         Ws = [a.astype(np.float64) for a in inp["W"]]
         bs = [a.astype(np.float64) for a in inp["bias"]]
         t0 = time.perf_counter()
-        y, hT, cT, tapes = oracle.stacked_forward(x, sl, Ws, bs, inp["h0"].astype(np.float64),
-                                                  inp["c0"].astype(np.float64), precision)
-        oracle.stacked_backward(tapes, dy, inp["dhT"].astype(np.float64),
-                                inp["dcT"].astype(np.float64))
+        if w.cell == "rnn":
+            _, _, tapes = oracle.stacked_rnn_forward(x, sl, Ws, bs, inp["h0"].astype(np.float64),
+                                                     precision)
+            oracle.stacked_rnn_backward(tapes, dy, inp["dhT"].astype(np.float64))
+        else:
+            y, hT, cT, tapes = oracle.stacked_forward(x, sl, Ws, bs, inp["h0"].astype(np.float64),
+                                                      inp["c0"].astype(np.float64), precision)
+            oracle.stacked_backward(tapes, dy, inp["dhT"].astype(np.float64),
+                                    inp["dcT"].astype(np.float64))
         return time.perf_counter() - t0, int(sl.sum())
 
     T_eff = int(inp["seq_len"].max())
@@ -164,7 +169,7 @@ def main():
     inp = wl.generate(w)
     sum_len = int(inp["seq_len"].sum())
     T_eff = int(inp["seq_len"].max())
-    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, device="cuda:0")
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, device="cuda:0", cell=w.cell)
     plan_kw = {}
     if w.spill:   # stack swapped to pinned host memory through a ring of 4 chunks of 32 steps
         C = 32
@@ -235,7 +240,7 @@ def main():
     measured_16 = lstmloop.ll_measure_mfma_peak(w.dtype, 16)
     # what a loop over T_eff (or T_max) padded steps would execute: every
     # sequence runs every step (a static unroll to the longest sequence)
-    padded = {f"T_{n}": sum(24.0 * w.H * ((w.I if l == 0 else w.H) + w.H) * w.B * T
+    padded = {f"T_{n}": sum(6.0 * w.gates * w.H * ((w.I if l == 0 else w.H) + w.H) * w.B * T
                             for l in range(w.layers)) for n, T in (("eff", T_eff), ("max", w.T_max))}
     q = np.percentile(per_step, [5, 50, 95])
     out = {
@@ -252,7 +257,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "I": w.I, "H": w.H, "T_max": w.T_max,
-                   "layers": w.layers, "seq_len": f"U{{{w.len_lo}..{w.len_hi}}}",
+                   "layers": w.layers, "cell": w.cell, "seq_len": f"U{{{w.len_lo}..{w.len_hi}}}",
                    "sum_len": sum_len, "T_eff": T_eff, "loop_workgroups": geom["workgroups"],
                    "units_per_workgroup": geom["units_per_workgroup"]},
         "mfma_util": mfma_util,

@@ -12,7 +12,9 @@
  *   gate, gate column blocks i, f, g, o):
  *       z = [x_t, h_{t-1}] W + b;  i,f,o = sigmoid;  g = tanh
  *       c_t = f*c_{t-1} + i*g;     h_t = o*tanh(c_t)
- *   Rows with t >= seq_len[b] keep their state and output y = 0.
+ *   Rows with t >= seq_len[b] keep their state and output y = 0.  The
+ *   body can instead be the Elman recurrence h_t = tanh([x_t, h_{t-1}] W + b)
+ *   (desc.cell = LL_CELL_RNN, below).
  *   Each iteration pushes what the gradient needs onto a stack (Section 5.1);
  *   the gradient loop runs the same number of iterations in reverse, pops
  *   the stack, carries dh/dc as loop variables and sums the gradients of the
@@ -30,7 +32,8 @@
  *   - W of layer l is [I_l + H, 4H]: rows 0..I_l-1 multiply x_t, rows
  *     I_l..I_l+H-1 multiply h_{t-1}; column blocks are gates i, f, g, o.
  *     I_0 = I, I_1 = H.  Its element type is desc.dtype (float or bfloat16
- *     bits); bias is always float [4H].
+ *     bits); bias is always float [4H].  (LL_CELL_RNN: 4H reads H here and
+ *     below: W [I_l + H, H], bias, dW and dbias [.., H].)
  *   - State, stack and accumulation are float32.  In LL_BF16 mode the
  *     matrix-core operands are bfloat16 (round to nearest even): x, W,
  *     h_{t-1} in the forward; dz, [x_t, h_{t-1}] and W in the backward.
@@ -65,6 +68,15 @@ typedef enum {
 } ll_status;
 
 typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
+
+/* Loop body (cell).  LL_CELL_LSTM: gates i, f, g, o (W [I_l + H, 4H], bias
+ * [4H]), state (h, c).  LL_CELL_RNN: the Elman recurrence h_t = tanh(x_t W_x
+ * + h_{t-1} W_h + b) (W [I_l + H, H], bias [H]), state h; c0, cT, dcT and dc0
+ * are ignored (cT and dc0, if given, are written as zeros).  The loop
+ * construct, masking, stack and gradient loop are the same for both: the
+ * paper's while-loop and its gradient (Sections 3 and 5) do not depend on
+ * the body. */
+typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1 } ll_cell;
 
 /* Device error word bits (ll_status_sync). */
 #define LL_DEVERR_SEQ_LEN 1      /* some seq_len[b] < 0 or > T_max          */
@@ -106,7 +118,8 @@ typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
  *     XCD-local loops and spill = 0 (else LL_EUNSUPPORTED); the two layers
  *     then run one after the other.  The bias passed to lstm_loop_fwd is
  *     copied into the plan for the gradient pass.
- *   reserved must be 0.
+ *   cell: an ll_cell.  LL_CELL_RNN needs the XCD-local loops, spill = 0
+ *     and recompute = 0 (else LL_EUNSUPPORTED); its stack holds h_t only.
  */
 typedef struct {
   int32_t T_max;
@@ -119,7 +132,7 @@ typedef struct {
   int32_t spill_chunk_steps;
   int64_t device_stack_budget_bytes;
   int32_t recompute;
-  int32_t reserved;
+  int32_t cell;
 } ll_desc;
 
 typedef struct ll_plan ll_plan;   /* opaque: owns the stack, scratch arrays,

@@ -248,8 +248,9 @@ struct XKernels {
   size_t lds_bwd;
 };
 
+// gates: 4 (LSTM) or 1 (Elman RNN)
 template <typename T>
-XKernels x_kernels(int hc, int mrt);
+XKernels x_kernels(int hc, int mrt, int gates = 4);
 hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd);
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s);
 // Two-layer wavefront: one launch runs both layers (a0 lower, a1 upper);

@@ -70,6 +70,7 @@ struct ll_plan {
   int device = 0;
   int es = 4;            // operand element bytes
   bool bf16 = false;
+  int G = 4;             // gate blocks of the cell: 4 (LSTM), 1 (Elman RNN)
   long cap = 0;          // compact-row capacity = T_max * B
   long ldT = 0;          // leading dimension of transposed per-row arrays
   ll::LoopGeom geom{};
@@ -293,7 +294,10 @@ ll_status validate_desc(const ll_desc* d) {
   if (d->recompute != 0 && d->recompute != 1) return fail(LL_EINVAL, "recompute must be 0 or 1");
   if (d->recompute && d->spill)
     return fail(LL_EUNSUPPORTED, "recompute and spill are alternatives; choose one");
-  if (d->reserved != 0) return fail(LL_EINVAL, "reserved must be 0");
+  if (d->cell != LL_CELL_LSTM && d->cell != LL_CELL_RNN)
+    return fail(LL_EINVAL, "cell must be LL_CELL_LSTM or LL_CELL_RNN (got %d)", d->cell);
+  if (d->cell == LL_CELL_RNN && (d->spill || d->recompute))
+    return fail(LL_EUNSUPPORTED, "spill and recompute are built for the LSTM cell only");
   if ((long)d->T_max * d->B > (1L << 30))
     return fail(LL_EUNSUPPORTED, "T_max * B = %ld exceeds 2^30 rows", (long)d->T_max * d->B);
   if (d->H % 32) return fail(LL_EUNSUPPORTED, "H = %d must be a multiple of 32", d->H);
@@ -349,6 +353,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   p->device = device;
   p->bf16 = desc->dtype == LL_BF16;
   p->es = p->bf16 ? 2 : 4;
+  p->G = desc->cell == LL_CELL_RNN ? 1 : 4;
   p->n_cu = prop.multiProcessorCount;
   p->cap = (long)desc->T_max * desc->B;
   p->ldT = round_up(p->cap, 64);
@@ -404,7 +409,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
       const int hc = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 0;
       const int mrt = ((B + 15) / 16 + 7) / 8;
       if (hc && mrt <= 16) {
-        ll::XKernels xk = p->bf16 ? ll::x_kernels<bf16_t>(hc, mrt) : ll::x_kernels<float>(hc, mrt);
+        ll::XKernels xk = p->bf16 ? ll::x_kernels<bf16_t>(hc, mrt, p->G) : ll::x_kernels<float>(hc, mrt, p->G);
         if (xk.fwd && xk.bwd && xk.lds_fwd <= lds_limit && xk.lds_bwd <= lds_limit) {
           int of = 0, ob = 0;
           if (ll::x_setup(xk, &of, &ob) == hipSuccess && of >= 1 && ob >= 1) {
@@ -419,6 +424,13 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
         }
       }
     }
+  }
+
+  // The Elman RNN cell runs on the XCD-local loops only.
+  if (p->G != 4 && !p->xmode) {
+    delete p;
+    return fail(LL_EUNSUPPORTED, "the RNN cell needs the XCD-local loops (H = %d, B = %d do not fit them)",
+                H, B);
   }
 
   // Chip-wide loops where one XCD cannot hold the recurrent weights (bf16
@@ -470,7 +482,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   // and P..2P-1 the upper one, so both layers' steps overlap in one launch.
   // LSTMLOOP_WAVEFRONT=off at plan creation runs the layers one after the
   // other.
-  if (L == 2 && p->xmode && !p->spill && !p->recompute && 2 * p->xP <= 32 && p->xhc <= 2) {
+  if (L == 2 && p->G == 4 && p->xmode && !p->spill && !p->recompute && 2 * p->xP <= 32 && p->xhc <= 2) {
     const char* wf = getenv("LSTMLOOP_WAVEFRONT");
     if (!(wf && strcmp(wf, "off") == 0)) {
       ll::XKernels xk2 = p->bf16 ? ll::x_kernels2<bf16_t>(p->xhc, p->xMRT)
@@ -494,13 +506,13 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     ll::GemmArgs g{};
     g.lda = g.ldb = p->ldT;
     g.M = M;
-    g.N = 4 * H;
+    g.N = p->G * H;
     g.K = (int)p->cap;
     g.splits = 1;
     g.k_zero_tail = 1;
     const bool big = ll::gemm_big_applies(g, (int)p->es);
     const long tile = big ? ll::kGemmBigTile : 128;
-    const long tiles = (long)((M + tile - 1) / tile) * ((4 * H + tile - 1) / tile);
+    const long tiles = (long)((M + tile - 1) / tile) * ((p->G * H + tile - 1) / tile);
     const long want = big ? p->n_cu : 2L * p->n_cu;
     long s = (want + tiles - 1) / tiles;
     s = std::max(1L, std::min(16L, s));
@@ -511,7 +523,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   p->ws_floats = 0;
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
-    if (p->dw_splits[l] > 1) p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[l] * (Il + H) * 4 * H);
+    if (p->dw_splits[l] > 1) p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[l] * (Il + H) * p->G * H);
   }
 
   const size_t es = p->es;
@@ -533,21 +545,21 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->rowmap, sizeof(int) * cap, "rowmap");
   ALLOC(p->meta, sizeof(int) * ll::META_INTS, "meta");
   for (int l = 0; l < L; ++l) {
-    ALLOC(p->WT[l], es * 4 * H * (in_width(p, l) + H), "transposed W");
+    ALLOC(p->WT[l], es * p->G * H * (in_width(p, l) + H), "transposed W");
     ALLOC(p->stack[l],
-          sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * (p->recompute ? 1 : 5) * H),
+          sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * (p->recompute || p->G == 1 ? 1 : 5) * H),
           "stack");
     // (recompute: B more rows hold h0 in the operand type, the h_{t-1} of step 0)
     ALLOC(p->HH[l], es * (cap + (p->recompute ? B : 0)) * H, "h history");
   }
-  ALLOC(p->Zx, sizeof(float) * cap * 4 * H, "input projection");
-  ALLOC(p->DZ, es * cap * 4 * H, "dz");
-  ALLOC(p->DZT, es * 4 * H * p->ldT, "dz transposed");
+  ALLOC(p->Zx, sizeof(float) * cap * p->G * H, "input projection");
+  ALLOC(p->DZ, es * cap * p->G * H, "dz");
+  ALLOC(p->DZT, es * p->G * H * p->ldT, "dz transposed");
   ALLOC(p->XT, es * (maxI + H) * p->ldT, "x and h_prev transposed");
   if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
   if (p->xmode) {
-    // two slots x 8 XCDs x row tiles x (4H / k-step) blocks of 1 KB
-    const long ks_b = 4L * H * (long)es / 64;
+    // two slots x 8 XCDs x row tiles x (G H / k-step) blocks of 1 KB
+    const long ks_b = (long)p->G * H * (long)es / 64;
     ALLOC(p->xring, 2L * 8 * p->xMRT * ks_b * 1024, "exchange ring");
     p->xflag_words = 8 + (p->wave ? 3 : 1) * 8 * p->xMRT * 32;
     ALLOC(p->xflags, sizeof(unsigned) * p->xflag_words, "exchange flags");
@@ -575,7 +587,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     ALLOC(p->carry, sizeof(float) * 4 * B * H, "chunk carry");
     ALLOC(p->db_state, sizeof(float) * 8 * 32 * 512 * 4, "db state");
   }
-  ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * 4 * H, "db partials");
+  ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * p->G * H, "db partials");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
 #undef ALLOC
   if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess) {
@@ -616,7 +628,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     }
   }
   const int64_t stack_dev = p->spill ? (int64_t)sizeof(float) * p->nslots * p->slot_floats
-                                     : (int64_t)sizeof(float) * cap * (p->recompute ? 1 : 5) * H;
+                                     : (int64_t)sizeof(float) * cap * (p->recompute || p->G == 1 ? 1 : 5) * H;
   p->stack_device_bytes = (int64_t)L * (stack_dev + (int64_t)es * (cap + (p->recompute ? B : 0)) * H);
   if (p->recompute) p->stack_device_bytes += (int64_t)sizeof(float) * p->rc_steps * B * 4 * H;
   p->stack_host_bytes =
@@ -727,9 +739,10 @@ ll::XLoopArgs x_common(const ll_plan* p) {
   a.t_end = p->d.T_max;
   a.chunk_steps = p->d.T_max;
   a.nslots = 1;
-  a.sld = 5 * p->d.H;
-  a.scoff = 4 * p->d.H;
-  a.sgates = 1;
+  // stack rows: LSTM i, f, g, o, c_t (5H); the RNN pushes h_t only
+  a.sld = p->G == 4 ? 5 * p->d.H : p->d.H;
+  a.scoff = p->G == 4 ? 4 * p->d.H : 0;
+  a.sgates = p->G == 4 ? 1 : 0;
   return a;
 }
 
@@ -831,7 +844,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     const int Il = in_width(p, l);
     ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
     // W^T: row n = gate column n, K-contiguous operand of both products
-    LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, 4 * H, 4 * H,
+    LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, p->G * H, p->G * H,
                                    reinterpret_cast<T*>(p->WT[l]), Il + H, s));
     // Zx = x_t W_x + b for every compact row (layer 0 gathers time-major x)
     ll::GemmArgs g{};
@@ -841,11 +854,11 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     g.Bm = p->WT[l];
     g.ldb = Il + H;
     g.C = p->Zx;
-    g.ldc = 4L * H;
+    g.ldc = (long)p->G * H;
     g.bias = bias[l];
     g.M = (int)p->cap;
     g.M_dev = p->meta + 1;
-    g.N = 4 * H;
+    g.N = p->G * H;
     g.K = Il;
     g.splits = 1;
     LL_HIP(ll::launch_gemm_nt<T>(g, s));
@@ -885,9 +898,10 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       xa.err = p->meta + 2;
       xa.limit = p->barrier_ticks;
       const float* hin = h0 ? h0 + (long)l * B * H : nullptr;
-      const float* cin = c0 ? c0 + (long)l * B * H : nullptr;
+      // (the RNN has no cell state: c0 is ignored, cT written as zeros if given)
+      const float* cin = c0 && p->G == 4 ? c0 + (long)l * B * H : nullptr;
       float* hout = hT + (long)l * B * H;
-      float* cout = cT + (long)l * B * H;
+      float* cout = cT ? cT + (long)l * B * H : nullptr;
       // one launch per chunk of steps when the stack spills, else one launch
       const int C = p->spill ? p->chunk_steps : d.T_max;
       const int nch = p->spill ? p->nchunks : 1;
@@ -999,14 +1013,15 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   // larger one runs after them on the call's stream (measured: two large
   // products side by side only slow each other).
   ll::GemmArgs gx{};
+  const int GH = p->G * H;
   gx.A = dz;
-  gx.lda = 4L * H;
+  gx.lda = GH;
   gx.Bm = p->W[l];
-  gx.ldb = 4L * H;
+  gx.ldb = GH;
   gx.M = (int)p->cap;
   gx.M_dev = p->meta + 1;
   gx.N = Il;
-  gx.K = 4 * H;
+  gx.K = GH;
   gx.splits = 1;
   gx.C = dx;
   if (l == 0) {
@@ -1032,7 +1047,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   }
   // db = sum of the row-group partials
   ev = tbeg(p, s, LL_STAGE_DW);
-  LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, 4L * H, 4L * H, dbias[l], s));
+  LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, GH, GH, dbias[l], s));
   tend(p, s, LL_STAGE_DW, ev);
   ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
   // transposed operands of the dW products (reduction over compact rows)
@@ -1045,7 +1060,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   gt.ldo = (int)p->ldT;
   gt.in = dz;
   gt.out = p->DZT;
-  gt.C = 4 * H;
+  gt.C = GH;
   gt.mode = 1;
   LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
   gt.in = l == 0 ? p->x : p->HH[0];
@@ -1070,20 +1085,20 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
     g.Bm = p->DZT;
     g.ldb = p->ldT;
     g.M = M;
-    g.N = 4 * H;
+    g.N = GH;
     g.K = (int)p->cap;
     g.K_dev = p->meta + 1;
     g.k_zero_tail = 1;   // the transposes write zeros past the last row, up to a multiple of 64
     g.splits = p->dw_splits[l];
     if (g.splits > 1) {
       g.C = p->ws;
-      g.ldc = 4L * H;
-      g.split_stride = (long)M * 4 * H;
+      g.ldc = GH;
+      g.split_stride = (long)M * GH;
       LL_HIP(ll::launch_gemm_nt<T>(g, s));
       LL_HIP(ll::launch_sum_slices(p->ws, g.splits, g.split_stride, g.split_stride, dW[l], s));
     } else {
       g.C = dW[l];
-      g.ldc = 4L * H;
+      g.ldc = GH;
       LL_HIP(ll::launch_gemm_nt<T>(g, s));
     }
   }
@@ -1240,7 +1255,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     if (p->xmode) {
       ll::XLoopArgs xa = x_common(p);
       xa.ring = p->xring;
-      xa.ring_ks = (int)(4L * H * p->es / 64);
+      xa.ring_ks = (int)((long)p->G * H * p->es / 64);
       xa.rank_ctr = p->xflags;
       xa.flags = p->xflags + 8;
       xa.B = B;
@@ -1255,7 +1270,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       xa.W = p->W[l];
       xa.woff = Il;
       xa.X = p->DZ;
-      xa.c0 = p->c0 ? p->c0 + (long)l * B * H : nullptr;
+      xa.c0 = p->c0 && p->G == 4 ? p->c0 + (long)l * B * H : nullptr;
       xa.stack = p->stack[l];
       if (l == L - 1) {
         xa.dy = dy;
@@ -1269,7 +1284,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       xa.err = p->meta + 2;
       xa.limit = p->barrier_ticks;
       const float* dhin = dhT ? dhT + (long)l * B * H : nullptr;
-      const float* dcin = dcT ? dcT + (long)l * B * H : nullptr;
+      const float* dcin = dcT && p->G == 4 ? dcT + (long)l * B * H : nullptr;
       float* dhout = dh0 ? dh0 + (long)l * B * H : nullptr;
       float* dcout = dc0 ? dc0 + (long)l * B * H : nullptr;
       const int C = p->spill ? p->chunk_steps : p->recompute ? p->rc_steps : d.T_max;
@@ -1398,8 +1413,8 @@ ll_status lstm_loop_fwd(ll_plan* p, void* stream, const void* x, const int32_t* 
                         const float* c0, float* y, float* hT, float* cT, int32_t* trip_count,
                         int32_t save_for_backward) {
   if (!p) return fail(LL_EINVAL, "plan is NULL");
-  if (!x || !seq_len || !W || !bias || !hT || !cT)
-    return fail(LL_EINVAL, "x, seq_len, W, bias, hT and cT are required");
+  if (!x || !seq_len || !W || !bias || !hT || (!cT && p->G == 4))
+    return fail(LL_EINVAL, "x, seq_len, W, bias, hT and (LSTM) cT are required");
   for (int l = 0; l < p->d.layers; ++l)
     if (!W[l] || !bias[l]) return fail(LL_EINVAL, "W[%d] or bias[%d] is NULL", l, l);
   DeviceGuard guard(p->device);

@@ -118,10 +118,11 @@ __device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp
 // lower layer's ring for step t (bf16(y1_t) in the bf16 contract: the ring
 // holds the operand-type h_t), the rest h_{t-1} from its own ring; the bias
 // replaces the hoisted input projection.
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP>
+// G: gate blocks of the cell (4: LSTM i, f, g, o; 1: Elman RNN, h = tanh(z)).
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP, int G = 4>
 __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
-  constexpr int HJ = 4 * NCT;
+  constexpr int HJ = 16 * NCT / G;
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
   constexpr int IS = xfwd_is(NCT);
   static_assert(16 * HJ <= XNT, "one cell thread per (row, unit) of a tile");
@@ -129,7 +130,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
   const int H = a.H, B = a.B;
-  const long G4 = 4L * H;
+  const long G4 = (long)G * H;                           // gate columns
   const int j0 = rank * HJ;
   const int KX = TOP ? a.in_ks : 0;                      // k-steps from the lower layer
   const int KS = KX + H / (4 * KPC);
@@ -194,19 +195,19 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   load_window(a, win, wlo);
   // input projections of the cell thread's (row, unit), one step ahead (the
   // upper wavefront layer: its bias)
-  float zf[MRT_MAX][4];
+  float zf[MRT_MAX][G];
   if constexpr (TOP) {
 #pragma unroll
     for (int mt = 0; mt < MRT_MAX; ++mt)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) zf[mt][g] = cellt ? a.zbias[(long)g * H + ju] : 0.f;
+      for (int g = 0; g < G; ++g) zf[mt][g] = cellt ? a.zbias[(long)g * H + ju] : 0.f;
   } else {
     const int A0 = t0 < t1 ? win[t0 - wlo] : 0, off0 = win[WIN + 1 + t0 - wlo];
 #pragma unroll
     for (int mt = 0; mt < MRT_MAX; ++mt) {
       const int r = (grp + 8 * mt) * 16 + crow;
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
+      for (int g = 0; g < G; ++g)
         zf[mt][g] = (cellt && mt < a.MRT && r < A0) ? a.Zx[(long)(off0 + r) * G4 + (long)g * H + ju] : 0.f;
     }
   }
@@ -251,22 +252,23 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         av[i] = ks < KX ? ld_chunk_l2(rsx, i < nks ? (unsigned)((ks << 10) + lane * 16) : kOOB)
                         : ld_chunk_l2(rs, i < nks ? (unsigned)(((ks - KX) << 10) + lane * 16) : kOOB);
       }
-      float zc[4];
+      float zc[G];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) zc[g] = zf[mt][g];
+      for (int g = 0; g < G; ++g) zc[g] = zf[mt][g];
       if constexpr (!TOP) {  // input projections of step t+1 (rows past A_n read zeros)
         const int nr = max(0, min(16, A_n - r0));
         const __amdgpu_buffer_rsrc_t rz = make_rsrc(a.Zx + (long)(off_n + r0) * G4, (unsigned)(nr * G4 * 4));
         const unsigned zo = cellt ? (unsigned)((crow * G4 + ju) * 4) : kOOB;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) zf[mt][g] = ld_f32(rz, zo + g * H * 4);
+        for (int g = 0; g < G; ++g) zf[mt][g] = ld_f32(rz, zo + g * H * 4);
       }
       // 2. partial products over this wave's k-steps, column tiles in two
       //    halves, into red[wave][i][ct][lane] (the previous tile's cell has
       //    read them: it ended at a barrier)
+      constexpr int NHALF = NCT >= 2 ? 2 : 1;
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        constexpr int NH = NCT / 2;
+      for (int hf = 0; hf < NHALF; ++hf) {
+        constexpr int NH = NCT / NHALF;
         f32x4 acc[NH];
 #pragma unroll
         for (int c = 0; c < NH; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -297,21 +299,25 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       const int r = r0 + crow;
       const bool act = cellt && r < A_t;
       if (cellt) {
-        float z[4];
+        float z[G];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int g = 0; g < G; ++g) {
           const float* p = rp + g * (HJ / 16) * 64;
           float v = p[0];
 #pragma unroll
           for (int w2 = 1; w2 < XNW; ++w2) v += p[w2 * 4 * IS];
           z[g] = v + zc[g];
         }
-        ig = sigmoidf_(z[0]);
-        fg = sigmoidf_(z[1]);
-        gg = tanhf_(z[2]);
-        og = sigmoidf_(z[3]);
-        cn = fg * cs[mt] + ig * gg;
-        hn = og * tanhf_(cn);
+        if constexpr (G == 4) {
+          ig = sigmoidf_(z[0]);
+          fg = sigmoidf_(z[1]);
+          gg = tanhf_(z[2]);
+          og = sigmoidf_(z[3]);
+          cn = fg * cs[mt] + ig * gg;
+          hn = og * tanhf_(cn);
+        } else {
+          hn = tanhf_(z[0]);
+        }
         if (act) {
           *reinterpret_cast<T*>(ring_tile(a, t & 1, grp, mt) + (rank << 10) + rbo) = Op<T>::from_f32(hn);
           cs[mt] = cn;
@@ -323,15 +329,19 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         const long cr = off_t + r;
         HH[cr * H + ju] = Op<T>::from_f32(hn);
         if (a.stack) {
-          // (c only: the gate stores all land on the c field, which the last
-          // store overwrites; no branch on the common path)
           float* st = a.stack + stack_row(a, t, r) * a.sld + ju;
-          const int gs = a.sgates ? H : 0;
-          st[0] = ig;
-          st[gs] = fg;
-          st[2 * gs] = gg;
-          st[3 * gs] = og;
-          st[a.scoff] = cn;
+          if constexpr (G == 4) {
+            // (c only: the gate stores all land on the c field, which the last
+            // store overwrites; no branch on the common path)
+            const int gs = a.sgates ? H : 0;
+            st[0] = ig;
+            st[gs] = fg;
+            st[2 * gs] = gg;
+            st[3 * gs] = og;
+            st[a.scoff] = cn;
+          } else {
+            st[a.scoff] = hn;   // the RNN's gradient needs only h_t
+          }
         }
       }
       if (a.y && cellt) {
@@ -347,14 +357,14 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       const int b = sperm[mt * 16 + crow];
       if (b < 0) continue;
       a.hT[(long)b * H + ju] = hs[mt];
-      a.cT[(long)b * H + ju] = cs[mt];
+      if (a.cT) a.cT[(long)b * H + ju] = cs[mt];
       if (a.y)
         for (int t = max(T_eff, t0); t < a.t_end; ++t) a.y[((long)t * B + b) * H + ju] = 0.f;
     }
   }
 }
 
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int G>
 __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
@@ -368,7 +378,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  xfwd_body<T, NCT, KSW, KSR, MRT_MAX, false>(a, grp, rank, lds);
+  xfwd_body<T, NCT, KSW, KSR, MRT_MAX, false, G>(a, grp, rank, lds);
 }
 
 // Two-layer wavefront, forward: members 0 .. P-1 of every XCD run the lower
@@ -411,7 +421,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd2_kernel(XLoopArgs a0, XLoopArgs a
 // (its dy comes from the upper layer's dyx ring, one step later); 2: the upper
 // layer, which also computes dy_{lower} = dz W_x^T for its units (NCO = 2 NCT
 // output column tiles: W_h rows, then W_x rows) and publishes it per step.
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE, bool DMA = false>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE, bool DMA = false, int G = 4>
 __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT;                 // units per work-group
@@ -424,9 +434,12 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
   const int H = a.H, B = a.B, P = a.P;
-  const long G4 = 4L * H;
+  const long G4 = (long)G * H;                          // gate columns (dz row width)
   const int j0 = rank * HJ;
   const int KS = (int)(G4 / (4 * KPC));
+  // pops per (step, tile) and thread: LSTM i, f, g, o, c_t, c_{t-1}, dy;
+  // RNN h_t, dy
+  constexpr int NPOP = G == 4 ? 7 : 2;
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
   const int nks = ks1 - ks0;                            // k-steps of this wave
   const T* W = reinterpret_cast<const T*>(a.W);
@@ -478,11 +491,13 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       if (a.dcT) dc[mt] = a.dcT[(long)b * H + ju];
     }
   }
-  float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
+  float dbacc[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) dbacc[g] = 0.f;
   float* dbst = a.db_state ? a.db_state + ((long)(grp * 32 + rank) * XNT + tid) * 4 : nullptr;
   if (dbst && a.db_resume) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) dbacc[g] = dbst[g];
+    for (int g = 0; g < G; ++g) dbacc[g] = dbst[g];
   }
 
   // pops of (step tt, tile mt) for this thread: i, f, g, o, c_t, c_{t-1}, dy;
@@ -494,14 +509,19 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
     const int b = sperm[mt * 16 + crow];
     const int ts = max(tt, 0);
     const long SL = a.sld, GL = a.gstk ? a.gld : a.sld;
+    const unsigned so = ok ? (unsigned)((crow * SL + ju) * 4) : kOOB;
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc(a.stack + stack_row(a, ts, r0) * SL + a.scoff, (unsigned)(nr * SL * 4));
+    if constexpr (G == 1) {   // RNN: h_t and dy
+      v[0] = ld_f32(rs, so);
+      v[1] = v[2] = v[3] = v[4] = v[5] = 0.f;
+      (void)b;
+    } else {
     const float* gbase = a.gstk ? a.gstk : a.stack;
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(gbase + gate_row(a, ts, r0) * GL, (unsigned)(nr * GL * 4));
     const unsigned go = ok ? (unsigned)((crow * GL + ju) * 4) : kOOB;
 #pragma unroll
     for (int c = 0; c < 4; ++c) v[c] = ld_f32(rg, go + c * H * 4);
-    const unsigned so = ok ? (unsigned)((crow * SL + ju) * 4) : kOOB;
-    const __amdgpu_buffer_rsrc_t rs =
-        make_rsrc(a.stack + stack_row(a, ts, r0) * SL + a.scoff, (unsigned)(nr * SL * 4));
     v[4] = ld_f32(rs, so);
     if (tt > 0) {
       const __amdgpu_buffer_rsrc_t rp2 =
@@ -510,6 +530,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
     } else {
       const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.c0, a.c0 ? (unsigned)(B * H * 4) : 0u);
       v[5] = ld_f32(rc, ok ? (unsigned)((b * H + ju) * 4) : kOOB);
+    }
     }
     if (a.dy_compact) {
       const __amdgpu_buffer_rsrc_t rd = make_rsrc(a.dy + (long)(off + r0) * H, (unsigned)(nr * H * 4));
@@ -570,28 +591,35 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
         dyl = ld_f32_l2(ry, act ? (unsigned)((crow * H + ju) * 4) : kOOB);
       }
       // phase 1
-      float dz[4] = {0.f, 0.f, 0.f, 0.f};
+      float dz[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) dz[g] = 0.f;
       if (act) {
         const float dht = dh[mt] + pv[mt][6] + dyl;
-        const float ig = pv[mt][0], fg = pv[mt][1], gg = pv[mt][2], og = pv[mt][3];
-        const float c = pv[mt][4], cp = pv[mt][5];
-        const float tc = tanhf_(c);
-        const float d_o = dht * tc;
-        const float dct = dc[mt] + dht * og * (1.f - tc * tc);
-        dz[0] = dct * gg * (ig * (1.f - ig));
-        dz[1] = dct * cp * (fg * (1.f - fg));
-        dz[2] = dct * ig * (1.f - gg * gg);
-        dz[3] = d_o * (og * (1.f - og));
-        dc[mt] = dct * fg;
+        if constexpr (G == 4) {
+          const float ig = pv[mt][0], fg = pv[mt][1], gg = pv[mt][2], og = pv[mt][3];
+          const float c = pv[mt][4], cp = pv[mt][5];
+          const float tc = tanhf_(c);
+          const float d_o = dht * tc;
+          const float dct = dc[mt] + dht * og * (1.f - tc * tc);
+          dz[0] = dct * gg * (ig * (1.f - ig));
+          dz[1] = dct * cp * (fg * (1.f - fg));
+          dz[2] = dct * ig * (1.f - gg * gg);
+          dz[3] = d_o * (og * (1.f - og));
+          dc[mt] = dct * fg;
+        } else {
+          const float hv = pv[mt][0];
+          dz[0] = dht * (1.f - hv * hv);
+        }
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < G; ++g)
           *reinterpret_cast<T*>(slot + ((g * P + rank) << 10) + rbo) = Op<T>::from_f32(dz[g]);
       }
       publish(flags + rank, (unsigned)(T_eff - t));
       if (act) {
         T* dzr = DZ + (long)(off_t + r0 + crow) * G4 + ju;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int g = 0; g < G; ++g) {
           dzr[(long)g * H] = Op<T>::from_f32(dz[g]);
           dbacc[g] += dz[g];
         }
@@ -604,7 +632,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       for (int ct = 0; ct < NCO; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
       if constexpr (DMA) {
         // every k-step of the wave in flight at once (no registers held):
-        // KSW loads into LDS, then the 7 pops of the next step behind them
+        // KSW loads into LDS, then the NPOP pops of the next step behind them
         asm volatile("" ::: "memory");
 #pragma unroll
         for (int i = 0; i < KSW; ++i)
@@ -618,7 +646,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       for (int b0 = 0; b0 < KSW; b0 += KB) {
         uint4 av[KB];
         if constexpr (DMA) {
-          wait_vm_n(7 + KSW - (b0 + KB < KSW ? b0 + KB : KSW));   // this batch has landed
+          wait_vm_n(NPOP + KSW - (b0 + KB < KSW ? b0 + KB : KSW));   // this batch has landed
 #pragma unroll
           for (int i = 0; i < KB; ++i) av[i] = b0 + i < KSW ? ds_rd(dza + (b0 + i) * 1024) : zero4();
           wait_lgkm<0>();
@@ -683,24 +711,24 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   }
   if (dbst) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) dbst[g] = dbacc[g];
+    for (int g = 0; g < G; ++g) dbst[g] = dbacc[g];
   }
   // db partial of this work-group (its rows of this XCD), fixed order
   __syncthreads();
   if (cellt) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) red[(crow * 4 + g) * HJ + cu] = dbacc[g];
+    for (int g = 0; g < G; ++g) red[(crow * G + g) * HJ + cu] = dbacc[g];
   }
   __syncthreads();
-  for (int c = tid; c < 4 * HJ; c += XNT) {
+  for (int c = tid; c < G * HJ; c += XNT) {
     float s = 0.f;
-    for (int m = 0; m < 16; ++m) s += red[m * 4 * HJ + c];
+    for (int m = 0; m < 16; ++m) s += red[m * G * HJ + c];
     const int g = c / HJ, u = c - (c / HJ) * HJ;
     a.db_part[(long)grp * G4 + (long)g * H + j0 + u] = s;
   }
 }
 
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool DMA>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool DMA, int G>
 __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
@@ -714,7 +742,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, DMA>(a, grp, rank, lds);
+  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, DMA, G>(a, grp, rank, lds);
 }
 
 // Two-layer wavefront, gradient: members 0 .. P-1 of every XCD run the lower
@@ -805,19 +833,19 @@ hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s) {
 // hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
 // row tiles per XCD.
 namespace {
-template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT>
+template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT, int G = 4>
 XKernels x_make() {
   XKernels k{};
-  k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT>);
+  k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT, G>);
   k.lds_fwd = xfwd_lds(HC, RF, NF, MRT);
   // the gradient loop loads its dz k-steps straight into LDS when they fit
-  const size_t dma_lds = xbwd_lds(4 * HC, RB, NB, MRT, true);
+  const size_t dma_lds = xbwd_lds(G * HC, RB, NB, MRT, true);
   if (dma_lds <= 160 * 1024) {
-    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, 4 * HC, RB, MRT, true>);
+    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, true, G>);
     k.lds_bwd = dma_lds;
   } else {
-    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, 4 * HC, RB, MRT, false>);
-    k.lds_bwd = xbwd_lds(4 * HC, RB, NB, MRT);
+    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, false, G>);
+    k.lds_bwd = xbwd_lds(G * HC, RB, NB, MRT);
   }
   return k;
 }
@@ -825,13 +853,28 @@ XKernels x_make() {
 
 // RF / RB: k-steps per wave whose weights stay in registers (the rest in LDS),
 // chosen so that no instantiation spills.
+//   bf16: HJ = 32 units, forward NCT 8, KSW = H/256; backward NCT 2, KSW = H/64.
+//   f32:  HJ = 16 units, forward NCT 4, KSW = H/128; backward NCT 1, KSW = H/32.
+// (LSTM; the Elman RNN has one gate block: forward NCT 2 / 1, backward KSW
+// = H/256 / H/128, every weight in registers.)
+// hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
 template <typename T>
-XKernels x_kernels(int hc, int mrt) {
+XKernels x_kernels(int hc, int mrt, int gates) {
   constexpr bool bf = sizeof(T) == 2;
   constexpr int NF = bf ? 8 : 4;
   constexpr int NB = bf ? 2 : 1;
   const bool one = mrt <= 1;
   if (mrt > 4) return XKernels{};
+  if (gates == 1) {
+    constexpr int NR = bf ? 2 : 1;
+    switch (hc) {
+      case 1: return one ? x_make<T, NR, NB, 1, 1, 1, 1, 1>() : x_make<T, NR, NB, 1, 1, 1, 4, 1>();
+      case 2: return one ? x_make<T, NR, NB, 2, 2, 2, 1, 1>() : x_make<T, NR, NB, 2, 2, 2, 4, 1>();
+      case 4: return one ? x_make<T, NR, NB, 4, 4, 4, 1, 1>() : x_make<T, NR, NB, 4, 4, 4, 4, 1>();
+      default: return XKernels{};
+    }
+  }
+  if (gates != 4) return XKernels{};
   switch (hc) {
     case 1: return one ? x_make<T, NF, NB, 1, 1, 4, 1>() : x_make<T, NF, NB, 1, 1, 4, 4>();
     case 2: return one ? x_make<T, NF, NB, 2, 2, 8, 1>() : x_make<T, NF, NB, 2, 2, 6, 4>();
@@ -840,8 +883,8 @@ XKernels x_kernels(int hc, int mrt) {
   }
 }
 
-template XKernels x_kernels<float>(int, int);
-template XKernels x_kernels<bf16_t>(int, int);
+template XKernels x_kernels<float>(int, int, int);
+template XKernels x_kernels<bf16_t>(int, int, int);
 
 // Two-layer wavefront kernels: the lower layer as in x_kernels, the upper one
 // with twice the forward k-steps (K = I_l + H = 2H) and, in the gradient, twice

@@ -18,6 +18,7 @@ LL_OK, LL_EINVAL, LL_ENOMEM, LL_EHIP, LL_ESTATE, LL_EUNSUPPORTED = range(6)
 LL_F32, LL_BF16 = 0, 1
 LL_DEVERR_SEQ_LEN, LL_DEVERR_BARRIER = 1, 2
 LL_LOOPS_GRID, LL_LOOPS_XCD, LL_LOOPS_CHIP = 0, 1, 2
+LL_CELL_LSTM, LL_CELL_RNN = 0, 1
 STATUS_NAMES = {0: "LL_OK", 1: "LL_EINVAL", 2: "LL_ENOMEM", 3: "LL_EHIP",
                 4: "LL_ESTATE", 5: "LL_EUNSUPPORTED"}
 
@@ -36,7 +37,7 @@ class ll_desc(ctypes.Structure):
                 ("layers", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("spill", ctypes.c_int32), ("spill_chunk_steps", ctypes.c_int32),
                 ("device_stack_budget_bytes", ctypes.c_int64),
-                ("recompute", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("recompute", ctypes.c_int32), ("cell", ctypes.c_int32)]
 
 
 class LoopError(RuntimeError):
@@ -140,12 +141,12 @@ class Plan:
     def __init__(self, T_max: int, B: int, I: int, H: int, layers: int = 1,
                  dtype: str = "f32", spill: int = 0, spill_chunk_steps: int = 0,
                  device_stack_budget_bytes: int = 0, device: int = 0, recompute: int = 0,
-                 reserved: int = 0):
+                 cell: int = 0):
         lib = load_library()
         self._lib = lib
         self.desc = ll_desc(T_max, B, I, H, layers,
                             LL_BF16 if dtype == "bf16" else LL_F32 if dtype == "f32" else int(dtype),
-                            spill, spill_chunk_steps, device_stack_budget_bytes, recompute, reserved)
+                            spill, spill_chunk_steps, device_stack_budget_bytes, recompute, cell)
         self.dtype = dtype
         self.device = device
         h = ctypes.c_void_p()

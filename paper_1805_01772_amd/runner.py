@@ -12,15 +12,16 @@ from typing import Optional
 import numpy as np
 import torch
 
-from .lstmloop import Plan
+from .lstmloop import LL_CELL_LSTM, LL_CELL_RNN, Plan
 
 
 class DeviceCase:
     def __init__(self, inputs: dict, H: int, I: int, layers: int, dtype: str,
-                 device: str = "cuda:0"):
+                 device: str = "cuda:0", cell: str = "lstm"):
         dev = torch.device(device)
         self.dev = dev
         self.dtype = dtype
+        self.cell = cell
         op = torch.bfloat16 if dtype == "bf16" else torch.float32
         f32 = torch.float32
         T, B, _ = inputs["x"].shape
@@ -51,7 +52,8 @@ class DeviceCase:
         self.dc0 = z(L, B, H)
 
     def plan(self, **kw) -> Plan:
-        return Plan(self.T, self.B, self.I, self.H, layers=self.L, dtype=self.dtype, **kw)
+        cell = LL_CELL_RNN if self.cell == "rnn" else LL_CELL_LSTM
+        return Plan(self.T, self.B, self.I, self.H, layers=self.L, dtype=self.dtype, cell=cell, **kw)
 
     def fwd(self, plan: Plan, save: bool = True, use_h0: bool = True) -> None:
         plan.fwd(self.x, self.seq_len, self.W, self.bias,

@@ -37,10 +37,15 @@ class Workload:
     random_state: bool = False        # h0, c0 ~ N(0, 0.5^2) instead of zeros
     spill: bool = False
     seed: int = 0
+    cell: str = "lstm"                # "lstm" (4 gate blocks) or "rnn" (Elman, 1 block)
     extra: dict = field(default_factory=dict)
 
     def with_(self, **kw) -> "Workload":
         return replace(self, **kw)
+
+    @property
+    def gates(self) -> int:
+        return 4 if self.cell == "lstm" else 1
 
 
 # The five workloads.  Seeds are 1000 + index.
@@ -57,7 +62,13 @@ TWO_LAYER = Workload("lstm2_b256_h2048_tmax128_varlen_bf16", B=256, I=2048, H=20
                      T_max=128, dtype="bf16", len_lo=64, len_hi=128, layers=2,
                      seed=1005)
 
-ALL = (TINY, FIXED_H512, VAR_H1024, LONG_SPILL, TWO_LAYER)
+# The same loop with the Elman RNN body (the loop engine is not tied to one
+# cell), at the H = 1024 variable-length shape.
+RNN_VAR_H1024 = Workload("rnn_b128_h1024_tmax200_varlen_bf16", B=128, I=1024, H=1024,
+                         T_max=200, dtype="bf16", len_lo=20, len_hi=200, cell="rnn",
+                         seed=1006)
+
+ALL = (TINY, FIXED_H512, VAR_H1024, LONG_SPILL, TWO_LAYER, RNN_VAR_H1024)
 BY_NAME = {w.name: w for w in ALL}
 
 
@@ -91,10 +102,11 @@ def generate(w: Workload, seed: Optional[int] = None, nan_padding: bool = False)
     x = rng.standard_normal((T, B, I), dtype=np.float32)
     s = w.w_scale if w.w_scale is not None else 1.0 / np.sqrt(H)
     Ws, biases = [], []
+    G = w.gates
     for l in range(w.layers):
         in_w = I if l == 0 else H
-        Ws.append(rng.uniform(-s, s, size=(in_w + H, 4 * H)).astype(np.float32))
-        biases.append(rng.uniform(-s, s, size=(4 * H,)).astype(np.float32))
+        Ws.append(rng.uniform(-s, s, size=(in_w + H, G * H)).astype(np.float32))
+        biases.append(rng.uniform(-s, s, size=(G * H,)).astype(np.float32))
     dy = rng.standard_normal((T, B, H), dtype=np.float32) if w.with_dy else None
     if w.random_state:
         h0 = (0.5 * rng.standard_normal((w.layers, B, H))).astype(np.float32)
@@ -116,11 +128,13 @@ def generate(w: Workload, seed: Optional[int] = None, nan_padding: bool = False)
 
 
 def algorithmic_flops(w: Workload, seq_len: np.ndarray) -> float:
-    """Forward + backward flops the method needs: 24*H*(I_l+H) per valid
-    (timestep, sequence) per layer; masked steps and padding excluded."""
+    """Forward + backward flops the method needs: 6*G*H*(I_l+H) per valid
+    (timestep, sequence) per layer (G = 4 gate blocks for the LSTM, 1 for
+    the RNN: one product forward, three backward); masked steps and padding
+    excluded."""
     n = float(np.asarray(seq_len, dtype=np.int64).sum())
     tot = 0.0
     for l in range(w.layers):
         in_w = w.I if l == 0 else w.H
-        tot += 24.0 * w.H * (in_w + w.H) * n
+        tot += 6.0 * w.gates * w.H * (in_w + w.H) * n
     return tot

@@ -55,7 +55,8 @@ def test_version_string():
     (dict(B=0), ll.LL_EINVAL),
     (dict(layers=3), ll.LL_EINVAL),
     (dict(dtype=7), ll.LL_EINVAL),
-    (dict(reserved=1), ll.LL_EINVAL),
+    (dict(cell=2), ll.LL_EINVAL),
+    (dict(cell=1, spill=1), ll.LL_EUNSUPPORTED),
     (dict(spill=2), ll.LL_EINVAL),
     (dict(recompute=2), ll.LL_EINVAL),
     (dict(recompute=1, spill=1), ll.LL_EUNSUPPORTED),
@@ -66,7 +67,7 @@ def test_version_string():
 def test_descriptor_validation(fields, status):
     lib = _lib()
     base = dict(T_max=8, B=4, I=32, H=32, layers=1, dtype=ll.LL_BF16, spill=0,
-                spill_chunk_steps=0, device_stack_budget_bytes=0, recompute=0, reserved=0)
+                spill_chunk_steps=0, device_stack_budget_bytes=0, recompute=0, cell=0)
     base.update(fields)
     d = ll.ll_desc(**base)
     h = ctypes.c_void_p(123)

@@ -534,3 +534,43 @@ def test_recompute_zero_trip():
     assert np.array_equal(got["hT"][0], inp["h0"][0]) and np.array_equal(got["cT"][0], inp["c0"][0])
     assert np.array_equal(got["dh0"][0], inp["dhT"][0]) and np.array_equal(got["dc0"][0], inp["dcT"][0])
     assert not np.any(got["dW"][0]) and not np.any(got["dx"])
+
+
+RNN_CASES = [
+    # (bf16 cases use the default U(+-1/sqrt(H)) weights: with larger ones the
+    # tanh recurrence is expanding, and bf16 rounding differences of one ulp
+    # in h grow step by step, the oracle's accumulation order being fp64)
+    W("rnn_f32_b20_i24_h64_t30", B=20, I=24, H=64, T_max=30, dtype="f32", len_lo=0, len_hi=30,
+      w_scale=0.3, random_state=True, cell="rnn", seed=41),
+    W("rnn_bf16_b40_i32_h128_t37", B=40, I=32, H=128, T_max=37, dtype="bf16", len_lo=1, len_hi=37,
+      random_state=True, cell="rnn", seed=42),
+    W("rnn_bf16_b130_i64_h256_t21", B=130, I=64, H=256, T_max=21, dtype="bf16", len_lo=0,
+      len_hi=21, random_state=True, cell="rnn", seed=43),
+    W("rnn_f32_2layer_b17_i16_h32_t29", B=17, I=16, H=32, T_max=29, dtype="f32", layers=2,
+      len_lo=0, len_hi=29, w_scale=0.3, random_state=True, cell="rnn", seed=44),
+    W("rnn_bf16_b9_i8_h1024_t12", B=9, I=8, H=1024, T_max=12, dtype="bf16", len_lo=0, len_hi=12,
+      random_state=True, cell="rnn", seed=45),
+]
+
+
+@pytest.mark.parametrize("w", RNN_CASES, ids=[w.name for w in RNN_CASES])
+def test_rnn_cell_parity(w):
+    """The same loop engine with the Elman RNN body: every output within the
+    tolerance of the RNN oracle; cT and dc0 are written as zeros."""
+    say(f"[rnn] {w.name}")
+    inp = wl.generate(w)
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell="rnn")
+    plan = dc.plan()
+    geom = plan.geometry()
+    assert geom["xcd_local"], geom
+    dc.fwd(plan)
+    dc.bwd(plan)
+    err = plan.status_sync()
+    res = dc.results()
+    plan.close()
+    assert err == 0
+    ref = oracle_reference(inp, w.layers, w.dtype, cell="rnn")
+    assert res["T_eff"] == ref["T_eff"] == int(inp["seq_len"].max())
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
