@@ -7,8 +7,11 @@ from .lstm import (bf16_round, sigmoid, lstm_forward_literal, lstm_forward,
                    matmul_chain_grad)
 from .rnn import (rnn_forward_literal, rnn_forward, rnn_backward,
                   stacked_rnn_forward, stacked_rnn_backward)
+from .gru import (gru_forward_literal, gru_forward, gru_backward,
+                  stacked_gru_forward, stacked_gru_backward)
 
 __all__ = ["bf16_round", "sigmoid", "lstm_forward_literal", "lstm_forward",
            "lstm_backward", "stacked_forward", "stacked_backward",
            "matmul_chain_grad", "rnn_forward_literal", "rnn_forward", "rnn_backward",
-           "stacked_rnn_forward", "stacked_rnn_backward"]
+           "stacked_rnn_forward", "stacked_rnn_backward", "gru_forward_literal",
+           "gru_forward", "gru_backward", "stacked_gru_forward", "stacked_gru_backward"]
