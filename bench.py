@@ -75,10 +75,11 @@ def cpu_baseline(w, inp, target_s):
         Ws = [a.astype(np.float64) for a in inp["W"]]
         bs = [a.astype(np.float64) for a in inp["bias"]]
         t0 = time.perf_counter()
-        if w.cell == "rnn":
-            _, _, tapes = oracle.stacked_rnn_forward(x, sl, Ws, bs, inp["h0"].astype(np.float64),
-                                                     precision)
-            oracle.stacked_rnn_backward(tapes, dy, inp["dhT"].astype(np.float64))
+        if w.cell in ("rnn", "gru"):
+            fwd, bwd = ((oracle.stacked_rnn_forward, oracle.stacked_rnn_backward) if w.cell == "rnn"
+                        else (oracle.stacked_gru_forward, oracle.stacked_gru_backward))
+            _, _, tapes = fwd(x, sl, Ws, bs, inp["h0"].astype(np.float64), precision)
+            bwd(tapes, dy, inp["dhT"].astype(np.float64))
         else:
             y, hT, cT, tapes = oracle.stacked_forward(x, sl, Ws, bs, inp["h0"].astype(np.float64),
                                                       inp["c0"].astype(np.float64), precision)

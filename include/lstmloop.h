@@ -14,7 +14,7 @@
  *       c_t = f*c_{t-1} + i*g;     h_t = o*tanh(c_t)
  *   Rows with t >= seq_len[b] keep their state and output y = 0.  The
  *   body can instead be the Elman recurrence h_t = tanh([x_t, h_{t-1}] W + b)
- *   (desc.cell = LL_CELL_RNN, below).
+ *   or a GRU step (desc.cell = LL_CELL_RNN / LL_CELL_GRU, below).
  *   Each iteration pushes what the gradient needs onto a stack (Section 5.1);
  *   the gradient loop runs the same number of iterations in reverse, pops
  *   the stack, carries dh/dc as loop variables and sums the gradients of the
@@ -33,7 +33,8 @@
  *     I_l..I_l+H-1 multiply h_{t-1}; column blocks are gates i, f, g, o.
  *     I_0 = I, I_1 = H.  Its element type is desc.dtype (float or bfloat16
  *     bits); bias is always float [4H].  (LL_CELL_RNN: 4H reads H here and
- *     below: W [I_l + H, H], bias, dW and dbias [.., H].)
+ *     below: W [I_l + H, H], bias, dW and dbias [.., H].  LL_CELL_GRU: W and
+ *     dW [I_l + H, 3H], bias and dbias [4H].)
  *   - State, stack and accumulation are float32.  In LL_BF16 mode the
  *     matrix-core operands are bfloat16 (round to nearest even): x, W,
  *     h_{t-1} in the forward; dz, [x_t, h_{t-1}] and W in the backward.
@@ -71,12 +72,19 @@ typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
 
 /* Loop body (cell).  LL_CELL_LSTM: gates i, f, g, o (W [I_l + H, 4H], bias
  * [4H]), state (h, c).  LL_CELL_RNN: the Elman recurrence h_t = tanh(x_t W_x
- * + h_{t-1} W_h + b) (W [I_l + H, H], bias [H]), state h; c0, cT, dcT and dc0
- * are ignored (cT and dc0, if given, are written as zeros).  The loop
- * construct, masking, stack and gradient loop are the same for both: the
- * paper's while-loop and its gradient (Sections 3 and 5) do not depend on
- * the body. */
-typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1 } ll_cell;
+ * + h_{t-1} W_h + b) (W [I_l + H, H], bias [H]), state h.  LL_CELL_GRU: the
+ * gated recurrent unit with the reset gate applied after the recurrent
+ * product, column blocks r, u, n (W [I_l + H, 3H]; bias [4H] = b_x [3H],
+ * then b_hn [H]):
+ *     zx = x_t W_x + b_x,  zh = h_{t-1} W_h
+ *     r = sigmoid(zx_r + zh_r),  u = sigmoid(zx_u + zh_u)
+ *     n = tanh(zx_n + r * (zh_n + b_hn)),  h_t = (1 - u) n + u h_{t-1}
+ * state h; dbias [4H] = [db_x, db_hn].  For both one-state cells c0, cT,
+ * dcT and dc0 are ignored (cT and dc0, if given, are written as zeros).  The
+ * loop construct, masking, stack and gradient loop are the same for every
+ * body: the paper's while-loop and its gradient (Sections 3 and 5) do not
+ * depend on it. */
+typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1, LL_CELL_GRU = 2 } ll_cell;
 
 /* Device error word bits (ll_status_sync). */
 #define LL_DEVERR_SEQ_LEN 1      /* some seq_len[b] < 0 or > T_max          */
@@ -118,8 +126,9 @@ typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1 } ll_cell;
  *     XCD-local loops and spill = 0 (else LL_EUNSUPPORTED); the two layers
  *     then run one after the other.  The bias passed to lstm_loop_fwd is
  *     copied into the plan for the gradient pass.
- *   cell: an ll_cell.  LL_CELL_RNN needs the XCD-local loops, spill = 0
- *     and recompute = 0 (else LL_EUNSUPPORTED); its stack holds h_t only.
+ *   cell: an ll_cell.  LL_CELL_RNN and LL_CELL_GRU need the XCD-local
+ *     loops, spill = 0 and recompute = 0 (else LL_EUNSUPPORTED); the RNN's
+ *     stack holds h_t only, the GRU's r, u, n, zh_n + b_hn and h_{t-1}.
  */
 typedef struct {
   int32_t T_max;
@@ -187,7 +196,8 @@ ll_status ll_plan_geometry(const ll_plan* plan, int32_t* loop_workgroups,
  *   y        [T_max,B,H] float output of the top layer (0 where t >=
  *            seq_len[b]), or NULL.
  *   hT, cT   [layers,B,H] float: state after seq_len[b] steps (h0/c0 for
- *            zero-length rows).  Required.
+ *            zero-length rows).  Required (cT: LSTM only; NULL allowed for
+ *            the one-state cells).
  *   trip_count  device int32 scalar receiving T_eff, or NULL.
  *   save_for_backward  nonzero: push the stack for lstm_loop_bwd; the plan
  *            keeps x, seq_len, W, h0, c0 pointers, which must stay valid and

@@ -238,12 +238,13 @@ __global__ __launch_bounds__(256) void h0_rows_kernel(const float* __restrict__ 
 
 // out[i] = sum_{s < S} ws[s * stride + i], fixed order.
 __global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict__ ws, int S,
-                                                         long stride, long n,
+                                                         long stride, long n, long cols, long ldo,
                                                          float* __restrict__ out) {
   for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
     float acc = 0.0f;
     for (int s = 0; s < S; ++s) acc += ws[s * stride + i];
-    out[i] = acc;
+    const long r = i / cols;
+    out[r * ldo + (i - r * cols)] = acc;
   }
 }
 
@@ -390,11 +391,18 @@ hipError_t launch_h0_rows(const float* h0, const int* perm, int B, int H, T* dst
 
 hipError_t launch_sum_slices(const float* ws, int S, long stride, long n, float* out,
                              hipStream_t s) {
+  return launch_sum_slices_2d(ws, S, stride, 1, n, out, n, s);
+}
+
+hipError_t launch_sum_slices_2d(const float* ws, int S, long stride, long rows, long cols, float* out,
+                                long ldo, hipStream_t s) {
+  const long n = rows * cols;
+  if (cols < 1 || ldo < cols) return hipErrorInvalidValue;
   long blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(sum_slices_kernel, dim3((unsigned)blocks), dim3(256), 0, s, ws, S, stride, n,
-                     out);
+                     cols, ldo, out);
   return hipGetLastError();
 }
 

@@ -129,10 +129,11 @@ struct XLoopArgs {
   const int* active;
   const int* off;
   const int* perm;
-  const void* W;          // forward: W^T [4H, ldw]; backward: W [rows, 4H]
+  // (G gate blocks: LSTM 4, GRU 3, RNN 1; GB = 4 for the GRU, else G)
+  const void* W;          // forward: W^T [G H, ldw]; backward: W [rows, G H]
   int ldw;
   int woff;               // forward: column of the h part in W^T; backward: row of W_h
-  void* X;                // forward: h history [cap, H]; backward: dz [cap, 4H] (operand type)
+  void* X;                // forward: h history [cap, H]; backward: dz [cap, GB H] (operand type)
   void* ring;             // exchange ring [2][8][MRT][ring_ks][1 KB] (forward: slot 1 holds h0)
   int ring_ks;            // k-step blocks per row tile: H / (4 KPC) forward, 4H / (4 KPC) backward
   unsigned* flags;        // [8][MRT][32] per-member step flags, zero before the launch
@@ -147,7 +148,8 @@ struct XLoopArgs {
   int dy_compact;
   const float* dhT;
   const float* dcT;
-  float* db_part;         // backward: [8, 4H]
+  float* db_part;         // backward: [8, GB H]
+  const float* bhn;       // GRU, forward: the candidate block's recurrent bias [H]
   float* dh0;
   float* dc0;
   unsigned* rank_ctr;     // [8], zero before the launch
@@ -179,7 +181,8 @@ struct XLoopArgs {
   // grow maps like stack_row with gchunk / gslots (gstk NULL: the gates sit
   // in the stack rows, at offsets 0 .. 3H)
   int sld, scoff;
-  int sgates;             // forward: 1 = push i, f, g, o with c (0: c only)
+  int sgates;             // forward: 1 = push i, f, g, o with c (0: c only); the
+                          // GRU pushes r, u, n, zh_n + b_hn and h_{t-1} in their places
   const float* gstk;
   int gld, gchunk, gslots;
 };
@@ -290,6 +293,10 @@ template <typename T>
 hipError_t launch_h0_rows(const float* h0, const int* perm, int B, int H, T* dst, hipStream_t s);
 hipError_t launch_sum_slices(const float* ws, int S, long stride, long n, float* out,
                              hipStream_t s);
+// out[r * ldo + c] = sum over s < S of ws[s * stride + r * cols + c], for
+// r < rows, c < cols.
+hipError_t launch_sum_slices_2d(const float* ws, int S, long stride, long rows, long cols, float* out,
+                                long ldo, hipStream_t s);
 template <typename T>
 hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s);
 

@@ -70,13 +70,15 @@ struct ll_plan {
   int device = 0;
   int es = 4;            // operand element bytes
   bool bf16 = false;
-  int G = 4;             // gate blocks of the cell: 4 (LSTM), 1 (Elman RNN)
+  int G = 4;             // gate blocks of the cell: 4 (LSTM), 3 (GRU), 1 (Elman RNN)
+  int GB = 4;            // dz row and bias blocks: the GRU's 4 (r, u, n, and the
+                         // candidate's recurrent side), else G
   long cap = 0;          // compact-row capacity = T_max * B
   long ldT = 0;          // leading dimension of transposed per-row arrays
   ll::LoopGeom geom{};
   int n_cu = 0;
   unsigned long long barrier_ticks = 0;
-  int dw_splits[2] = {1, 1};   // split-K of the dW product of layer 0 / 1
+  int dw_splits[2][3] = {{1, 1, 1}, {1, 1, 1}};   // split-K of each dW product (layer, part)
   bool xmode = false;          // XCD-local loops (ll_xloop.hip)
   ll::XKernels xk{};
   int xP = 0;                  // unit blocks per XCD
@@ -170,6 +172,27 @@ struct ll_plan {
 namespace {
 
 int in_width(const ll_plan* p, int l) { return l == 0 ? p->d.I : p->d.H; }
+
+// The dW products of layer l: dW[a_row .. a_row+m, c_col .. c_col+n] =
+// XT[a_row .. a_row+m]  DZT[b_row .. b_row+n]^T, XT = [X^T; Hprev^T] and DZT
+// the transposed dz rows.  One product over the stacked operand; the GRU's
+// two sides differ in the candidate block (dz_n on the input side, da_n * r
+// on the recurrent side, dz columns 2H and 3H), so its r, u blocks take one
+// product over the stacked operand and the candidate block one per side.
+struct DwPart {
+  int a_row, m, b_row, n, c_col;
+};
+int dw_parts(const ll_plan* p, int l, DwPart* out) {
+  const int H = p->d.H, Il = in_width(p, l);
+  if (p->G == 3) {
+    out[0] = DwPart{0, Il + H, 0, 2 * H, 0};
+    out[1] = DwPart{0, Il, 2 * H, H, 2 * H};
+    out[2] = DwPart{Il, H, 3 * H, H, 2 * H};
+    return 3;
+  }
+  out[0] = DwPart{0, Il + H, 0, p->G * H, 0};
+  return 1;
+}
 
 hipEvent_t take_event(ll_plan* p) {
   if (!p->ev_pool.empty()) {
@@ -294,9 +317,9 @@ ll_status validate_desc(const ll_desc* d) {
   if (d->recompute != 0 && d->recompute != 1) return fail(LL_EINVAL, "recompute must be 0 or 1");
   if (d->recompute && d->spill)
     return fail(LL_EUNSUPPORTED, "recompute and spill are alternatives; choose one");
-  if (d->cell != LL_CELL_LSTM && d->cell != LL_CELL_RNN)
-    return fail(LL_EINVAL, "cell must be LL_CELL_LSTM or LL_CELL_RNN (got %d)", d->cell);
-  if (d->cell == LL_CELL_RNN && (d->spill || d->recompute))
+  if (d->cell != LL_CELL_LSTM && d->cell != LL_CELL_RNN && d->cell != LL_CELL_GRU)
+    return fail(LL_EINVAL, "cell must be LL_CELL_LSTM, LL_CELL_RNN or LL_CELL_GRU (got %d)", d->cell);
+  if (d->cell != LL_CELL_LSTM && (d->spill || d->recompute))
     return fail(LL_EUNSUPPORTED, "spill and recompute are built for the LSTM cell only");
   if ((long)d->T_max * d->B > (1L << 30))
     return fail(LL_EUNSUPPORTED, "T_max * B = %ld exceeds 2^30 rows", (long)d->T_max * d->B);
@@ -353,7 +376,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   p->device = device;
   p->bf16 = desc->dtype == LL_BF16;
   p->es = p->bf16 ? 2 : 4;
-  p->G = desc->cell == LL_CELL_RNN ? 1 : 4;
+  p->G = desc->cell == LL_CELL_RNN ? 1 : desc->cell == LL_CELL_GRU ? 3 : 4;
+  p->GB = desc->cell == LL_CELL_GRU ? 4 : p->G;
   p->n_cu = prop.multiProcessorCount;
   p->cap = (long)desc->T_max * desc->B;
   p->ldT = round_up(p->cap, 64);
@@ -426,11 +450,11 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     }
   }
 
-  // The Elman RNN cell runs on the XCD-local loops only.
+  // The Elman RNN and GRU cells run on the XCD-local loops only.
   if (p->G != 4 && !p->xmode) {
     delete p;
-    return fail(LL_EUNSUPPORTED, "the RNN cell needs the XCD-local loops (H = %d, B = %d do not fit them)",
-                H, B);
+    return fail(LL_EUNSUPPORTED, "the %s cell needs the XCD-local loops (H = %d, B = %d do not fit them)",
+                p->G == 1 ? "RNN" : "GRU", H, B);
   }
 
   // Chip-wide loops where one XCD cannot hold the recurrent weights (bf16
@@ -499,32 +523,35 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     }
   }
 
-  // dW split-K: enough work-groups to cover the chip (one 256x256 tile per
-  // compute unit for the large-tile bf16 kernel, two 128x128 tiles else).
-  for (int l = 0; l < L; ++l) {
-    const int M = (l == 0 ? desc->I : H) + H;
-    ll::GemmArgs g{};
-    g.lda = g.ldb = p->ldT;
-    g.M = M;
-    g.N = p->G * H;
-    g.K = (int)p->cap;
-    g.splits = 1;
-    g.k_zero_tail = 1;
-    const bool big = ll::gemm_big_applies(g, (int)p->es);
-    const long tile = big ? ll::kGemmBigTile : 128;
-    const long tiles = (long)((M + tile - 1) / tile) * ((p->G * H + tile - 1) / tile);
-    const long want = big ? p->n_cu : 2L * p->n_cu;
-    long s = (want + tiles - 1) / tiles;
-    s = std::max(1L, std::min(16L, s));
-    const long max_by_k = std::max(1L, p->cap / 256);
-    p->dw_splits[l] = (int)std::min(s, max_by_k);
-  }
-  const int maxI = std::max(desc->I, H);
+  // dW split-K, per product: enough work-groups to cover the chip (one
+  // 256x256 tile per compute unit for the large-tile bf16 kernel, two 128x128
+  // tiles else).  The products run one after the other and share the
+  // workspace of the partial sums.
   p->ws_floats = 0;
   for (int l = 0; l < L; ++l) {
-    const int Il = in_width(p, l);
-    if (p->dw_splits[l] > 1) p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[l] * (Il + H) * p->G * H);
+    DwPart parts[3];
+    const int np = dw_parts(p, l, parts);
+    for (int k = 0; k < np; ++k) {
+      ll::GemmArgs g{};
+      g.lda = g.ldb = p->ldT;
+      g.M = parts[k].m;
+      g.N = parts[k].n;
+      g.K = (int)p->cap;
+      g.splits = 1;
+      g.k_zero_tail = 1;
+      const bool big = ll::gemm_big_applies(g, (int)p->es);
+      const long tile = big ? ll::kGemmBigTile : 128;
+      const long tiles = (long)((g.M + tile - 1) / tile) * ((g.N + tile - 1) / tile);
+      const long want = big ? p->n_cu : 2L * p->n_cu;
+      long s = (want + tiles - 1) / tiles;
+      s = std::max(1L, std::min(16L, s));
+      const long max_by_k = std::max(1L, p->cap / 256);
+      p->dw_splits[l][k] = (int)std::min(s, max_by_k);
+      if (p->dw_splits[l][k] > 1)
+        p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[l][k] * g.M * g.N);
+    }
   }
+  const int maxI = std::max(desc->I, H);
 
   const size_t es = p->es;
   const long cap = p->cap;
@@ -553,8 +580,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     ALLOC(p->HH[l], es * (cap + (p->recompute ? B : 0)) * H, "h history");
   }
   ALLOC(p->Zx, sizeof(float) * cap * p->G * H, "input projection");
-  ALLOC(p->DZ, es * cap * p->G * H, "dz");
-  ALLOC(p->DZT, es * p->G * H * p->ldT, "dz transposed");
+  ALLOC(p->DZ, es * cap * p->GB * H, "dz");
+  ALLOC(p->DZT, es * p->GB * H * p->ldT, "dz transposed");
   ALLOC(p->XT, es * (maxI + H) * p->ldT, "x and h_prev transposed");
   if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
   if (p->xmode) {
@@ -587,7 +614,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     ALLOC(p->carry, sizeof(float) * 4 * B * H, "chunk carry");
     ALLOC(p->db_state, sizeof(float) * 8 * 32 * 512 * 4, "db state");
   }
-  ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * p->G * H, "db partials");
+  ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * p->GB * H, "db partials");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
 #undef ALLOC
   if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess) {
@@ -739,10 +766,12 @@ ll::XLoopArgs x_common(const ll_plan* p) {
   a.t_end = p->d.T_max;
   a.chunk_steps = p->d.T_max;
   a.nslots = 1;
-  // stack rows: LSTM i, f, g, o, c_t (5H); the RNN pushes h_t only
-  a.sld = p->G == 4 ? 5 * p->d.H : p->d.H;
-  a.scoff = p->G == 4 ? 4 * p->d.H : 0;
-  a.sgates = p->G == 4 ? 1 : 0;
+  // stack rows: LSTM i, f, g, o, c_t (5H); GRU r, u, n, zh_n + b_hn,
+  // h_{t-1} (5H); the RNN pushes h_t only
+  const bool five = p->G == 4 || p->G == 3;
+  a.sld = five ? 5 * p->d.H : p->d.H;
+  a.scoff = five ? 4 * p->d.H : 0;
+  a.sgates = five ? 1 : 0;
   return a;
 }
 
@@ -892,13 +921,15 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       xa.woff = Il;
       xa.X = p->HH[l];
       xa.Zx = p->Zx;
+      xa.bhn = p->G == 3 ? bias[l] + 3L * H : nullptr;
       xa.stack = save ? p->stack[l] : nullptr;
       xa.y = (l == L - 1) ? y : nullptr;
       xa.abort_flag = p->meta + 3;
       xa.err = p->meta + 2;
       xa.limit = p->barrier_ticks;
       const float* hin = h0 ? h0 + (long)l * B * H : nullptr;
-      // (the RNN has no cell state: c0 is ignored, cT written as zeros if given)
+      // (the RNN and GRU have no cell state: c0 is ignored, cT written as
+      // zeros if given)
       const float* cin = c0 && p->G == 4 ? c0 + (long)l * B * H : nullptr;
       float* hout = hT + (long)l * B * H;
       float* cout = cT ? cT + (long)l * B * H : nullptr;
@@ -1013,9 +1044,10 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   // larger one runs after them on the call's stream (measured: two large
   // products side by side only slow each other).
   ll::GemmArgs gx{};
-  const int GH = p->G * H;
+  const int GH = p->G * H;     // gate columns of W
+  const int GBH = p->GB * H;   // dz row width, bias length
   gx.A = dz;
-  gx.lda = GH;
+  gx.lda = GBH;
   gx.Bm = p->W[l];
   gx.ldb = GH;
   gx.M = (int)p->cap;
@@ -1047,7 +1079,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   }
   // db = sum of the row-group partials
   ev = tbeg(p, s, LL_STAGE_DW);
-  LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, GH, GH, dbias[l], s));
+  LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, GBH, GBH, dbias[l], s));
   tend(p, s, LL_STAGE_DW, ev);
   ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
   // transposed operands of the dW products (reduction over compact rows)
@@ -1060,7 +1092,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   gt.ldo = (int)p->ldT;
   gt.in = dz;
   gt.out = p->DZT;
-  gt.C = GH;
+  gt.C = GBH;
   gt.mode = 1;
   LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
   gt.in = l == 0 ? p->x : p->HH[0];
@@ -1075,31 +1107,37 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   gt.h0f = p->h0 ? p->h0 + (long)l * B * H : nullptr;
   LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
   tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
-  // [dW_x; dW_h] = [X^T; Hprev^T] DZ: one product over the stacked operand
+  // dW = [X^T; Hprev^T] DZ (the parts of dw_parts)
   ev = tbeg(p, s, LL_STAGE_DW);
   {
-    const int M = Il + H;
-    ll::GemmArgs g{};
-    g.A = p->XT;
-    g.lda = p->ldT;
-    g.Bm = p->DZT;
-    g.ldb = p->ldT;
-    g.M = M;
-    g.N = GH;
-    g.K = (int)p->cap;
-    g.K_dev = p->meta + 1;
-    g.k_zero_tail = 1;   // the transposes write zeros past the last row, up to a multiple of 64
-    g.splits = p->dw_splits[l];
-    if (g.splits > 1) {
-      g.C = p->ws;
-      g.ldc = GH;
-      g.split_stride = (long)M * GH;
-      LL_HIP(ll::launch_gemm_nt<T>(g, s));
-      LL_HIP(ll::launch_sum_slices(p->ws, g.splits, g.split_stride, g.split_stride, dW[l], s));
-    } else {
-      g.C = dW[l];
-      g.ldc = GH;
-      LL_HIP(ll::launch_gemm_nt<T>(g, s));
+    DwPart parts[3];
+    const int np = dw_parts(p, l, parts);
+    const long rowb = p->es * p->ldT;   // bytes per transposed row
+    for (int k = 0; k < np; ++k) {
+      const DwPart& q = parts[k];
+      float* out = dW[l] + (long)q.a_row * GH + q.c_col;
+      ll::GemmArgs g{};
+      g.A = static_cast<const char*>(p->XT) + q.a_row * rowb;
+      g.lda = p->ldT;
+      g.Bm = static_cast<const char*>(p->DZT) + q.b_row * rowb;
+      g.ldb = p->ldT;
+      g.M = q.m;
+      g.N = q.n;
+      g.K = (int)p->cap;
+      g.K_dev = p->meta + 1;
+      g.k_zero_tail = 1;   // the transposes write zeros past the last row, up to a multiple of 64
+      g.splits = p->dw_splits[l][k];
+      if (g.splits > 1) {
+        g.C = p->ws;
+        g.ldc = q.n;
+        g.split_stride = (long)q.m * q.n;
+        LL_HIP(ll::launch_gemm_nt<T>(g, s));
+        LL_HIP(ll::launch_sum_slices_2d(p->ws, g.splits, g.split_stride, q.m, q.n, out, GH, s));
+      } else {
+        g.C = out;
+        g.ldc = GH;
+        LL_HIP(ll::launch_gemm_nt<T>(g, s));
+      }
     }
   }
   tend(p, s, LL_STAGE_DW, ev);

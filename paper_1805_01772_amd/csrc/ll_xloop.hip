@@ -118,7 +118,8 @@ __device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp
 // lower layer's ring for step t (bf16(y1_t) in the bf16 contract: the ring
 // holds the operand-type h_t), the rest h_{t-1} from its own ring; the bias
 // replaces the hoisted input projection.
-// G: gate blocks of the cell (4: LSTM i, f, g, o; 1: Elman RNN, h = tanh(z)).
+// G: gate blocks of the cell (4: LSTM i, f, g, o; 1: Elman RNN, h = tanh(z);
+// 3: GRU r, u, n with the reset gate applied after the recurrent product).
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP, int G = 4>
 __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
@@ -172,6 +173,8 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   const float* rp = red + (crow & 3) * IS + (cu >> 4) * 64 + (crow >> 2) * 16 + (cu & 15);
   // byte offset of (crow, cu) in a ring block
   const int rbo = ((crow + 16 * (cu / KPC)) * KPC + cu % KPC) * (int)sizeof(T);
+  // GRU: recurrent bias of the candidate block, added before the reset gate
+  const float bhn = (G == 3 && cellt) ? a.bhn[ju] : 0.f;
   float hs[MRT_MAX], cs[MRT_MAX];
   if (tid < MRT_MAX * 16) {
     const int r = (grp + 8 * (tid >> 4)) * 16 + (tid & 15);
@@ -265,7 +268,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       // 2. partial products over this wave's k-steps, column tiles in two
       //    halves, into red[wave][i][ct][lane] (the previous tile's cell has
       //    read them: it ended at a barrier)
-      constexpr int NHALF = NCT >= 2 ? 2 : 1;
+      constexpr int NHALF = NCT % 2 == 0 ? 2 : 1;
 #pragma unroll
       for (int hf = 0; hf < NHALF; ++hf) {
         constexpr int NH = NCT / NHALF;
@@ -299,13 +302,14 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       const int r = r0 + crow;
       const bool act = cellt && r < A_t;
       if (cellt) {
-        float z[G];
+        float z[G], zh[G];
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           const float* p = rp + g * (HJ / 16) * 64;
           float v = p[0];
 #pragma unroll
           for (int w2 = 1; w2 < XNW; ++w2) v += p[w2 * 4 * IS];
+          zh[g] = v;
           z[g] = v + zc[g];
         }
         if constexpr (G == 4) {
@@ -315,12 +319,21 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
           og = sigmoidf_(z[3]);
           cn = fg * cs[mt] + ig * gg;
           hn = og * tanhf_(cn);
+        } else if constexpr (G == 3) {
+          // GRU: r, u, n, zh_n + b_hn and h_{t-1} take the places of the
+          // LSTM's i, f, g, o and c_t in the stack row
+          ig = sigmoidf_(z[0]);
+          fg = sigmoidf_(z[1]);
+          og = zh[2] + bhn;
+          gg = tanhf_(zc[2] + ig * og);
+          cn = hs[mt];
+          hn = (1.f - fg) * gg + fg * cn;
         } else {
           hn = tanhf_(z[0]);
         }
         if (act) {
           *reinterpret_cast<T*>(ring_tile(a, t & 1, grp, mt) + (rank << 10) + rbo) = Op<T>::from_f32(hn);
-          cs[mt] = cn;
+          if constexpr (G == 4) cs[mt] = cn;
           hs[mt] = hn;
         }
       }
@@ -330,7 +343,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         HH[cr * H + ju] = Op<T>::from_f32(hn);
         if (a.stack) {
           float* st = a.stack + stack_row(a, t, r) * a.sld + ju;
-          if constexpr (G == 4) {
+          if constexpr (G == 4 || G == 3) {
             // (c only: the gate stores all land on the c field, which the last
             // store overwrites; no branch on the common path)
             const int gs = a.sgates ? H : 0;
@@ -434,12 +447,16 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int q = lane >> 4, l16 = lane & 15;
   const int H = a.H, B = a.B, P = a.P;
-  const long G4 = (long)G * H;                          // gate columns (dz row width)
+  const long G4 = (long)G * H;                          // gate columns (ring blocks, W_h row width)
+  // dz rows for the products after the loop: the gate blocks, and for the GRU
+  // a fourth, the candidate block's recurrent-side value da_n * r
+  constexpr int GB = G == 3 ? 4 : G;
+  const long GBH = (long)GB * H;
   const int j0 = rank * HJ;
   const int KS = (int)(G4 / (4 * KPC));
   // pops per (step, tile) and thread: LSTM i, f, g, o, c_t, c_{t-1}, dy;
-  // RNN h_t, dy
-  constexpr int NPOP = G == 4 ? 7 : 2;
+  // GRU r, u, n, zh_n + b_hn, h_{t-1}, dy; RNN h_t, dy
+  constexpr int NPOP = G == 4 ? 7 : G == 3 ? 6 : 2;
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
   const int nks = ks1 - ks0;                            // k-steps of this wave
   const T* W = reinterpret_cast<const T*>(a.W);
@@ -491,13 +508,13 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       if (a.dcT) dc[mt] = a.dcT[(long)b * H + ju];
     }
   }
-  float dbacc[G];
+  float dbacc[GB];
 #pragma unroll
-  for (int g = 0; g < G; ++g) dbacc[g] = 0.f;
+  for (int g = 0; g < GB; ++g) dbacc[g] = 0.f;
   float* dbst = a.db_state ? a.db_state + ((long)(grp * 32 + rank) * XNT + tid) * 4 : nullptr;
   if (dbst && a.db_resume) {
 #pragma unroll
-    for (int g = 0; g < G; ++g) dbacc[g] = dbst[g];
+    for (int g = 0; g < GB; ++g) dbacc[g] = dbst[g];
   }
 
   // pops of (step tt, tile mt) for this thread: i, f, g, o, c_t, c_{t-1}, dy;
@@ -523,7 +540,9 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
 #pragma unroll
     for (int c = 0; c < 4; ++c) v[c] = ld_f32(rg, go + c * H * 4);
     v[4] = ld_f32(rs, so);
-    if (tt > 0) {
+    if constexpr (G == 3) {   // GRU: h_{t-1} was pushed with the step
+      v[5] = 0.f;
+    } else if (tt > 0) {
       const __amdgpu_buffer_rsrc_t rp2 =
           make_rsrc(a.stack + stack_row(a, tt - 1, r0) * SL + a.scoff, (unsigned)(nr * SL * 4));
       v[5] = ld_f32(rp2, so);
@@ -590,8 +609,9 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
             make_rsrc(reinterpret_cast<const float*>(a.dyx_ring) + dyx_off, (unsigned)(16 * H * 4));
         dyl = ld_f32_l2(ry, act ? (unsigned)((crow * H + ju) * 4) : kOOB);
       }
-      // phase 1
-      float dz[G];
+      // phase 1 (dz: the ring's values, the recurrent side; GRU: dzx_n is
+      // the input side's candidate value, dhu the direct term of dh_{t-1})
+      float dz[G], dzx_n = 0.f, dhu = 0.f;
 #pragma unroll
       for (int g = 0; g < G; ++g) dz[g] = 0.f;
       if (act) {
@@ -607,6 +627,15 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
           dz[2] = dct * ig * (1.f - gg * gg);
           dz[3] = d_o * (og * (1.f - og));
           dc[mt] = dct * fg;
+        } else if constexpr (G == 3) {
+          const float rg = pv[mt][0], ug = pv[mt][1], ng = pv[mt][2], hnv = pv[mt][3];
+          const float hp = pv[mt][4];
+          const float dan = dht * (1.f - ug) * (1.f - ng * ng);
+          dz[0] = dan * hnv * (rg * (1.f - rg));
+          dz[1] = dht * (hp - ng) * (ug * (1.f - ug));
+          dz[2] = dan * rg;
+          dzx_n = dan;
+          dhu = dht * ug;
         } else {
           const float hv = pv[mt][0];
           dz[0] = dht * (1.f - hv * hv);
@@ -617,11 +646,22 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       }
       publish(flags + rank, (unsigned)(T_eff - t));
       if (act) {
-        T* dzr = DZ + (long)(off_t + r0 + crow) * G4 + ju;
+        T* dzr = DZ + (long)(off_t + r0 + crow) * GBH + ju;
+        if constexpr (G == 3) {   // [da_r, da_u, da_n, da_n * r]
+          dzr[0] = Op<T>::from_f32(dz[0]);
+          dzr[H] = Op<T>::from_f32(dz[1]);
+          dzr[2L * H] = Op<T>::from_f32(dzx_n);
+          dzr[3L * H] = Op<T>::from_f32(dz[2]);
+          dbacc[0] += dz[0];
+          dbacc[1] += dz[1];
+          dbacc[2] += dzx_n;
+          dbacc[3] += dz[2];
+        } else {
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          dzr[(long)g * H] = Op<T>::from_f32(dz[g]);
-          dbacc[g] += dz[g];
+          for (int g = 0; g < G; ++g) {
+            dzr[(long)g * H] = Op<T>::from_f32(dz[g]);
+            dbacc[g] += dz[g];
+          }
         }
       }
       // phase 2
@@ -682,7 +722,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
         float s = rp[0];
 #pragma unroll
         for (int w2 = 1; w2 < XNW; ++w2) s += rp[w2 * 4 * IS];
-        dh[mt] = s;
+        dh[mt] = G == 3 ? s + dhu : s;
       }
       if constexpr (ROLE == 2) {
         // dy of the lower layer's output at step t for the own units; the
@@ -711,20 +751,20 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   }
   if (dbst) {
 #pragma unroll
-    for (int g = 0; g < G; ++g) dbst[g] = dbacc[g];
+    for (int g = 0; g < GB; ++g) dbst[g] = dbacc[g];
   }
   // db partial of this work-group (its rows of this XCD), fixed order
   __syncthreads();
   if (cellt) {
 #pragma unroll
-    for (int g = 0; g < G; ++g) red[(crow * G + g) * HJ + cu] = dbacc[g];
+    for (int g = 0; g < GB; ++g) red[(crow * GB + g) * HJ + cu] = dbacc[g];
   }
   __syncthreads();
-  for (int c = tid; c < G * HJ; c += XNT) {
+  for (int c = tid; c < GB * HJ; c += XNT) {
     float s = 0.f;
-    for (int m = 0; m < 16; ++m) s += red[m * G * HJ + c];
+    for (int m = 0; m < 16; ++m) s += red[m * GB * HJ + c];
     const int g = c / HJ, u = c - (c / HJ) * HJ;
-    a.db_part[(long)grp * G4 + (long)g * H + j0 + u] = s;
+    a.db_part[(long)grp * GBH + (long)g * H + j0 + u] = s;
   }
 }
 
@@ -856,7 +896,8 @@ XKernels x_make() {
 //   bf16: HJ = 32 units, forward NCT 8, KSW = H/256; backward NCT 2, KSW = H/64.
 //   f32:  HJ = 16 units, forward NCT 4, KSW = H/128; backward NCT 1, KSW = H/32.
 // (LSTM; the Elman RNN has one gate block: forward NCT 2 / 1, backward KSW
-// = H/256 / H/128, every weight in registers.)
+// = H/256 / H/128, every weight in registers; the GRU three: forward NCT
+// 6 / 3, backward KSW = 3H/256 / 3H/128.)
 // hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
 template <typename T>
 XKernels x_kernels(int hc, int mrt, int gates) {
@@ -871,6 +912,15 @@ XKernels x_kernels(int hc, int mrt, int gates) {
       case 1: return one ? x_make<T, NR, NB, 1, 1, 1, 1, 1>() : x_make<T, NR, NB, 1, 1, 1, 4, 1>();
       case 2: return one ? x_make<T, NR, NB, 2, 2, 2, 1, 1>() : x_make<T, NR, NB, 2, 2, 2, 4, 1>();
       case 4: return one ? x_make<T, NR, NB, 4, 4, 4, 1, 1>() : x_make<T, NR, NB, 4, 4, 4, 4, 1>();
+      default: return XKernels{};
+    }
+  }
+  if (gates == 3) {
+    constexpr int NG = bf ? 6 : 3;
+    switch (hc) {
+      case 1: return one ? x_make<T, NG, NB, 1, 1, 3, 1, 3>() : x_make<T, NG, NB, 1, 1, 3, 4, 3>();
+      case 2: return one ? x_make<T, NG, NB, 2, 2, 6, 1, 3>() : x_make<T, NG, NB, 2, 2, 6, 4, 3>();
+      case 4: return one ? x_make<T, NG, NB, 4, 4, 12, 1, 3>() : x_make<T, NG, NB, 4, 4, 8, 4, 3>();
       default: return XKernels{};
     }
   }

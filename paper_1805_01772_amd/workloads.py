@@ -37,7 +37,7 @@ class Workload:
     random_state: bool = False        # h0, c0 ~ N(0, 0.5^2) instead of zeros
     spill: bool = False
     seed: int = 0
-    cell: str = "lstm"                # "lstm" (4 gate blocks) or "rnn" (Elman, 1 block)
+    cell: str = "lstm"                # "lstm" (4 gate blocks), "gru" (3) or "rnn" (Elman, 1)
     extra: dict = field(default_factory=dict)
 
     def with_(self, **kw) -> "Workload":
@@ -45,7 +45,12 @@ class Workload:
 
     @property
     def gates(self) -> int:
-        return 4 if self.cell == "lstm" else 1
+        return {"lstm": 4, "gru": 3, "rnn": 1}[self.cell]
+
+    @property
+    def bias_len(self) -> int:
+        """Bias entries per layer: G*H, and the GRU's extra b_hn block."""
+        return (4 if self.cell == "gru" else self.gates) * self.H
 
 
 # The five workloads.  Seeds are 1000 + index.
@@ -68,7 +73,12 @@ RNN_VAR_H1024 = Workload("rnn_b128_h1024_tmax200_varlen_bf16", B=128, I=1024, H=
                          T_max=200, dtype="bf16", len_lo=20, len_hi=200, cell="rnn",
                          seed=1006)
 
-ALL = (TINY, FIXED_H512, VAR_H1024, LONG_SPILL, TWO_LAYER, RNN_VAR_H1024)
+# ... and with the GRU body.
+GRU_VAR_H1024 = Workload("gru_b128_h1024_tmax200_varlen_bf16", B=128, I=1024, H=1024,
+                         T_max=200, dtype="bf16", len_lo=20, len_hi=200, cell="gru",
+                         seed=1007)
+
+ALL = (TINY, FIXED_H512, VAR_H1024, LONG_SPILL, TWO_LAYER, RNN_VAR_H1024, GRU_VAR_H1024)
 BY_NAME = {w.name: w for w in ALL}
 
 
@@ -89,7 +99,7 @@ def generate(w: Workload, seed: Optional[int] = None, nan_padding: bool = False)
     """Draw the inputs of workload ``w``.
 
     Returns a dict of float32 / int32 numpy arrays:
-      seq_len [B] int32, x [T_max,B,I], W [layers][I_l+H,4H], bias [layers][4H],
+      seq_len [B] int32, x [T_max,B,I], W [layers][I_l+H,G*H], bias [layers][bias_len],
       dy [T_max,B,H] or None, h0/c0 [layers,B,H], dhT [layers,B,H] (ones on
       the top layer), dcT [layers,B,H] (zeros).
     With ``nan_padding`` the x entries at t >= seq_len[b] are NaN.
@@ -106,7 +116,7 @@ def generate(w: Workload, seed: Optional[int] = None, nan_padding: bool = False)
     for l in range(w.layers):
         in_w = I if l == 0 else H
         Ws.append(rng.uniform(-s, s, size=(in_w + H, G * H)).astype(np.float32))
-        biases.append(rng.uniform(-s, s, size=(G * H,)).astype(np.float32))
+        biases.append(rng.uniform(-s, s, size=(w.bias_len,)).astype(np.float32))
     dy = rng.standard_normal((T, B, H), dtype=np.float32) if w.with_dy else None
     if w.random_state:
         h0 = (0.5 * rng.standard_normal((w.layers, B, H))).astype(np.float32)
@@ -129,9 +139,9 @@ def generate(w: Workload, seed: Optional[int] = None, nan_padding: bool = False)
 
 def algorithmic_flops(w: Workload, seq_len: np.ndarray) -> float:
     """Forward + backward flops the method needs: 6*G*H*(I_l+H) per valid
-    (timestep, sequence) per layer (G = 4 gate blocks for the LSTM, 1 for
-    the RNN: one product forward, three backward); masked steps and padding
-    excluded."""
+    (timestep, sequence) per layer (G = 4 gate blocks for the LSTM, 3 for
+    the GRU, 1 for the RNN: one product forward, three backward); masked
+    steps and padding excluded."""
     n = float(np.asarray(seq_len, dtype=np.int64).sum())
     tot = 0.0
     for l in range(w.layers):

@@ -16,16 +16,19 @@ def say(msg):
 
 def oracle_reference(inp, layers, dtype, cell="lstm"):
     """fp64 oracle (bf16-emulating for bf16 workloads) of the full fwd + bwd.
-    For the RNN cell, cT and dc0 are zeros (the library writes zeros there)."""
+    For the RNN and GRU cells, cT and dc0 are zeros (the library writes zeros
+    there)."""
     precision = "bf16" if dtype == "bf16" else "fp64"
-    if cell == "rnn":
+    if cell in ("rnn", "gru"):
+        fwd, bwd = ((oracle.stacked_rnn_forward, oracle.stacked_rnn_backward) if cell == "rnn"
+                    else (oracle.stacked_gru_forward, oracle.stacked_gru_backward))
         x = inp["x"].astype(np.float64)
         Ws = [w.astype(np.float64) for w in inp["W"]]
         bs = [b.astype(np.float64) for b in inp["bias"]]
         h0 = inp["h0"].astype(np.float64)
         dy = None if inp["dy"] is None else inp["dy"].astype(np.float64)
-        y, hT, tapes = oracle.stacked_rnn_forward(x, inp["seq_len"], Ws, bs, h0, precision)
-        g = oracle.stacked_rnn_backward(tapes, dy, inp["dhT"].astype(np.float64))
+        y, hT, tapes = fwd(x, inp["seq_len"], Ws, bs, h0, precision)
+        g = bwd(tapes, dy, inp["dhT"].astype(np.float64))
         return dict(y=y, hT=hT, cT=np.zeros_like(hT), dx=g["dx"], dW=g["dW"], dbias=g["dbias"],
                     dh0=g["dh0"], dc0=np.zeros_like(hT), T_eff=tapes[0]["T_eff"])
     x = inp["x"].astype(np.float64)

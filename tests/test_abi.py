@@ -55,8 +55,11 @@ def test_version_string():
     (dict(B=0), ll.LL_EINVAL),
     (dict(layers=3), ll.LL_EINVAL),
     (dict(dtype=7), ll.LL_EINVAL),
-    (dict(cell=2), ll.LL_EINVAL),
+    (dict(cell=3), ll.LL_EINVAL),
+    (dict(cell=-1), ll.LL_EINVAL),
     (dict(cell=1, spill=1), ll.LL_EUNSUPPORTED),
+    (dict(cell=2, spill=1), ll.LL_EUNSUPPORTED),
+    (dict(cell=2, recompute=1), ll.LL_EUNSUPPORTED),
     (dict(spill=2), ll.LL_EINVAL),
     (dict(recompute=2), ll.LL_EINVAL),
     (dict(recompute=1, spill=1), ll.LL_EUNSUPPORTED),

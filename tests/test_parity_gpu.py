@@ -574,3 +574,43 @@ def test_rnn_cell_parity(w):
     errs, bad = compare(res, ref, TOL[w.dtype])
     say(f"    errors {errs}")
     assert not bad, bad
+
+
+GRU_CASES = [
+    W("gru_f32_b20_i24_h64_t30", B=20, I=24, H=64, T_max=30, dtype="f32", len_lo=0, len_hi=30,
+      w_scale=0.3, random_state=True, cell="gru", seed=51),
+    W("gru_bf16_b40_i32_h128_t37", B=40, I=32, H=128, T_max=37, dtype="bf16", len_lo=1, len_hi=37,
+      random_state=True, cell="gru", seed=52),
+    W("gru_bf16_b130_i64_h256_t21", B=130, I=64, H=256, T_max=21, dtype="bf16", len_lo=0,
+      len_hi=21, random_state=True, cell="gru", seed=53),
+    W("gru_f32_2layer_b17_i16_h32_t29", B=17, I=16, H=32, T_max=29, dtype="f32", layers=2,
+      len_lo=0, len_hi=29, w_scale=0.3, random_state=True, cell="gru", seed=54),
+    W("gru_f32_b33_i20_h512_t9", B=33, I=20, H=512, T_max=9, dtype="f32", len_lo=0, len_hi=9,
+      random_state=True, cell="gru", seed=55),
+    W("gru_bf16_b9_i8_h1024_t12", B=9, I=8, H=1024, T_max=12, dtype="bf16", len_lo=0, len_hi=12,
+      random_state=True, cell="gru", seed=56),
+]
+
+
+@pytest.mark.parametrize("w", GRU_CASES, ids=[w.name for w in GRU_CASES])
+def test_gru_cell_parity(w):
+    """The loop engine with the GRU body (three gate blocks; the candidate
+    block's two sides differ in the gradient): every output within the
+    tolerance of the GRU oracle; cT and dc0 are written as zeros."""
+    say(f"[gru] {w.name}")
+    inp = wl.generate(w)
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell="gru")
+    plan = dc.plan()
+    geom = plan.geometry()
+    assert geom["xcd_local"], geom
+    dc.fwd(plan)
+    dc.bwd(plan)
+    err = plan.status_sync()
+    res = dc.results()
+    plan.close()
+    assert err == 0
+    ref = oracle_reference(inp, w.layers, w.dtype, cell="gru")
+    assert res["T_eff"] == ref["T_eff"] == int(inp["seq_len"].max())
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
