@@ -9,9 +9,13 @@ from .rnn import (rnn_forward_literal, rnn_forward, rnn_backward,
                   stacked_rnn_forward, stacked_rnn_backward)
 from .gru import (gru_forward_literal, gru_forward, gru_backward,
                   stacked_gru_forward, stacked_gru_backward)
+from .skip import (skip_forward_literal, skip_forward, skip_backward,
+                   stacked_skip_forward, stacked_skip_backward)
 
 __all__ = ["bf16_round", "sigmoid", "lstm_forward_literal", "lstm_forward",
            "lstm_backward", "stacked_forward", "stacked_backward",
            "matmul_chain_grad", "rnn_forward_literal", "rnn_forward", "rnn_backward",
            "stacked_rnn_forward", "stacked_rnn_backward", "gru_forward_literal",
-           "gru_forward", "gru_backward", "stacked_gru_forward", "stacked_gru_backward"]
+           "gru_forward", "gru_backward", "stacked_gru_forward", "stacked_gru_backward",
+           "skip_forward_literal", "skip_forward", "skip_backward", "stacked_skip_forward",
+           "stacked_skip_backward"]
