@@ -80,11 +80,21 @@ typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
  *     r = sigmoid(zx_r + zh_r),  u = sigmoid(zx_u + zh_u)
  *     n = tanh(zx_n + r * (zh_n + b_hn)),  h_t = (1 - u) n + u h_{t-1}
  * state h; dbias [4H] = [db_x, db_hn].  For both one-state cells c0, cT,
- * dcT and dc0 are ignored (cT and dc0, if given, are written as zeros).  The
- * loop construct, masking, stack and gradient loop are the same for every
- * body: the paper's while-loop and its gradient (Sections 3 and 5) do not
- * depend on it. */
-typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1, LL_CELL_GRU = 2 } ll_cell;
+ * dcT and dc0 are ignored (cT and dc0, if given, are written as zeros).
+ * LL_CELL_LSTM_SKIP: the LSTM body holding a data-dependent conditional
+ * (Section 2.1, cond(pred, true_fn, false_fn)), decided per row and step:
+ *     s = (x_t . w_px + h_{t-1} . w_ph) + b_p     (float32 sums of operands)
+ *     (h_t, c_t) = s > 0 ? LSTM step : (h_{t-1}, c_{t-1})
+ * and y_t = h_t at every valid step.  W is the LSTM's [I_l + H, 4H]; bias
+ * [4H + I_l + H + 1] = [b (4H), w_px (I_l), w_ph (H), b_p] (w_p rounded to
+ * the operand type like W).  The forward pushes every guard value onto the
+ * stack and the gradient loop pops it to run the gradient of the branch
+ * taken (Section 5.1, conditionals nested in a loop): the LSTM step's, or
+ * the identity.  dbias has the bias's length, zero in the predicate part
+ * (a step function has no gradient).  The loop construct, masking, stack and
+ * gradient loop are the same for every body: the paper's while-loop and its
+ * gradient (Sections 3 and 5) do not depend on it. */
+typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1, LL_CELL_GRU = 2, LL_CELL_LSTM_SKIP = 3 } ll_cell;
 
 /* Device error word bits (ll_status_sync). */
 #define LL_DEVERR_SEQ_LEN 1      /* some seq_len[b] < 0 or > T_max          */
@@ -126,9 +136,11 @@ typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1, LL_CELL_GRU = 2 } ll_cell;
  *     XCD-local loops and spill = 0 (else LL_EUNSUPPORTED); the two layers
  *     then run one after the other.  The bias passed to lstm_loop_fwd is
  *     copied into the plan for the gradient pass.
- *   cell: an ll_cell.  LL_CELL_RNN and LL_CELL_GRU need the XCD-local
- *     loops, spill = 0 and recompute = 0 (else LL_EUNSUPPORTED); the RNN's
- *     stack holds h_t only, the GRU's r, u, n, zh_n + b_hn and h_{t-1}.
+ *   cell: an ll_cell.  LL_CELL_RNN, LL_CELL_GRU and LL_CELL_LSTM_SKIP need
+ *     the XCD-local loops, spill = 0 and recompute = 0 (else
+ *     LL_EUNSUPPORTED); the RNN's stack holds h_t only, the GRU's r, u, n,
+ *     zh_n + b_hn and h_{t-1}, the cond body's the LSTM's values and one
+ *     guard per (step, row).
  */
 typedef struct {
   int32_t T_max;

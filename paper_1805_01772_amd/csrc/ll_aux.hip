@@ -248,6 +248,28 @@ __global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict
   }
 }
 
+// out[r] = sum_k A[row(r)][k] * op(w[k]) for the compact rows r < meta[1]
+// (row(r) = rowmap[r], or r without a map; op = rounding to the operand
+// type): the input part of the cond body's predicate.  One wave per row;
+// fixed summation order (lane partials, then a butterfly over the wave).
+template <typename T>
+__global__ __launch_bounds__(256) void row_dot_kernel(const T* __restrict__ A, int lda,
+                                                      const int* __restrict__ rowmap,
+                                                      const int* __restrict__ meta,
+                                                      const float* __restrict__ w, int K,
+                                                      float* __restrict__ out) {
+  const int rows = meta[1];
+  const int lane = threadIdx.x & 63;
+  for (long r = blockIdx.x * 4L + (threadIdx.x >> 6); r < rows; r += gridDim.x * 4L) {
+    const T* a = A + (long)(rowmap ? rowmap[r] : r) * lda;
+    float p = 0.f;
+    for (int k = lane; k < K; k += 64) p += Op<T>::to_f32(a[k]) * Op<T>::to_f32(Op<T>::from_f32(w[k]));
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) p += __shfl_xor(p, m, 64);
+    if (lane == 0) out[r] = p;
+  }
+}
+
 // float -> operand type copy (used for bf16(h0) and similar small arrays).
 template <typename T>
 __global__ __launch_bounds__(256) void convert_kernel(const float* __restrict__ in, long n,
@@ -422,6 +444,20 @@ template hipError_t launch_gather_transpose<float>(const GatherTArgs&, int, hipS
 template hipError_t launch_gather_transpose<bf16_t>(const GatherTArgs&, int, hipStream_t);
 template hipError_t launch_h0_rows<float>(const float*, const int*, int, int, float*, hipStream_t);
 template hipError_t launch_h0_rows<bf16_t>(const float*, const int*, int, int, bf16_t*, hipStream_t);
+template <typename T>
+hipError_t launch_row_dot(const T* A, int lda, const int* rowmap, const int* meta, long cap, const float* w,
+                          int K, float* out, hipStream_t s) {
+  long blocks = (cap + 3) / 4;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(row_dot_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, A, lda, rowmap, meta, w, K,
+                     out);
+  return hipGetLastError();
+}
+template hipError_t launch_row_dot<float>(const float*, int, const int*, const int*, long, const float*, int,
+                                          float*, hipStream_t);
+template hipError_t launch_row_dot<bf16_t>(const bf16_t*, int, const int*, const int*, long, const float*, int,
+                                           float*, hipStream_t);
 template hipError_t launch_convert<float>(const float*, long, float*, hipStream_t);
 template hipError_t launch_convert<bf16_t>(const float*, long, bf16_t*, hipStream_t);
 

@@ -150,6 +150,12 @@ struct XLoopArgs {
   const float* dcT;
   float* db_part;         // backward: [8, GB H]
   const float* bhn;       // GRU, forward: the candidate block's recurrent bias [H]
+  // LSTM with a cond body: predicate s = (x_t . w_px + h_{t-1} . w_ph) + b_p
+  const float* wp;        // forward: w_ph [H] (float, rounded to the operand type)
+  const float* bp;        // forward: b_p (device scalar)
+  const float* sx;        // forward: x_t . w_px per compact row [cap]
+  float* guard;           // guard per compact row [cap] (1 = the LSTM step ran):
+                          // pushed by the forward, popped by the gradient
   float* dh0;
   float* dc0;
   unsigned* rank_ctr;     // [8], zero before the launch
@@ -251,9 +257,9 @@ struct XKernels {
   size_t lds_bwd;
 };
 
-// gates: 4 (LSTM) or 1 (Elman RNN)
+// gates: 4 (LSTM), 3 (GRU) or 1 (Elman RNN); skip: the LSTM body with a cond
 template <typename T>
-XKernels x_kernels(int hc, int mrt, int gates = 4);
+XKernels x_kernels(int hc, int mrt, int gates = 4, bool skip = false);
 hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd);
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s);
 // Two-layer wavefront: one launch runs both layers (a0 lower, a1 upper);
@@ -299,6 +305,11 @@ hipError_t launch_sum_slices_2d(const float* ws, int S, long stride, long rows, 
                                 long ldo, hipStream_t s);
 template <typename T>
 hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s);
+// out[r] = sum_k A[rowmap ? rowmap[r] : r][k] * op(w[k]) for r < meta[1]
+// (at most cap rows); the input part of the cond body's predicate.
+template <typename T>
+hipError_t launch_row_dot(const T* A, int lda, const int* rowmap, const int* meta, long cap, const float* w,
+                          int K, float* out, hipStream_t s);
 
 template <typename T>
 hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s);

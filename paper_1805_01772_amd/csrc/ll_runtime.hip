@@ -147,6 +147,11 @@ struct ll_plan {
   float* db_part = nullptr;
   float* ws = nullptr;
   long ws_floats = 0;
+  // LSTM body with a cond: the predicate's input part per compact row, and
+  // the guard stack of each layer ([layers][cap], 1 = the LSTM step ran)
+  bool skip = false;
+  float* sx = nullptr;
+  float* guards = nullptr;
   int64_t stack_device_bytes = 0;
   int64_t stack_host_bytes = 0;
   // saved forward
@@ -246,7 +251,7 @@ void free_plan_memory(ll_plan* p) {
                   p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT,
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
                   p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags,
-                  p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias};
+                  p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias, p->sx, p->guards};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -317,8 +322,10 @@ ll_status validate_desc(const ll_desc* d) {
   if (d->recompute != 0 && d->recompute != 1) return fail(LL_EINVAL, "recompute must be 0 or 1");
   if (d->recompute && d->spill)
     return fail(LL_EUNSUPPORTED, "recompute and spill are alternatives; choose one");
-  if (d->cell != LL_CELL_LSTM && d->cell != LL_CELL_RNN && d->cell != LL_CELL_GRU)
-    return fail(LL_EINVAL, "cell must be LL_CELL_LSTM, LL_CELL_RNN or LL_CELL_GRU (got %d)", d->cell);
+  if (d->cell != LL_CELL_LSTM && d->cell != LL_CELL_RNN && d->cell != LL_CELL_GRU &&
+      d->cell != LL_CELL_LSTM_SKIP)
+    return fail(LL_EINVAL, "cell must be LL_CELL_LSTM, LL_CELL_RNN, LL_CELL_GRU or LL_CELL_LSTM_SKIP (got %d)",
+                d->cell);
   if (d->cell != LL_CELL_LSTM && (d->spill || d->recompute))
     return fail(LL_EUNSUPPORTED, "spill and recompute are built for the LSTM cell only");
   if ((long)d->T_max * d->B > (1L << 30))
@@ -377,6 +384,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   p->bf16 = desc->dtype == LL_BF16;
   p->es = p->bf16 ? 2 : 4;
   p->G = desc->cell == LL_CELL_RNN ? 1 : desc->cell == LL_CELL_GRU ? 3 : 4;
+  p->skip = desc->cell == LL_CELL_LSTM_SKIP;
   p->GB = desc->cell == LL_CELL_GRU ? 4 : p->G;
   p->n_cu = prop.multiProcessorCount;
   p->cap = (long)desc->T_max * desc->B;
@@ -433,7 +441,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
       const int hc = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 0;
       const int mrt = ((B + 15) / 16 + 7) / 8;
       if (hc && mrt <= 16) {
-        ll::XKernels xk = p->bf16 ? ll::x_kernels<bf16_t>(hc, mrt, p->G) : ll::x_kernels<float>(hc, mrt, p->G);
+        ll::XKernels xk = p->bf16 ? ll::x_kernels<bf16_t>(hc, mrt, p->G, p->skip)
+                                  : ll::x_kernels<float>(hc, mrt, p->G, p->skip);
         if (xk.fwd && xk.bwd && xk.lds_fwd <= lds_limit && xk.lds_bwd <= lds_limit) {
           int of = 0, ob = 0;
           if (ll::x_setup(xk, &of, &ob) == hipSuccess && of >= 1 && ob >= 1) {
@@ -450,11 +459,11 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     }
   }
 
-  // The Elman RNN and GRU cells run on the XCD-local loops only.
-  if (p->G != 4 && !p->xmode) {
+  // The Elman RNN, GRU and cond-body cells run on the XCD-local loops only.
+  if ((p->G != 4 || p->skip) && !p->xmode) {
     delete p;
     return fail(LL_EUNSUPPORTED, "the %s cell needs the XCD-local loops (H = %d, B = %d do not fit them)",
-                p->G == 1 ? "RNN" : "GRU", H, B);
+                p->G == 1 ? "RNN" : p->G == 3 ? "GRU" : "cond-body LSTM", H, B);
   }
 
   // Chip-wide loops where one XCD cannot hold the recurrent weights (bf16
@@ -506,7 +515,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   // and P..2P-1 the upper one, so both layers' steps overlap in one launch.
   // LSTMLOOP_WAVEFRONT=off at plan creation runs the layers one after the
   // other.
-  if (L == 2 && p->G == 4 && p->xmode && !p->spill && !p->recompute && 2 * p->xP <= 32 && p->xhc <= 2) {
+  if (L == 2 && p->G == 4 && !p->skip && p->xmode && !p->spill && !p->recompute && 2 * p->xP <= 32 &&
+      p->xhc <= 2) {
     const char* wf = getenv("LSTMLOOP_WAVEFRONT");
     if (!(wf && strcmp(wf, "off") == 0)) {
       ll::XKernels xk2 = p->bf16 ? ll::x_kernels2<bf16_t>(p->xhc, p->xMRT)
@@ -615,6 +625,10 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     ALLOC(p->db_state, sizeof(float) * 8 * 32 * 512 * 4, "db state");
   }
   ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * p->GB * H, "db partials");
+  if (p->skip) {
+    ALLOC(p->sx, sizeof(float) * cap, "predicate input part");
+    ALLOC(p->guards, sizeof(float) * L * cap, "guard stack");
+  }
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
 #undef ALLOC
   if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess) {
@@ -891,6 +905,10 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     g.K = Il;
     g.splits = 1;
     LL_HIP(ll::launch_gemm_nt<T>(g, s));
+    // cond body: the input part of the predicate, x_t . w_px per compact row
+    if (p->skip)
+      LL_HIP(ll::launch_row_dot<T>(static_cast<const T*>(g.A), Il, g.a_rowmap, p->meta, p->cap, bias[l] + 4L * H,
+                                   Il, p->sx, s));
     tend(p, s, LL_STAGE_INPUT_PROJ, ev);
     if (p->xmode) {
       const int ring_ks = (int)((long)H * p->es / 64);
@@ -922,6 +940,12 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       xa.X = p->HH[l];
       xa.Zx = p->Zx;
       xa.bhn = p->G == 3 ? bias[l] + 3L * H : nullptr;
+      if (p->skip) {   // bias[l] = [b (4H), w_px (I_l), w_ph (H), b_p]
+        xa.wp = bias[l] + 4L * H + Il;
+        xa.bp = bias[l] + 4L * H + Il + H;
+        xa.sx = p->sx;
+        xa.guard = p->guards + (long)l * p->cap;
+      }
       xa.stack = save ? p->stack[l] : nullptr;
       xa.y = (l == L - 1) ? y : nullptr;
       xa.abort_flag = p->meta + 3;
@@ -1080,6 +1104,8 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   // db = sum of the row-group partials
   ev = tbeg(p, s, LL_STAGE_DW);
   LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, GBH, GBH, dbias[l], s));
+  // cond body: the predicate's parameters get no gradient (a step function)
+  if (p->skip) LL_HIP(ll::launch_zero_u32(reinterpret_cast<unsigned*>(dbias[l] + GBH), Il + H + 1, s));
   tend(p, s, LL_STAGE_DW, ev);
   ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
   // transposed operands of the dW products (reduction over compact rows)
@@ -1310,6 +1336,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       xa.X = p->DZ;
       xa.c0 = p->c0 && p->G == 4 ? p->c0 + (long)l * B * H : nullptr;
       xa.stack = p->stack[l];
+      xa.guard = p->skip ? p->guards + (long)l * p->cap : nullptr;
       if (l == L - 1) {
         xa.dy = dy;
         xa.dy_compact = 0;

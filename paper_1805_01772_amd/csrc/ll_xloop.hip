@@ -55,11 +55,16 @@ __host__ __device__ constexpr int xbwd_red_floats(int NCT) {
 
 // LDS of the forward kernel: weight k-steps not in registers, partial
 // products, metadata window, perm rows.
-size_t xfwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
+// (cond body: the waves' partial predicate sums and the h part of the
+// predicate weights, skip_floats more)
+size_t xfwd_lds(int KSW, int KSR, int NCT, int mrt_max, int skip_floats = 0) {
   const int KSL = KSW > KSR ? KSW - KSR : 0;
   return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)XNW * 4 * xfwd_is(NCT) * 4 +
-         (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4;
+         (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4 + (size_t)skip_floats * 4;
 }
+// floats of the cond body's LDS: XNW x 16 partial sums, the predicate's h
+// weights (H <= 32 KSW KPC, the forward's k-steps)
+constexpr int xfwd_skip_floats(int KSW, int KPC) { return XNW * 16 + 32 * KSW * KPC; }
 // LDS of the gradient kernel: weight k-steps not in registers, partial
 // products (reused for the db rows at the end), metadata window, perm rows,
 // and with DMA the dz tile (KSW k-steps of 1 KB per wave).
@@ -120,7 +125,13 @@ __device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp
 // replaces the hoisted input projection.
 // G: gate blocks of the cell (4: LSTM i, f, g, o; 1: Elman RNN, h = tanh(z);
 // 3: GRU r, u, n with the reset gate applied after the recurrent product).
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP, int G = 4>
+// SKIP (LSTM only): the body is cond(s > 0, LSTM step, keep the state) with
+// s = (x_t . w_px + h_{t-1} . w_ph) + b_p per row.  The x part comes
+// precomputed per compact row (a.sx); the h part is summed here from the
+// h_{t-1} chunks each wave already holds for the recurrent product (every
+// member of an XCD computes it identically, so all take the same branch);
+// the guard of every (step, row) is pushed for the gradient loop.
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP, int G = 4, bool SKIP = false>
 __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT / G;
@@ -162,6 +173,13 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCT * 64);   // [XNW][4][IS]
   int* win = reinterpret_cast<int*>(red + XNW * 4 * IS);               // [2][WIN+1]
   int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
+  float* sred = reinterpret_cast<float*>(sperm + MRT_MAX * 16);       // SKIP: [XNW][16]
+  float* wph = sred + XNW * 16;                                       // SKIP: [H]
+  static_assert(!(SKIP && (TOP || G != 4)), "the cond body is built on the single-layer LSTM loop");
+  if constexpr (SKIP) {   // operand-rounded h weights of the predicate (read after a barrier below)
+    for (int k = threadIdx.x; k < H; k += XNT) wph[k] = Op<T>::to_f32(Op<T>::from_f32(a.wp[k]));
+  }
+  const float bp = SKIP ? a.bp[0] : 0.f;
 
   // cell thread: 16 lanes take 16 consecutive units of one row, a wave four
   // rows (the four MFMA result elements of one lane group)
@@ -199,6 +217,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   // input projections of the cell thread's (row, unit), one step ahead (the
   // upper wavefront layer: its bias)
   float zf[MRT_MAX][G];
+  float sxf[MRT_MAX];   // SKIP: x part of the predicate, one step ahead
   if constexpr (TOP) {
 #pragma unroll
     for (int mt = 0; mt < MRT_MAX; ++mt)
@@ -212,6 +231,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
 #pragma unroll
       for (int g = 0; g < G; ++g)
         zf[mt][g] = (cellt && mt < a.MRT && r < A0) ? a.Zx[(long)(off0 + r) * G4 + (long)g * H + ju] : 0.f;
+      sxf[mt] = (SKIP && cellt && mt < a.MRT && r < A0) ? a.sx[off0 + r] : 0.f;
     }
   }
 
@@ -258,12 +278,17 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       float zc[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) zc[g] = zf[mt][g];
+      const float sxc = sxf[mt];
       if constexpr (!TOP) {  // input projections of step t+1 (rows past A_n read zeros)
         const int nr = max(0, min(16, A_n - r0));
         const __amdgpu_buffer_rsrc_t rz = make_rsrc(a.Zx + (long)(off_n + r0) * G4, (unsigned)(nr * G4 * 4));
         const unsigned zo = cellt ? (unsigned)((crow * G4 + ju) * 4) : kOOB;
 #pragma unroll
         for (int g = 0; g < G; ++g) zf[mt][g] = ld_f32(rz, zo + g * H * 4);
+        if constexpr (SKIP) {
+          const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.sx + off_n + r0, (unsigned)(nr * 4));
+          sxf[mt] = ld_f32(rx, cellt ? (unsigned)(crow * 4) : kOOB);
+        }
       }
       // 2. partial products over this wave's k-steps, column tiles in two
       //    halves, into red[wave][i][ct][lane] (the previous tile's cell has
@@ -292,6 +317,23 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
 #pragma unroll
           for (int i = 0; i < 4; ++i) red[(wave * 4 + i) * IS + (hf * NH + c) * 64 + lane] = acc[c][i];
       }
+      if constexpr (SKIP) {
+        // h part of the predicate over this wave's k-steps: lane l holds row
+        // l % 16, columns (ks * 4 + l / 16) * KPC .. + KPC of each k-step
+        float ps = 0.f;
+#pragma unroll
+        for (int i = 0; i < KSW; ++i) {
+          if (i < nks) {
+            const T* hv = reinterpret_cast<const T*>(&av[i]);
+            const float* wk = wph + ((ks0 + i) * 4 + q) * KPC;
+#pragma unroll
+            for (int e = 0; e < KPC; ++e) ps += Op<T>::to_f32(hv[e]) * wk[e];
+          }
+        }
+        ps += __shfl_xor(ps, 16, 64);
+        ps += __shfl_xor(ps, 32, 64);
+        if (q == 0) sred[wave * 16 + l16] = ps;
+      }
       __syncthreads();
       // the lower wavefront layer rewrites ring slot t % 2 only after the
       // upper layer has published step t - 2, its last read of that slot
@@ -301,6 +343,13 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       float ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cn = 0.f, hn = 0.f;
       const int r = r0 + crow;
       const bool act = cellt && r < A_t;
+      bool run = true;   // SKIP: the branch this row takes
+      if constexpr (SKIP) {
+        float sh = sred[crow];
+#pragma unroll
+        for (int w2 = 1; w2 < XNW; ++w2) sh += sred[w2 * 16 + crow];
+        run = (sxc + sh) + bp > 0.f;
+      }
       if (cellt) {
         float z[G], zh[G];
 #pragma unroll
@@ -319,6 +368,10 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
           og = sigmoidf_(z[3]);
           cn = fg * cs[mt] + ig * gg;
           hn = og * tanhf_(cn);
+          if (SKIP && !run) {   // the false branch keeps the state
+            cn = cs[mt];
+            hn = hs[mt];
+          }
         } else if constexpr (G == 3) {
           // GRU: r, u, n, zh_n + b_hn and h_{t-1} take the places of the
           // LSTM's i, f, g, o and c_t in the stack row
@@ -352,6 +405,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
             st[2 * gs] = gg;
             st[3 * gs] = og;
             st[a.scoff] = cn;
+            if (SKIP && rank == 0 && cu == 0) a.guard[cr] = run ? 1.f : 0.f;
           } else {
             st[a.scoff] = hn;   // the RNN's gradient needs only h_t
           }
@@ -377,7 +431,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   }
 }
 
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int G>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int G, bool SKIP>
 __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
@@ -391,7 +445,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  xfwd_body<T, NCT, KSW, KSR, MRT_MAX, false, G>(a, grp, rank, lds);
+  xfwd_body<T, NCT, KSW, KSR, MRT_MAX, false, G, SKIP>(a, grp, rank, lds);
 }
 
 // Two-layer wavefront, forward: members 0 .. P-1 of every XCD run the lower
@@ -434,7 +488,11 @@ __global__ __launch_bounds__(XNT, 1) void xfwd2_kernel(XLoopArgs a0, XLoopArgs a
 // (its dy comes from the upper layer's dyx ring, one step later); 2: the upper
 // layer, which also computes dy_{lower} = dz W_x^T for its units (NCO = 2 NCT
 // output column tiles: W_h rows, then W_x rows) and publishes it per step.
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE, bool DMA = false, int G = 4>
+// SKIP: the LSTM body with a cond (see xfwd_body); the popped guard picks
+// each row's branch gradient: the LSTM step's, or the identity (dz = 0,
+// dh_{t-1} = dh_tot, dc_{t-1} = dc_t).
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE, bool DMA = false, int G = 4,
+          bool SKIP = false>
 __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT;                 // units per work-group
@@ -456,7 +514,9 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   const int KS = (int)(G4 / (4 * KPC));
   // pops per (step, tile) and thread: LSTM i, f, g, o, c_t, c_{t-1}, dy;
   // GRU r, u, n, zh_n + b_hn, h_{t-1}, dy; RNN h_t, dy
-  constexpr int NPOP = G == 4 ? 7 : G == 3 ? 6 : 2;
+  constexpr int NPOP = (G == 4 ? 7 : G == 3 ? 6 : 2) + (SKIP ? 1 : 0);
+  constexpr int NPV = SKIP ? 8 : 7;   // popped values kept per (tile, thread); [7] = guard
+  static_assert(!(SKIP && (ROLE != 0 || G != 4)), "the cond body is built on the single-layer LSTM loop");
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
   const int nks = ks1 - ks0;                            // k-steps of this wave
   const T* W = reinterpret_cast<const T*>(a.W);
@@ -519,7 +579,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
 
   // pops of (step tt, tile mt) for this thread: i, f, g, o, c_t, c_{t-1}, dy;
   // zeros for rows not running at tt (every read is issued, out of range)
-  auto fetch = [&](float (&v)[7], int tt, int mt, int A, int off, int offp) {
+  auto fetch = [&](float (&v)[NPV], int tt, int mt, int A, int off, int offp) {
     const int r0 = (grp + 8 * mt) * 16;
     const int nr = tt >= 0 ? max(0, min(16, A - r0)) : 0;
     const bool ok = cellt && crow < nr;
@@ -559,6 +619,10 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
           make_rsrc(a.dy ? a.dy + (long)ts * B * H : nullptr, a.dy ? (unsigned)(B * H * 4) : 0u);
       v[6] = ld_f32(rd, ok ? (unsigned)((b * H + ju) * 4) : kOOB);
     }
+    if constexpr (SKIP) {
+      const __amdgpu_buffer_rsrc_t rgd = make_rsrc(a.guard + off + r0, (unsigned)(nr * 4));
+      v[NPV - 1] = ld_f32(rgd, ok ? (unsigned)(crow * 4) : kOOB);
+    }
     (void)offp;
   };
 
@@ -567,7 +631,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   // the window covers steps t-2 .. t+2 of every step t of the loop
   int wlo = t1 + 1 - WIN > 0 ? t1 + 1 - WIN : 0;
   load_window(a, win, wlo);
-  float pv[MRT_MAX][7];
+  float pv[MRT_MAX][NPV];
   {
     const int t = t1 - 1;
     const int A_t = t >= 0 ? win[t - wlo] : 0;
@@ -626,7 +690,12 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
           dz[1] = dct * cp * (fg * (1.f - fg));
           dz[2] = dct * ig * (1.f - gg * gg);
           dz[3] = d_o * (og * (1.f - og));
-          dc[mt] = dct * fg;
+          if (SKIP && pv[mt][NPV - 1] == 0.f) {   // the row kept its state at step t
+            dz[0] = dz[1] = dz[2] = dz[3] = 0.f;
+            dhu = dht;
+          } else {
+            dc[mt] = dct * fg;
+          }
         } else if constexpr (G == 3) {
           const float rg = pv[mt][0], ug = pv[mt][1], ng = pv[mt][2], hnv = pv[mt][3];
           const float hp = pv[mt][4];
@@ -722,7 +791,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
         float s = rp[0];
 #pragma unroll
         for (int w2 = 1; w2 < XNW; ++w2) s += rp[w2 * 4 * IS];
-        dh[mt] = G == 3 ? s + dhu : s;
+        dh[mt] = (G == 3 || SKIP) ? s + dhu : s;
       }
       if constexpr (ROLE == 2) {
         // dy of the lower layer's output at step t for the own units; the
@@ -768,7 +837,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   }
 }
 
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool DMA, int G>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool DMA, int G, bool SKIP>
 __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
@@ -782,7 +851,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, DMA, G>(a, grp, rank, lds);
+  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, DMA, G, SKIP>(a, grp, rank, lds);
 }
 
 // Two-layer wavefront, gradient: members 0 .. P-1 of every XCD run the lower
@@ -873,18 +942,18 @@ hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s) {
 // hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
 // row tiles per XCD.
 namespace {
-template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT, int G = 4>
+template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT, int G = 4, bool SKIP = false>
 XKernels x_make() {
   XKernels k{};
-  k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT, G>);
-  k.lds_fwd = xfwd_lds(HC, RF, NF, MRT);
+  k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT, G, SKIP>);
+  k.lds_fwd = xfwd_lds(HC, RF, NF, MRT, SKIP ? xfwd_skip_floats(HC, Op<T>::kPerChunk) : 0);
   // the gradient loop loads its dz k-steps straight into LDS when they fit
   const size_t dma_lds = xbwd_lds(G * HC, RB, NB, MRT, true);
   if (dma_lds <= 160 * 1024) {
-    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, true, G>);
+    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, true, G, SKIP>);
     k.lds_bwd = dma_lds;
   } else {
-    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, false, G>);
+    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, false, G, SKIP>);
     k.lds_bwd = xbwd_lds(G * HC, RB, NB, MRT);
   }
   return k;
@@ -900,12 +969,21 @@ XKernels x_make() {
 // 6 / 3, backward KSW = 3H/256 / 3H/128.)
 // hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
 template <typename T>
-XKernels x_kernels(int hc, int mrt, int gates) {
+XKernels x_kernels(int hc, int mrt, int gates, bool skip) {
   constexpr bool bf = sizeof(T) == 2;
   constexpr int NF = bf ? 8 : 4;
   constexpr int NB = bf ? 2 : 1;
   const bool one = mrt <= 1;
   if (mrt > 4) return XKernels{};
+  if (skip) {   // the LSTM tiling with the cond body
+    if (gates != 4) return XKernels{};
+    switch (hc) {
+      case 1: return one ? x_make<T, NF, NB, 1, 1, 4, 1, 4, true>() : x_make<T, NF, NB, 1, 1, 4, 4, 4, true>();
+      case 2: return one ? x_make<T, NF, NB, 2, 2, 8, 1, 4, true>() : x_make<T, NF, NB, 2, 2, 6, 4, 4, true>();
+      case 4: return one ? x_make<T, NF, NB, 4, 4, 16, 1, 4, true>() : x_make<T, NF, NB, 4, 3, 8, 4, 4, true>();
+      default: return XKernels{};
+    }
+  }
   if (gates == 1) {
     constexpr int NR = bf ? 2 : 1;
     switch (hc) {
@@ -933,8 +1011,8 @@ XKernels x_kernels(int hc, int mrt, int gates) {
   }
 }
 
-template XKernels x_kernels<float>(int, int, int);
-template XKernels x_kernels<bf16_t>(int, int, int);
+template XKernels x_kernels<float>(int, int, int, bool);
+template XKernels x_kernels<bf16_t>(int, int, int, bool);
 
 // Two-layer wavefront kernels: the lower layer as in x_kernels, the upper one
 // with twice the forward k-steps (K = I_l + H = 2H) and, in the gradient, twice

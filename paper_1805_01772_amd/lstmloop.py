@@ -18,7 +18,7 @@ LL_OK, LL_EINVAL, LL_ENOMEM, LL_EHIP, LL_ESTATE, LL_EUNSUPPORTED = range(6)
 LL_F32, LL_BF16 = 0, 1
 LL_DEVERR_SEQ_LEN, LL_DEVERR_BARRIER = 1, 2
 LL_LOOPS_GRID, LL_LOOPS_XCD, LL_LOOPS_CHIP = 0, 1, 2
-LL_CELL_LSTM, LL_CELL_RNN, LL_CELL_GRU = 0, 1, 2
+LL_CELL_LSTM, LL_CELL_RNN, LL_CELL_GRU, LL_CELL_LSTM_SKIP = 0, 1, 2, 3
 STATUS_NAMES = {0: "LL_OK", 1: "LL_EINVAL", 2: "LL_ENOMEM", 3: "LL_EHIP",
                 4: "LL_ESTATE", 5: "LL_EUNSUPPORTED"}
 

@@ -12,7 +12,7 @@ from typing import Optional
 import numpy as np
 import torch
 
-from .lstmloop import LL_CELL_GRU, LL_CELL_LSTM, LL_CELL_RNN, Plan
+from .lstmloop import LL_CELL_GRU, LL_CELL_LSTM, LL_CELL_LSTM_SKIP, LL_CELL_RNN, Plan
 
 
 class DeviceCase:
@@ -52,7 +52,8 @@ class DeviceCase:
         self.dc0 = z(L, B, H)
 
     def plan(self, **kw) -> Plan:
-        cell = {"lstm": LL_CELL_LSTM, "rnn": LL_CELL_RNN, "gru": LL_CELL_GRU}[self.cell]
+        cell = {"lstm": LL_CELL_LSTM, "rnn": LL_CELL_RNN, "gru": LL_CELL_GRU,
+                "skip": LL_CELL_LSTM_SKIP}[self.cell]
         return Plan(self.T, self.B, self.I, self.H, layers=self.L, dtype=self.dtype, cell=cell, **kw)
 
     def fwd(self, plan: Plan, save: bool = True, use_h0: bool = True) -> None:

@@ -37,7 +37,8 @@ class Workload:
     random_state: bool = False        # h0, c0 ~ N(0, 0.5^2) instead of zeros
     spill: bool = False
     seed: int = 0
-    cell: str = "lstm"                # "lstm" (4 gate blocks), "gru" (3) or "rnn" (Elman, 1)
+    cell: str = "lstm"                # "lstm" (4 gate blocks), "gru" (3), "rnn" (Elman, 1),
+                                      # "skip" (the LSTM body with a cond)
     extra: dict = field(default_factory=dict)
 
     def with_(self, **kw) -> "Workload":
@@ -45,12 +46,16 @@ class Workload:
 
     @property
     def gates(self) -> int:
-        return {"lstm": 4, "gru": 3, "rnn": 1}[self.cell]
+        return {"lstm": 4, "gru": 3, "rnn": 1, "skip": 4}[self.cell]
 
-    @property
-    def bias_len(self) -> int:
-        """Bias entries per layer: G*H, and the GRU's extra b_hn block."""
-        return (4 if self.cell == "gru" else self.gates) * self.H
+    def bias_len(self, layer: int = 0) -> int:
+        """Bias entries of a layer: G*H, the GRU's extra b_hn block, the cond
+        body's predicate weights over [x_t, h_{t-1}] and its offset."""
+        if self.cell == "gru":
+            return 4 * self.H
+        if self.cell == "skip":
+            return 4 * self.H + (self.I if layer == 0 else self.H) + self.H + 1
+        return self.gates * self.H
 
 
 # The five workloads.  Seeds are 1000 + index.
@@ -99,7 +104,7 @@ def generate(w: Workload, seed: Optional[int] = None, nan_padding: bool = False)
     """Draw the inputs of workload ``w``.
 
     Returns a dict of float32 / int32 numpy arrays:
-      seq_len [B] int32, x [T_max,B,I], W [layers][I_l+H,G*H], bias [layers][bias_len],
+      seq_len [B] int32, x [T_max,B,I], W [layers][I_l+H,G*H], bias [layers][bias_len(l)],
       dy [T_max,B,H] or None, h0/c0 [layers,B,H], dhT [layers,B,H] (ones on
       the top layer), dcT [layers,B,H] (zeros).
     With ``nan_padding`` the x entries at t >= seq_len[b] are NaN.
@@ -116,7 +121,7 @@ def generate(w: Workload, seed: Optional[int] = None, nan_padding: bool = False)
     for l in range(w.layers):
         in_w = I if l == 0 else H
         Ws.append(rng.uniform(-s, s, size=(in_w + H, G * H)).astype(np.float32))
-        biases.append(rng.uniform(-s, s, size=(w.bias_len,)).astype(np.float32))
+        biases.append(rng.uniform(-s, s, size=(w.bias_len(l),)).astype(np.float32))
     dy = rng.standard_normal((T, B, H), dtype=np.float32) if w.with_dy else None
     if w.random_state:
         h0 = (0.5 * rng.standard_normal((w.layers, B, H))).astype(np.float32)

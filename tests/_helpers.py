@@ -37,11 +37,16 @@ def oracle_reference(inp, layers, dtype, cell="lstm"):
     h0 = inp["h0"].astype(np.float64)
     c0 = inp["c0"].astype(np.float64)
     dy = None if inp["dy"] is None else inp["dy"].astype(np.float64)
-    y, hT, cT, tapes = oracle.stacked_forward(x, inp["seq_len"], Ws, bs, h0, c0, precision)
-    g = oracle.stacked_backward(tapes, dy, inp["dhT"].astype(np.float64),
-                                inp["dcT"].astype(np.float64))
-    return dict(y=y, hT=hT, cT=cT, dx=g["dx"], dW=g["dW"], dbias=g["dbias"],
-                dh0=g["dh0"], dc0=g["dc0"], T_eff=tapes[0]["T_eff"])
+    fwd, bwd = ((oracle.stacked_skip_forward, oracle.stacked_skip_backward) if cell == "skip"
+                else (oracle.stacked_forward, oracle.stacked_backward))
+    y, hT, cT, tapes = fwd(x, inp["seq_len"], Ws, bs, h0, c0, precision)
+    g = bwd(tapes, dy, inp["dhT"].astype(np.float64), inp["dcT"].astype(np.float64))
+    out = dict(y=y, hT=hT, cT=cT, dx=g["dx"], dW=g["dW"], dbias=g["dbias"],
+               dh0=g["dh0"], dc0=g["dc0"], T_eff=tapes[0]["T_eff"])
+    if cell == "skip":
+        out["guards"] = [t["guards"] for t in tapes]
+        out["min_margin"] = min(t["min_margin"] for t in tapes)
+    return out
 
 
 def rel_err(got, ref):

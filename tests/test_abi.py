@@ -55,7 +55,9 @@ def test_version_string():
     (dict(B=0), ll.LL_EINVAL),
     (dict(layers=3), ll.LL_EINVAL),
     (dict(dtype=7), ll.LL_EINVAL),
-    (dict(cell=3), ll.LL_EINVAL),
+    (dict(cell=4), ll.LL_EINVAL),
+    (dict(cell=3, spill=1), ll.LL_EUNSUPPORTED),
+    (dict(cell=3, recompute=1), ll.LL_EUNSUPPORTED),
     (dict(cell=-1), ll.LL_EINVAL),
     (dict(cell=1, spill=1), ll.LL_EUNSUPPORTED),
     (dict(cell=2, spill=1), ll.LL_EUNSUPPORTED),

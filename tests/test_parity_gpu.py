@@ -614,3 +614,55 @@ def test_gru_cell_parity(w):
     errs, bad = compare(res, ref, TOL[w.dtype])
     say(f"    errors {errs}")
     assert not bad, bad
+
+
+# The LSTM body with a data-dependent cond.  The predicate is an integer
+# decided by floating point on both sides (float32 sums in different orders,
+# and the bf16 runs' trajectories differ within the tolerance), so every case
+# uses a seed whose decisions all sit at least MARGIN from the threshold in
+# the oracle; both branches occur in each.
+SKIP_CASES = [
+    (W("skip_f32_b20_i24_h64_t30", B=20, I=24, H=64, T_max=30, dtype="f32", len_lo=0, len_hi=30,
+       w_scale=0.3, random_state=True, cell="skip", seed=89), 1e-3),
+    (W("skip_bf16_b40_i32_h128_t37", B=40, I=32, H=128, T_max=37, dtype="bf16", len_lo=1, len_hi=37,
+       random_state=True, cell="skip", seed=86), 5e-4),
+    (W("skip_bf16_b130_i64_h256_t21", B=130, I=64, H=256, T_max=21, dtype="bf16", len_lo=0,
+       len_hi=21, random_state=True, cell="skip", seed=89), 5e-4),
+    (W("skip_f32_2layer_b17_i16_h32_t29", B=17, I=16, H=32, T_max=29, dtype="f32", layers=2,
+       len_lo=0, len_hi=29, w_scale=0.3, random_state=True, cell="skip", seed=98), 1e-3),
+    (W("skip_f32_b33_i20_h512_t9", B=33, I=20, H=512, T_max=9, dtype="f32", len_lo=0, len_hi=9,
+       random_state=True, cell="skip", seed=81), 1e-3),
+    (W("skip_bf16_b9_i8_h1024_t12", B=9, I=8, H=1024, T_max=12, dtype="bf16", len_lo=0, len_hi=12,
+       random_state=True, cell="skip", seed=87), 5e-4),
+]
+
+
+@pytest.mark.parametrize("w,margin", SKIP_CASES, ids=[c[0].name for c in SKIP_CASES])
+def test_skip_cell_parity(w, margin):
+    """The loop engine with the cond body: guards pushed in the forward and
+    popped in the gradient loop; every output within the tolerance of the
+    cond-body oracle, dbias zero in the predicate part."""
+    say(f"[skip] {w.name}")
+    inp = wl.generate(w)
+    ref = oracle_reference(inp, w.layers, w.dtype, cell="skip")
+    assert ref["min_margin"] > margin, "ill-conditioned case: a decision sits at the threshold"
+    for l, gd in enumerate(ref["guards"]):
+        valid = np.arange(w.T_max)[:, None] < inp["seq_len"][None, :]
+        assert gd[valid].any() and not gd[valid].all(), f"layer {l}: one branch only"
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell="skip")
+    plan = dc.plan()
+    geom = plan.geometry()
+    assert geom["xcd_local"], geom
+    dc.fwd(plan)
+    dc.bwd(plan)
+    err = plan.status_sync()
+    res = dc.results()
+    plan.close()
+    assert err == 0
+    assert res["T_eff"] == ref["T_eff"] == int(inp["seq_len"].max())
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
+    for l in range(w.layers):
+        I_l = w.I if l == 0 else w.H
+        assert not res["dbias"][l][4 * w.H:].any() and res["dbias"][l].shape[0] == 4 * w.H + I_l + w.H + 1
