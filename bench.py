@@ -81,10 +81,11 @@ def cpu_baseline(w, inp, target_s):
             _, _, tapes = fwd(x, sl, Ws, bs, inp["h0"].astype(np.float64), precision)
             bwd(tapes, dy, inp["dhT"].astype(np.float64))
         else:
-            y, hT, cT, tapes = oracle.stacked_forward(x, sl, Ws, bs, inp["h0"].astype(np.float64),
-                                                      inp["c0"].astype(np.float64), precision)
-            oracle.stacked_backward(tapes, dy, inp["dhT"].astype(np.float64),
-                                    inp["dcT"].astype(np.float64))
+            fwd, bwd = ((oracle.stacked_skip_forward, oracle.stacked_skip_backward) if w.cell == "skip"
+                        else (oracle.stacked_forward, oracle.stacked_backward))
+            y, hT, cT, tapes = fwd(x, sl, Ws, bs, inp["h0"].astype(np.float64),
+                                   inp["c0"].astype(np.float64), precision)
+            bwd(tapes, dy, inp["dhT"].astype(np.float64), inp["dcT"].astype(np.float64))
         return time.perf_counter() - t0, int(sl.sum())
 
     T_eff = int(inp["seq_len"].max())

@@ -55,16 +55,14 @@ __host__ __device__ constexpr int xbwd_red_floats(int NCT) {
 
 // LDS of the forward kernel: weight k-steps not in registers, partial
 // products, metadata window, perm rows.
-// (cond body: the waves' partial predicate sums and the h part of the
-// predicate weights, skip_floats more)
+// (cond body: the waves' partial predicate sums, skip_floats more)
 size_t xfwd_lds(int KSW, int KSR, int NCT, int mrt_max, int skip_floats = 0) {
   const int KSL = KSW > KSR ? KSW - KSR : 0;
   return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)XNW * 4 * xfwd_is(NCT) * 4 +
          (size_t)2 * (WIN + 1) * 4 + (size_t)mrt_max * 16 * 4 + (size_t)skip_floats * 4;
 }
-// floats of the cond body's LDS: XNW x 16 partial sums, the predicate's h
-// weights (H <= 32 KSW KPC, the forward's k-steps)
-constexpr int xfwd_skip_floats(int KSW, int KPC) { return XNW * 16 + 32 * KSW * KPC; }
+// floats of the cond body's LDS: XNW x 16 partial sums
+constexpr int xfwd_skip_floats() { return XNW * 16; }
 // LDS of the gradient kernel: weight k-steps not in registers, partial
 // products (reused for the db rows at the end), metadata window, perm rows,
 // and with DMA the dz tile (KSW k-steps of 1 KB per wave).
@@ -127,10 +125,11 @@ __device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp
 // 3: GRU r, u, n with the reset gate applied after the recurrent product).
 // SKIP (LSTM only): the body is cond(s > 0, LSTM step, keep the state) with
 // s = (x_t . w_px + h_{t-1} . w_ph) + b_p per row.  The x part comes
-// precomputed per compact row (a.sx); the h part is summed here from the
-// h_{t-1} chunks each wave already holds for the recurrent product (every
-// member of an XCD computes it identically, so all take the same branch);
-// the guard of every (step, row) is pushed for the gradient loop.
+// precomputed per compact row (a.sx); the h part is one more matrix-core
+// column of the recurrent product (w_ph as column 0 of an extra 16-column
+// tile, over the h_{t-1} chunks each wave already holds; every member of an
+// XCD computes it identically, so all take the same branch); the guard of
+// every (step, row) is pushed for the gradient loop.
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP, int G = 4, bool SKIP = false>
 __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
@@ -174,10 +173,20 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   int* win = reinterpret_cast<int*>(red + XNW * 4 * IS);               // [2][WIN+1]
   int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
   float* sred = reinterpret_cast<float*>(sperm + MRT_MAX * 16);       // SKIP: [XNW][16]
-  float* wph = sred + XNW * 16;                                       // SKIP: [H]
   static_assert(!(SKIP && (TOP || G != 4)), "the cond body is built on the single-layer LSTM loop");
-  if constexpr (SKIP) {   // operand-rounded h weights of the predicate (read after a barrier below)
-    for (int k = threadIdx.x; k < H; k += XNT) wph[k] = Op<T>::to_f32(Op<T>::from_f32(a.wp[k]));
+  // SKIP: the predicate's h weights as the B operand of a 16-column tile
+  // whose column 0 is w_ph (operand-rounded) and the rest zero
+  uint4 wpr[SKIP ? KSW : 1];
+  if constexpr (SKIP) {
+#pragma unroll
+    for (int i = 0; i < KSW; ++i) {
+      const int ks = ks0 + i;
+      alignas(16) T v[KPC];
+#pragma unroll
+      for (int e = 0; e < KPC; ++e)
+        v[e] = Op<T>::from_f32(l16 == 0 && ks < ks1 ? a.wp[(ks * 4 + q) * KPC + e] : 0.f);
+      wpr[i] = *reinterpret_cast<const uint4*>(v);
+    }
   }
   const float bp = SKIP ? a.bp[0] : 0.f;
 
@@ -318,21 +327,16 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
           for (int i = 0; i < 4; ++i) red[(wave * 4 + i) * IS + (hf * NH + c) * 64 + lane] = acc[c][i];
       }
       if constexpr (SKIP) {
-        // h part of the predicate over this wave's k-steps: lane l holds row
-        // l % 16, columns (ks * 4 + l / 16) * KPC .. + KPC of each k-step
-        float ps = 0.f;
+        // h part of the predicate over this wave's k-steps: column 0 of the
+        // extra tile; result element i of lane 16 q is row 4 q + i
+        f32x4 accp = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int i = 0; i < KSW; ++i) {
-          if (i < nks) {
-            const T* hv = reinterpret_cast<const T*>(&av[i]);
-            const float* wk = wph + ((ks0 + i) * 4 + q) * KPC;
+        for (int i = 0; i < KSW; ++i)
+          if (i < nks) accp = Mfma<T>::step(av[i], wpr[i], accp);
+        if (l16 == 0) {
 #pragma unroll
-            for (int e = 0; e < KPC; ++e) ps += Op<T>::to_f32(hv[e]) * wk[e];
-          }
+          for (int i = 0; i < 4; ++i) sred[wave * 16 + q * 4 + i] = accp[i];
         }
-        ps += __shfl_xor(ps, 16, 64);
-        ps += __shfl_xor(ps, 32, 64);
-        if (q == 0) sred[wave * 16 + l16] = ps;
       }
       __syncthreads();
       // the lower wavefront layer rewrites ring slot t % 2 only after the
@@ -946,7 +950,7 @@ template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT, int G = 4
 XKernels x_make() {
   XKernels k{};
   k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT, G, SKIP>);
-  k.lds_fwd = xfwd_lds(HC, RF, NF, MRT, SKIP ? xfwd_skip_floats(HC, Op<T>::kPerChunk) : 0);
+  k.lds_fwd = xfwd_lds(HC, RF, NF, MRT, SKIP ? xfwd_skip_floats() : 0);
   // the gradient loop loads its dz k-steps straight into LDS when they fit
   const size_t dma_lds = xbwd_lds(G * HC, RB, NB, MRT, true);
   if (dma_lds <= 160 * 1024) {

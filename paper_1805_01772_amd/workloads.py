@@ -83,7 +83,14 @@ GRU_VAR_H1024 = Workload("gru_b128_h1024_tmax200_varlen_bf16", B=128, I=1024, H=
                          T_max=200, dtype="bf16", len_lo=20, len_hi=200, cell="gru",
                          seed=1007)
 
-ALL = (TINY, FIXED_H512, VAR_H1024, LONG_SPILL, TWO_LAYER, RNN_VAR_H1024, GRU_VAR_H1024)
+# ... and with the LSTM body holding a data-dependent cond (a row runs the
+# step or keeps its state; the predicate weights are drawn with the bias).
+SKIP_VAR_H1024 = Workload("skip_b128_h1024_tmax200_varlen_bf16", B=128, I=1024, H=1024,
+                          T_max=200, dtype="bf16", len_lo=20, len_hi=200, cell="skip",
+                          seed=1008)
+
+ALL = (TINY, FIXED_H512, VAR_H1024, LONG_SPILL, TWO_LAYER, RNN_VAR_H1024, GRU_VAR_H1024,
+       SKIP_VAR_H1024)
 BY_NAME = {w.name: w for w in ALL}
 
 
