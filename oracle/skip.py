@@ -128,7 +128,7 @@ def skip_forward(x, seq_len, W, bias, h0=None, c0=None, precision="fp64"):
     c = np.zeros((B, H), dt) if c0 is None else np.array(c0, dt)
     y = np.zeros((T_max, B, H), dt)
     guards = np.zeros((T_max, B), np.int8)
-    margins = []
+    margin = np.full((T_max, B), np.inf)       # |s| of every valid decision
     T_eff = int(seq_len.max()) if B else 0
     stack = []
     t = 0
@@ -144,11 +144,10 @@ def skip_forward(x, seq_len, W, bias, h0=None, c0=None, precision="fp64"):
         h = np.where(guard[:, None], h_new, h)
         y[t] = np.where(valid[:, None], h, 0.0)
         guards[t] = guard
-        margins.append(np.abs(s[valid]))
+        margin[t] = np.where(valid, np.abs(s), np.inf)
         t += 1
     tape = dict(stack=stack, T_eff=T_eff, x=x, W=W, precision=precision, I=I, H=H,
-                guards=guards,
-                min_margin=float(min((m.min() for m in margins if m.size), default=np.inf)))
+                guards=guards, margin=margin, min_margin=float(margin.min()) if margin.size else np.inf)
     return y, h, c, tape
 
 

@@ -45,6 +45,7 @@ def oracle_reference(inp, layers, dtype, cell="lstm"):
                dh0=g["dh0"], dc0=g["dc0"], T_eff=tapes[0]["T_eff"])
     if cell == "skip":
         out["guards"] = [t["guards"] for t in tapes]
+        out["margin"] = [t["margin"] for t in tapes]
         out["min_margin"] = min(t["min_margin"] for t in tapes)
     return out
 
