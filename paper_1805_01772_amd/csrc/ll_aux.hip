@@ -270,6 +270,25 @@ __global__ __launch_bounds__(256) void row_dot_kernel(const T* __restrict__ A, i
   }
 }
 
+// dst[j][4 u + g] = W[row0 + j][g H + u] for j, u < H, g < 4: W_h in the
+// unit-major reduction order of the single-layer LSTM gradient loop.
+// One thread per (j, u): four coalesced reads (consecutive threads take
+// consecutive u) and one 4-element store.
+template <typename T>
+__global__ __launch_bounds__(256) void permute_um_kernel(const T* __restrict__ W, int row0, int H,
+                                                         T* __restrict__ dst) {
+  const long n = (long)H * H;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+    const long j = i / H;
+    const int u = (int)(i - j * H);
+    const T* src = W + (row0 + j) * 4L * H + u;
+    struct alignas(4 * sizeof(T)) Quad { T v[4]; } q;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) q.v[g] = src[(long)g * H];
+    *reinterpret_cast<Quad*>(dst + 4 * i) = q;
+  }
+}
+
 // float -> operand type copy (used for bf16(h0) and similar small arrays).
 template <typename T>
 __global__ __launch_bounds__(256) void convert_kernel(const float* __restrict__ in, long n,
@@ -458,6 +477,16 @@ template hipError_t launch_row_dot<float>(const float*, int, const int*, const i
                                           float*, hipStream_t);
 template hipError_t launch_row_dot<bf16_t>(const bf16_t*, int, const int*, const int*, long, const float*, int,
                                            float*, hipStream_t);
+template <typename T>
+hipError_t launch_permute_um(const T* W, int row0, int H, T* dst, hipStream_t s) {
+  long blocks = ((long)H * H + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(permute_um_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, W, row0, H, dst);
+  return hipGetLastError();
+}
+template hipError_t launch_permute_um<float>(const float*, int, int, float*, hipStream_t);
+template hipError_t launch_permute_um<bf16_t>(const bf16_t*, int, int, bf16_t*, hipStream_t);
 template hipError_t launch_convert<float>(const float*, long, float*, hipStream_t);
 template hipError_t launch_convert<bf16_t>(const float*, long, bf16_t*, hipStream_t);
 

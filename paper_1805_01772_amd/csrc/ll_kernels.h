@@ -305,6 +305,11 @@ hipError_t launch_sum_slices_2d(const float* ws, int S, long stride, long rows, 
                                 long ldo, hipStream_t s);
 template <typename T>
 hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s);
+// dst[j][4 u + g] = W[row0 + j][g H + u] (j, u < H, g < 4): the recurrent
+// weights in the unit-major reduction order of the single-layer LSTM
+// gradient loop.
+template <typename T>
+hipError_t launch_permute_um(const T* W, int row0, int H, T* dst, hipStream_t s);
 // out[r] = sum_k A[rowmap ? rowmap[r] : r][k] * op(w[k]) for r < meta[1]
 // (at most cap rows); the input part of the cond body's predicate.
 template <typename T>

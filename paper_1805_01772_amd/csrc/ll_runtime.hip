@@ -152,6 +152,9 @@ struct ll_plan {
   bool skip = false;
   float* sx = nullptr;
   float* guards = nullptr;
+  // XCD-local LSTM gradient loops: W_h of each layer in the unit-major
+  // reduction order ([H, 4H], operand type)
+  void* Wum[2] = {nullptr, nullptr};
   int64_t stack_device_bytes = 0;
   int64_t stack_host_bytes = 0;
   // saved forward
@@ -251,7 +254,8 @@ void free_plan_memory(ll_plan* p) {
                   p->stack[0], p->stack[1], p->HH[0], p->HH[1], p->DZ, p->DZT, p->XT,
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
                   p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags,
-                  p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias, p->sx, p->guards};
+                  p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias, p->sx, p->guards, p->Wum[0],
+                  p->Wum[1]};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -625,6 +629,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     ALLOC(p->db_state, sizeof(float) * 8 * 32 * 512 * 4, "db state");
   }
   ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * p->GB * H, "db partials");
+  if (p->xmode && p->G == 4)
+    for (int l = 0; l < L; ++l) ALLOC(p->Wum[l], es * 4L * H * H, "permuted recurrent weights");
   if (p->skip) {
     ALLOC(p->sx, sizeof(float) * cap, "predicate input part");
     ALLOC(p->guards, sizeof(float) * L * cap, "guard stack");
@@ -1333,6 +1339,13 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       xa.perm = p->perm;
       xa.W = p->W[l];
       xa.woff = Il;
+      if (p->G == 4) {   // the LSTM loop reduces in unit-major order
+        ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
+        LL_HIP(ll::launch_permute_um<T>(static_cast<const T*>(p->W[l]), Il, H, static_cast<T*>(p->Wum[l]), s));
+        tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+        xa.W = p->Wum[l];
+        xa.woff = 0;
+      }
       xa.X = p->DZ;
       xa.c0 = p->c0 && p->G == 4 ? p->c0 + (long)l * B * H : nullptr;
       xa.stack = p->stack[l];

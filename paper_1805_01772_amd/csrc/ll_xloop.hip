@@ -477,7 +477,9 @@ __global__ __launch_bounds__(XNT, 1) void xfwd2_kernel(XLoopArgs a0, XLoopArgs a
 // Gradient loop, XCD-local.  Member `rank` owns hidden units j0 .. j0+HJ-1
 // (HJ = 16 NCT); thread (row, unit) of the first 16*HJ threads keeps dh, dc
 // of that row and unit.  The dz columns of gate g of the member's units are
-// k-step g*P + rank of the product dz W_h^T.  Step t (descending), per row
+// k-step g*P + rank of the product dz W_h^T (the single-layer LSTM loop
+// orders the reduction unit-major instead: its k-steps 4 rank .. 4 rank + 3
+// hold the member's units, four gates each).  Step t (descending), per row
 // tile:
 //   phase 1: from the values popped during step t+1: dh_tot, dz, dc; store
 //     dz into the ring and publish it; then the dz rows for the dW and dx
@@ -520,6 +522,12 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   // GRU r, u, n, zh_n + b_hn, h_{t-1}, dy; RNN h_t, dy
   constexpr int NPOP = (G == 4 ? 7 : G == 3 ? 6 : 2) + (SKIP ? 1 : 0);
   constexpr int NPV = SKIP ? 8 : 7;   // popped values kept per (tile, thread); [7] = guard
+  // Unit-major reduction order (single-layer LSTM loop): k = 4 u + g over
+  // units u and gates g, so a member's dz values of one unit are adjacent in
+  // the ring and k-steps 4 r .. 4 r + 3 are member r's; the weights come
+  // from W_h permuted to that order (a.W = [H, 4H], a.woff = 0).  Otherwise
+  // k = g H + u and k-step g P + r is member r's gate g.
+  constexpr bool UM = G == 4 && ROLE == 0;
   static_assert(!(SKIP && (ROLE != 0 || G != 4)), "the cond body is built on the single-layer LSTM loop");
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
   const int nks = ks1 - ks0;                            // k-steps of this wave
@@ -713,9 +721,23 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
           const float hv = pv[mt][0];
           dz[0] = dht * (1.f - hv * hv);
         }
+        if constexpr (UM) {
+          // the unit's four gate values are adjacent in the unit-major order:
+          // one 8-byte (bf16) / 16-byte (f32) store
+          const int u = j0 + cu, ku = (u % KPC) * 4;
+          char* dst = slot + ((u / KPC) << 10) + ((crow + 16 * (ku / KPC)) * KPC + ku % KPC) * (int)sizeof(T);
+          if constexpr (sizeof(T) == 2) {
+            const unsigned lo = (unsigned)Op<T>::from_f32(dz[0]) | ((unsigned)Op<T>::from_f32(dz[1]) << 16);
+            const unsigned hi = (unsigned)Op<T>::from_f32(dz[2]) | ((unsigned)Op<T>::from_f32(dz[3]) << 16);
+            *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+          } else {
+            *reinterpret_cast<float4*>(dst) = make_float4(dz[0], dz[1], dz[2], dz[3]);
+          }
+        } else {
 #pragma unroll
-        for (int g = 0; g < G; ++g)
-          *reinterpret_cast<T*>(slot + ((g * P + rank) << 10) + rbo) = Op<T>::from_f32(dz[g]);
+          for (int g = 0; g < G; ++g)
+            *reinterpret_cast<T*>(slot + ((g * P + rank) << 10) + rbo) = Op<T>::from_f32(dz[g]);
+        }
       }
       publish(flags + rank, (unsigned)(T_eff - t));
       if (act) {
@@ -738,7 +760,10 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
         }
       }
       // phase 2
-      wait_flags(a, flags, ks0, nks < 64 ? nks : 64, P, (unsigned)(T_eff - t));
+      if constexpr (UM)   // k-steps 4 r .. 4 r + 3 come from member r
+        wait_flags(a, flags, ks0 / 4, (nks + 3) / 4, P, (unsigned)(T_eff - t));
+      else
+        wait_flags(a, flags, ks0, nks < 64 ? nks : 64, P, (unsigned)(T_eff - t));
       const __amdgpu_buffer_rsrc_t rs = make_rsrc(slot, (unsigned)(a.ring_ks << 10));
       f32x4 acc[NCO];
 #pragma unroll
