@@ -225,6 +225,16 @@ __global__ __launch_bounds__(256) void rc_maps_kernel(const int* __restrict__ ac
   }
 }
 
+__global__ __launch_bounds__(256) void prev_rows_kernel(const int* __restrict__ active,
+                                                        const int* __restrict__ off, int B, int T_max,
+                                                        long cap, int* __restrict__ prev) {
+  const long n = (long)T_max * B;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+    const int t = (int)(i / B), r = (int)(i % B);
+    if (r < active[t]) prev[off[t] + r] = t > 0 ? off[t - 1] + r : (int)(cap + r);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void h0_rows_kernel(const float* __restrict__ h0,
                                                       const int* __restrict__ perm, int B, int H,
@@ -419,6 +429,16 @@ hipError_t launch_rc_maps(const int* active, const int* off, const int* perm, in
   if (blocks > 4096) blocks = 4096;
   hipLaunchKernelGGL(rc_maps_kernel, dim3((unsigned)blocks), dim3(256), 0, s, active, off, perm, B,
                      T_max, cap, xmap, cmap, prevmap);
+  return hipGetLastError();
+}
+
+hipError_t launch_prev_rows(const int* active, const int* off, int B, int T_max, long cap, int* prev,
+                            hipStream_t s) {
+  long blocks = ((long)T_max * B + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(prev_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, s, active, off, B, T_max, cap,
+                     prev);
   return hipGetLastError();
 }
 

@@ -345,6 +345,215 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_nt_bf16_lds_kernel(GemmAr
   }
 }
 
+// ---------------------------------------------------------------------------
+// Product over rows, bf16: C[m][n] = sum_k A[arow(k)][m] B[k][n] (dW = [X;
+// Hprev]^T DZ straight from the row-major operands).  The same work-group
+// shape, tile order, two LDS stages and epilogue as the kernel above; what
+// differs is the operand layout.  A k-tile of either operand is 64 rows
+// (k) x 256 columns, loaded row by row (a row's 512 bytes are contiguous
+// in memory): LDS holds [k][32 chunks of 16 bytes], chunk c of row k in
+// slot c ^ tn_swz(k).  The matrix-core operands need 8 consecutive k per
+// lane; gfx950's transposing LDS read (ds_read_b64_tr_b16) gives them: in
+// each 16-lane group, lane i's j-th element is the (i % 4)-th element of the
+// 8 bytes that lane 4 j + i / 4 addressed.  Lane s of the group therefore
+// addresses row k0 + s / 4, columns c0 + 4 (s % 4) .. + 3, and lane i
+// receives column c0 + i at rows k0 .. k0 + 3; two such reads (k0, k0 + 4)
+// make the 8 k of a 32x32x16 operand.  The swizzle (slot XOR 0, 6, 10, 12
+// for rows k % 4 = 0 .. 3) puts the four rows a 16-lane group reads at
+// distinct 32-byte bank groups within 128 bytes, and the eight row pieces of
+// two neighbouring groups at distinct ones within 256 bytes (measured on
+// the dW shape: 0.81 PFLOP/s against 0.70 without a swizzle).  The row map
+// of the next k-tile is loaded one k-tile ahead, so no fill waits on it.
+// ---------------------------------------------------------------------------
+namespace {
+
+__device__ __forceinline__ int tn_swz(int k) { return (0x0c0a0600u >> ((k & 3) * 8)) & 31; }
+
+typedef short tn_v4s __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint2 ds_read_tr16(const uint4* base, unsigned byte_off) {
+  const tn_v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) tn_v4s*)((__attribute__((address_space(3))) char*)base + byte_off));
+  return __builtin_bit_cast(uint2, v);
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kBigThreads, 1) void gemm_tn_bf16_lds_kernel(GemmTnArgs g, unsigned a_bytes,
+                                                                         unsigned b_bytes, unsigned a2_bytes) {
+  constexpr int BM = kBigTile, BN = kBigTile;
+  constexpr int NW = kBigThreads / 64;       // 8 waves
+  constexpr int WGN = 2;
+  constexpr int WM = BM / (NW / WGN), WN = BN / WGN;   // 64 x 128 per wave
+  constexpr int MI = WM / 32, NI = WN / 32;
+  constexpr int KT = 64;                     // rows (k) per k-tile
+  constexpr int RC = BM * 2 / 16;            // 16-byte chunks per row of a k-tile (32)
+  constexpr int CH = KT * RC;                // chunks per operand and stage
+  constexpr int LI = CH / 64 / NW;           // load instructions per wave and operand (4)
+  __shared__ uint4 sA0[CH], sA1[CH], sB0[CH], sB1[CH];
+
+  const int M = g.M;
+  const int K = g.K_dev ? min(*g.K_dev, g.K) : g.K;
+  const int nmt = (M + BM - 1) / BM, nnt = (g.N + BN - 1) / BN;
+  const int per_split = nmt * nnt;
+  const int ntiles = per_split * g.splits;
+  const int share = (ntiles + 7) / 8;
+  const int L = blockIdx.x;
+  const int t = (L & 7) * share + (L >> 3);
+  if ((L >> 3) >= share || t >= ntiles) return;
+  const int z = t / per_split;
+  const int tt = t - z * per_split;
+  const int grp = tt / (kBigGroupRows * nnt);
+  const int fm = grp * kBigGroupRows;
+  const int gsz = min(nmt - fm, kBigGroupRows);
+  const int within = tt - grp * kBigGroupRows * nnt;
+  const int m0 = (fm + within % gsz) * BM, n0 = (within / gsz) * BN;
+
+  const int kper = ((K + g.splits - 1) / g.splits + KT - 1) / KT * KT;
+  const int kb = min(K, z * kper);
+  const int ke = min(K, kb + kper);
+  const int nkt = (ke - kb + KT - 1) / KT;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  // the operand this tile's rows come from
+  const bool second = g.A2 && m0 >= g.M1;
+  const __amdgpu_buffer_rsrc_t ra = second ? make_rsrc(g.A2, a2_bytes) : make_rsrc(g.A, a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.Bm, b_bytes);
+  const long lda = second ? g.lda2 : g.lda;
+  const int* a_rowmap = second ? g.a2_rowmap : g.a_rowmap;
+  const int am0 = second ? m0 - g.M1 : m0, aM = second ? M - g.M1 : (g.A2 ? g.M1 : M);
+  // load instruction i of this wave: k-tile rows (i NW + wave) 2 + lane / 32,
+  // LDS slot lane % 32 of that row, which holds column chunk slot ^ tn_swz(row)
+  int lrow[LI];
+  unsigned acol[LI], bcol[LI];   // byte offset of the chunk within a row (kOOB: past M / N)
+#pragma unroll
+  for (int i = 0; i < LI; ++i) {
+    lrow[i] = (i * NW + wave) * 2 + (lane >> 5);
+    const int c = (lane & 31) ^ tn_swz(lrow[i]);
+    acol[i] = am0 + c * 8 < aM ? (unsigned)((am0 + c * 8) * 2) : kOOB;
+    bcol[i] = n0 + c * 8 < g.N ? (unsigned)((n0 + c * 8) * 2) : kOOB;
+  }
+  // A rows of the k-tile the next fill loads (-1: past the end)
+  int amap[LI];
+  auto load_map = [&](int kt) {
+    const int k0 = kb + kt * KT;
+#pragma unroll
+    for (int i = 0; i < LI; ++i) {
+      const int k = k0 + lrow[i];
+      amap[i] = k < ke ? (a_rowmap ? a_rowmap[k] : k) : -1;
+    }
+  };
+  auto fill = [&](int kt, uint4* a_dst, uint4* b_dst) {
+    const int k0 = kb + kt * KT;
+#pragma unroll
+    for (int i = 0; i < LI; ++i) {
+      const int k = k0 + lrow[i];
+      const bool ok = k < ke;
+      const unsigned ao = ok && acol[i] != kOOB ? (unsigned)((long)amap[i] * lda * 2) + acol[i] : kOOB;
+      const unsigned bo = ok && bcol[i] != kOOB ? (unsigned)((long)k * g.ldb * 2) + bcol[i] : kOOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(a_dst + (i * NW + wave) * 64), 16, ao, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(b_dst + (i * NW + wave) * 64), 16, bo, 0, 0, 0);
+    }
+    if (kt + 1 < nkt) load_map(kt + 1);
+  };
+
+  f32x16 acc[MI][NI];
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{};
+
+  // transposing reads: group G = lane / 16 takes k-half G / 2 and column half
+  // G % 2 of a 32-wide operand block; lane s of the group addresses row
+  // s / 4 (+ 4 for the second read), columns 4 (s % 4) .. + 3
+  const int G = lane >> 4, s16 = lane & 15;
+  const int rk = (G >> 1) * 8 + (s16 >> 2);          // row within a 16-row k-step
+  const int cc = (G & 1) * 16 + 4 * (s16 & 3);       // column within a 32-column block
+  auto rd = [&](const uint4* base, int k_local, int col) -> uint2 {
+    const unsigned off = (unsigned)((k_local * RC + ((col >> 3) ^ tn_swz(k_local))) * 16 + (col & 7) * 2);
+    return ds_read_tr16(base, off);
+  };
+  auto step = [&](int kt, const uint4* a, const uint4* b, uint4* a_next, uint4* b_next) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (kt + 1 < nkt) fill(kt + 1, a_next, b_next);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int k_local = ks * 16 + rk;
+      uint4 av[MI], bv[NI];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int col = wm * WM + i * 32 + cc;
+        const uint2 lo = rd(a, k_local, col), hi = rd(a, k_local + 4, col);
+        av[i] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int col = wn * WN + j * 32 + cc;
+        const uint2 lo = rd(b, k_local, col), hi = rd(b, k_local + 4, col);
+        bv[j] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+      }
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, av[i]), __builtin_bit_cast(bf16x8_t, bv[j]), acc[i][j], 0, 0, 0);
+    }
+  };
+  if (nkt > 0) {
+    load_map(0);
+    fill(0, sA0, sB0);
+  }
+  for (int kt = 0; kt < nkt; kt += 2) {
+    step(kt, sA0, sB0, sA1, sB1);
+    if (kt + 1 < nkt) step(kt + 1, sA1, sB1, sA0, sB0);
+  }
+
+  // result register r of lane l: row (r % 4) + 8 (r / 4) + 4 (l / 32), column l % 32
+  const int l32 = lane & 31, kc = lane >> 5;
+  float* Cb = g.C + (g.splits > 1 ? (long)z * g.split_stride : 0L);
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + wm * WM + i * 32 + (r & 3) + 8 * (r >> 2) + 4 * kc;
+      if (m >= M) continue;
+      float* cr = Cb + (long)m * g.ldc;
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int n = n0 + wn * WN + j * 32 + l32;
+        if (n < g.N) cr[n] = acc[i][j][r];
+      }
+    }
+  }
+}
+
+bool gemm_tn_applies(const GemmTnArgs& g) {
+  if (g.M % 8 || g.N % 8 || g.lda % 8 || g.ldb % 8 || g.splits < 1) return false;
+  if ((reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.Bm) |
+       reinterpret_cast<uintptr_t>(g.A2)) & 15)
+    return false;
+  if (g.A2 && (g.M1 % kBigTile || g.M1 <= 0 || g.M1 >= g.M || g.lda2 % 8)) return false;
+  const long ab = (long)(g.a_rows > 0 ? g.a_rows : g.K) * g.lda * 2, bb = (long)g.b_rows * g.ldb * 2;
+  const long a2b = g.A2 ? (long)g.a2_rows * g.lda2 * 2 : 0;
+  return ab < (long)kOOB && bb < (long)kOOB && a2b < (long)kOOB;
+}
+
+hipError_t launch_gemm_tn(const GemmTnArgs& g, hipStream_t s) {
+  if (!gemm_tn_applies(g)) return hipErrorInvalidValue;
+  const long ab = (long)(g.a_rows > 0 ? g.a_rows : g.K) * g.lda * 2, bb = (long)g.b_rows * g.ldb * 2;
+  const long a2b = g.A2 ? (long)g.a2_rows * g.lda2 * 2 : 0;
+  const long tiles = (long)((g.M + kBigTile - 1) / kBigTile) * ((g.N + kBigTile - 1) / kBigTile) * g.splits;
+  const long grid = (tiles + 7) / 8 * 8;
+  hipLaunchKernelGGL(gemm_tn_bf16_lds_kernel, dim3((unsigned)grid), dim3(kBigThreads), 0, s, g, (unsigned)ab,
+                     (unsigned)bb, (unsigned)a2b);
+  return hipGetLastError();
+}
+
 namespace {
 
 // Bytes of A and B the products of g may address (0 if past a 31-bit range).

@@ -305,6 +305,11 @@ hipError_t launch_sum_slices_2d(const float* ws, int S, long stride, long rows, 
                                 long ldo, hipStream_t s);
 template <typename T>
 hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s);
+// prev[off[t] + r] = off[t-1] + r (t > 0) or cap + r (t = 0) for r <
+// active[t]: the h history row of each compact row's h_{t-1} (rows cap ..
+// cap + B - 1 hold h0 in length order).
+hipError_t launch_prev_rows(const int* active, const int* off, int B, int T_max, long cap, int* prev,
+                            hipStream_t s);
 // dst[j][4 u + g] = W[row0 + j][g H + u] (j, u < H, g < 4): the recurrent
 // weights in the unit-major reduction order of the single-layer LSTM
 // gradient loop.
@@ -318,6 +323,35 @@ hipError_t launch_row_dot(const T* A, int lda, const int* rowmap, const int* met
 
 template <typename T>
 hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s);
+
+// C[m][n] = sum over k < K of A[arow(k)][m] B[k][n] (bf16 operands, fp32
+// result): the product over the rows of two row-major operands, as dW =
+// [X; Hprev]^T DZ needs, with no transposed copies.  arow(k) = a_rowmap[k]
+// (NULL: k).  Needs M and N multiples of 8 and 16-byte aligned rows.
+struct GemmTnArgs {
+  const void* A;
+  long lda;
+  const int* a_rowmap;
+  int a_rows;            // rows of A the row map addresses
+  const void* Bm;
+  long ldb;
+  int b_rows;            // rows of B (>= K)
+  float* C;
+  long ldc;
+  int M, N, K;
+  const int* K_dev;      // NULL or device scalar: rows actually present (<= K)
+  int splits;            // > 1: split-K; slice z written to C + z * split_stride
+  long split_stride;
+  // optional second operand for the C rows from M1 on (M1 a multiple of the
+  // 256-row tile): C[m][n] for m >= M1 reads A2[a2row(k)][m - M1]
+  const void* A2;
+  long lda2;
+  const int* a2_rowmap;
+  int a2_rows;
+  int M1;
+};
+bool gemm_tn_applies(const GemmTnArgs& g);
+hipError_t launch_gemm_tn(const GemmTnArgs& g, hipStream_t s);
 // Whether launch_gemm_nt takes the large-tile bf16 kernel for g, and how
 // many times the launch fills n_cu compute units (row capacity g.M).
 bool gemm_big_applies(const GemmArgs& g, int elem_bytes);

@@ -155,6 +155,10 @@ struct ll_plan {
   // XCD-local LSTM gradient loops: W_h of each layer in the unit-major
   // reduction order ([H, 4H], operand type)
   void* Wum[2] = {nullptr, nullptr};
+  // bf16 dW from the row-major operands: h history row of each compact row's
+  // h_{t-1} (h0 rows after the history), and the split-K of each product
+  int* prevc = nullptr;
+  int tn_splits[2][3] = {{1, 1, 1}, {1, 1, 1}};
   int64_t stack_device_bytes = 0;
   int64_t stack_host_bytes = 0;
   // saved forward
@@ -200,6 +204,30 @@ int dw_parts(const ll_plan* p, int l, DwPart* out) {
   }
   out[0] = DwPart{0, Il + H, 0, p->G * H, 0};
   return 1;
+}
+
+// The same products taken straight from the row-major operands (bf16): the
+// input part (rows 0 .. Il - 1 of dW, A = the layer's input rows) and the
+// recurrent part (rows Il .., A = the h history rows of h_{t-1}) read
+// different arrays, so each is a product of its own; b_row is the dz column.
+// When the input width is a multiple of the 256-row tile the two parts of
+// one dz column range are one launch (m = Il + H; rows from Il on read the
+// h history).
+int dw_parts_rows(const ll_plan* p, int l, DwPart* out) {
+  const int H = p->d.H, Il = in_width(p, l);
+  if (p->G == 3) {
+    out[0] = DwPart{0, Il, 0, 3 * H, 0};
+    out[1] = DwPart{Il, H, 0, 2 * H, 0};
+    out[2] = DwPart{Il, H, 3 * H, H, 2 * H};
+    return 3;
+  }
+  if (Il % ll::kGemmBigTile == 0) {
+    out[0] = DwPart{0, Il + H, 0, p->G * H, 0};
+    return 1;
+  }
+  out[0] = DwPart{0, Il, 0, p->G * H, 0};
+  out[1] = DwPart{Il, H, 0, p->G * H, 0};
+  return 2;
 }
 
 hipEvent_t take_event(ll_plan* p) {
@@ -255,7 +283,7 @@ void free_plan_memory(ll_plan* p) {
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
                   p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags,
                   p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias, p->sx, p->guards, p->Wum[0],
-                  p->Wum[1]};
+                  p->Wum[1], p->prevc};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -542,7 +570,19 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   // tiles else).  The products run one after the other and share the
   // workspace of the partial sums.
   p->ws_floats = 0;
-  for (int l = 0; l < L; ++l) {
+  for (int l = 0; l < L && p->bf16; ++l) {   // bf16: the products over rows
+    DwPart parts[3];
+    const int np = dw_parts_rows(p, l, parts);
+    for (int k = 0; k < np; ++k) {
+      const long tiles = (long)((parts[k].m + ll::kGemmBigTile - 1) / ll::kGemmBigTile) *
+                         ((parts[k].n + ll::kGemmBigTile - 1) / ll::kGemmBigTile);
+      long sp = (p->n_cu + tiles - 1) / tiles;
+      sp = std::max(1L, std::min(16L, std::min(sp, std::max(1L, p->cap / 256))));
+      p->tn_splits[l][k] = (int)sp;
+      if (sp > 1) p->ws_floats = std::max(p->ws_floats, sp * parts[k].m * parts[k].n);
+    }
+  }
+  for (int l = 0; l < L && !p->bf16; ++l) {
     DwPart parts[3];
     const int np = dw_parts(p, l, parts);
     for (int k = 0; k < np; ++k) {
@@ -591,12 +631,15 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
           sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * (p->recompute || p->G == 1 ? 1 : 5) * H),
           "stack");
     // (recompute: B more rows hold h0 in the operand type, the h_{t-1} of step 0)
-    ALLOC(p->HH[l], es * (cap + (p->recompute ? B : 0)) * H, "h history");
+    // (B more rows hold h0 in the operand type, the h_{t-1} of step 0)
+    ALLOC(p->HH[l], es * (cap + B) * H, "h history");
   }
   ALLOC(p->Zx, sizeof(float) * cap * p->G * H, "input projection");
   ALLOC(p->DZ, es * cap * p->GB * H, "dz");
-  ALLOC(p->DZT, es * p->GB * H * p->ldT, "dz transposed");
-  ALLOC(p->XT, es * (maxI + H) * p->ldT, "x and h_prev transposed");
+  if (!p->bf16) {   // (bf16 dW reads the row-major operands directly)
+    ALLOC(p->DZT, es * p->GB * H * p->ldT, "dz transposed");
+    ALLOC(p->XT, es * (maxI + H) * p->ldT, "x and h_prev transposed");
+  }
   if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
   if (p->xmode) {
     // two slots x 8 XCDs x row tiles x (G H / k-step) blocks of 1 KB
@@ -631,6 +674,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * p->GB * H, "db partials");
   if (p->xmode && p->G == 4)
     for (int l = 0; l < L; ++l) ALLOC(p->Wum[l], es * 4L * H * H, "permuted recurrent weights");
+  if (p->bf16) ALLOC(p->prevc, sizeof(int) * cap, "previous-row map");
   if (p->skip) {
     ALLOC(p->sx, sizeof(float) * cap, "predicate input part");
     ALLOC(p->guards, sizeof(float) * L * cap, "guard stack");
@@ -1113,62 +1157,117 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   // cond body: the predicate's parameters get no gradient (a step function)
   if (p->skip) LL_HIP(ll::launch_zero_u32(reinterpret_cast<unsigned*>(dbias[l] + GBH), Il + H + 1, s));
   tend(p, s, LL_STAGE_DW, ev);
-  ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
-  // transposed operands of the dW products (reduction over compact rows)
-  ll::GatherTArgs gt{};
-  gt.B = B;
-  gt.meta = p->meta;
-  gt.rowmap = p->rowmap;
-  gt.off = p->off;
-  gt.perm = p->perm;
-  gt.ldo = (int)p->ldT;
-  gt.in = dz;
-  gt.out = p->DZT;
-  gt.C = GBH;
-  gt.mode = 1;
-  LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
-  gt.in = l == 0 ? p->x : p->HH[0];
-  gt.out = p->XT;
-  gt.C = Il;
-  gt.mode = l == 0 ? 0 : 1;
-  LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
-  gt.in = p->HH[l];
-  gt.out = static_cast<char*>(p->XT) + p->es * Il * p->ldT;
-  gt.C = H;
-  gt.mode = 2;
-  gt.h0f = p->h0 ? p->h0 + (long)l * B * H : nullptr;
-  LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
-  tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
-  // dW = [X^T; Hprev^T] DZ (the parts of dw_parts)
-  ev = tbeg(p, s, LL_STAGE_DW);
-  {
+  if (p->bf16) {
+    // dW straight from the row-major operands: the h history row of every
+    // compact row's h_{t-1}, and h0 (length order) after the history
+    ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
+    LL_HIP(ll::launch_prev_rows(p->active, p->off, B, d.T_max, p->cap, p->prevc, s));
+    LL_HIP(ll::launch_h0_rows<T>(p->h0 ? p->h0 + (long)l * B * H : nullptr, p->perm, B, H,
+                                 reinterpret_cast<T*>(p->HH[l]) + p->cap * H, s));
+    tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
+    ev = tbeg(p, s, LL_STAGE_DW);
     DwPart parts[3];
-    const int np = dw_parts(p, l, parts);
-    const long rowb = p->es * p->ldT;   // bytes per transposed row
+    const int np = dw_parts_rows(p, l, parts);
     for (int k = 0; k < np; ++k) {
       const DwPart& q = parts[k];
-      float* out = dW[l] + (long)q.a_row * GH + q.c_col;
-      ll::GemmArgs g{};
-      g.A = static_cast<const char*>(p->XT) + q.a_row * rowb;
-      g.lda = p->ldT;
-      g.Bm = static_cast<const char*>(p->DZT) + q.b_row * rowb;
-      g.ldb = p->ldT;
+      const bool in_part = q.a_row == 0;
+      ll::GemmTnArgs g{};
+      if (in_part) {
+        g.A = l == 0 ? p->x : p->HH[0];
+        g.a_rowmap = l == 0 ? p->rowmap : nullptr;
+        g.a_rows = (int)p->cap;
+        if (q.m > Il) {   // both parts in one launch
+          g.A2 = p->HH[l];
+          g.lda2 = H;
+          g.a2_rowmap = p->prevc;
+          g.a2_rows = (int)(p->cap + B);
+          g.M1 = Il;
+        }
+      } else {
+        g.A = p->HH[l];
+        g.a_rowmap = p->prevc;
+        g.a_rows = (int)(p->cap + B);
+      }
+      g.lda = in_part ? Il : H;
+      g.Bm = static_cast<const T*>(dz) + q.b_row;
+      g.ldb = GBH;
+      g.b_rows = (int)p->cap;
       g.M = q.m;
       g.N = q.n;
       g.K = (int)p->cap;
       g.K_dev = p->meta + 1;
-      g.k_zero_tail = 1;   // the transposes write zeros past the last row, up to a multiple of 64
-      g.splits = p->dw_splits[l][k];
+      g.splits = p->tn_splits[l][k];
+      float* out = dW[l] + (long)q.a_row * GH + q.c_col;
       if (g.splits > 1) {
         g.C = p->ws;
         g.ldc = q.n;
         g.split_stride = (long)q.m * q.n;
-        LL_HIP(ll::launch_gemm_nt<T>(g, s));
+        LL_HIP(ll::launch_gemm_tn(g, s));
         LL_HIP(ll::launch_sum_slices_2d(p->ws, g.splits, g.split_stride, q.m, q.n, out, GH, s));
       } else {
         g.C = out;
         g.ldc = GH;
-        LL_HIP(ll::launch_gemm_nt<T>(g, s));
+        LL_HIP(ll::launch_gemm_tn(g, s));
+      }
+    }
+  } else {
+    ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
+    // transposed operands of the dW products (reduction over compact rows)
+    ll::GatherTArgs gt{};
+    gt.B = B;
+    gt.meta = p->meta;
+    gt.rowmap = p->rowmap;
+    gt.off = p->off;
+    gt.perm = p->perm;
+    gt.ldo = (int)p->ldT;
+    gt.in = dz;
+    gt.out = p->DZT;
+    gt.C = GBH;
+    gt.mode = 1;
+    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+    gt.in = l == 0 ? p->x : p->HH[0];
+    gt.out = p->XT;
+    gt.C = Il;
+    gt.mode = l == 0 ? 0 : 1;
+    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+    gt.in = p->HH[l];
+    gt.out = static_cast<char*>(p->XT) + p->es * Il * p->ldT;
+    gt.C = H;
+    gt.mode = 2;
+    gt.h0f = p->h0 ? p->h0 + (long)l * B * H : nullptr;
+    LL_HIP(ll::launch_gather_transpose<T>(gt, (int)p->cap, s));
+    tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
+    // dW = [X^T; Hprev^T] DZ (the parts of dw_parts)
+    ev = tbeg(p, s, LL_STAGE_DW);
+    {
+      DwPart parts[3];
+      const int np = dw_parts(p, l, parts);
+      const long rowb = p->es * p->ldT;   // bytes per transposed row
+      for (int k = 0; k < np; ++k) {
+        const DwPart& q = parts[k];
+        float* out = dW[l] + (long)q.a_row * GH + q.c_col;
+        ll::GemmArgs g{};
+        g.A = static_cast<const char*>(p->XT) + q.a_row * rowb;
+        g.lda = p->ldT;
+        g.Bm = static_cast<const char*>(p->DZT) + q.b_row * rowb;
+        g.ldb = p->ldT;
+        g.M = q.m;
+        g.N = q.n;
+        g.K = (int)p->cap;
+        g.K_dev = p->meta + 1;
+        g.k_zero_tail = 1;   // the transposes write zeros past the last row, up to a multiple of 64
+        g.splits = p->dw_splits[l][k];
+        if (g.splits > 1) {
+          g.C = p->ws;
+          g.ldc = q.n;
+          g.split_stride = (long)q.m * q.n;
+          LL_HIP(ll::launch_gemm_nt<T>(g, s));
+          LL_HIP(ll::launch_sum_slices_2d(p->ws, g.splits, g.split_stride, q.m, q.n, out, GH, s));
+        } else {
+          g.C = out;
+          g.ldc = GH;
+          LL_HIP(ll::launch_gemm_nt<T>(g, s));
+        }
       }
     }
   }
