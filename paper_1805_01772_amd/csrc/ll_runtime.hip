@@ -159,6 +159,7 @@ struct ll_plan {
   // h_{t-1} (h0 rows after the history), and the split-K of each product
   int* prevc = nullptr;
   int tn_splits[2][3] = {{1, 1, 1}, {1, 1, 1}};
+  bool dw_rows[2] = {false, false};   // layer's dW from the row-major operands
   int64_t stack_device_bytes = 0;
   int64_t stack_host_bytes = 0;
   // saved forward
@@ -569,8 +570,19 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   // 256x256 tile per compute unit for the large-tile bf16 kernel, two 128x128
   // tiles else).  The products run one after the other and share the
   // workspace of the partial sums.
+  // bf16 dW: the product over rows (no transposed copies, but its operand
+  // reads run it at ~0.65 of the rate of the product on transposed copies,
+  // measured ~0.65 vs ~1.0 PFLOP/s) or the transposes (~2.2 TB/s) plus that
+  // product, whichever the model says is shorter: rows win while
+  // flops / transposed bytes < ~845 (H = I = 1024: ~683; H = I = 2048: ~1365)
   p->ws_floats = 0;
-  for (int l = 0; l < L && p->bf16; ++l) {   // bf16: the products over rows
+  for (int l = 0; l < L; ++l) {
+    const double Il = in_width(p, l);
+    const double flops = 2.0 * (Il + H) * p->G * H, bytes = (Il + H + p->GB * H) * 2.0 * p->es;
+    p->dw_rows[l] = p->bf16 && flops / bytes < 845.0;
+  }
+  for (int l = 0; l < L; ++l) {   // the products over rows
+    if (!p->dw_rows[l]) continue;
     DwPart parts[3];
     const int np = dw_parts_rows(p, l, parts);
     for (int k = 0; k < np; ++k) {
@@ -582,7 +594,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
       if (sp > 1) p->ws_floats = std::max(p->ws_floats, sp * parts[k].m * parts[k].n);
     }
   }
-  for (int l = 0; l < L && !p->bf16; ++l) {
+  for (int l = 0; l < L; ++l) {
+    if (p->dw_rows[l]) continue;
     DwPart parts[3];
     const int np = dw_parts(p, l, parts);
     for (int k = 0; k < np; ++k) {
@@ -636,7 +649,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   }
   ALLOC(p->Zx, sizeof(float) * cap * p->G * H, "input projection");
   ALLOC(p->DZ, es * cap * p->GB * H, "dz");
-  if (!p->bf16) {   // (bf16 dW reads the row-major operands directly)
+  if (!p->dw_rows[0] || (L == 2 && !p->dw_rows[1])) {   // (transposed copies for the NT products)
     ALLOC(p->DZT, es * p->GB * H * p->ldT, "dz transposed");
     ALLOC(p->XT, es * (maxI + H) * p->ldT, "x and h_prev transposed");
   }
@@ -674,7 +687,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->db_part, sizeof(float) * std::max(p->geom.RG, 8) * p->GB * H, "db partials");
   if (p->xmode && p->G == 4)
     for (int l = 0; l < L; ++l) ALLOC(p->Wum[l], es * 4L * H * H, "permuted recurrent weights");
-  if (p->bf16) ALLOC(p->prevc, sizeof(int) * cap, "previous-row map");
+  if (p->dw_rows[0] || p->dw_rows[1]) ALLOC(p->prevc, sizeof(int) * cap, "previous-row map");
   if (p->skip) {
     ALLOC(p->sx, sizeof(float) * cap, "predicate input part");
     ALLOC(p->guards, sizeof(float) * L * cap, "guard stack");
@@ -1157,7 +1170,7 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   // cond body: the predicate's parameters get no gradient (a step function)
   if (p->skip) LL_HIP(ll::launch_zero_u32(reinterpret_cast<unsigned*>(dbias[l] + GBH), Il + H + 1, s));
   tend(p, s, LL_STAGE_DW, ev);
-  if (p->bf16) {
+  if (p->dw_rows[l]) {
     // dW straight from the row-major operands: the h history row of every
     // compact row's h_{t-1}, and h0 (length order) after the history
     ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
