@@ -436,15 +436,17 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_tn_bf16_lds_kernel(GemmTn
     acol[i] = am0 + c * 8 < aM ? (unsigned)((am0 + c * 8) * 2) : kOOB;
     bcol[i] = n0 + c * 8 < g.N ? (unsigned)((n0 + c * 8) * 2) : kOOB;
   }
-  // A rows of the k-tile the next fill loads (-1: past the end)
-  int amap[LI];
+  // row-map entries of the k-tile the next fill loads, read with no branch
+  // (past the map's end: zero), so the compiler does not wait for them
+  // before the fill that uses them, and with that for the fills in flight
+  const bool has_map = a_rowmap != nullptr;
+  const __amdgpu_buffer_rsrc_t rmap = make_rsrc(a_rowmap, has_map ? (unsigned)ke * 4u : 0u);
+  unsigned amap[LI];
   auto load_map = [&](int kt) {
     const int k0 = kb + kt * KT;
 #pragma unroll
-    for (int i = 0; i < LI; ++i) {
-      const int k = k0 + lrow[i];
-      amap[i] = k < ke ? (a_rowmap ? a_rowmap[k] : k) : -1;
-    }
+    for (int i = 0; i < LI; ++i)
+      amap[i] = __builtin_amdgcn_raw_buffer_load_b32(rmap, (unsigned)(k0 + lrow[i]) * 4u, 0, 0);
   };
   auto fill = [&](int kt, uint4* a_dst, uint4* b_dst) {
     const int k0 = kb + kt * KT;
@@ -452,7 +454,8 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_tn_bf16_lds_kernel(GemmTn
     for (int i = 0; i < LI; ++i) {
       const int k = k0 + lrow[i];
       const bool ok = k < ke;
-      const unsigned ao = ok && acol[i] != kOOB ? (unsigned)((long)amap[i] * lda * 2) + acol[i] : kOOB;
+      const long ar = has_map ? (long)amap[i] : (long)k;
+      const unsigned ao = ok && acol[i] != kOOB ? (unsigned)(ar * lda * 2) + acol[i] : kOOB;
       const unsigned bo = ok && bcol[i] != kOOB ? (unsigned)((long)k * g.ldb * 2) + bcol[i] : kOOB;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(a_dst + (i * NW + wave) * 64), 16, ao, 0, 0, 0);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(b_dst + (i * NW + wave) * 64), 16, bo, 0, 0, 0);

@@ -571,15 +571,15 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   // tiles else).  The products run one after the other and share the
   // workspace of the partial sums.
   // bf16 dW: the product over rows (no transposed copies, but its operand
-  // reads run it at ~0.65 of the rate of the product on transposed copies,
-  // measured ~0.65 vs ~1.0 PFLOP/s) or the transposes (~2.2 TB/s) plus that
+  // reads run it at ~0.72 of the rate of the product on transposed copies,
+  // measured ~0.72 vs ~1.0 PFLOP/s) or the transposes (~2.2 TB/s) plus that
   // product, whichever the model says is shorter: rows win while
-  // flops / transposed bytes < ~845 (H = I = 1024: ~683; H = I = 2048: ~1365)
+  // flops / transposed bytes < ~1170 (H = I = 1024: ~683; H = I = 2048: ~1365)
   p->ws_floats = 0;
   for (int l = 0; l < L; ++l) {
     const double Il = in_width(p, l);
     const double flops = 2.0 * (Il + H) * p->G * H, bytes = (Il + H + p->GB * H) * 2.0 * p->es;
-    p->dw_rows[l] = p->bf16 && flops / bytes < 845.0;
+    p->dw_rows[l] = p->bf16 && flops / bytes < 1170.0;
   }
   for (int l = 0; l < L; ++l) {   // the products over rows
     if (!p->dw_rows[l]) continue;
