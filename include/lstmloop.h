@@ -200,8 +200,9 @@ ll_status ll_plan_geometry(const ll_plan* plan, int32_t* loop_workgroups,
 
 /*
  * Forward while-loop (Sections 2.1, 4.2, 5.1).
- *   x        [T_max,B,I] dtype; entries at t >= seq_len[b] are never read
- *            into a kept result (they may hold NaN).
+ *   x        [T_max,B,I] dtype, 16-byte aligned (LL_BF16: lstm_loop_bwd
+ *            returns LL_EUNSUPPORTED otherwise); entries at t >= seq_len[b]
+ *            are never read into a kept result (they may hold NaN).
  *   seq_len  [B] int32, each in [0, T_max].
  *   W, bias  host arrays of `layers` device pointers (see conventions).
  *   h0, c0   [layers,B,H] float, or NULL for zeros.

@@ -1210,6 +1210,9 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
       g.K = (int)p->cap;
       g.K_dev = p->meta + 1;
       g.splits = p->tn_splits[l][k];
+      if (!ll::gemm_tn_applies(g))
+        return fail(LL_EUNSUPPORTED, "bf16 dW reads x, the h history and dz as 16-byte aligned rows; x = %p is not",
+                    p->x);
       float* out = dW[l] + (long)q.a_row * GH + q.c_col;
       if (g.splits > 1) {
         g.C = p->ws;
