@@ -140,6 +140,7 @@ struct ll_plan {
   // the gradient loop (forked from and joined back into the call's stream)
   hipStream_t gstream = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipEvent_t ev_side = nullptr;   // side-stream work started at a call's beginning
   hipEvent_t ev_compute = nullptr;
   std::vector<hipEvent_t> ev_d2h, ev_h2d;   // per (layer, slot)
   float* carry = nullptr;      // [4][B, H]: h, c (forward) / dh, dc (backward) between chunks
@@ -297,6 +298,7 @@ void free_plan_memory(ll_plan* p) {
   if (p->cstream) (void)hipStreamDestroy(p->cstream);
   if (p->ev_fork) (void)hipEventDestroy(p->ev_fork);
   if (p->ev_join) (void)hipEventDestroy(p->ev_join);
+  if (p->ev_side) (void)hipEventDestroy(p->ev_side);
   if (p->gstream) (void)hipStreamDestroy(p->gstream);
 }
 
@@ -701,7 +703,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   }
   if (hipStreamCreateWithFlags(&p->gstream, hipStreamNonBlocking) != hipSuccess ||
       hipEventCreateWithFlags(&p->ev_fork, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&p->ev_join, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&p->ev_join, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&p->ev_side, hipEventDisableTiming) != hipSuccess) {
     free_plan_memory(p);
     delete p;
     return fail(LL_EHIP, "creating the plan's side stream failed");
@@ -941,17 +944,28 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
                       bool save) {
   const ll_desc& d = p->d;
   const int H = d.H, B = d.B, L = d.layers;
+  // W^T of every layer (row n = gate column n, the K-contiguous operand of
+  // the input projection and the loop) on the side stream, beside prep,
+  // which runs on one compute unit
+  if (!p->wave) {
+    LL_HIP(hipEventRecord(p->ev_fork, s));
+    LL_HIP(hipStreamWaitEvent(p->gstream, p->ev_fork, 0));
+    for (int l = 0; l < L; ++l) {
+      const int Il = in_width(p, l);
+      LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, p->G * H, p->G * H,
+                                     reinterpret_cast<T*>(p->WT[l]), Il + H, p->gstream));
+    }
+    LL_HIP(hipEventRecord(p->ev_side, p->gstream));
+  }
   hipEvent_t ev = tbeg(p, s, LL_STAGE_PREP);
   LL_HIP(ll::launch_prep(seq_len, B, d.T_max, p->perm, p->active, p->off, p->rowmap, p->meta,
                          trip, s));
   tend(p, s, LL_STAGE_PREP, ev);
   if (p->wave) return enqueue_fwd_wave<T>(p, s, x, W, bias, h0, c0, y, hT, cT, save);
+  LL_HIP(hipStreamWaitEvent(s, p->ev_side, 0));
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
     ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
-    // W^T: row n = gate column n, K-contiguous operand of both products
-    LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, p->G * H, p->G * H,
-                                   reinterpret_cast<T*>(p->WT[l]), Il + H, s));
     // Zx = x_t W_x + b for every compact row (layer 0 gathers time-major x)
     ll::GemmArgs g{};
     g.A = l == 0 ? x : p->HH[0];
@@ -1431,10 +1445,23 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
                       float* dh0, float* dc0) {
   const ll_desc& d = p->d;
   const int H = d.H, B = d.B, L = d.layers;
-  hipEvent_t ev = tbeg(p, s, LL_STAGE_DX);
-  if (dx) LL_HIP(ll::launch_zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta, s));
-  tend(p, s, LL_STAGE_DX, ev);
-  if (p->wave) return enqueue_bwd_wave<T>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
+  hipEvent_t ev = nullptr;
+  if (p->wave) {
+    ev = tbeg(p, s, LL_STAGE_DX);
+    if (dx) LL_HIP(ll::launch_zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta, s));
+    tend(p, s, LL_STAGE_DX, ev);
+    return enqueue_bwd_wave<T>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
+  }
+  // dx rows of finished steps to zero on the side stream, beside the set-up
+  // and the start of the gradient loop (joined before layer 0's products)
+  if (dx) {
+    LL_HIP(hipEventRecord(p->ev_fork, s));
+    LL_HIP(hipStreamWaitEvent(p->gstream, p->ev_fork, 0));
+    ev = tbeg(p, p->gstream, LL_STAGE_DX);
+    LL_HIP(ll::launch_zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta, p->gstream));
+    tend(p, p->gstream, LL_STAGE_DX, ev);
+    LL_HIP(hipEventRecord(p->ev_side, p->gstream));
+  }
   for (int l = L - 1; l >= 0; --l) {
     const int Il = in_width(p, l);
     if (p->xmode) {
@@ -1592,6 +1619,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       LL_HIP(ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s));
       tend(p, s, LL_STAGE_BWD_LOOP, ev);
     }
+    if (l == 0 && dx) LL_HIP(hipStreamWaitEvent(s, p->ev_side, 0));
     LL_STATUS(bwd_products<T>(p, s, l, p->DZ, p->db_part, l == 0 ? dx : p->dyc, dW, dbias));
   }
   return LL_OK;
