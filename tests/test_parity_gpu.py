@@ -88,6 +88,30 @@ def test_small_parity(w, loop_mode):
     assert not bad, bad
 
 
+MAX_BATCH = [
+    W("f32_b4096_i8_h32_t4_maxbatch", B=4096, I=8, H=32, T_max=4, dtype="f32", len_lo=0, len_hi=4,
+      w_scale=0.3, random_state=True, seed=61),
+    W("bf16_b4096_i16_h64_t3_maxbatch", B=4096, I=16, H=64, T_max=3, dtype="bf16", len_lo=0,
+      len_hi=3, random_state=True, seed=62),
+]
+
+
+@pytest.mark.parametrize("w", MAX_BATCH, ids=[w.name for w in MAX_BATCH])
+def test_maximum_batch_parity(w):
+    """The largest batch a plan accepts (4096 rows: 256 row tiles, beyond the
+    XCD-local loops' row tiles, so the library's own choice of loops), with
+    zero-length rows among them, against the oracle."""
+    inp = wl.generate(w)
+    say(f"[maxbatch] {w.name}")
+    res, err = run_case(w, inp)
+    assert err == 0
+    ref = oracle_reference(inp, w.layers, w.dtype)
+    assert res["T_eff"] == ref["T_eff"] == int(inp["seq_len"].max())
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
+
+
 # Shapes whose recurrent weights need more than one XCD: the chip-wide form
 # (bf16 H = 2048, f32 H = 1024), one row tile to all 16, ragged lengths, two
 # layers; against the oracle in that form and in the grid-barrier form.
