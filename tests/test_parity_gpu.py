@@ -748,3 +748,30 @@ def test_skip_cell_parity(w, margin):
     for l in range(w.layers):
         I_l = w.I if l == 0 else w.H
         assert not res["dbias"][l][4 * w.H:].any() and res["dbias"][l].shape[0] == 4 * w.H + I_l + w.H + 1
+
+
+@pytest.mark.parametrize("cell", ["rnn", "gru", "skip"])
+def test_other_cells_zero_trip(cell):
+    """Every length 0: the loop runs no iteration with any body, returns its
+    inits (hT = h0; the LSTM-state cT = c0 for the cond body, zeros for the
+    one-state cells) and passes the state gradients through; dW, db, dx are
+    zero (bitwise)."""
+    w = W(f"{cell}_zero_trip", B=20, I=16, H=64, T_max=5, dtype="bf16", len_lo=0, len_hi=0,
+          random_state=True, cell=cell, seed=71)
+    inp = wl.generate(w)
+    assert not inp["seq_len"].any()
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell=cell)
+    plan = dc.plan()
+    dc.fwd(plan)
+    dc.bwd(plan)
+    err = plan.status_sync()
+    res = dc.results()
+    plan.close()
+    assert err == 0 and res["T_eff"] == 0
+    np.testing.assert_array_equal(res["hT"], inp["h0"])
+    np.testing.assert_array_equal(res["cT"], inp["c0"] if cell == "skip" else 0 * inp["c0"])
+    np.testing.assert_array_equal(res["dh0"], inp["dhT"])
+    np.testing.assert_array_equal(res["dc0"], inp["dcT"] if cell == "skip" else 0 * inp["dcT"])
+    for k in ("y", "dx"):
+        assert not res[k].any(), k
+    assert not any(d.any() for d in res["dW"]) and not any(b.any() for b in res["dbias"])
