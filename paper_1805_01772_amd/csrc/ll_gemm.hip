@@ -386,11 +386,15 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_tn_bf16_lds_kernel(GemmTn
   constexpr int WGN = 2;
   constexpr int WM = BM / (NW / WGN), WN = BN / WGN;   // 64 x 128 per wave
   constexpr int MI = WM / 32, NI = WN / 32;
-  constexpr int KT = 64;                     // rows (k) per k-tile
+  constexpr int KT = 32;                     // rows (k) per k-tile
   constexpr int RC = BM * 2 / 16;            // 16-byte chunks per row of a k-tile (32)
   constexpr int CH = KT * RC;                // chunks per operand and stage
-  constexpr int LI = CH / 64 / NW;           // load instructions per wave and operand (4)
-  __shared__ uint4 sA0[CH], sA1[CH], sB0[CH], sB1[CH];
+  constexpr int LI = CH / 64 / NW;           // load instructions per wave and operand (2)
+  // four stages: the fills run three k-tiles ahead.  Every fill, map read
+  // and step is issued unconditionally (k-tiles past the end load zeros and
+  // add nothing), so each wave's memory operations follow one fixed pattern
+  // and the compiler's wait counts across the loop stay exact
+  __shared__ uint4 sA0[CH], sA1[CH], sA2[CH], sA3[CH], sB0[CH], sB1[CH], sB2[CH], sB3[CH];
 
   const int M = g.M;
   const int K = g.K_dev ? min(*g.K_dev, g.K) : g.K;
@@ -436,31 +440,30 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_tn_bf16_lds_kernel(GemmTn
     acol[i] = am0 + c * 8 < aM ? (unsigned)((am0 + c * 8) * 2) : kOOB;
     bcol[i] = n0 + c * 8 < g.N ? (unsigned)((n0 + c * 8) * 2) : kOOB;
   }
-  // row-map entries of the k-tile the next fill loads, read with no branch
-  // (past the map's end: zero), so the compiler does not wait for them
-  // before the fill that uses them, and with that for the fills in flight
+  // row-map entries, read with no branch (past the map's end: zero) four
+  // k-tiles ahead of the fill that uses them (buffer kt % 4)
   const bool has_map = a_rowmap != nullptr;
   const __amdgpu_buffer_rsrc_t rmap = make_rsrc(a_rowmap, has_map ? (unsigned)ke * 4u : 0u);
-  unsigned amap[LI];
-  auto load_map = [&](int kt) {
+  unsigned amap[4][LI];
+  auto load_map = [&](int kt, unsigned (&dst)[LI]) {
     const int k0 = kb + kt * KT;
 #pragma unroll
     for (int i = 0; i < LI; ++i)
-      amap[i] = __builtin_amdgcn_raw_buffer_load_b32(rmap, (unsigned)(k0 + lrow[i]) * 4u, 0, 0);
+      dst[i] = __builtin_amdgcn_raw_buffer_load_b32(rmap, (unsigned)(k0 + lrow[i]) * 4u, 0, 0);
   };
-  auto fill = [&](int kt, uint4* a_dst, uint4* b_dst) {
+  auto fill = [&](int kt, uint4* a_dst, uint4* b_dst, unsigned (&am)[LI]) {
     const int k0 = kb + kt * KT;
 #pragma unroll
     for (int i = 0; i < LI; ++i) {
       const int k = k0 + lrow[i];
       const bool ok = k < ke;
-      const long ar = has_map ? (long)amap[i] : (long)k;
+      const long ar = has_map ? (long)am[i] : (long)k;
       const unsigned ao = ok && acol[i] != kOOB ? (unsigned)(ar * lda * 2) + acol[i] : kOOB;
       const unsigned bo = ok && bcol[i] != kOOB ? (unsigned)((long)k * g.ldb * 2) + bcol[i] : kOOB;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(a_dst + (i * NW + wave) * 64), 16, ao, 0, 0, 0);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(b_dst + (i * NW + wave) * 64), 16, bo, 0, 0, 0);
     }
-    if (kt + 1 < nkt) load_map(kt + 1);
+    load_map(kt + 4, am);
   };
 
   f32x16 acc[MI][NI];
@@ -479,12 +482,17 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_tn_bf16_lds_kernel(GemmTn
     const unsigned off = (unsigned)((k_local * RC + ((col >> 3) ^ tn_swz(k_local))) * 16 + (col & 7) * 2);
     return ds_read_tr16(base, off);
   };
-  auto step = [&](int kt, const uint4* a, const uint4* b, uint4* a_next, uint4* b_next) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (kt + 1 < nkt) fill(kt + 1, a_next, b_next);
+  auto step = [&](int kt, const uint4* a, const uint4* b, uint4* a_fill, uint4* b_fill, unsigned (&am)[LI]) {
+    // k-tile kt's loads have landed (in flight still: the map reads its fill
+    // issued after them, 3 LI operations for each of the fills of kt + 1 and
+    // kt + 2); the barrier makes every wave's visible and ends every wave's
+    // reads of the stage refilled next (k-tile kt - 1's)
+    static_assert(7 * LI <= 15, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(0xF70 | (7 * LI));
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    fill(kt + 3, a_fill, b_fill, am);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < KT / 16; ++ks) {
       const int k_local = ks * 16 + rk;
       uint4 av[MI], bv[NI];
 #pragma unroll
@@ -507,14 +515,24 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_tn_bf16_lds_kernel(GemmTn
               __builtin_bit_cast(bf16x8_t, av[i]), __builtin_bit_cast(bf16x8_t, bv[j]), acc[i][j], 0, 0, 0);
     }
   };
-  if (nkt > 0) {
-    load_map(0);
-    fill(0, sA0, sB0);
+  // prologue: the maps of k-tiles 0 .. 3, the fills of 0 .. 2 (each fill
+  // then reads the map four k-tiles ahead into the buffer it just used)
+  load_map(0, amap[0]);
+  load_map(1, amap[1]);
+  load_map(2, amap[2]);
+  load_map(3, amap[3]);
+  fill(0, sA0, sB0, amap[0]);
+  fill(1, sA1, sB1, amap[1]);
+  fill(2, sA2, sB2, amap[2]);
+  for (int kt = 0; kt < nkt; kt += 4) {
+    step(kt, sA0, sB0, sA3, sB3, amap[3]);
+    step(kt + 1, sA1, sB1, sA0, sB0, amap[0]);
+    step(kt + 2, sA2, sB2, sA1, sB1, amap[1]);
+    step(kt + 3, sA3, sB3, sA2, sB2, amap[2]);
   }
-  for (int kt = 0; kt < nkt; kt += 2) {
-    step(kt, sA0, sB0, sA1, sB1);
-    if (kt + 1 < nkt) step(kt + 1, sA1, sB1, sA0, sB0);
-  }
+  // the fills issued past the last k-tile write this work-group's LDS:
+  // they land before the work-group (and its LDS) ends
+  __builtin_amdgcn_s_waitcnt(0xF70);
 
   // result register r of lane l: row (r % 4) + 8 (r / 4) + 4 (l / 32), column l % 32
   const int l32 = lane & 31, kc = lane >> 5;
