@@ -348,9 +348,9 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_nt_bf16_lds_kernel(GemmAr
 // ---------------------------------------------------------------------------
 // Product over rows, bf16: C[m][n] = sum_k A[arow(k)][m] B[k][n] (dW = [X;
 // Hprev]^T DZ straight from the row-major operands).  The same work-group
-// shape, tile order, two LDS stages and epilogue as the kernel above; what
-// differs is the operand layout.  A k-tile of either operand is 64 rows
-// (k) x 256 columns, loaded row by row (a row's 512 bytes are contiguous
+// shape, tile order and epilogue as the kernel above; what differs is the
+// operand layout and the pipeline depth (four LDS stages).  A k-tile of
+// either operand is 32 rows (k) x 256 columns, loaded row by row (a row's 512 bytes are contiguous
 // in memory): LDS holds [k][32 chunks of 16 bytes], chunk c of row k in
 // slot c ^ tn_swz(k).  The matrix-core operands need 8 consecutive k per
 // lane; gfx950's transposing LDS read (ds_read_b64_tr_b16) gives them: in
@@ -363,7 +363,7 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_nt_bf16_lds_kernel(GemmAr
 // distinct 32-byte bank groups within 128 bytes, and the eight row pieces of
 // two neighbouring groups at distinct ones within 256 bytes (measured on
 // the dW shape: 0.81 PFLOP/s against 0.70 without a swizzle).  The row map
-// of the next k-tile is loaded one k-tile ahead, so no fill waits on it.
+// of a k-tile is loaded four k-tiles ahead, so no fill waits on it.
 // ---------------------------------------------------------------------------
 namespace {
 
