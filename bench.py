@@ -55,56 +55,70 @@ def stage_flops(w, sum_len):
     return {k: float(np.mean(v)) for k, v in out.items()}
 
 
-def cpu_baseline(w, inp, target_s):
-    """The oracle as it is (float64, bf16-emulating for bf16 workloads) on the
-    full batch: the first T_s loop iterations when the whole run would take
-    longer than `target_s`, else the whole run repeated up to about
-    `target_s` seconds."""
-    import oracle
+def _blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = len(os.sched_getaffinity(0))
-    precision = "bf16" if w.dtype == "bf16" else "fp64"
+        return None
+
+
+def cpu_baseline(w, inp, target_s, precision="fp32", threads=None):
+    """The oracle as it is, in its batched masked form (BLAS products per
+    step, hand-written gradient loop) on the full batch: the first T_s loop
+    iterations when the whole run would take longer than `target_s`, else the
+    whole run repeated up to about `target_s` seconds.  precision "fp32" is
+    the float32 form; "bf16" the bfloat16-emulating float64 form the parity
+    tests use.  threads: BLAS threads (None: every core available to the
+    process)."""
+    import oracle
+    from threadpoolctl import threadpool_limits
+    avail = len(os.sched_getaffinity(0))
+    nthr = avail if threads is None else threads
+    dt_in = np.float32 if precision == "fp32" else np.float64
 
     def run(Ts):
         sl = np.minimum(inp["seq_len"], Ts)
-        x = inp["x"][:Ts].astype(np.float64)
-        dy = inp["dy"][:Ts].astype(np.float64) if inp["dy"] is not None else None
-        Ws = [a.astype(np.float64) for a in inp["W"]]
-        bs = [a.astype(np.float64) for a in inp["bias"]]
+        x = inp["x"][:Ts].astype(dt_in)
+        dy = inp["dy"][:Ts].astype(dt_in) if inp["dy"] is not None else None
+        Ws = [a.astype(dt_in) for a in inp["W"]]
+        bs = [a.astype(dt_in) for a in inp["bias"]]
+        h0, c0 = inp["h0"].astype(dt_in), inp["c0"].astype(dt_in)
+        dhT, dcT = inp["dhT"].astype(dt_in), inp["dcT"].astype(dt_in)
         t0 = time.perf_counter()
         if w.cell in ("rnn", "gru"):
             fwd, bwd = ((oracle.stacked_rnn_forward, oracle.stacked_rnn_backward) if w.cell == "rnn"
                         else (oracle.stacked_gru_forward, oracle.stacked_gru_backward))
-            _, _, tapes = fwd(x, sl, Ws, bs, inp["h0"].astype(np.float64), precision)
-            bwd(tapes, dy, inp["dhT"].astype(np.float64))
+            _, _, tapes = fwd(x, sl, Ws, bs, h0, precision)
+            bwd(tapes, dy, dhT)
         else:
             fwd, bwd = ((oracle.stacked_skip_forward, oracle.stacked_skip_backward) if w.cell == "skip"
                         else (oracle.stacked_forward, oracle.stacked_backward))
-            y, hT, cT, tapes = fwd(x, sl, Ws, bs, inp["h0"].astype(np.float64),
-                                   inp["c0"].astype(np.float64), precision)
-            bwd(tapes, dy, inp["dhT"].astype(np.float64), inp["dcT"].astype(np.float64))
+            y, hT, cT, tapes = fwd(x, sl, Ws, bs, h0, c0, precision)
+            bwd(tapes, dy, dhT, dcT)
         return time.perf_counter() - t0, int(sl.sum())
 
-    T_eff = int(inp["seq_len"].max())
-    dt, _ = run(2)
-    Ts = int(max(2, min(T_eff, target_s / max(dt / 2, 1e-6))))
-    dt, n = run(Ts)
-    reps = 1
-    if Ts == T_eff:
-        while dt < target_s and reps < 16:
-            d2, n2 = run(Ts)
-            dt += d2
-            n += n2
-            reps += 1
+    with threadpool_limits(limits=nthr):
+        used = _blas_threads() or nthr
+        T_eff = int(inp["seq_len"].max())
+        dt, _ = run(2)
+        Ts = int(max(2, min(T_eff, target_s / max(dt / 2, 1e-6))))
+        dt, n = run(Ts)
+        reps = 1
+        if Ts == T_eff:
+            while dt < target_s and reps < 16:
+                d2, n2 = run(Ts)
+                dt += d2
+                n += n2
+                reps += 1
     what = (f"first {Ts} of {T_eff} loop iterations" if Ts < T_eff
             else f"all {T_eff} loop iterations, {reps} runs")
-    return {"value": n / dt, "unit": "timesteps·seqs/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"full batch B={w.B}, {what} ({n} timesteps*seqs), "
-                      f"{precision} oracle fwd+bwd, {dt:.1f} s"}
+    form = ("float32 batched masked form (BLAS)" if precision == "fp32"
+            else "bfloat16-emulating float64 batched masked form")
+    return {"value": n / dt, "unit": "timesteps·seqs/s", "cores": int(used),
+            "cores_available": avail, "kind": "oracle",
+            "sample": f"full batch B={w.B}, {what} ({n} timesteps*seqs), oracle {form}, "
+                      f"fwd+bwd, {dt:.1f} s on {used} BLAS thread(s) of {avail} cores available"}
 
 
 # HBM traffic of the loop kernels, from rocprofv3 PMC runs (FETCH_SIZE and
@@ -278,13 +292,23 @@ def main():
                      "unit": "TFLOP/s", "frac": achieved / peak_tf,
                      "frac_of_measured_peak": achieved / measured_peak,
                      "traffic": recorded_traffic(dom, w.name),
+                     "traffic_source": "stored record in profiles/pmc_traffic.md (two rocprofv3 "
+                                       "--pmc passes, FETCH_SIZE and WRITE_SIZE, scaled by a plain "
+                                       "copy), used only while the kernel sources hash to the "
+                                       "recorded value, else null",
                      "per_launch_ms": per_launch[dom],
                      "algorithmic_flops_per_launch": sflops[dom]},
     }
     if spill:
         out["spill"] = spill
     if args.cpu_seconds > 0:
+        # the float32 form on every core available to the process, and on one
+        # core; the bfloat16-emulating form (the parity reference) for context
         out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
+        out["cpu_baseline_1core"] = cpu_baseline(w, inp, args.cpu_seconds / 3, threads=1)
+        if w.dtype == "bf16":
+            out["cpu_baseline_bf16_emulating"] = cpu_baseline(w, inp, args.cpu_seconds / 3,
+                                                              precision="bf16")
     print(json.dumps(out), flush=True)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)

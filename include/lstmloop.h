@@ -43,6 +43,8 @@
  *     asynchronous on it; they return after enqueueing.
  *   - A plan serves one stream at a time.  Calls on one plan must not
  *     overlap.
+ *   - Every array pointer is 16-byte aligned (the kernels move 16-byte
+ *     chunks); lstm_loop_fwd and lstm_loop_bwd return LL_EINVAL otherwise.
  *   - Errors: checkable arguments give an error code synchronously and the
  *     thread-local message of ll_last_error(); nothing is enqueued then.
  *     Data-dependent errors (seq_len outside [0, T_max]) are detected on the
@@ -136,6 +138,8 @@ typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1, LL_CELL_GRU = 2, LL_CELL_LSTM_
  *     XCD-local loops and spill = 0 (else LL_EUNSUPPORTED); the two layers
  *     then run one after the other.  The bias passed to lstm_loop_fwd is
  *     copied into the plan for the gradient pass.
+ *   reserved: must be 0 (LL_EINVAL otherwise), so that a later field can
+ *     take its place without changing what a zero-filled descriptor means.
  *   cell: an ll_cell.  LL_CELL_RNN, LL_CELL_GRU and LL_CELL_LSTM_SKIP need
  *     the XCD-local loops, spill = 0 and recompute = 0 (else
  *     LL_EUNSUPPORTED); the RNN's stack holds h_t only, the GRU's r, u, n,
@@ -154,6 +158,7 @@ typedef struct {
   int64_t device_stack_budget_bytes;
   int32_t recompute;
   int32_t cell;
+  int32_t reserved;   /* must be 0 (LL_EINVAL otherwise): room for later fields */
 } ll_desc;
 
 typedef struct ll_plan ll_plan;   /* opaque: owns the stack, scratch arrays,
@@ -165,8 +170,10 @@ typedef struct ll_plan ll_plan;   /* opaque: owns the stack, scratch arrays,
  * new plan; on failure *out is NULL and nothing stays allocated. */
 ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out);
 
-/* Free everything the plan owns.  Waits for the plan's outstanding work.
- * NULL is accepted. */
+/* Free everything the plan owns.  Waits for the plan's outstanding work (the
+ * last call's work on its stream, and the plan's own side and copy streams;
+ * no device-wide synchronisation).  Call it before the process exits: the HIP
+ * runtime may already be torn down inside exit handlers.  NULL is accepted. */
 ll_status ll_plan_destroy(ll_plan* plan);
 
 /* Bytes of stack storage the plan holds in device memory and in pinned host
@@ -192,17 +199,20 @@ ll_status ll_plan_stack_bytes(const ll_plan* plan, int64_t* device_bytes,
  * the grid-barrier form; LSTMLOOP_WAVEFRONT=off runs the layers one after
  * the other.  The wavefront needs the XCD-local loops, no spill and
  * 2H / units_per_workgroup <= 32; its results equal the layer-by-layer
- * ones up to the order of floating-point sums. */
+ * ones up to the order of floating-point sums.  dw_in_place: bit l set when
+ * layer l's dW products read x (or the layer below's h history), the h history
+ * and dz in place, row by row (bfloat16 layers whose reduction is short enough
+ * for that to be faster and whose operands stay below 2^31 bytes); clear when
+ * they read transposed copies. */
 ll_status ll_plan_geometry(const ll_plan* plan, int32_t* loop_workgroups,
                            int32_t* units_per_workgroup,
                            int32_t* row_groups, int32_t* loop_form,
-                           int32_t* wavefront);
+                           int32_t* wavefront, int32_t* dw_in_place);
 
 /*
  * Forward while-loop (Sections 2.1, 4.2, 5.1).
- *   x        [T_max,B,I] dtype, 16-byte aligned (LL_BF16: lstm_loop_bwd
- *            returns LL_EUNSUPPORTED otherwise); entries at t >= seq_len[b]
- *            are never read into a kept result (they may hold NaN).
+ *   x        [T_max,B,I] dtype; entries at t >= seq_len[b] are never read
+ *            into a kept result (they may hold NaN).
  *   seq_len  [B] int32, each in [0, T_max].
  *   W, bias  host arrays of `layers` device pointers (see conventions).
  *   h0, c0   [layers,B,H] float, or NULL for zeros.
@@ -214,7 +224,9 @@ ll_status ll_plan_geometry(const ll_plan* plan, int32_t* loop_workgroups,
  *   trip_count  device int32 scalar receiving T_eff, or NULL.
  *   save_for_backward  nonzero: push the stack for lstm_loop_bwd; the plan
  *            keeps x, seq_len, W, h0, c0 pointers, which must stay valid and
- *            unchanged until the backward has been enqueued.
+ *            unchanged until the backward has been enqueued (lstm_loop_bwd
+ *            takes x, seq_len and W again and checks that they are the same
+ *            pointers).
  *            Zero: inference, nothing is saved.
  */
 ll_status lstm_loop_fwd(ll_plan* plan, void* stream,
@@ -228,6 +240,12 @@ ll_status lstm_loop_fwd(ll_plan* plan, void* stream,
  * Gradient while-loop (Sections 5.1, 5.2): runs T_eff iterations in reverse,
  * popping the stack of the last lstm_loop_fwd(save_for_backward=1) on this
  * plan.  Returns LL_ESTATE if there is none.  Consumes the saved stack.
+ *   x, seq_len, W  the same device pointers (W: host array of `layers`
+ *            device pointers) as the matching lstm_loop_fwd; the gradient
+ *            pass reads x and W again (dW products, dx = dz W_x^T) and the
+ *            lengths through the forward's length order.  A pointer that
+ *            differs from the saved forward's gives LL_EINVAL; nothing is
+ *            enqueued and the saved stack is kept.
  *   dy       [T_max,B,H] float gradient of y, or NULL (zero).
  *   dhT, dcT [layers,B,H] float gradients of hT/cT, or NULL (zero).
  *   dx       [T_max,B,I] float output (0 where t >= seq_len[b]) or NULL.
@@ -238,6 +256,7 @@ ll_status lstm_loop_fwd(ll_plan* plan, void* stream,
  *   dh0, dc0 [layers,B,H] float outputs, or NULL.
  */
 ll_status lstm_loop_bwd(ll_plan* plan, void* stream,
+                        const void* x, const int32_t* seq_len, const void* const* W,
                         const float* dy, const float* dhT, const float* dcT,
                         float* dx, float* const* dW, float* const* dbias,
                         float* dh0, float* dc0);
@@ -290,6 +309,14 @@ ll_status ll_plan_read_timing(ll_plan* plan, int32_t stage, double* total_ms,
  *               gfx950 runs at the datasheet rate.
  * Other shape values give LL_EINVAL. */
 ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, int32_t shape, double* tflops);
+
+/* Diagnostic: the cell's activation functions exactly as the loop kernels
+ * compute them, applied to n floats on `device` (in, out: device pointers;
+ * synchronous).  fn = 0: the logistic sigmoid 1 / (1 + e^-u) of the i, f, o
+ * gates; fn = 1: tanh (the g gate, tanh(c_t), the Elman and GRU bodies).  The
+ * paper gives no cell equations; these are the textbook LSTM's.  Other fn
+ * values or n < 0 give LL_EINVAL. */
+ll_status ll_eval_activations(int32_t device, const float* in, float* out, int64_t n, int32_t fn);
 
 /* Library version string. */
 const char* ll_version(void);

@@ -23,12 +23,12 @@ __global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_
                                                     int T_max, int* __restrict__ perm,
                                                     int* __restrict__ active, int* __restrict__ off,
                                                     int* __restrict__ rowmap, int* __restrict__ meta,
-                                                    int* __restrict__ trip_out, int t_in_lds) {
+                                                    int* __restrict__ trip_out, int t_in_lds, int n_pow2) {
   extern __shared__ int smem[];
-  int* s_len = smem;              // [B]
-  int* s_sorted = smem + B;       // [B] lengths in perm order
-  int* s_perm = smem + 2 * B;     // [B]
-  int* s_act = smem + 3 * B;      // [T_max + 1] when t_in_lds
+  // sort keys: (T_max - length) << 32 | row, ascending = decreasing length,
+  // ties by row index; entries n_pow2 > B pad with the largest key
+  unsigned long long* s_key = reinterpret_cast<unsigned long long*>(smem);   // [n_pow2]
+  int* s_act = smem + 2 * n_pow2; // [T_max + 1] when t_in_lds
   int* s_off = s_act + T_max + 1; // [T_max + 1] when t_in_lds
   __shared__ int s_bad;
   __shared__ int s_wsum[16];
@@ -39,30 +39,41 @@ __global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_
   __syncthreads();
   for (int b = tid; b < B; b += nt) {
     const int L = seq_len[b];
-    s_len[b] = L;
     if (L < 0 || L > T_max) s_bad = 1;
+    s_key[b] = ((unsigned long long)(unsigned)(T_max - (L < 0 || L > T_max ? 0 : L)) << 32) | (unsigned)b;
   }
+  for (int b = B + tid; b < n_pow2; b += nt) s_key[b] = ~0ull;
   __syncthreads();
   const int bad = s_bad;
-  for (int b = tid; b < B; b += nt) {
-    const int L = s_len[b];
-    int rank = 0;
-    for (int o = 0; o < B; ++o) {
-      const int Lo = s_len[o];
-      rank += (Lo > L) || (Lo == L && o < b);
+  // bitonic sort of the n_pow2 keys (O(B log^2 B) compare-exchanges, all in LDS)
+  for (int k = 2; k <= n_pow2; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < n_pow2; i += nt) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const unsigned long long u = s_key[i], v = s_key[ixj];
+          const bool up = (i & k) == 0;
+          if ((u > v) == up) {
+            s_key[i] = v;
+            s_key[ixj] = u;
+          }
+        }
+      }
+      __syncthreads();
     }
-    perm[rank] = b;
-    s_perm[rank] = b;
-    s_sorted[rank] = bad ? 0 : L;
   }
-  __syncthreads();
-  const int T_eff = B > 0 ? s_sorted[0] : 0;
+  // sorted row r: perm[r] = row index, length T_max - (key >> 32) (0 for
+  // every row when some length is out of range)
+  auto s_perm = [&](int r) { return (int)(unsigned)(s_key[r] & 0xffffffffu); };
+  auto s_sorted = [&](int r) { return bad ? 0 : T_max - (int)(unsigned)(s_key[r] >> 32); };
+  for (int r = tid; r < B; r += nt) perm[r] = s_perm(r);
+  const int T_eff = B > 0 ? s_sorted(0) : 0;
   // active[t] = #{r : sorted length > t}; lengths are non-increasing in r
   for (int t = tid; t <= T_max; t += nt) {
     int lo = 0, hi = B;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
-      if (s_sorted[mid] > t) lo = mid + 1; else hi = mid;
+      if (s_sorted(mid) > t) lo = mid + 1; else hi = mid;
     }
     active[t] = lo;
     if (t_in_lds) s_act[t] = lo;
@@ -99,7 +110,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_
   for (int t = wave; t < T_eff; t += nwaves) {
     const int n = t_in_lds ? s_act[t] : active[t];
     const int o = t_in_lds ? s_off[t] : off[t];
-    for (int r = lane; r < n; r += 64) rowmap[o + r] = t * B + s_perm[r];
+    for (int r = lane; r < n; r += 64) rowmap[o + r] = t * B + s_perm(r);
   }
   if (tid == 0) {
     meta[0] = T_eff;
@@ -310,11 +321,15 @@ __global__ __launch_bounds__(256) void convert_kernel(const float* __restrict__ 
 // ------------------------------------------------------------ launchers
 hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
                        int* rowmap, int* meta, int* trip_out, hipStream_t s) {
-  // per-step counts and offsets stay in LDS when all fits in 64 KB
-  const int t_in_lds = (3 * (size_t)B + 2 * ((size_t)T_max + 1)) * sizeof(int) <= 64 * 1024;
-  const size_t smem = sizeof(int) * (3 * (size_t)B + (t_in_lds ? 2 * ((size_t)T_max + 1) : 0));
+  int n_pow2 = 1;
+  while (n_pow2 < B) n_pow2 <<= 1;
+  // sort keys (8 bytes per row, B <= 4096: at most 32 KB), and the per-step
+  // counts and offsets when all fits in 64 KB
+  const size_t keys = (size_t)n_pow2 * 8;
+  const int t_in_lds = keys + 2 * ((size_t)T_max + 1) * sizeof(int) <= 64 * 1024;
+  const size_t smem = keys + (t_in_lds ? 2 * ((size_t)T_max + 1) * sizeof(int) : 0);
   hipLaunchKernelGGL(prep_kernel, dim3(1), dim3(1024), smem, s, seq_len, B, T_max, perm, active,
-                     off, rowmap, meta, trip_out, t_in_lds);
+                     off, rowmap, meta, trip_out, t_in_lds, n_pow2);
   return hipGetLastError();
 }
 
@@ -365,6 +380,24 @@ __global__ __launch_bounds__(256) void mfma_peak_kernel(int iters, float* sink) 
     for (int c = 0; c < 8; ++c) s += acc[c][0] + acc[c][1] + acc[c][2] + acc[c][3];
   }
   if (s == 1234.5f) sink[threadIdx.x] = s;
+}
+
+// The cell's activation functions applied element-wise (fn 0: sigmoid,
+// 1: tanh), for checking them against a float64 reference.
+__global__ __launch_bounds__(256) void eval_activations_kernel(const float* __restrict__ in,
+                                                               float* __restrict__ out, long n, int fn) {
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
+    const float u = in[i];
+    out[i] = fn == 0 ? sigmoidf_(u) : tanhf_(u);
+  }
+}
+
+hipError_t eval_activations(const float* in, float* out, long n, int fn, hipStream_t s) {
+  long blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(eval_activations_kernel, dim3((unsigned)blocks), dim3(256), 0, s, in, out, n, fn);
+  return hipGetLastError();
 }
 
 template <typename T>

@@ -278,6 +278,8 @@ hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s);
 // k-step the loops use, or the 32x32 shape.
 template <typename T>
 hipError_t measure_mfma_peak(int n_cu, bool shape32, double* tflops);
+// sigmoid (fn 0) or tanh (fn 1) of n floats, as the loop kernels compute them
+hipError_t eval_activations(const float* in, float* out, long n, int fn, hipStream_t s);
 
 hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
                        int* rowmap, int* meta, int* trip_out, hipStream_t s);

@@ -142,6 +142,8 @@ struct ll_plan {
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   hipEvent_t ev_side = nullptr;   // side-stream work started at a call's beginning
   hipEvent_t ev_compute = nullptr;
+  hipEvent_t ev_done = nullptr;   // recorded on the call's stream at the end of every call
+  bool done_recorded = false;
   std::vector<hipEvent_t> ev_d2h, ev_h2d;   // per (layer, slot)
   float* carry = nullptr;      // [4][B, H]: h, c (forward) / dh, dc (backward) between chunks
   float* db_state = nullptr;   // per-thread db sums between backward chunks
@@ -299,6 +301,7 @@ void free_plan_memory(ll_plan* p) {
   if (p->ev_fork) (void)hipEventDestroy(p->ev_fork);
   if (p->ev_join) (void)hipEventDestroy(p->ev_join);
   if (p->ev_side) (void)hipEventDestroy(p->ev_side);
+  if (p->ev_done) (void)hipEventDestroy(p->ev_done);
   if (p->gstream) (void)hipStreamDestroy(p->gstream);
 }
 
@@ -370,6 +373,7 @@ ll_status validate_desc(const ll_desc* d) {
   if (d->I % ialign)
     return fail(LL_EUNSUPPORTED, "I = %d must be a multiple of %d for this dtype", d->I, ialign);
   if (d->B > 4096) return fail(LL_EUNSUPPORTED, "B = %d exceeds 4096", d->B);
+  if (d->reserved != 0) return fail(LL_EINVAL, "desc.reserved must be 0 (got %d)", d->reserved);
   return LL_OK;
 }
 
@@ -394,6 +398,20 @@ ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, int32_t shape, dou
   *tflops = 0.0;
   LL_HIP(dtype == LL_BF16 ? ll::measure_mfma_peak<bf16_t>(prop.multiProcessorCount, shape == 32, tflops)
                           : ll::measure_mfma_peak<float>(prop.multiProcessorCount, shape == 32, tflops));
+  return LL_OK;
+}
+
+ll_status ll_eval_activations(int32_t device, const float* in, float* out, int64_t n, int32_t fn) {
+  if (fn != 0 && fn != 1) return fail(LL_EINVAL, "fn must be 0 (sigmoid) or 1 (tanh), got %d", fn);
+  if (n < 0) return fail(LL_EINVAL, "n = %lld is negative", (long long)n);
+  if (n > 0 && (!in || !out)) return fail(LL_EINVAL, "in and out are required");
+  int ndev = 0;
+  LL_HIP(hipGetDeviceCount(&ndev));
+  if (device < 0 || device >= ndev) return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
+  if (n == 0) return LL_OK;
+  DeviceGuard guard(device);
+  LL_HIP(ll::eval_activations(in, out, (long)n, fn, nullptr));
+  LL_HIP(hipStreamSynchronize(nullptr));
   return LL_OK;
 }
 
@@ -578,10 +596,17 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   // product, whichever the model says is shorter: rows win while
   // flops / transposed bytes < ~1170 (H = I = 1024: ~683; H = I = 2048: ~1365)
   p->ws_floats = 0;
+  // The product over rows addresses each operand (x or the layer below's
+  // h history, this layer's h history with the h0 rows, dz) through 32-bit
+  // buffer offsets: a layer whose operand reaches 2^31 bytes takes the
+  // transposes instead, whatever the model says.
   for (int l = 0; l < L; ++l) {
     const double Il = in_width(p, l);
     const double flops = 2.0 * (Il + H) * p->G * H, bytes = (Il + H + p->GB * H) * 2.0 * p->es;
-    p->dw_rows[l] = p->bf16 && flops / bytes < 1170.0;
+    const long lim = 1L << 31;
+    const bool fits = p->cap * (long)Il * 2 < lim && (p->cap + B) * (long)H * 2 < lim &&
+                      p->cap * (long)p->GB * H * 2 < lim;
+    p->dw_rows[l] = p->bf16 && fits && flops / bytes < 1170.0;
   }
   for (int l = 0; l < L; ++l) {   // the products over rows
     if (!p->dw_rows[l]) continue;
@@ -704,7 +729,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   if (hipStreamCreateWithFlags(&p->gstream, hipStreamNonBlocking) != hipSuccess ||
       hipEventCreateWithFlags(&p->ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&p->ev_join, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&p->ev_side, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&p->ev_side, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&p->ev_done, hipEventDisableTiming) != hipSuccess) {
     free_plan_memory(p);
     delete p;
     return fail(LL_EHIP, "creating the plan's side stream failed");
@@ -747,7 +773,12 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
 ll_status ll_plan_destroy(ll_plan* p) {
   if (!p) return LL_OK;
   DeviceGuard guard(p->device);
-  hipDeviceSynchronize();
+  // the plan's own work only: the last call's work (its closing event, which
+  // stays valid even if the caller has destroyed that stream), the side
+  // stream and the copy stream
+  if (p->ev_done && p->done_recorded) (void)hipEventSynchronize(p->ev_done);
+  if (p->gstream) (void)hipStreamSynchronize(p->gstream);
+  if (p->cstream) (void)hipStreamSynchronize(p->cstream);
   drain_timing(p);
   for (hipEvent_t e : p->ev_pool) hipEventDestroy(e);
   free_plan_memory(p);
@@ -790,8 +821,9 @@ ll_status ll_plan_stack_bytes(const ll_plan* p, int64_t* dev, int64_t* host) {
 }
 
 ll_status ll_plan_geometry(const ll_plan* p, int32_t* nwg, int32_t* hj, int32_t* rg,
-                           int32_t* loop_form, int32_t* wavefront) {
+                           int32_t* loop_form, int32_t* wavefront, int32_t* dw_in_place) {
   if (!p) return fail(LL_EINVAL, "plan is NULL");
+  if (dw_in_place) *dw_in_place = (p->dw_rows[0] ? 1 : 0) | (p->dw_rows[1] ? 2 : 0);
   if (nwg) *nwg = (p->xmode || p->cmode) ? 256 : p->geom.nwg;
   if (hj) *hj = p->xmode ? (p->bf16 ? 32 : 16) : p->cmode ? p->d.H / 256 : p->geom.HJ;
   if (rg) *rg = p->xmode ? 8 : p->cmode ? 1 : p->geom.RG;
@@ -1224,9 +1256,10 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
       g.K = (int)p->cap;
       g.K_dev = p->meta + 1;
       g.splits = p->tn_splits[l][k];
+      // (the plan chose this path only for operands below 2^31 bytes, and
+      // lstm_loop_fwd accepted only a 16-byte aligned x)
       if (!ll::gemm_tn_applies(g))
-        return fail(LL_EUNSUPPORTED, "bf16 dW reads x, the h history and dz as 16-byte aligned rows; x = %p is not",
-                    p->x);
+        return fail(LL_EHIP, "internal: the dW product over rows does not apply to layer %d", l);
       float* out = dW[l] + (long)q.a_row * GH + q.c_col;
       if (g.splits > 1) {
         g.C = p->ws;
@@ -1638,6 +1671,18 @@ ll_status lstm_loop_fwd(ll_plan* p, void* stream, const void* x, const int32_t* 
     return fail(LL_EINVAL, "x, seq_len, W, bias, hT and (LSTM) cT are required");
   for (int l = 0; l < p->d.layers; ++l)
     if (!W[l] || !bias[l]) return fail(LL_EINVAL, "W[%d] or bias[%d] is NULL", l, l);
+  // the kernels read and write every array in 16-byte chunks
+  {
+    const void* ptrs[] = {x, seq_len, h0, c0, y, hT, cT, trip_count};
+    const char* names[] = {"x", "seq_len", "h0", "c0", "y", "hT", "cT", "trip_count"};
+    for (int i = 0; i < 8; ++i)
+      if (reinterpret_cast<uintptr_t>(ptrs[i]) & 15)
+        return fail(LL_EINVAL, "%s = %p is not 16-byte aligned", names[i], ptrs[i]);
+    for (int l = 0; l < p->d.layers; ++l)
+      if ((reinterpret_cast<uintptr_t>(W[l]) | reinterpret_cast<uintptr_t>(bias[l])) & 15)
+        return fail(LL_EINVAL, "W[%d] = %p or bias[%d] = %p is not 16-byte aligned", l, W[l], l,
+                    (const void*)bias[l]);
+  }
   DeviceGuard guard(p->device);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   p->state = ST_EMPTY;
@@ -1646,6 +1691,7 @@ ll_status lstm_loop_fwd(ll_plan* p, void* stream, const void* x, const int32_t* 
                          : enqueue_fwd<float>(p, s, x, seq_len, W, bias, h0, c0, y, hT, cT,
                                               trip_count, save_for_backward != 0);
   p->last_stream = s;
+  if (hipEventRecord(p->ev_done, s) == hipSuccess) p->done_recorded = true;
   if (st != LL_OK) return st;
   if (save_for_backward) {
     p->state = ST_FWD_DONE;
@@ -1658,21 +1704,41 @@ ll_status lstm_loop_fwd(ll_plan* p, void* stream, const void* x, const int32_t* 
   return LL_OK;
 }
 
-ll_status lstm_loop_bwd(ll_plan* p, void* stream, const float* dy, const float* dhT,
+ll_status lstm_loop_bwd(ll_plan* p, void* stream, const void* x, const int32_t* seq_len,
+                        const void* const* W, const float* dy, const float* dhT,
                         const float* dcT, float* dx, float* const* dW, float* const* dbias,
                         float* dh0, float* dc0) {
   if (!p) return fail(LL_EINVAL, "plan is NULL");
   if (p->state != ST_FWD_DONE)
     return fail(LL_ESTATE, "no saved forward on this plan (call lstm_loop_fwd with "
                            "save_for_backward=1 first)");
+  if (!x || !seq_len || !W) return fail(LL_EINVAL, "x, seq_len and W are required");
+  if (x != p->x || seq_len != p->seq_len)
+    return fail(LL_EINVAL, "x or seq_len differs from the saved forward's (%p, %p saved; %p, %p given)",
+                p->x, (const void*)p->seq_len, x, (const void*)seq_len);
+  for (int l = 0; l < p->d.layers; ++l)
+    if (W[l] != p->W[l])
+      return fail(LL_EINVAL, "W[%d] = %p differs from the saved forward's %p", l, W[l], p->W[l]);
   if (!dW || !dbias) return fail(LL_EINVAL, "dW and dbias are required");
   for (int l = 0; l < p->d.layers; ++l)
     if (!dW[l] || !dbias[l]) return fail(LL_EINVAL, "dW[%d] or dbias[%d] is NULL", l, l);
+  {
+    const void* ptrs[] = {dy, dhT, dcT, dx, dh0, dc0};
+    const char* names[] = {"dy", "dhT", "dcT", "dx", "dh0", "dc0"};
+    for (int i = 0; i < 6; ++i)
+      if (reinterpret_cast<uintptr_t>(ptrs[i]) & 15)
+        return fail(LL_EINVAL, "%s = %p is not 16-byte aligned", names[i], ptrs[i]);
+    for (int l = 0; l < p->d.layers; ++l)
+      if ((reinterpret_cast<uintptr_t>(dW[l]) | reinterpret_cast<uintptr_t>(dbias[l])) & 15)
+        return fail(LL_EINVAL, "dW[%d] = %p or dbias[%d] = %p is not 16-byte aligned", l, (void*)dW[l], l,
+                    (void*)dbias[l]);
+  }
   DeviceGuard guard(p->device);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   ll_status st = p->bf16 ? enqueue_bwd<bf16_t>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0)
                          : enqueue_bwd<float>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
   p->last_stream = s;
+  if (hipEventRecord(p->ev_done, s) == hipSuccess) p->done_recorded = true;
   p->state = ST_EMPTY;
   return st;
 }
@@ -1680,7 +1746,7 @@ ll_status lstm_loop_bwd(ll_plan* p, void* stream, const float* dy, const float* 
 ll_status ll_status_sync(ll_plan* p, int32_t* device_error) {
   if (!p) return fail(LL_EINVAL, "plan is NULL");
   DeviceGuard guard(p->device);
-  LL_HIP(hipStreamSynchronize(p->last_stream));
+  if (p->done_recorded) LL_HIP(hipEventSynchronize(p->ev_done));
   int32_t e = 0;
   LL_HIP(hipMemcpy(&e, p->meta + 2, sizeof(int32_t), hipMemcpyDeviceToHost));
   const int32_t zero = 0;

@@ -7,8 +7,10 @@ If the library has not been built, every call raises; there is no fallback.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import weakref
 from typing import Optional, Sequence
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -26,7 +28,7 @@ EXPORTED = ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes",
             "ll_plan_geometry", "lstm_loop_fwd", "lstm_loop_bwd",
             "ll_status_sync", "ll_last_error", "ll_version",
             "ll_plan_set_timing", "ll_plan_set_timing_stages", "ll_plan_read_timing",
-            "ll_measure_mfma_peak")
+            "ll_measure_mfma_peak", "ll_eval_activations")
 STAGES = ("prep", "input_proj", "fwd_loop", "bwd_loop", "bwd_operands", "dw", "dx", "loop_setup",
           "recompute")
 
@@ -37,7 +39,8 @@ class ll_desc(ctypes.Structure):
                 ("layers", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("spill", ctypes.c_int32), ("spill_chunk_steps", ctypes.c_int32),
                 ("device_stack_budget_bytes", ctypes.c_int64),
-                ("recompute", ctypes.c_int32), ("cell", ctypes.c_int32)]
+                ("recompute", ctypes.c_int32), ("cell", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class LoopError(RuntimeError):
@@ -47,6 +50,20 @@ class LoopError(RuntimeError):
 
 
 _lib = None
+# Plans still open: closed by an exit hook that runs while the HIP runtime is
+# alive (its own teardown happens later, in the C library's exit handlers).
+_live_plans: "weakref.WeakSet[Plan]" = weakref.WeakSet()
+
+
+def _close_live_plans() -> None:
+    for plan in list(_live_plans):
+        try:
+            plan.close()
+        except Exception:
+            pass
+
+
+atexit.register(_close_live_plans)
 
 
 def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -69,22 +86,24 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ll_plan_stack_bytes.argtypes = [vp, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.ll_plan_geometry.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32),
                                      ctypes.POINTER(i32), ctypes.POINTER(i32),
-                                     ctypes.POINTER(i32)]
+                                     ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.lstm_loop_fwd.argtypes = [vp, vp, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp),
                                   vp, vp, vp, vp, vp, vp, i32]
-    lib.lstm_loop_bwd.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.POINTER(vp),
-                                  ctypes.POINTER(vp), vp, vp]
+    lib.lstm_loop_bwd.argtypes = [vp, vp, vp, vp, ctypes.POINTER(vp), vp, vp, vp, vp,
+                                  ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp]
     lib.ll_status_sync.argtypes = [vp, ctypes.POINTER(i32)]
     lib.ll_plan_set_timing.argtypes = [vp, i32]
     lib.ll_plan_set_timing_stages.argtypes = [vp, ctypes.c_uint32]
     lib.ll_plan_read_timing.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(i64)]
     lib.ll_measure_mfma_peak.argtypes = [ctypes.c_int, i32, i32, ctypes.POINTER(ctypes.c_double)]
+    lib.ll_eval_activations.argtypes = [ctypes.c_int32, vp, vp, i64, i32]
     lib.ll_last_error.restype = ctypes.c_char_p
     lib.ll_version.restype = ctypes.c_char_p
     for name in ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes", "ll_plan_geometry",
                  "lstm_loop_fwd", "lstm_loop_bwd", "ll_status_sync", "ll_plan_set_timing",
-                 "ll_plan_set_timing_stages", "ll_plan_read_timing", "ll_measure_mfma_peak"):
+                 "ll_plan_set_timing_stages", "ll_plan_read_timing", "ll_measure_mfma_peak",
+                 "ll_eval_activations"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -101,6 +120,16 @@ def ll_measure_mfma_peak(dtype: str, shape: int = 32, device: int = 0) -> float:
     _check(load_library().ll_measure_mfma_peak(device, LL_BF16 if dtype == "bf16" else LL_F32, shape,
                                                ctypes.byref(v)))
     return v.value
+
+
+def ll_eval_activations(x, fn: str):
+    """The loop kernels' sigmoid ("sigmoid") or tanh ("tanh") of the float32
+    device tensor x (ll_eval_activations); returns a new tensor."""
+    import torch
+    out = torch.empty_like(x)
+    _check(load_library().ll_eval_activations(x.device.index or 0, _ptr(x), _ptr(out), x.numel(),
+                                              {"sigmoid": 0, "tanh": 1}[fn]))
+    return out
 
 
 def ll_version() -> str:
@@ -152,6 +181,7 @@ class Plan:
         h = ctypes.c_void_p()
         _check(lib.ll_plan_create(ctypes.byref(self.desc), device, ctypes.byref(h)))
         self._h = h
+        _live_plans.add(self)
 
     def close(self) -> None:
         if getattr(self, "_h", None) is not None and self._h.value:
@@ -180,12 +210,14 @@ class Plan:
         return d.value, h.value
 
     def geometry(self):
-        n, hj, rg, xl, wf = (ctypes.c_int32() for _ in range(5))
+        n, hj, rg, xl, wf, dwp = (ctypes.c_int32() for _ in range(6))
         _check(self._lib.ll_plan_geometry(self._h, ctypes.byref(n), ctypes.byref(hj),
-                                          ctypes.byref(rg), ctypes.byref(xl), ctypes.byref(wf)))
+                                          ctypes.byref(rg), ctypes.byref(xl), ctypes.byref(wf),
+                                          ctypes.byref(dwp)))
         form = {LL_LOOPS_GRID: "grid", LL_LOOPS_XCD: "xcd", LL_LOOPS_CHIP: "chip"}[xl.value]
         return dict(workgroups=n.value, units_per_workgroup=hj.value, row_groups=rg.value,
-                    loops=form, xcd_local=form == "xcd", wavefront=bool(wf.value))
+                    loops=form, xcd_local=form == "xcd", wavefront=bool(wf.value),
+                    dw_in_place=[bool(dwp.value >> l & 1) for l in range(self.desc.layers)])
 
     def fwd(self, x, seq_len, W: Sequence, bias: Sequence, h0, c0, y, hT, cT,
             trip_count=None, save_for_backward: bool = True, stream=None) -> None:
@@ -195,12 +227,14 @@ class Plan:
             _ptr(h0), _ptr(c0), _ptr(y), _ptr(hT), _ptr(cT), _ptr(trip_count),
             1 if save_for_backward else 0))
 
-    def bwd(self, dy, dhT, dcT, dx, dW: Sequence, dbias: Sequence, dh0, dc0,
-            stream=None) -> None:
-        """lstm_loop_bwd (asynchronous on `stream`)."""
+    def bwd(self, x, seq_len, W: Sequence, dy, dhT, dcT, dx, dW: Sequence, dbias: Sequence,
+            dh0, dc0, stream=None) -> None:
+        """lstm_loop_bwd (asynchronous on `stream`); x, seq_len and W are the
+        tensors the saved forward was given."""
         _check(self._lib.lstm_loop_bwd(
-            self._h, _stream(stream), _ptr(dy), _ptr(dhT), _ptr(dcT), _ptr(dx),
-            _ptr_array(dW), _ptr_array(dbias), _ptr(dh0), _ptr(dc0)))
+            self._h, _stream(stream), _ptr(x), _ptr(seq_len), _ptr_array(W), _ptr(dy),
+            _ptr(dhT), _ptr(dcT), _ptr(dx), _ptr_array(dW), _ptr_array(dbias), _ptr(dh0),
+            _ptr(dc0)))
 
     def set_timing(self, enable) -> None:
         """ll_plan_set_timing: clear the stage accumulators, start/stop recording

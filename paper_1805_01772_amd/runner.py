@@ -62,8 +62,8 @@ class DeviceCase:
                  self.y, self.hT, self.cT, self.trip, save_for_backward=save)
 
     def bwd(self, plan: Plan, with_dy: bool = True) -> None:
-        plan.bwd(self.dy if with_dy else None, self.dhT, self.dcT, self.dx, self.dW,
-                 self.dbias, self.dh0, self.dc0)
+        plan.bwd(self.x, self.seq_len, self.W, self.dy if with_dy else None, self.dhT,
+                 self.dcT, self.dx, self.dW, self.dbias, self.dh0, self.dc0)
 
     def results(self) -> dict:
         torch.cuda.synchronize(self.dev)

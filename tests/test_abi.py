@@ -68,11 +68,13 @@ def test_version_string():
     (dict(H=48), ll.LL_EUNSUPPORTED),
     (dict(I=6), ll.LL_EUNSUPPORTED),
     (dict(B=5000), ll.LL_EUNSUPPORTED),
+    (dict(reserved=1), ll.LL_EINVAL),
+    (dict(reserved=-7), ll.LL_EINVAL),
 ])
 def test_descriptor_validation(fields, status):
     lib = _lib()
     base = dict(T_max=8, B=4, I=32, H=32, layers=1, dtype=ll.LL_BF16, spill=0,
-                spill_chunk_steps=0, device_stack_budget_bytes=0, recompute=0, cell=0)
+                spill_chunk_steps=0, device_stack_budget_bytes=0, recompute=0, cell=0, reserved=0)
     base.update(fields)
     d = ll.ll_desc(**base)
     h = ctypes.c_void_p(123)
@@ -85,8 +87,8 @@ def test_descriptor_validation(fields, status):
 def test_null_arguments_rejected():
     lib = _lib()
     assert lib.ll_plan_create(None, 0, None) == ll.LL_EINVAL
-    assert lib.lstm_loop_bwd(None, None, None, None, None, None, None, None, None, None) \
-        == ll.LL_EINVAL
+    assert lib.lstm_loop_bwd(None, None, None, None, None, None, None, None, None, None, None,
+                             None, None) == ll.LL_EINVAL
     assert lib.ll_plan_destroy(None) == ll.LL_OK
 
 
@@ -105,3 +107,30 @@ def test_binding_constants_match_the_header():
     assert len(forms) == 3
     for name, val in forms.items():
         assert getattr(ll, name) == int(val), name
+
+
+def test_descriptor_layout_matches_the_header():
+    """The binding's ll_desc has the header's fields in the header's order
+    (the C struct is passed by pointer, so a mismatch would shift fields)."""
+    text = open(HEADER).read()
+    body = text[text.index("typedef struct {", text.index("Problem description")):]
+    body = body[:body.index("} ll_desc;")]
+    fields = re.findall(r"^\s*(int32_t|int64_t)\s+([a-z_A-Z0-9]+);", body, flags=re.M)
+    names = [f[1] for f in fields]
+    assert names == [f[0] for f in ll.ll_desc._fields_]
+    for (ctype, name), (bname, btype) in zip(fields, ll.ll_desc._fields_):
+        assert ctypes.sizeof(btype) == (8 if ctype == "int64_t" else 4), name
+    assert names[-1] == "reserved"
+
+
+def test_bwd_signature_takes_the_forward_operands():
+    """lstm_loop_bwd takes x, seq_len and W (checked against the saved
+    forward) before the gradients."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    decl = text[text.index("ll_status lstm_loop_bwd("):]
+    decl = decl[:decl.index(");")]
+    params = [p.strip() for p in decl[decl.index("(") + 1:].split(",")]
+    names = [re.findall(r"([A-Za-z_0-9]+)$", p)[0] for p in params]
+    assert names[:5] == ["plan", "stream", "x", "seq_len", "W"]
+    assert names[5:] == ["dy", "dhT", "dcT", "dx", "dW", "dbias", "dh0", "dc0"]
+    assert len(ll.load_library().lstm_loop_bwd.argtypes) == len(names)

@@ -433,14 +433,59 @@ def test_other_cells_full_size_parity(w):
     assert not bad, bad
 
 
+def _clear_skip_margins(inp, w, margin, max_rounds=12):
+    """Redraw x_t of the (step, row) pairs whose decision sits within
+    `margin` of the threshold in the oracle, until no valid decision does
+    (each redraw changes that row's trajectory from t on, so it can move a
+    later decision of the same row; a few rounds settle it).  Only the oracle
+    decides; the returned inputs feed both sides."""
+    inp = dict(inp, x=inp["x"].copy())
+    rng = np.random.default_rng(4242)
+    for _ in range(max_rounds):
+        ref = oracle_reference(inp, w.layers, w.dtype, cell="skip")
+        close = np.zeros(inp["x"].shape[:2], bool)
+        for m in ref["margin"]:
+            close |= m <= margin
+        if not close.any():
+            return inp, ref
+        ts, bs = np.nonzero(close)
+        say(f"    redrawing x at {len(ts)} close decisions")
+        fresh = rng.standard_normal((len(ts), w.I), dtype=np.float32)
+        inp["x"][ts, bs] = wl.round_to_bf16(fresh) if w.dtype == "bf16" else fresh
+    raise AssertionError("decisions did not clear the margin")
+
+
+def test_skip_full_size_all_outputs():
+    """The cond-body workload at full size with every decision at least 1e-3
+    from the threshold in the oracle (x redrawn at the few close decisions,
+    chosen by the oracle alone), so every output, dW and db included, is
+    compared with the oracle."""
+    w = wl.SKIP_VAR_H1024
+    say(f"[full] {w.name} (all decisions clear)")
+    inp, ref = _clear_skip_margins(wl.generate(w), w, 1e-3)
+    assert min(float(m.min()) for m in ref["margin"]) > 1e-3
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell="skip")
+    plan = dc.plan()
+    assert plan.geometry()["xcd_local"]
+    dc.fwd(plan)
+    dc.bwd(plan)
+    err = plan.status_sync()
+    res = dc.results()
+    plan.close()
+    assert err == 0
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
+
+
 def test_skip_full_size_parity():
-    """The benchmark's cond-body workload at full size.  Its ~2.6e4 decisions
-    include some within the two sides' float32 rounding of the threshold, and
-    a row that decides differently follows another trajectory, so the
-    comparison is per row: every row whose decisions all sit at least 1e-3
-    from the threshold in the oracle must match it within the tolerance (rows
-    do not interact in the loop); dW and db, sums over all rows, are compared
-    only if every row qualifies.  At least 75% of the rows must qualify."""
+    """The benchmark's cond-body workload at full size, inputs as generated.
+    Its ~2.6e4 decisions include some within the two sides' float32 rounding
+    of the threshold, and a row that decides differently follows another
+    trajectory, so the comparison is per row: every row whose decisions all
+    sit at least 1e-3 from the threshold in the oracle must match it within
+    the tolerance (rows do not interact in the loop).  At least 75% of the
+    rows must qualify.  (dW and db over every row: the test above.)"""
     w = wl.SKIP_VAR_H1024
     say(f"[full] {w.name}")
     inp = wl.generate(w)
@@ -465,9 +510,34 @@ def test_skip_full_size_parity():
     for key in ("hT", "cT", "dh0", "dc0"):
         e = rel_err(res[key][:, good], ref[key][:, good])
         assert e <= tol, (key, e)
-    if good.all():
-        errs, bad = compare(res, ref, tol)
-        assert not bad, bad
+
+
+# The two-layer H = 2048 workload's shape (bf16, I = H = 2048: chip-wide
+# loops, and dW through the gather-transposes and the split-K NT product,
+# which the plan's cost model picks for these long reductions) at batches the
+# oracle finishes in seconds; every output, dW and db of both layers included.
+TWO_LAYER_H2048_REDUCED = [
+    W("lstm2_b24_h2048_t6_bf16", B=24, I=2048, H=2048, T_max=6, dtype="bf16", layers=2,
+      len_lo=0, len_hi=6, random_state=True, seed=1105),
+    W("lstm2_b64_h2048_t4_bf16", B=64, I=2048, H=2048, T_max=4, dtype="bf16", layers=2,
+      len_lo=1, len_hi=4, seed=1205),
+]
+
+
+@pytest.mark.parametrize("w", TWO_LAYER_H2048_REDUCED, ids=[w.name for w in TWO_LAYER_H2048_REDUCED])
+def test_two_layer_h2048_reduced_batch_every_output(w):
+    say(f"[h2048] {w.name}")
+    inp = wl.generate(w)
+    geom = {}
+    res, err = run_case(w, inp, geometry=geom)
+    assert geom["loops"] == "chip", geom
+    assert err == 0
+    say("    oracle running")
+    ref = oracle_reference(inp, w.layers, w.dtype)
+    assert res["T_eff"] == ref["T_eff"]
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
 
 
 def test_two_layer_full_size_sampled_rows():
@@ -567,6 +637,25 @@ def test_spill_long_sequences():
     ref_o = oracle_reference(sub, w.layers, w.dtype)
     gsub = {k: got[k][:, rows] for k in ("y", "hT", "cT", "dx", "dh0", "dc0")}
     errs, bad = compare(gsub, ref_o, TOL[w.dtype], keys=("y", "hT", "cT", "dx", "dh0", "dc0"))
+    say(f"    errors {errs}")
+    assert not bad, bad
+
+
+def test_spill_h512_every_output_against_the_oracle():
+    """The spill workload's shape (f32, I = H = 512, B = 64, every length T)
+    at T = 96 with chunks of 16 steps and a ring of 4 (two chunks swapped out
+    and back): every output, dW and db included, against the oracle."""
+    w = W("spill_f32_b64_h512_t96", B=64, I=512, H=512, T_max=96, dtype="f32", len_lo=96,
+          len_hi=96, spill=True, seed=1304)
+    say(f"[spill] {w.name}")
+    inp = wl.generate(w)
+    C = 16
+    slot_bytes = C * w.B * 5 * w.H * 4
+    got, err, dev, host = _run_plan(w, inp, spill=1, spill_chunk_steps=C,
+                                    device_stack_budget_bytes=4 * slot_bytes)
+    assert err == 0 and host == 2 * slot_bytes
+    say("    oracle running")
+    errs, bad = compare(got, oracle_reference(inp, w.layers, w.dtype), TOL[w.dtype])
     say(f"    errors {errs}")
     assert not bad, bad
 
@@ -775,3 +864,99 @@ def test_other_cells_zero_trip(cell):
     for k in ("y", "dx"):
         assert not res[k].any(), k
     assert not any(d.any() for d in res["dW"]) and not any(b.any() for b in res["dbias"])
+
+
+# ------------------------------------------------------------ ABI contract
+def test_bwd_rejects_operands_other_than_the_saved_forwards():
+    """lstm_loop_bwd with an x, seq_len or W other than the saved forward's:
+    LL_EINVAL, nothing enqueued, the saved stack kept for the right call."""
+    from paper_1805_01772_amd.lstmloop import LL_EINVAL
+    w = wl.TINY.with_(random_state=True, with_dy=True, seed=77)
+    inp = wl.generate(w)
+    dc = DeviceCase(inp, w.H, w.I, 1, w.dtype)
+    plan = dc.plan()
+    dc.fwd(plan)
+    other_x = dc.x.clone()
+    other_len = dc.seq_len.clone()
+    other_W = [t.clone() for t in dc.W]
+    for args in ((other_x, dc.seq_len, dc.W), (dc.x, other_len, dc.W), (dc.x, dc.seq_len, other_W)):
+        with pytest.raises(LoopError) as e:
+            plan.bwd(*args, dc.dy, dc.dhT, dc.dcT, dc.dx, dc.dW, dc.dbias, dc.dh0, dc.dc0)
+        assert e.value.status == LL_EINVAL
+    dc.bwd(plan)
+    assert plan.status_sync() == 0
+    res = dc.results()
+    plan.close()
+    ref = oracle_reference(inp, 1, w.dtype)
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    assert not bad, bad
+
+
+def _offset_copy(t, elems):
+    """A contiguous copy of t whose data starts `elems` elements into a larger
+    allocation (for alignment tests)."""
+    flat = torch.empty(t.numel() + elems, dtype=t.dtype, device=t.device)
+    v = flat[elems:].view(t.shape)
+    v.copy_(t)
+    return v
+
+
+def test_misaligned_arrays_rejected_before_anything_is_enqueued():
+    """An array that is not 16-byte aligned (here x, then dx) gives LL_EINVAL
+    before anything is enqueued; the plan then runs normally."""
+    from paper_1805_01772_amd.lstmloop import LL_EINVAL
+    w = W("align_bf16_b16_i1024_h1024_t5", B=16, I=1024, H=1024, T_max=5, dtype="bf16",
+          len_lo=0, len_hi=5, random_state=True, seed=78)
+    inp = wl.generate(w)
+    dc = DeviceCase(inp, w.H, w.I, 1, w.dtype)
+    plan = dc.plan()
+    assert plan.geometry()["dw_in_place"] == [True]
+    x_al = dc.x
+    dc.x = _offset_copy(x_al, 1)                 # 2 bytes off
+    assert dc.x.data_ptr() % 16 != 0
+    for save in (True, False):
+        with pytest.raises(LoopError) as e:
+            dc.fwd(plan, save=save)
+        assert e.value.status == LL_EINVAL
+    dc.x = x_al
+    dc.fwd(plan)
+    dx_al = dc.dx
+    dc.dx = _offset_copy(dx_al, 2)               # 8 bytes off
+    with pytest.raises(LoopError) as e:
+        dc.bwd(plan)
+    assert e.value.status == LL_EINVAL
+    dc.dx = dx_al
+    dc.bwd(plan)                                 # the saved stack was kept
+    assert plan.status_sync() == 0
+    res = dc.results()
+    plan.close()
+    errs, bad = compare(res, oracle_reference(inp, 1, w.dtype), TOL[w.dtype])
+    assert not bad, bad
+
+
+def test_dw_operands_past_two_gib_take_the_transposes():
+    """bf16 I = H = 1024, B = 128, T_max = 2048: the dz rows of the row
+    capacity reach 2 GiB, past the 32-bit offsets of the dW product over rows,
+    so the plan takes the gather-transposes instead (the same shape at
+    T_max = 200 reads in place); short lengths keep the oracle quick.  Every
+    output against the oracle."""
+    w = W("big_bf16_b128_i1024_h1024_t2048", B=128, I=1024, H=1024, T_max=2048, dtype="bf16",
+          len_lo=0, len_hi=5, random_state=True, seed=79)
+    inp = wl.generate(w)
+    say(f"[abi] {w.name}")
+    dc = DeviceCase(inp, w.H, w.I, 1, w.dtype)
+    plan = dc.plan()
+    assert plan.geometry()["dw_in_place"] == [False]
+    dc.fwd(plan)
+    dc.bwd(plan)
+    assert plan.status_sync() == 0
+    res = dc.results()
+    plan.close()
+    small = wl.Workload("b128_t200", B=128, I=1024, H=1024, T_max=200, dtype="bf16", len_lo=0,
+                        len_hi=5)
+    with DeviceCase(wl.generate(small), small.H, small.I, 1, small.dtype).plan() as p2:
+        assert p2.geometry()["dw_in_place"] == [True]
+    say("    oracle running")
+    errs, bad = compare(res, oracle_reference(inp, 1, w.dtype), TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
