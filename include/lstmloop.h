@@ -261,6 +261,41 @@ ll_status lstm_loop_bwd(ll_plan* plan, void* stream,
                         float* dx, float* const* dW, float* const* dbias,
                         float* dh0, float* dc0);
 
+/*
+ * Inference forward without allocation, for callers that cannot allocate
+ * device memory or create streams (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): computes exactly what
+ * lstm_loop_fwd(plan for *desc, ..., save_for_backward = 0) computes, with the
+ * same kernels, but without a plan.  Every buffer the forward needs (length
+ * order, transposed weights, input projections, h history, exchange rings and
+ * flags) is carved from a scratch array of LL_NOALLOC_SCRATCH_BYTES bytes that
+ * the library holds in each device's memory from the moment it is loaded
+ * until the process ends.  The call makes no hipMalloc or hipFree, creates no
+ * stream or event, and sets up no memory with hipMemset: what must start at
+ * zero is cleared by kernels on `stream`.
+ *   desc     as for ll_plan_create; spill and recompute must be 0
+ *            (LL_EUNSUPPORTED otherwise: nothing is saved).  A problem whose
+ *            buffers exceed the scratch array gives LL_EUNSUPPORTED with the
+ *            bytes it would need (roughly T_max * B * (4 H * 4 + H * operand
+ *            bytes) plus the weights; use a plan for it).
+ *   stream   the call's stream; the call runs on the current device.
+ *   x .. trip_count  as for lstm_loop_fwd.
+ *   device_error  device int32 that receives the device error word
+ *            (LL_DEVERR_* bits) at the end of the call, or NULL.
+ * Every call on one device shares that device's scratch array and leaves its
+ * contents behind: two calls whose work overlaps on one device (different
+ * streams, or different threads) race and give wrong results, so callers
+ * serialise them (one stream, or their own ordering).  The loops also need
+ * the whole device (as for plans): no plan's loop may run beside it.
+ */
+#define LL_NOALLOC_SCRATCH_BYTES (128ull << 20)
+ll_status lstm_loop_fwd_noalloc(const ll_desc* desc, void* stream,
+                                const void* x, const int32_t* seq_len,
+                                const void* const* W, const float* const* bias,
+                                const float* h0, const float* c0,
+                                float* y, float* hT, float* cT,
+                                int32_t* trip_count, int32_t* device_error);
+
 /* Wait for the plan's work on the stream of its last call, then read and
  * clear the device error word (LL_DEVERR_* bits) into *device_error
  * (may be NULL). */

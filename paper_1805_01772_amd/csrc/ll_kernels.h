@@ -272,6 +272,8 @@ hipError_t x_launch2(const void* fn, const XLoopArgs& a0, const XLoopArgs& a1, i
 template <typename T>
 hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, int mrt, int ring_ks,
                                 int slot, void* ring, unsigned* flags, int nflags, hipStream_t s);
+// dst[0 .. n) = src[0 .. n) (one wave; n small)
+hipError_t launch_copy_i32(const int* src, int* dst, int n, hipStream_t s);
 hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s);
 
 // Sustained matrix-core rate of the device (TFLOP/s), for reports: the 16x16

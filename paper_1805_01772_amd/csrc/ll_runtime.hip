@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -377,61 +378,12 @@ ll_status validate_desc(const ll_desc* d) {
   return LL_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char* ll_last_error(void) { return g_last_error.c_str(); }
-
-const char* ll_version(void) { return "lstmloop 0.1 (gfx950)"; }
-
-ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, int32_t shape, double* tflops) {
-  if (!tflops) return fail(LL_EINVAL, "tflops is NULL");
-  if (dtype != LL_F32 && dtype != LL_BF16) return fail(LL_EINVAL, "dtype must be LL_F32 or LL_BF16");
-  if (shape != 16 && shape != 32) return fail(LL_EINVAL, "shape must be 16 or 32 (got %d)", shape);
-  int ndev = 0;
-  LL_HIP(hipGetDeviceCount(&ndev));
-  if (device < 0 || device >= ndev) return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
-  DeviceGuard guard(device);
-  hipDeviceProp_t prop;
-  LL_HIP(hipGetDeviceProperties(&prop, device));
-  *tflops = 0.0;
-  LL_HIP(dtype == LL_BF16 ? ll::measure_mfma_peak<bf16_t>(prop.multiProcessorCount, shape == 32, tflops)
-                          : ll::measure_mfma_peak<float>(prop.multiProcessorCount, shape == 32, tflops));
-  return LL_OK;
-}
-
-ll_status ll_eval_activations(int32_t device, const float* in, float* out, int64_t n, int32_t fn) {
-  if (fn != 0 && fn != 1) return fail(LL_EINVAL, "fn must be 0 (sigmoid) or 1 (tanh), got %d", fn);
-  if (n < 0) return fail(LL_EINVAL, "n = %lld is negative", (long long)n);
-  if (n > 0 && (!in || !out)) return fail(LL_EINVAL, "in and out are required");
-  int ndev = 0;
-  LL_HIP(hipGetDeviceCount(&ndev));
-  if (device < 0 || device >= ndev) return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
-  if (n == 0) return LL_OK;
-  DeviceGuard guard(device);
-  LL_HIP(ll::eval_activations(in, out, (long)n, fn, nullptr));
-  LL_HIP(hipStreamSynchronize(nullptr));
-  return LL_OK;
-}
-
-ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
-  if (!out) return fail(LL_EINVAL, "out is NULL");
-  *out = nullptr;
-  ll_status st = validate_desc(desc);
-  if (st != LL_OK) return st;
-  int ndev = 0;
-  LL_HIP(hipGetDeviceCount(&ndev));
-  if (device < 0 || device >= ndev)
-    return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
-  DeviceGuard guard(device);
-  hipDeviceProp_t prop;
-  LL_HIP(hipGetDeviceProperties(&prop, device));
-  if (!prop.cooperativeLaunch)
-    return fail(LL_EUNSUPPORTED, "device %d does not support cooperative launches", device);
-
-  ll_plan* p = new (std::nothrow) ll_plan();
-  if (!p) return fail(LL_ENOMEM, "host allocation of the plan failed");
+// Every decision of a plan that needs no device memory: problem, launch
+// forms (XCD-local, chip-wide or grid-barrier loops; wavefront), memory
+// policy, dW paths and their split-K.  Used by ll_plan_create and by the
+// forward that allocates nothing.  `prop` is the device's properties, the
+// device current.
+ll_status plan_configure(ll_plan* p, const ll_desc* desc, int device, const hipDeviceProp_t& prop) {
   p->d = *desc;
   p->device = device;
   p->bf16 = desc->dtype == LL_BF16;
@@ -459,7 +411,6 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   }
   const int H = desc->H, B = desc->B, L = desc->layers;
   if (!choose_geometry(B, H, p->es, p->n_cu, lds_limit, &p->geom)) {
-    delete p;
     return fail(LL_EUNSUPPORTED,
                 "no loop geometry fits: H = %d, B = %d, %d CUs, %zu bytes of LDS per group", H,
                 B, prop.multiProcessorCount, lds_limit);
@@ -470,11 +421,9 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
                           : ll::loop_kernel_setup<float>(p->geom.MRT, p->geom.lds_fwd,
                                                          p->geom.lds_bwd, &occ_f, &occ_b);
   if (he != hipSuccess) {
-    delete p;
     return fail(LL_EHIP, "loop kernel setup failed: %s", hipGetErrorString(he));
   }
   if ((long)occ_f * p->n_cu < p->geom.nwg || (long)occ_b * p->n_cu < p->geom.nwg) {
-    delete p;
     return fail(LL_EUNSUPPORTED,
                 "loops need %d co-resident work-groups; occupancy allows %d/%d per CU x %d CUs",
                 p->geom.nwg, occ_f, occ_b, p->n_cu);
@@ -514,7 +463,6 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
 
   // The Elman RNN, GRU and cond-body cells run on the XCD-local loops only.
   if ((p->G != 4 || p->skip) && !p->xmode) {
-    delete p;
     return fail(LL_EUNSUPPORTED, "the %s cell needs the XCD-local loops (H = %d, B = %d do not fit them)",
                 p->G == 1 ? "RNN" : p->G == 3 ? "GRU" : "cond-body LSTM", H, B);
   }
@@ -541,7 +489,6 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   // stack becomes a device ring of nslots chunks.
   if (desc->spill) {
     if (!p->xmode) {
-      delete p;
       return fail(LL_EUNSUPPORTED, "spill needs the XCD-local loops (H = %d, B = %d do not fit them)",
                   H, B);
     }
@@ -555,7 +502,6 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   }
   if (desc->recompute) {
     if (!p->xmode) {
-      delete p;
       return fail(LL_EUNSUPPORTED,
                   "recompute needs the XCD-local loops (H = %d, B = %d do not fit them)", H, B);
     }
@@ -645,6 +591,17 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
         p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[l][k] * g.M * g.N);
     }
   }
+  return LL_OK;
+}
+
+// The plan's device buffers in one place: `take(slot, bytes, what)` gives
+// each its memory (ll_plan_create: a device allocation; the forward that
+// allocates nothing: a piece of the library's scratch array).  fwd_only:
+// only what an inference forward touches (no stack, no gradient buffers).
+template <typename Take>
+ll_status plan_layout(ll_plan* p, bool fwd_only, Take&& take) {
+  const ll_desc* desc = &p->d;
+  const int H = desc->H, B = desc->B, L = desc->layers;
   const int maxI = std::max(desc->I, H);
 
   const size_t es = p->es;
@@ -652,12 +609,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
 #define ALLOC(ptr, bytes, what)                                      \
   do {                                                               \
     void* tmp_ = nullptr;                                            \
-    ll_status s_ = dalloc(&tmp_, (size_t)(bytes), what);             \
-    if (s_ != LL_OK) {                                               \
-      free_plan_memory(p);                                           \
-      delete p;                                                      \
-      return s_;                                                     \
-    }                                                                \
+    ll_status s_ = take(&tmp_, (size_t)(bytes), what);               \
+    if (s_ != LL_OK) return s_;                                      \
     ptr = reinterpret_cast<decltype(ptr)>(tmp_);                     \
   } while (0)
   ALLOC(p->perm, sizeof(int) * B, "perm");
@@ -667,20 +620,20 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   ALLOC(p->meta, sizeof(int) * ll::META_INTS, "meta");
   for (int l = 0; l < L; ++l) {
     ALLOC(p->WT[l], es * p->G * H * (in_width(p, l) + H), "transposed W");
-    ALLOC(p->stack[l],
-          sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * (p->recompute || p->G == 1 ? 1 : 5) * H),
-          "stack");
-    // (recompute: B more rows hold h0 in the operand type, the h_{t-1} of step 0)
+    if (!fwd_only)
+      ALLOC(p->stack[l],
+            sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * (p->recompute || p->G == 1 ? 1 : 5) * H),
+            "stack");
     // (B more rows hold h0 in the operand type, the h_{t-1} of step 0)
     ALLOC(p->HH[l], es * (cap + B) * H, "h history");
   }
   ALLOC(p->Zx, sizeof(float) * cap * p->G * H, "input projection");
-  ALLOC(p->DZ, es * cap * p->GB * H, "dz");
-  if (!p->dw_rows[0] || (L == 2 && !p->dw_rows[1])) {   // (transposed copies for the NT products)
+  if (!fwd_only) ALLOC(p->DZ, es * cap * p->GB * H, "dz");
+  if (!fwd_only && (!p->dw_rows[0] || (L == 2 && !p->dw_rows[1]))) {   // (transposed copies for the NT products)
     ALLOC(p->DZT, es * p->GB * H * p->ldT, "dz transposed");
     ALLOC(p->XT, es * (maxI + H) * p->ldT, "x and h_prev transposed");
   }
-  if (L == 2) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
+  if (L == 2 && !fwd_only) ALLOC(p->dyc, sizeof(float) * cap * H, "inter-layer gradient");
   if (p->xmode) {
     // two slots x 8 XCDs x row tiles x (G H / k-step) blocks of 1 KB
     const long ks_b = (long)p->G * H * (long)es / 64;
@@ -689,9 +642,11 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     ALLOC(p->xflags, sizeof(unsigned) * p->xflag_words, "exchange flags");
     if (p->wave) {
       ALLOC(p->xring2, 2L * 8 * p->xMRT * ks_b * 1024, "exchange ring");
-      ALLOC(p->DZ2, es * cap * 4 * H, "dz");
-      ALLOC(p->dyx, sizeof(float) * 2L * 8 * p->xMRT * 16 * H, "dy exchange");
-      ALLOC(p->db_part2, sizeof(float) * 8 * 4 * H, "db partials");
+      if (!fwd_only) {
+        ALLOC(p->DZ2, es * cap * 4 * H, "dz");
+        ALLOC(p->dyx, sizeof(float) * 2L * 8 * p->xMRT * 16 * H, "dy exchange");
+        ALLOC(p->db_part2, sizeof(float) * 8 * 4 * H, "db partials");
+      }
     }
   }
   if (p->cmode) {
@@ -701,6 +656,8 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     p->cflag_words = 8 + p->cMRT * 256 + 8 * p->cMRT * 32;
     ALLOC(p->cflags, sizeof(unsigned) * p->cflag_words, "exchange flags");
   }
+  if (p->skip) ALLOC(p->sx, sizeof(float) * cap, "predicate input part");
+  if (fwd_only) return LL_OK;   // the rest serves the saved stack and the gradient pass
   if (p->recompute) {
     ALLOC(p->gslot, sizeof(float) * (long)p->rc_steps * B * 4 * H, "recomputed gates");
     ALLOC(p->rc_inmap, sizeof(int) * 2 * cap, "recomputation row maps");
@@ -715,12 +672,84 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
   if (p->xmode && p->G == 4)
     for (int l = 0; l < L; ++l) ALLOC(p->Wum[l], es * 4L * H * H, "permuted recurrent weights");
   if (p->dw_rows[0] || p->dw_rows[1]) ALLOC(p->prevc, sizeof(int) * cap, "previous-row map");
-  if (p->skip) {
-    ALLOC(p->sx, sizeof(float) * cap, "predicate input part");
-    ALLOC(p->guards, sizeof(float) * L * cap, "guard stack");
-  }
+  if (p->skip) ALLOC(p->guards, sizeof(float) * L * cap, "guard stack");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
 #undef ALLOC
+  return LL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ll_last_error(void) { return g_last_error.c_str(); }
+
+const char* ll_version(void) { return "lstmloop 0.1 (gfx950)"; }
+
+ll_status ll_measure_mfma_peak(int32_t device, int32_t dtype, int32_t shape, double* tflops) {
+  if (!tflops) return fail(LL_EINVAL, "tflops is NULL");
+  if (dtype != LL_F32 && dtype != LL_BF16) return fail(LL_EINVAL, "dtype must be LL_F32 or LL_BF16");
+  if (shape != 16 && shape != 32) return fail(LL_EINVAL, "shape must be 16 or 32 (got %d)", shape);
+  int ndev = 0;
+  LL_HIP(hipGetDeviceCount(&ndev));
+  if (device < 0 || device >= ndev) return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
+  DeviceGuard guard(device);
+  hipDeviceProp_t prop;
+  LL_HIP(hipGetDeviceProperties(&prop, device));
+  *tflops = 0.0;
+  LL_HIP(dtype == LL_BF16 ? ll::measure_mfma_peak<bf16_t>(prop.multiProcessorCount, shape == 32, tflops)
+                          : ll::measure_mfma_peak<float>(prop.multiProcessorCount, shape == 32, tflops));
+  return LL_OK;
+}
+
+ll_status ll_eval_activations(int32_t device, const float* in, float* out, int64_t n, int32_t fn) {
+  if (fn != 0 && fn != 1) return fail(LL_EINVAL, "fn must be 0 (sigmoid) or 1 (tanh), got %d", fn);
+  if (n < 0) return fail(LL_EINVAL, "n = %lld is negative", (long long)n);
+  if (n > 0 && (!in || !out)) return fail(LL_EINVAL, "in and out are required");
+  int ndev = 0;
+  LL_HIP(hipGetDeviceCount(&ndev));
+  if (device < 0 || device >= ndev) return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
+  if (n == 0) return LL_OK;
+  DeviceGuard guard(device);
+  LL_HIP(ll::eval_activations(in, out, (long)n, fn, nullptr));
+  LL_HIP(hipStreamSynchronize(nullptr));
+  return LL_OK;
+}
+
+ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
+  if (!out) return fail(LL_EINVAL, "out is NULL");
+  *out = nullptr;
+  ll_status st = validate_desc(desc);
+  if (st != LL_OK) return st;
+  int ndev = 0;
+  LL_HIP(hipGetDeviceCount(&ndev));
+  if (device < 0 || device >= ndev)
+    return fail(LL_EINVAL, "device %d out of range (%d devices)", device, ndev);
+  DeviceGuard guard(device);
+  hipDeviceProp_t prop;
+  LL_HIP(hipGetDeviceProperties(&prop, device));
+  if (!prop.cooperativeLaunch)
+    return fail(LL_EUNSUPPORTED, "device %d does not support cooperative launches", device);
+
+  ll_plan* p = new (std::nothrow) ll_plan();
+  if (!p) return fail(LL_ENOMEM, "host allocation of the plan failed");
+  st = plan_configure(p, desc, device, prop);
+  if (st != LL_OK) {
+    delete p;
+    return st;
+  }
+  const int H = desc->H, B = desc->B, L = desc->layers;
+  const long cap = p->cap;
+  const size_t es = p->es;
+  {
+    auto take = [](void** slot, size_t bytes, const char* what) { return dalloc(slot, bytes, what); };
+    st = plan_layout(p, false, take);
+    if (st != LL_OK) {
+      free_plan_memory(p);
+      delete p;
+      return st;
+    }
+  }
   if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess) {
     free_plan_memory(p);
     delete p;
@@ -979,7 +1008,10 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
   // W^T of every layer (row n = gate column n, the K-contiguous operand of
   // the input projection and the loop) on the side stream, beside prep,
   // which runs on one compute unit
-  if (!p->wave) {
+  // (without a side stream, in the forward that allocates nothing: on the
+  // call's stream, after prep)
+  const bool side = !p->wave && p->gstream;
+  if (side) {
     LL_HIP(hipEventRecord(p->ev_fork, s));
     LL_HIP(hipStreamWaitEvent(p->gstream, p->ev_fork, 0));
     for (int l = 0; l < L; ++l) {
@@ -994,7 +1026,15 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
                          trip, s));
   tend(p, s, LL_STAGE_PREP, ev);
   if (p->wave) return enqueue_fwd_wave<T>(p, s, x, W, bias, h0, c0, y, hT, cT, save);
-  LL_HIP(hipStreamWaitEvent(s, p->ev_side, 0));
+  if (side) {
+    LL_HIP(hipStreamWaitEvent(s, p->ev_side, 0));
+  } else {
+    for (int l = 0; l < L; ++l) {
+      const int Il = in_width(p, l);
+      LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, p->G * H, p->G * H,
+                                     reinterpret_cast<T*>(p->WT[l]), Il + H, s));
+    }
+  }
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
     ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
@@ -1053,7 +1093,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
         xa.wp = bias[l] + 4L * H + Il;
         xa.bp = bias[l] + 4L * H + Il + H;
         xa.sx = p->sx;
-        xa.guard = p->guards + (long)l * p->cap;
+        xa.guard = p->guards ? p->guards + (long)l * p->cap : nullptr;
       }
       xa.stack = save ? p->stack[l] : nullptr;
       xa.y = (l == L - 1) ? y : nullptr;
@@ -1741,6 +1781,103 @@ ll_status lstm_loop_bwd(ll_plan* p, void* stream, const void* x, const int32_t* 
   if (hipEventRecord(p->ev_done, s) == hipSuccess) p->done_recorded = true;
   p->state = ST_EMPTY;
   return st;
+}
+
+// ---------------------------------------------------------------------------
+// The inference forward that allocates nothing: every buffer of an inference
+// plan comes from this file-scope device array.  Host code never passes the
+// array's name to a kernel or a copy (in host code it is only a stand-in
+// symbol): it uses the device address hipGetSymbolAddress returns, looked up
+// once per device with that device current.
+// ---------------------------------------------------------------------------
+}  // extern "C"
+
+namespace {
+
+static __device__ __align__(256) unsigned char scratch[LL_NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64] = {};
+
+ll_status scratch_address(int device, unsigned char** out) {
+  if (device < 0 || device >= 64) return fail(LL_EUNSUPPORTED, "device %d: at most 64 devices", device);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(LL_EHIP, "hipGetSymbolAddress of the scratch array on device %d failed: %s", device,
+                  hipGetErrorString(e));
+    g_scratch_ptr[device] = ptr;
+  }
+  *out = static_cast<unsigned char*>(g_scratch_ptr[device]);
+  return LL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ll_status lstm_loop_fwd_noalloc(const ll_desc* desc, void* stream, const void* x,
+                                const int32_t* seq_len, const void* const* W,
+                                const float* const* bias, const float* h0, const float* c0,
+                                float* y, float* hT, float* cT, int32_t* trip_count,
+                                int32_t* device_error) {
+  ll_status st = validate_desc(desc);
+  if (st != LL_OK) return st;
+  if (desc->spill || desc->recompute)
+    return fail(LL_EUNSUPPORTED, "the forward without allocation saves no stack: spill and recompute "
+                                 "(memory policies of the saved stack) must be 0");
+  const bool two_state = desc->cell == LL_CELL_LSTM || desc->cell == LL_CELL_LSTM_SKIP;
+  if (!x || !seq_len || !W || !bias || !hT || (!cT && two_state))
+    return fail(LL_EINVAL, "x, seq_len, W, bias, hT and (LSTM) cT are required");
+  for (int l = 0; l < desc->layers; ++l)
+    if (!W[l] || !bias[l]) return fail(LL_EINVAL, "W[%d] or bias[%d] is NULL", l, l);
+  {
+    const void* ptrs[] = {x, seq_len, h0, c0, y, hT, cT, trip_count, device_error};
+    const char* names[] = {"x", "seq_len", "h0", "c0", "y", "hT", "cT", "trip_count", "device_error"};
+    for (int i = 0; i < 9; ++i)
+      if (reinterpret_cast<uintptr_t>(ptrs[i]) & 15)
+        return fail(LL_EINVAL, "%s = %p is not 16-byte aligned", names[i], ptrs[i]);
+    for (int l = 0; l < desc->layers; ++l)
+      if ((reinterpret_cast<uintptr_t>(W[l]) | reinterpret_cast<uintptr_t>(bias[l])) & 15)
+        return fail(LL_EINVAL, "W[%d] = %p or bias[%d] = %p is not 16-byte aligned", l, W[l], l,
+                    (const void*)bias[l]);
+  }
+  int device = 0;
+  LL_HIP(hipGetDevice(&device));
+  hipDeviceProp_t prop;
+  LL_HIP(hipGetDeviceProperties(&prop, device));
+  ll_plan p;   // decisions only: no stream, no event, no device allocation
+  st = plan_configure(&p, desc, device, prop);
+  if (st != LL_OK) return st;
+  unsigned char* base = nullptr;
+  st = scratch_address(device, &base);
+  if (st != LL_OK) return st;
+  size_t used = 0;
+  auto take = [&](void** slot, size_t bytes, const char* what) -> ll_status {
+    const size_t at = (used + 255) & ~(size_t)255;
+    if (bytes > LL_NOALLOC_SCRATCH_BYTES || at + bytes > LL_NOALLOC_SCRATCH_BYTES)
+      return fail(LL_EUNSUPPORTED,
+                  "T_max = %d, B = %d, I = %d, H = %d, layers = %d need more than the %llu bytes of "
+                  "scratch of the forward without allocation (%s: %zu bytes at offset %zu); use a plan",
+                  desc->T_max, desc->B, desc->I, desc->H, desc->layers,
+                  (unsigned long long)LL_NOALLOC_SCRATCH_BYTES, what, bytes, at);
+    *slot = base + at;
+    used = at + bytes;
+    return LL_OK;
+  };
+  st = plan_layout(&p, true, take);
+  if (st != LL_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  // the device error word must start at zero (prep only ORs into it); the
+  // exchange flags are cleared by each loop's set-up kernel
+  LL_HIP(ll::launch_zero_u32(reinterpret_cast<unsigned*>(p.meta), ll::META_INTS, s));
+  st = p.bf16 ? enqueue_fwd<bf16_t>(&p, s, x, seq_len, W, bias, h0, c0, y, hT, cT, trip_count, false)
+              : enqueue_fwd<float>(&p, s, x, seq_len, W, bias, h0, c0, y, hT, cT, trip_count, false);
+  if (st != LL_OK) return st;
+  if (device_error) LL_HIP(ll::launch_copy_i32(p.meta + 2, device_error, 1, s));
+  return LL_OK;
 }
 
 ll_status ll_status_sync(ll_plan* p, int32_t* device_error) {

@@ -955,6 +955,15 @@ template hipError_t launch_x_prepare_fwd<float>(const float*, const int*, int, i
 template hipError_t launch_x_prepare_fwd<bf16_t>(const float*, const int*, int, int, int, int, int, void*,
                                                  unsigned*, int, hipStream_t);
 
+__global__ __launch_bounds__(64) void copy_i32_kernel(const int* __restrict__ src, int* __restrict__ dst, int n) {
+  for (int i = threadIdx.x; i < n; i += 64) dst[i] = src[i];
+}
+
+hipError_t launch_copy_i32(const int* src, int* dst, int n, hipStream_t s) {
+  hipLaunchKernelGGL(copy_i32_kernel, dim3(1), dim3(64), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s) {
   int blocks = (n + 255) / 256;
   if (blocks > 1024) blocks = 1024;

@@ -28,7 +28,7 @@ EXPORTED = ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes",
             "ll_plan_geometry", "lstm_loop_fwd", "lstm_loop_bwd",
             "ll_status_sync", "ll_last_error", "ll_version",
             "ll_plan_set_timing", "ll_plan_set_timing_stages", "ll_plan_read_timing",
-            "ll_measure_mfma_peak", "ll_eval_activations")
+            "ll_measure_mfma_peak", "ll_eval_activations", "lstm_loop_fwd_noalloc")
 STAGES = ("prep", "input_proj", "fwd_loop", "bwd_loop", "bwd_operands", "dw", "dx", "loop_setup",
           "recompute")
 
@@ -98,12 +98,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.POINTER(i64)]
     lib.ll_measure_mfma_peak.argtypes = [ctypes.c_int, i32, i32, ctypes.POINTER(ctypes.c_double)]
     lib.ll_eval_activations.argtypes = [ctypes.c_int32, vp, vp, i64, i32]
+    lib.lstm_loop_fwd_noalloc.argtypes = [ctypes.POINTER(ll_desc), vp, vp, vp, ctypes.POINTER(vp),
+                                          ctypes.POINTER(vp), vp, vp, vp, vp, vp, vp, vp]
     lib.ll_last_error.restype = ctypes.c_char_p
     lib.ll_version.restype = ctypes.c_char_p
     for name in ("ll_plan_create", "ll_plan_destroy", "ll_plan_stack_bytes", "ll_plan_geometry",
                  "lstm_loop_fwd", "lstm_loop_bwd", "ll_status_sync", "ll_plan_set_timing",
                  "ll_plan_set_timing_stages", "ll_plan_read_timing", "ll_measure_mfma_peak",
-                 "ll_eval_activations"):
+                 "ll_eval_activations", "lstm_loop_fwd_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -173,9 +175,8 @@ class Plan:
                  cell: int = 0):
         lib = load_library()
         self._lib = lib
-        self.desc = ll_desc(T_max, B, I, H, layers,
-                            LL_BF16 if dtype == "bf16" else LL_F32 if dtype == "f32" else int(dtype),
-                            spill, spill_chunk_steps, device_stack_budget_bytes, recompute, cell)
+        self.desc = make_desc(T_max, B, I, H, layers, dtype, spill, spill_chunk_steps,
+                              device_stack_budget_bytes, recompute, cell)
         self.dtype = dtype
         self.device = device
         h = ctypes.c_void_p()
@@ -270,6 +271,26 @@ def lstm_loop_fwd(plan: Plan, *args, **kw):
 
 def lstm_loop_bwd(plan: Plan, *args, **kw):
     return plan.bwd(*args, **kw)
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20   # LL_NOALLOC_SCRATCH_BYTES
+
+
+def make_desc(T_max: int, B: int, I: int, H: int, layers: int = 1, dtype: str = "f32",
+              spill: int = 0, spill_chunk_steps: int = 0, device_stack_budget_bytes: int = 0,
+              recompute: int = 0, cell: int = 0) -> ll_desc:
+    return ll_desc(T_max, B, I, H, layers,
+                   LL_BF16 if dtype == "bf16" else LL_F32 if dtype == "f32" else int(dtype),
+                   spill, spill_chunk_steps, device_stack_budget_bytes, recompute, cell, 0)
+
+
+def lstm_loop_fwd_noalloc(desc: ll_desc, x, seq_len, W: Sequence, bias: Sequence, h0, c0, y, hT,
+                          cT, trip_count=None, device_error=None, stream=None) -> None:
+    """lstm_loop_fwd_noalloc: the inference forward without a plan, every
+    buffer carved from the library's scratch array (asynchronous on `stream`)."""
+    _check(load_library().lstm_loop_fwd_noalloc(
+        ctypes.byref(desc), _stream(stream), _ptr(x), _ptr(seq_len), _ptr_array(W), _ptr_array(bias),
+        _ptr(h0), _ptr(c0), _ptr(y), _ptr(hT), _ptr(cT), _ptr(trip_count), _ptr(device_error)))
 
 
 def ll_plan_create(*args, **kw) -> Plan:
