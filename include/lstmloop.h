@@ -42,7 +42,14 @@
  *   - `stream` is a hipStream_t passed as void*.  Compute calls are
  *     asynchronous on it; they return after enqueueing.
  *   - A plan serves one stream at a time.  Calls on one plan must not
- *     overlap.
+ *     overlap.  The recurrent loops are persistent kernels that need every
+ *     compute unit of the device at once: the library chains the loop
+ *     launches of all plans on one device (each waits for the previous one to
+ *     complete, whichever stream enqueued it), so plans on different streams
+ *     are safe; other work that holds compute units for long (another
+ *     process's kernels) delays a loop's start (waits are bounded: 5 s, then
+ *     LL_DEVERR_BARRIER).  Under graph capture the chain is not used: the
+ *     caller orders captured loops itself.
  *   - Every array pointer is 16-byte aligned (the kernels move 16-byte
  *     chunks); lstm_loop_fwd and lstm_loop_bwd return LL_EINVAL otherwise.
  *   - Errors: checkable arguments give an error code synchronously and the

@@ -137,7 +137,13 @@ __device__ __forceinline__ void join_group(unsigned* rank_ctr, int* s_info) {
 }
 
 // Publish: every wave waits until its stores are acknowledged by the L2, the
-// work-group meets, and thread 0 stores `value` into the flag.
+// work-group meets, and thread 0 stores `value` into the flag.  The flag
+// store has work-group scope (cache policy sc0): the CU's vector L1 is
+// write-through, so the store reaches the XCD's L2, where the consumers
+// (CUs of the same XCD) poll with sc1 loads.  An agent-scope store (sc1) is
+// written through past the L2 and was measured to slow the loops down
+// (forward 0.58 -> 0.75 ms, gradient 0.75 -> 1.47 ms at the H = 1024
+// workload); consumers on other XCDs use publish_dev.
 __device__ __forceinline__ void publish(unsigned* flag, unsigned value) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();

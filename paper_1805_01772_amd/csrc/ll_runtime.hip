@@ -64,6 +64,43 @@ class DeviceGuard {
 
 long round_up(long v, long m) { return (v + m - 1) / m * m; }
 
+// Loop launches of every plan on one device form one chain: each waits for
+// the previous one (whatever plan or stream enqueued it) to complete.  The
+// loops need all compute units co-resident, so two of them must never run
+// at once.  (Skipped on a stream that is being captured into a graph: an
+// event recorded outside the capture cannot be waited on there.)
+struct LoopChain {
+  std::mutex mu;
+  hipEvent_t last = nullptr;
+  bool recorded = false;
+};
+LoopChain g_loop_chain[64];
+
+template <typename Launch>
+hipError_t chained_loop_launch(int device, hipStream_t s, Launch&& launch) {
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cap) != hipSuccess) cap = hipStreamCaptureStatusNone;
+  if (cap != hipStreamCaptureStatusNone || device < 0 || device >= 64) return launch();
+  LoopChain& c = g_loop_chain[device];
+  std::lock_guard<std::mutex> lock(c.mu);
+  if (!c.last) {
+    hipError_t e = hipEventCreateWithFlags(&c.last, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      c.last = nullptr;
+      return e;
+    }
+  }
+  if (c.recorded) {
+    hipError_t e = hipStreamWaitEvent(s, c.last, 0);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(c.last, s);
+  if (e == hipSuccess) c.recorded = true;
+  return e;
+}
+
 }  // namespace
 
 struct ll_plan {
@@ -993,7 +1030,7 @@ ll_status enqueue_fwd_wave(ll_plan* p, hipStream_t s, const void* x, const void*
   a1.in_flags = F0;
   a1.in_ks = ring_ks;
   ev = tbeg(p, s, LL_STAGE_FWD_LOOP);
-  LL_HIP(ll::x_launch2(p->xk2.fwd, a0, a1, 256, p->xk2.lds_fwd, s));
+  LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::x_launch2(p->xk2.fwd, a0, a1, 256, p->xk2.lds_fwd, s); }));
   tend(p, s, LL_STAGE_FWD_LOOP, ev);
   return LL_OK;
 }
@@ -1128,7 +1165,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
         xa.c0 = cin;
         xa.hT = last ? hout : p->carry;
         xa.cT = last ? cout : p->carry + (long)B * H;
-        LL_HIP(ll::x_launch(p->xk.fwd, xa, 256, p->xk.lds_fwd, s));
+        LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::x_launch(p->xk.fwd, xa, 256, p->xk.lds_fwd, s); }));
         tend(p, s, LL_STAGE_FWD_LOOP, ev);
         if (p->spill && save && k < nch - p->nslots) {   // evicted later: swap it out on the copy stream
           LL_HIP(hipEventRecord(p->ev_compute, s));
@@ -1162,7 +1199,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       ca.hT = hT + (long)l * B * H;
       ca.cT = cT + (long)l * B * H;
       ev = tbeg(p, s, LL_STAGE_FWD_LOOP);
-      LL_HIP(ll::c_launch(p->ck.fwd, ca, p->ck.lds_fwd, s));
+      LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::c_launch(p->ck.fwd, ca, p->ck.lds_fwd, s); }));
       tend(p, s, LL_STAGE_FWD_LOOP, ev);
       continue;
     }
@@ -1193,7 +1230,7 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     a.err = p->meta + 2;
     a.limit = p->barrier_ticks;
     ev = tbeg(p, s, LL_STAGE_FWD_LOOP);
-    LL_HIP(ll::launch_fwd_loop<T>(a, p->geom.nwg, p->geom.lds_fwd, s));
+    LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::launch_fwd_loop<T>(a, p->geom.nwg, p->geom.lds_fwd, s); }));
     tend(p, s, LL_STAGE_FWD_LOOP, ev);
   }
   return LL_OK;
@@ -1437,7 +1474,7 @@ ll_status enqueue_bwd_wave(ll_plan* p, hipStream_t s, const float* dy, const flo
   a1.dyx_flags = FY;
   a1.peer_flags = F0;
   ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
-  LL_HIP(ll::x_launch2(p->xk2.bwd, a0, a1, 256, p->xk2.lds_bwd, s));
+  LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::x_launch2(p->xk2.bwd, a0, a1, 256, p->xk2.lds_bwd, s); }));
   tend(p, s, LL_STAGE_BWD_LOOP, ev);
   LL_STATUS(bwd_products<T>(p, s, 1, p->DZ2, p->db_part2, nullptr, dW, dbias));
   return bwd_products<T>(p, s, 0, p->DZ, p->db_part, dx, dW, dbias);
@@ -1620,7 +1657,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
         xa.dcT = first ? dcin : p->carry + 3L * B * H;
         xa.dh0 = last ? dhout : p->carry + 2L * B * H;
         xa.dc0 = last ? dcout : p->carry + 3L * B * H;
-        LL_HIP(ll::x_launch(p->xk.bwd, xa, 256, p->xk.lds_bwd, s));
+        LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::x_launch(p->xk.bwd, xa, 256, p->xk.lds_bwd, s); }));
         tend(p, s, LL_STAGE_BWD_LOOP, ev);
         const int j = k - R;   // swap chunk j into the slot chunk k leaves
         if (p->spill && j >= 0) {
@@ -1652,7 +1689,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       ca.dh0 = dh0 ? dh0 + (long)l * B * H : nullptr;
       ca.dc0 = dc0 ? dc0 + (long)l * B * H : nullptr;
       ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
-      LL_HIP(ll::c_launch(p->ck.bwd, ca, p->ck.lds_bwd, s));
+      LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::c_launch(p->ck.bwd, ca, p->ck.lds_bwd, s); }));
       tend(p, s, LL_STAGE_BWD_LOOP, ev);
     }
     ll::BwdLoopArgs a{};
@@ -1689,7 +1726,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     a.limit = p->barrier_ticks;
     if (!p->xmode && !p->cmode) {
       ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
-      LL_HIP(ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s));
+      LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s); }));
       tend(p, s, LL_STAGE_BWD_LOOP, ev);
     }
     if (l == 0 && dx) LL_HIP(hipStreamWaitEvent(s, p->ev_side, 0));
