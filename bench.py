@@ -157,6 +157,33 @@ def recorded_traffic(kernel, workload):
     return float(ent["bytes_per_launch"])
 
 
+def pinned_copy_peak(nbytes, streams=1, reps=5):
+    """Host-link rate of plain copies between pinned host memory and device
+    memory: GB/s for device-to-host and host-to-device, each direction alone,
+    `streams` copies of nbytes in flight at once (one per stream)."""
+    import torch
+    n = nbytes // 4
+    dev = [torch.ones(n, dtype=torch.float32, device="cuda:0") for _ in range(streams)]
+    host = [torch.empty(n, dtype=torch.float32, pin_memory=True) for _ in range(streams)]
+    ss = [torch.cuda.Stream() for _ in range(streams)]
+    out = {}
+    for name in ("d2h", "h2d"):
+        best = 0.0
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(streams):
+                with torch.cuda.stream(ss[i]):
+                    if name == "d2h":
+                        host[i].copy_(dev[i], non_blocking=True)
+                    else:
+                        dev[i].copy_(host[i], non_blocking=True)
+            torch.cuda.synchronize()
+            best = max(best, streams * nbytes / (time.perf_counter() - t0) / 1e9)
+        out[name] = best
+    return out
+
+
 def copy_calibration(mib):
     """A plain device copy of `mib` MiB, five times (for counter scaling)."""
     import torch
@@ -238,11 +265,19 @@ def main():
         # the alternative to swapping: push c_t only, recompute each chunk's
         # gates in the gradient pass (two products over the chunk's rows)
         rc = timed({"recompute": 1, "spill_chunk_steps": C}, False)
+        slot_bytes = C * w.B * 5 * w.H * 4
+        peak1 = pinned_copy_peak(slot_bytes, 1)
+        peak2 = pinned_copy_peak(slot_bytes, 2)
+        link = moved / (gpu_ms / args.steps / 1e3) / 1e9
         spill = {"chunk_steps": C, "ring_slots": 4, "device_stack_bytes": sbytes[0],
                  "host_stack_bytes": sbytes[1], "ms_per_step_resident": res_ms / args.steps,
                  "ms_per_step_recompute": rc[0] / args.steps, "device_stack_bytes_recompute": rc[4][0],
                  "overlap_efficiency": (res_ms / args.steps) / (gpu_ms / args.steps),
-                 "host_link_GBps": moved / (gpu_ms / args.steps / 1e3) / 1e9}
+                 "host_link_GBps": link,
+                 "pinned_copy_peak_GBps": {"chunk_bytes": slot_bytes, "one_stream": peak1,
+                                           "two_streams": peak2},
+                 "host_link_fraction_of_peak": link / max(peak1["d2h"], peak1["h2d"], 1e-9),
+                 "seconds_at_peak": moved / 2 / peak1["d2h"] / 1e9 + moved / 2 / peak1["h2d"] / 1e9}
 
     ms_per_step = gpu_ms / args.steps
     value = sum_len / (ms_per_step / 1e3)
