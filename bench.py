@@ -91,6 +91,9 @@ def cpu_baseline(w, inp, target_s, precision="fp32", threads=None):
                         else (oracle.stacked_gru_forward, oracle.stacked_gru_backward))
             _, _, tapes = fwd(x, sl, Ws, bs, h0, precision)
             bwd(tapes, dy, dhT)
+        elif w.cell == "act":
+            _, _, _, tapes = oracle.stacked_act_forward(x, sl, Ws, bs, h0, c0, precision, w.ponder_max)
+            oracle.stacked_act_backward(tapes, dy, dhT, dcT)
         else:
             fwd, bwd = ((oracle.stacked_skip_forward, oracle.stacked_skip_backward) if w.cell == "skip"
                         else (oracle.stacked_forward, oracle.stacked_backward))
@@ -212,7 +215,8 @@ def main():
     inp = wl.generate(w)
     sum_len = int(inp["seq_len"].sum())
     T_eff = int(inp["seq_len"].max())
-    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, device="cuda:0", cell=w.cell)
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, device="cuda:0", cell=w.cell,
+                    ponder_max=w.ponder_max)
     plan_kw = {}
     if w.spill:   # stack swapped to pinned host memory through a ring of 4 chunks of 32 steps
         C = 32

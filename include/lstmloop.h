@@ -103,7 +103,34 @@ typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
  * (a step function has no gradient).  The loop construct, masking, stack and
  * gradient loop are the same for every body: the paper's while-loop and its
  * gradient (Sections 3 and 5) do not depend on it. */
-typedef enum { LL_CELL_LSTM = 0, LL_CELL_RNN = 1, LL_CELL_GRU = 2, LL_CELL_LSTM_SKIP = 3 } ll_cell;
+typedef enum {
+  LL_CELL_LSTM = 0,
+  LL_CELL_RNN = 1,
+  LL_CELL_GRU = 2,
+  LL_CELL_LSTM_SKIP = 3,
+  LL_CELL_LSTM_ACT = 4
+} ll_cell;
+
+/* LL_CELL_LSTM_ACT: the LSTM body holding a nested while-loop whose trip
+ * count is decided on the device from the state (Section 2.2 motivates it
+ * with Adaptive Computation Time; Section 5.1 gives the gradient of nested
+ * loops).  For each row still running at step t:
+ *     (h, c) = (h_{t-1}, c_{t-1}); P = 0; n = 0
+ *     repeat: (h, c) = LSTM step(x_t, h, c); n += 1;
+ *             if n == ponder_max: stop
+ *             P += sigmoid(h . w_p + b_p)   (float32 sums of operands)
+ *             if P >= 1 - eps: stop          (eps = LL_ACT_EPS)
+ *     (h_t, c_t) = (h, c); y_t = h_t
+ * with the same x_t at every ponder step.  The forward pushes every ponder
+ * step's values and the inner trip count of each (step, row tile); the
+ * gradient loop runs the nested gradient loop in reverse, popping them.  W
+ * is the LSTM's [I + H, 4H]; bias [5H + 1] = [b (4H), w_p (H), b_p]; dbias
+ * has the bias's length, zero in the halting part (the halting decision is a
+ * step function).  dx_t sums the ponder steps' dz W_x^T.  Single layer,
+ * XCD-local loops, no spill or recompute (else LL_EUNSUPPORTED); ACT's
+ * mean-field output and ponder cost are not part of this body. */
+#define LL_ACT_EPS 0.01f
+#define LL_ACT_PONDER_MAX 8
 
 /* Device error word bits (ll_status_sync). */
 #define LL_DEVERR_SEQ_LEN 1      /* some seq_len[b] < 0 or > T_max          */
@@ -165,6 +192,8 @@ typedef struct {
   int64_t device_stack_budget_bytes;
   int32_t recompute;
   int32_t cell;
+  int32_t ponder_max; /* LL_CELL_LSTM_ACT: at most this many ponder steps per
+                         step, 1 .. LL_ACT_PONDER_MAX; 0 for every other cell */
   int32_t reserved;   /* must be 0 (LL_EINVAL otherwise): room for later fields */
 } ll_desc;
 

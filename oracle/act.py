@@ -154,6 +154,7 @@ def act_forward(x, seq_len, W, bias, h0=None, c0=None, precision="fp64", ponder_
     y = np.zeros((T_max, B, H), dt)
     trips = np.zeros((T_max, B), np.int64)
     margins = []
+    row_margin = np.full(B, np.inf)    # per row: the closest of its decisions
     T_eff = int(seq_len.max()) if B else 0
     stack = []          # one entry per outer step: that step's ponder steps
     t = 0
@@ -176,7 +177,9 @@ def act_forward(x, seq_len, W, bias, h0=None, c0=None, precision="fp64", ponder_
             if cont.any():
                 P_new = (P + _halt_prob(_operand(h, precision), wp_op, bp)).astype(np.float32)
                 P = np.where(cont, P_new, P)
-                margins.append(np.abs(P_new[cont] - thr).astype(np.float64))
+                dist = np.abs(P_new - thr).astype(np.float64)
+                margins.append(dist[cont])
+                row_margin = np.where(cont, np.minimum(row_margin, dist), row_margin)
                 stop |= cont & (P_new >= thr)
             running &= ~stop
         stack.append(dict(steps=steps, valid=valid[:, None], trips=n.copy()))
@@ -185,7 +188,7 @@ def act_forward(x, seq_len, W, bias, h0=None, c0=None, precision="fp64", ponder_
         t += 1
     m = np.concatenate(margins) if margins else np.zeros(0)
     tape = dict(stack=stack, T_eff=T_eff, x=x, W=W, precision=precision, I=I, H=H, trips=trips,
-                min_margin=float(m.min()) if m.size else np.inf)
+                min_margin=float(m.min()) if m.size else np.inf, row_margin=row_margin)
     return y, h, c, tape
 
 

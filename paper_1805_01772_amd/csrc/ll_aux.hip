@@ -446,6 +446,32 @@ hipError_t launch_gather_transpose(const GatherTArgs& g, int cap_rows, hipStream
   return hipGetLastError();
 }
 
+// out[rowmap[r] * C + c] = sum_k ws[k * stride + r * C + c] for the compact
+// rows r < meta[1] (the sum over ponder slots of the nested-loop body's dx).
+__global__ __launch_bounds__(256) void sum_scatter_rows_kernel(const float* __restrict__ ws, int nsl, long stride,
+                                                               const int* __restrict__ meta,
+                                                               const int* __restrict__ rowmap, int C,
+                                                               float* __restrict__ out) {
+  const long N = meta[1];
+  const long total = N * C;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
+    const long r = i / C, c = i - r * C;
+    float v = 0.f;
+    for (int k = 0; k < nsl; ++k) v += ws[k * stride + i];
+    out[(long)rowmap[r] * C + c] = v;
+  }
+}
+
+hipError_t launch_sum_scatter_rows(const float* ws, int nsl, long stride, const int* meta, const int* rowmap,
+                                   int C, float* out, long cap_rows, hipStream_t s) {
+  long blocks = (cap_rows * C + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(sum_scatter_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, s, ws, nsl, stride, meta,
+                     rowmap, C, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_zero_finished_rows(float* dst, int T_max, int B, int C, const int* seq_len,
                                      const int* meta, hipStream_t s) {
   const long rows = (long)T_max * B;

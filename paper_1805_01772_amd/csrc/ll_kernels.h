@@ -191,6 +191,13 @@ struct XLoopArgs {
                           // GRU pushes r, u, n, zh_n + b_hn and h_{t-1} in their places
   const float* gstk;
   int gld, gchunk, gslots;
+  // LSTM with a nested loop (ACT): at most ponder_max ponder steps per step;
+  // ponder step k of compact row cr sits at row k * slot_rows + cr of the
+  // stack, the guards, HI (forward: h^{k+1}, operand type) and dz (backward)
+  int ponder_max;
+  long slot_rows;
+  int* ntrip;             // [T_max][8 * MRT] inner trip count per (step, row tile)
+  void* HI;
 };
 
 // Chip-wide loops (ll_cloop.hip), for shapes whose recurrent weights need
@@ -257,9 +264,10 @@ struct XKernels {
   size_t lds_bwd;
 };
 
-// gates: 4 (LSTM), 3 (GRU) or 1 (Elman RNN); skip: the LSTM body with a cond
+// gates: 4 (LSTM), 3 (GRU) or 1 (Elman RNN); skip: the LSTM body with a
+// cond; act: the LSTM body with a nested loop (ACT's halting rule)
 template <typename T>
-XKernels x_kernels(int hc, int mrt, int gates = 4, bool skip = false);
+XKernels x_kernels(int hc, int mrt, int gates = 4, bool skip = false, bool act = false);
 hipError_t x_setup(const XKernels& k, int* occ_fwd, int* occ_bwd);
 hipError_t x_launch(const void* fn, const XLoopArgs& a, int nwg, size_t lds, hipStream_t s);
 // Two-layer wavefront: one launch runs both layers (a0 lower, a1 upper);
@@ -274,6 +282,9 @@ hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, 
                                 int slot, void* ring, unsigned* flags, int nflags, hipStream_t s);
 // dst[0 .. n) = src[0 .. n) (one wave; n small)
 hipError_t launch_copy_i32(const int* src, int* dst, int n, hipStream_t s);
+// out[rowmap[r]] = sum of nsl slices (stride floats apart) of compact row r, r < meta[1]
+hipError_t launch_sum_scatter_rows(const float* ws, int nsl, long stride, const int* meta, const int* rowmap,
+                                   int C, float* out, long cap_rows, hipStream_t s);
 hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s);
 
 // Sustained matrix-core rate of the device (TFLOP/s), for reports: the 16x16

@@ -194,6 +194,12 @@ struct ll_plan {
   bool skip = false;
   float* sx = nullptr;
   float* guards = nullptr;
+  // LSTM body with a nested loop: at most M ponder steps; per ponder slot k
+  // the stack, guards, dz rows and (forward) h^{k+1} in HI; inner trip counts
+  bool act = false;
+  int M = 1;
+  void* HI = nullptr;
+  int* ntrip = nullptr;
   // XCD-local LSTM gradient loops: W_h of each layer in the unit-major
   // reduction order ([H, 4H], operand type)
   void* Wum[2] = {nullptr, nullptr};
@@ -326,7 +332,7 @@ void free_plan_memory(ll_plan* p) {
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
                   p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags,
                   p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias, p->sx, p->guards, p->Wum[0],
-                  p->Wum[1], p->prevc};
+                  p->Wum[1], p->prevc, p->HI, p->ntrip};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -401,9 +407,18 @@ ll_status validate_desc(const ll_desc* d) {
   if (d->recompute && d->spill)
     return fail(LL_EUNSUPPORTED, "recompute and spill are alternatives; choose one");
   if (d->cell != LL_CELL_LSTM && d->cell != LL_CELL_RNN && d->cell != LL_CELL_GRU &&
-      d->cell != LL_CELL_LSTM_SKIP)
-    return fail(LL_EINVAL, "cell must be LL_CELL_LSTM, LL_CELL_RNN, LL_CELL_GRU or LL_CELL_LSTM_SKIP (got %d)",
+      d->cell != LL_CELL_LSTM_SKIP && d->cell != LL_CELL_LSTM_ACT)
+    return fail(LL_EINVAL,
+                "cell must be LL_CELL_LSTM, LL_CELL_RNN, LL_CELL_GRU, LL_CELL_LSTM_SKIP or LL_CELL_LSTM_ACT (got %d)",
                 d->cell);
+  if (d->cell == LL_CELL_LSTM_ACT) {
+    if (d->ponder_max < 1 || d->ponder_max > LL_ACT_PONDER_MAX)
+      return fail(LL_EINVAL, "ponder_max must be in 1 .. %d for LL_CELL_LSTM_ACT (got %d)", LL_ACT_PONDER_MAX,
+                  d->ponder_max);
+    if (d->layers != 1) return fail(LL_EUNSUPPORTED, "the nested-loop body is built for one layer");
+  } else if (d->ponder_max != 0) {
+    return fail(LL_EINVAL, "ponder_max must be 0 for cells other than LL_CELL_LSTM_ACT (got %d)", d->ponder_max);
+  }
   if (d->cell != LL_CELL_LSTM && (d->spill || d->recompute))
     return fail(LL_EUNSUPPORTED, "spill and recompute are built for the LSTM cell only");
   if ((long)d->T_max * d->B > (1L << 30))
@@ -429,6 +444,8 @@ ll_status plan_configure(ll_plan* p, const ll_desc* desc, int device, const hipD
   p->es = p->bf16 ? 2 : 4;
   p->G = desc->cell == LL_CELL_RNN ? 1 : desc->cell == LL_CELL_GRU ? 3 : 4;
   p->skip = desc->cell == LL_CELL_LSTM_SKIP;
+  p->act = desc->cell == LL_CELL_LSTM_ACT;
+  p->M = p->act ? desc->ponder_max : 1;
   p->GB = desc->cell == LL_CELL_GRU ? 4 : p->G;
   p->n_cu = prop.multiProcessorCount;
   p->cap = (long)desc->T_max * desc->B;
@@ -482,8 +499,8 @@ ll_status plan_configure(ll_plan* p, const ll_desc* desc, int device, const hipD
       const int hc = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 0;
       const int mrt = ((B + 15) / 16 + 7) / 8;
       if (hc && mrt <= 16) {
-        ll::XKernels xk = p->bf16 ? ll::x_kernels<bf16_t>(hc, mrt, p->G, p->skip)
-                                  : ll::x_kernels<float>(hc, mrt, p->G, p->skip);
+        ll::XKernels xk = p->bf16 ? ll::x_kernels<bf16_t>(hc, mrt, p->G, p->skip, p->act)
+                                  : ll::x_kernels<float>(hc, mrt, p->G, p->skip, p->act);
         if (xk.fwd && xk.bwd && xk.lds_fwd <= lds_limit && xk.lds_bwd <= lds_limit) {
           int of = 0, ob = 0;
           if (ll::x_setup(xk, &of, &ob) == hipSuccess && of >= 1 && ob >= 1) {
@@ -501,9 +518,9 @@ ll_status plan_configure(ll_plan* p, const ll_desc* desc, int device, const hipD
   }
 
   // The Elman RNN, GRU and cond-body cells run on the XCD-local loops only.
-  if ((p->G != 4 || p->skip) && !p->xmode) {
+  if ((p->G != 4 || p->skip || p->act) && !p->xmode) {
     return fail(LL_EUNSUPPORTED, "the %s cell needs the XCD-local loops (H = %d, B = %d do not fit them)",
-                p->G == 1 ? "RNN" : p->G == 3 ? "GRU" : "cond-body LSTM", H, B);
+                p->G == 1 ? "RNN" : p->G == 3 ? "GRU" : p->act ? "nested-loop LSTM" : "cond-body LSTM", H, B);
   }
 
   // Chip-wide loops where one XCD cannot hold the recurrent weights (bf16
@@ -630,6 +647,19 @@ ll_status plan_configure(ll_plan* p, const ll_desc* desc, int device, const hipD
         p->ws_floats = std::max(p->ws_floats, (long)p->dw_splits[l][k] * g.M * g.N);
     }
   }
+  // nested-loop body: the dW products of the M ponder slots all go to the
+  // workspace before one sum, and so do the M dx products (compact rows)
+  if (p->act) {
+    long need = (long)p->M * p->cap * desc->I;
+    for (int k = 0; k < 3; ++k) {
+      DwPart parts[3];
+      const int np = p->dw_rows[0] ? dw_parts_rows(p, 0, parts) : dw_parts(p, 0, parts);
+      if (k >= np) break;
+      const long sp = p->dw_rows[0] ? p->tn_splits[0][k] : p->dw_splits[0][k];
+      need = std::max(need, (long)p->M * sp * parts[k].m * parts[k].n);
+    }
+    p->ws_floats = std::max(p->ws_floats, need);
+  }
   return LL_OK;
 }
 
@@ -661,13 +691,18 @@ ll_status plan_layout(ll_plan* p, bool fwd_only, Take&& take) {
     ALLOC(p->WT[l], es * p->G * H * (in_width(p, l) + H), "transposed W");
     if (!fwd_only)
       ALLOC(p->stack[l],
-            sizeof(float) * (p->spill ? p->nslots * p->slot_floats : cap * (p->recompute || p->G == 1 ? 1 : 5) * H),
+            sizeof(float) * (p->spill ? p->nslots * p->slot_floats
+                                      : (long)p->M * cap * (p->recompute || p->G == 1 ? 1 : 5) * H),
             "stack");
     // (B more rows hold h0 in the operand type, the h_{t-1} of step 0)
     ALLOC(p->HH[l], es * (cap + B) * H, "h history");
   }
   ALLOC(p->Zx, sizeof(float) * cap * p->G * H, "input projection");
-  if (!fwd_only) ALLOC(p->DZ, es * cap * p->GB * H, "dz");
+  if (!fwd_only) ALLOC(p->DZ, es * p->M * cap * p->GB * H, "dz");
+  if (p->act && !fwd_only) {
+    ALLOC(p->HI, es * p->M * cap * H, "ponder states");
+    ALLOC(p->ntrip, sizeof(int) * (long)desc->T_max * 8 * std::max(p->xMRT, 1), "inner trip counts");
+  }
   if (!fwd_only && (!p->dw_rows[0] || (L == 2 && !p->dw_rows[1]))) {   // (transposed copies for the NT products)
     ALLOC(p->DZT, es * p->GB * H * p->ldT, "dz transposed");
     ALLOC(p->XT, es * (maxI + H) * p->ldT, "x and h_prev transposed");
@@ -711,7 +746,7 @@ ll_status plan_layout(ll_plan* p, bool fwd_only, Take&& take) {
   if (p->xmode && p->G == 4)
     for (int l = 0; l < L; ++l) ALLOC(p->Wum[l], es * 4L * H * H, "permuted recurrent weights");
   if (p->dw_rows[0] || p->dw_rows[1]) ALLOC(p->prevc, sizeof(int) * cap, "previous-row map");
-  if (p->skip) ALLOC(p->guards, sizeof(float) * L * cap, "guard stack");
+  if (p->skip || p->act) ALLOC(p->guards, sizeof(float) * L * p->M * cap, "guard stack");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
 #undef ALLOC
   return LL_OK;
@@ -808,6 +843,11 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
       return st;
     }
   }
+  if (p->HI && hipMemset(p->HI, 0, es * p->M * cap * H) != hipSuccess) {
+    free_plan_memory(p);
+    delete p;
+    return fail(LL_EHIP, "hipMemset of the ponder states failed");
+  }
   if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess) {
     free_plan_memory(p);
     delete p;
@@ -849,7 +889,7 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     }
   }
   const int64_t stack_dev = p->spill ? (int64_t)sizeof(float) * p->nslots * p->slot_floats
-                                     : (int64_t)sizeof(float) * cap * (p->recompute || p->G == 1 ? 1 : 5) * H;
+                                     : (int64_t)sizeof(float) * p->M * cap * (p->recompute || p->G == 1 ? 1 : 5) * H;
   p->stack_device_bytes = (int64_t)L * (stack_dev + (int64_t)es * (cap + (p->recompute ? B : 0)) * H);
   if (p->recompute) p->stack_device_bytes += (int64_t)sizeof(float) * p->rc_steps * B * 4 * H;
   p->stack_host_bytes =
@@ -1155,6 +1195,15 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
         xa.sx = p->sx;
         xa.guard = p->guards ? p->guards + (long)l * p->cap : nullptr;
       }
+      if (p->act) {    // bias = [b (4H), w_p (H), b_p]
+        xa.wp = bias[l] + 4L * H;
+        xa.bp = bias[l] + 5L * H;
+        xa.guard = p->guards;
+        xa.ponder_max = p->M;
+        xa.slot_rows = p->cap;
+        xa.ntrip = p->ntrip;
+        xa.HI = p->HI;
+      }
       xa.stack = save ? p->stack[l] : nullptr;
       xa.y = (l == L - 1) ? y : nullptr;
       xa.abort_flag = p->meta + 3;
@@ -1442,6 +1491,167 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   return LL_OK;
 }
 
+// Products after the gradient loop of the nested-loop body (one layer):
+// dW = sum over ponder slots k of [x_t, h^k_prev]^T dz_k, where the h part of
+// slot 0 is h_{t-1} (the h history's previous row, h0 after it) and that of
+// slot k > 0 is h^k (HI slot k-1, the same compact row); db from the loop's
+// partials, zero in the halting part; dx_t = sum_k dz_k W_x^T.  Every slot's
+// product goes to the workspace and one sum follows (dz rows of slots a row
+// tile did not run are zero).
+template <typename T>
+ll_status act_products(ll_plan* p, hipStream_t s, float* dx, float* const* dW, float* const* dbias) {
+  const ll_desc& d = p->d;
+  const int H = d.H, B = d.B, I = d.I, M = p->M;
+  const long cap = p->cap;
+  const int GH = 4 * H;
+  const T* DZ = static_cast<const T*>(p->DZ);
+  const T* HI = static_cast<const T*>(p->HI);
+  hipEvent_t ev = tbeg(p, s, LL_STAGE_DW);
+  LL_HIP(ll::launch_sum_slices(p->db_part, 8, GH, GH, dbias[0], s));
+  LL_HIP(ll::launch_zero_u32(reinterpret_cast<unsigned*>(dbias[0] + GH), H + 1, s));
+  tend(p, s, LL_STAGE_DW, ev);
+  if (p->dw_rows[0]) {
+    ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
+    LL_HIP(ll::launch_prev_rows(p->active, p->off, B, d.T_max, cap, p->prevc, s));
+    LL_HIP(ll::launch_h0_rows<T>(p->h0, p->perm, B, H, reinterpret_cast<T*>(p->HH[0]) + cap * H, s));
+    tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
+    ev = tbeg(p, s, LL_STAGE_DW);
+    DwPart parts[3];
+    const int np = dw_parts_rows(p, 0, parts);
+    for (int q = 0; q < np; ++q) {
+      const DwPart& pt = parts[q];
+      const bool in_part = pt.a_row == 0;
+      const int sp = p->tn_splits[0][q];
+      for (int k = 0; k < M; ++k) {
+        // the h rows of slot k: h_{t-1} through the previous-row map, or h^k
+        const void* hsrc = k == 0 ? p->HH[0] : static_cast<const void*>(HI + (long)(k - 1) * cap * H);
+        const int* hmap = k == 0 ? p->prevc : nullptr;
+        const int hrows = k == 0 ? (int)(cap + B) : (int)cap;
+        ll::GemmTnArgs g{};
+        if (in_part) {
+          g.A = p->x;
+          g.a_rowmap = p->rowmap;
+          g.a_rows = (int)cap;
+          g.lda = I;
+          if (pt.m > I) {
+            g.A2 = hsrc;
+            g.lda2 = H;
+            g.a2_rowmap = hmap;
+            g.a2_rows = hrows;
+            g.M1 = I;
+          }
+        } else {
+          g.A = hsrc;
+          g.a_rowmap = hmap;
+          g.a_rows = hrows;
+          g.lda = H;
+        }
+        g.Bm = DZ + (long)k * cap * GH + pt.b_row;
+        g.ldb = GH;
+        g.b_rows = (int)cap;
+        g.M = pt.m;
+        g.N = pt.n;
+        g.K = (int)cap;
+        g.K_dev = p->meta + 1;
+        g.splits = sp;
+        g.C = p->ws + (long)k * sp * pt.m * pt.n;
+        g.ldc = pt.n;
+        g.split_stride = (long)pt.m * pt.n;
+        if (!ll::gemm_tn_applies(g))
+          return fail(LL_EHIP, "internal: the dW product over rows does not apply (ponder slot %d)", k);
+        LL_HIP(ll::launch_gemm_tn(g, s));
+      }
+      LL_HIP(ll::launch_sum_slices_2d(p->ws, M * sp, (long)pt.m * pt.n, pt.m, pt.n,
+                                      dW[0] + (long)pt.a_row * GH + pt.c_col, GH, s));
+    }
+    tend(p, s, LL_STAGE_DW, ev);
+  } else {
+    DwPart parts[3];
+    const int np = dw_parts(p, 0, parts);
+    const DwPart& pt = parts[0];   // (one product over the stacked [X^T; Hprev^T] for the LSTM)
+    const int sp = p->dw_splits[0][0];
+    const long rowb = p->es * p->ldT;
+    (void)np;
+    for (int k = 0; k < M; ++k) {
+      ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
+      ll::GatherTArgs gt{};
+      gt.B = B;
+      gt.meta = p->meta;
+      gt.rowmap = p->rowmap;
+      gt.off = p->off;
+      gt.perm = p->perm;
+      gt.ldo = (int)p->ldT;
+      gt.in = DZ + (long)k * cap * GH;
+      gt.out = p->DZT;
+      gt.C = GH;
+      gt.mode = 1;
+      LL_HIP(ll::launch_gather_transpose<T>(gt, (int)cap, s));
+      if (k == 0) {   // x rows: the same for every slot
+        gt.in = p->x;
+        gt.out = p->XT;
+        gt.C = I;
+        gt.mode = 0;
+        LL_HIP(ll::launch_gather_transpose<T>(gt, (int)cap, s));
+      }
+      gt.out = static_cast<char*>(p->XT) + p->es * I * p->ldT;
+      gt.C = H;
+      if (k == 0) {
+        gt.in = p->HH[0];
+        gt.mode = 2;
+        gt.h0f = p->h0;
+      } else {
+        gt.in = HI + (long)(k - 1) * cap * H;
+        gt.mode = 1;
+        gt.h0f = nullptr;
+      }
+      LL_HIP(ll::launch_gather_transpose<T>(gt, (int)cap, s));
+      tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
+      ev = tbeg(p, s, LL_STAGE_DW);
+      ll::GemmArgs g{};
+      g.A = p->XT;
+      g.lda = p->ldT;
+      g.Bm = static_cast<const char*>(p->DZT) + pt.b_row * rowb;
+      g.ldb = p->ldT;
+      g.M = pt.m;
+      g.N = pt.n;
+      g.K = (int)cap;
+      g.K_dev = p->meta + 1;
+      g.k_zero_tail = 1;
+      g.splits = sp;
+      g.C = p->ws + (long)k * sp * pt.m * pt.n;
+      g.ldc = pt.n;
+      g.split_stride = (long)pt.m * pt.n;
+      LL_HIP(ll::launch_gemm_nt<T>(g, s));
+      tend(p, s, LL_STAGE_DW, ev);
+    }
+    ev = tbeg(p, s, LL_STAGE_DW);
+    LL_HIP(ll::launch_sum_slices_2d(p->ws, M * sp, (long)pt.m * pt.n, pt.m, pt.n, dW[0], GH, s));
+    tend(p, s, LL_STAGE_DW, ev);
+  }
+  if (!dx) return LL_OK;
+  // dx: one product per slot into compact rows of the workspace, then the
+  // sum over slots scattered to time-major rows
+  ev = tbeg(p, s, LL_STAGE_DX);
+  for (int k = 0; k < M; ++k) {
+    ll::GemmArgs gx{};
+    gx.A = DZ + (long)k * cap * GH;
+    gx.lda = GH;
+    gx.Bm = p->W[0];
+    gx.ldb = GH;
+    gx.M = (int)cap;
+    gx.M_dev = p->meta + 1;
+    gx.N = I;
+    gx.K = GH;
+    gx.splits = 1;
+    gx.C = p->ws + (long)k * cap * I;
+    gx.ldc = I;
+    LL_HIP(ll::launch_gemm_nt<T>(gx, s));
+  }
+  LL_HIP(ll::launch_sum_scatter_rows(p->ws, M, cap * I, p->meta, p->rowmap, I, dx, cap, s));
+  tend(p, s, LL_STAGE_DX, ev);
+  return LL_OK;
+}
+
 // Two-layer wavefront, gradient: one launch in which the upper layer's step t
 // runs beside the lower layer's step t+1 on every XCD; the upper layer hands
 // dy of the lower layer's output over per step (dz W_x^T of its own units),
@@ -1626,7 +1836,12 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       xa.X = p->DZ;
       xa.c0 = p->c0 && p->G == 4 ? p->c0 + (long)l * B * H : nullptr;
       xa.stack = p->stack[l];
-      xa.guard = p->skip ? p->guards + (long)l * p->cap : nullptr;
+      xa.guard = p->skip ? p->guards + (long)l * p->cap : p->act ? p->guards : nullptr;
+      if (p->act) {
+        xa.ponder_max = p->M;
+        xa.slot_rows = p->cap;
+        xa.ntrip = p->ntrip;
+      }
       if (l == L - 1) {
         xa.dy = dy;
         xa.dy_compact = 0;
@@ -1756,6 +1971,10 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       tend(p, s, LL_STAGE_BWD_LOOP, ev);
     }
     if (l == 0 && dx) LL_HIP(hipStreamWaitEvent(s, p->ev_side, 0));
+    if (p->act) {
+      LL_STATUS(act_products<T>(p, s, dx, dW, dbias));
+      continue;
+    }
     LL_STATUS(bwd_products<T>(p, s, l, p->DZ, p->db_part, l == 0 ? dx : p->dyc, dW, dbias));
   }
   return LL_OK;

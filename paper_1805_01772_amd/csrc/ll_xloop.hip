@@ -130,8 +130,22 @@ __device__ __forceinline__ char* ring_tile(const XLoopArgs& a, int slot, int grp
 // tile, over the h_{t-1} chunks each wave already holds; every member of an
 // XCD computes it identically, so all take the same branch); the guard of
 // every (step, row) is pushed for the gradient loop.
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP, int G = 4, bool SKIP = false>
+// ACT (LSTM only): the body is a nested while-loop (Adaptive Computation
+// Time's halting rule): the LSTM step applied to (x_t, h, c) up to
+// a.ponder_max times; after ponder step k a row's halting probability
+// p = sigmoid(h^k . w_p + b_p) (h part by the same extra matrix-core column
+// as the cond body's) is summed into P, and the row stops pondering once
+// P >= 1 - eps.  The row tile runs a ponder iteration while any of its rows
+// still ponders (every member computes the same sums, so all agree), and
+// each iteration is one exchange round; rows that stopped keep their state.
+// The forward pushes, per (step, ponder step k, row), the step's values at
+// stack slot k (rows k * slot_rows + compact row), the guard (1 = the row
+// pondered) and the state h^{k+1} (into HI); per (step, row tile) the inner
+// trip count (ntrip).  The exchange counts ponder iterations, not steps.
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool TOP, int G = 4, bool SKIP = false,
+          bool ACT = false>
 __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
+  constexpr bool PRED = SKIP || ACT;   // the extra predicate column of the recurrent product
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT / G;
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
@@ -173,11 +187,12 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   int* win = reinterpret_cast<int*>(red + XNW * 4 * IS);               // [2][WIN+1]
   int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
   float* sred = reinterpret_cast<float*>(sperm + MRT_MAX * 16);       // SKIP: [XNW][16]
-  static_assert(!(SKIP && (TOP || G != 4)), "the cond body is built on the single-layer LSTM loop");
-  // SKIP: the predicate's h weights as the B operand of a 16-column tile
-  // whose column 0 is w_ph (operand-rounded) and the rest zero
-  uint4 wpr[SKIP ? KSW : 1];
-  if constexpr (SKIP) {
+  static_assert(!(PRED && (TOP || G != 4)), "the cond and nested-loop bodies are built on the single-layer LSTM loop");
+  static_assert(!(SKIP && ACT), "one body");
+  // SKIP / ACT: the predicate's (halting unit's) h weights as the B operand
+  // of a 16-column tile whose column 0 is w_p (operand-rounded), the rest zero
+  uint4 wpr[PRED ? KSW : 1];
+  if constexpr (PRED) {
 #pragma unroll
     for (int i = 0; i < KSW; ++i) {
       const int ks = ks0 + i;
@@ -188,7 +203,13 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       wpr[i] = *reinterpret_cast<const uint4*>(v);
     }
   }
-  const float bp = SKIP ? a.bp[0] : 0.f;
+  const float bp = PRED ? a.bp[0] : 0.f;
+  // ACT: halting threshold 1 - eps (eps = 0.01) and the ponder counters of
+  // each row tile (exchange rounds so far)
+  const float act_thr = 1.0f - 0.01f;
+  int itc[MRT_MAX];
+#pragma unroll
+  for (int mt = 0; mt < MRT_MAX; ++mt) itc[mt] = 0;
 
   // cell thread: 16 lanes take 16 consecutive units of one row, a wave four
   // rows (the four MFMA result elements of one lane group)
@@ -263,15 +284,29 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         continue;
       }
       unsigned* flags = a.flags + (grp * a.MRT + mt) * 32;
+      const int r = r0 + crow;
+      const bool act = cellt && r < A_t;
+      float zc[G];
+      float sxc = 0.f;
+      // ACT: this thread's row still ponders; the row's summed halting
+      // probability
+      bool prow = act;
+      float Psum = 0.f;
+      const int nk = ACT ? a.ponder_max : 1;
+      int k = 0;
+      for (; k < nk; ++k) {
+      // exchange round of this iteration: the step (one round per step), or
+      // the tile's ponder counter
+      const int cnt = ACT ? itc[mt] : t;
       // 1. h_{t-1} of this wave's k-steps (for the launch's first step the
       //    ring holds the entering state); the upper wavefront layer first
       //    takes y1_t from the lower layer's ring
       const int kx1 = min(ks1, KX);                        // [ks0, kx1): lower layer's k-steps
       if (TOP && ks0 < kx1)
         wait_flags(a, a.in_flags + (grp * a.MRT + mt) * 32, ks0, kx1 - ks0, a.in_ks, (unsigned)(t + 2));
-      if (t > t0 && max(ks0, KX) < ks1)
-        wait_flags(a, flags, max(ks0, KX) - KX, ks1 - max(ks0, KX), a.P, (unsigned)(t + 1));
-      const __amdgpu_buffer_rsrc_t rs = make_rsrc(ring_tile(a, (t + 1) & 1, grp, mt), (unsigned)(a.ring_ks << 10));
+      if ((ACT ? cnt > 0 : t > t0) && max(ks0, KX) < ks1)
+        wait_flags(a, flags, max(ks0, KX) - KX, ks1 - max(ks0, KX), a.P, (unsigned)(cnt + 1));
+      const __amdgpu_buffer_rsrc_t rs = make_rsrc(ring_tile(a, (cnt + 1) & 1, grp, mt), (unsigned)(a.ring_ks << 10));
       __amdgpu_buffer_rsrc_t rsx = rs;
       if constexpr (TOP)
         rsx = make_rsrc(reinterpret_cast<const char*>(a.in_ring) +
@@ -284,10 +319,10 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         av[i] = ks < KX ? ld_chunk_l2(rsx, i < nks ? (unsigned)((ks << 10) + lane * 16) : kOOB)
                         : ld_chunk_l2(rs, i < nks ? (unsigned)(((ks - KX) << 10) + lane * 16) : kOOB);
       }
-      float zc[G];
+      if (k == 0) {
 #pragma unroll
       for (int g = 0; g < G; ++g) zc[g] = zf[mt][g];
-      const float sxc = sxf[mt];
+      sxc = sxf[mt];
       if constexpr (!TOP) {  // input projections of step t+1 (rows past A_n read zeros)
         const int nr = max(0, min(16, A_n - r0));
         const __amdgpu_buffer_rsrc_t rz = make_rsrc(a.Zx + (long)(off_n + r0) * G4, (unsigned)(nr * G4 * 4));
@@ -298,6 +333,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
           const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.sx + off_n + r0, (unsigned)(nr * 4));
           sxf[mt] = ld_f32(rx, cellt ? (unsigned)(crow * 4) : kOOB);
         }
+      }
       }
       // 2. partial products over this wave's k-steps, column tiles in two
       //    halves, into red[wave][i][ct][lane] (the previous tile's cell has
@@ -326,9 +362,9 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
 #pragma unroll
           for (int i = 0; i < 4; ++i) red[(wave * 4 + i) * IS + (hf * NH + c) * 64 + lane] = acc[c][i];
       }
-      if constexpr (SKIP) {
-        // h part of the predicate over this wave's k-steps: column 0 of the
-        // extra tile; result element i of lane 16 q is row 4 q + i
+      if constexpr (PRED) {
+        // h part of the predicate (halting unit) over this wave's k-steps:
+        // column 0 of the extra tile; result element i of lane 16 q is row 4 q + i
         f32x4 accp = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < KSW; ++i)
@@ -345,14 +381,27 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         wait_flags(a, a.out_flags + (grp * a.MRT + mt) * 32, 0, a.P, a.P, (unsigned)t);
       // 3. cell of (crow, cu): gate g is local column g*HJ + cu
       float ig = 0.f, fg = 0.f, gg = 0.f, og = 0.f, cn = 0.f, hn = 0.f;
-      const int r = r0 + crow;
-      const bool act = cellt && r < A_t;
-      bool run = true;   // SKIP: the branch this row takes
+      bool run = true;   // SKIP: the branch this row takes; ACT: the row ponders
       if constexpr (SKIP) {
         float sh = sred[crow];
 #pragma unroll
         for (int w2 = 1; w2 < XNW; ++w2) sh += sred[w2 * 16 + crow];
         run = (sxc + sh) + bp > 0.f;
+      }
+      if constexpr (ACT) {
+        // halting after ponder step k (its state h^k is this iteration's
+        // operand): p = sigmoid(h^k . w_p + b_p), summed in float32
+        if (k > 0 && prow) {
+          float sh = sred[crow];
+#pragma unroll
+          for (int w2 = 1; w2 < XNW; ++w2) sh += sred[w2 * 16 + crow];
+          Psum += sigmoidf_(sh + bp);
+          if (Psum >= act_thr) prow = false;
+        }
+        run = prow;
+        // no row of the tile ponders any more: the nested loop ends (every
+        // member takes the same decision from the same sums)
+        if (__syncthreads_or(prow ? 1 : 0) == 0) break;
       }
       if (cellt) {
         float z[G], zh[G];
@@ -372,7 +421,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
           og = sigmoidf_(z[3]);
           cn = fg * cs[mt] + ig * gg;
           hn = og * tanhf_(cn);
-          if (SKIP && !run) {   // the false branch keeps the state
+          if ((SKIP || ACT) && !run) {   // the false branch / a halted row keeps the state
             cn = cs[mt];
             hn = hs[mt];
           }
@@ -389,12 +438,28 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
           hn = tanhf_(z[0]);
         }
         if (act) {
-          *reinterpret_cast<T*>(ring_tile(a, t & 1, grp, mt) + (rank << 10) + rbo) = Op<T>::from_f32(hn);
+          *reinterpret_cast<T*>(ring_tile(a, cnt & 1, grp, mt) + (rank << 10) + rbo) = Op<T>::from_f32(hn);
           if constexpr (G == 4) cs[mt] = cn;
           hs[mt] = hn;
         }
       }
-      publish(flags + rank, (unsigned)(t + 2));
+      publish(flags + rank, (unsigned)(cnt + 2));
+      if constexpr (ACT) {
+        itc[mt] = cnt + 1;
+        // ponder step k's values at stack slot k, its guard, and h^{k+1}
+        if (act && a.stack) {
+          const long vr = (long)k * a.slot_rows + off_t + r;
+          float* st = a.stack + vr * a.sld + ju;
+          st[0] = ig;
+          st[H] = fg;
+          st[2 * H] = gg;
+          st[3 * H] = og;
+          st[a.scoff] = cn;
+          reinterpret_cast<T*>(a.HI)[vr * H + ju] = Op<T>::from_f32(hn);
+          if (rank == 0 && cu == 0) a.guard[vr] = run ? 1.f : 0.f;
+        }
+        continue;
+      }
       if (act) {
         const long cr = off_t + r;
         HH[cr * H + ju] = Op<T>::from_f32(hn);
@@ -419,6 +484,16 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         const int b = sperm[mt * 16 + crow];
         if (b >= 0) a.y[((long)t * B + b) * H + ju] = act ? hn : 0.f;
       }
+      }   // ponder iterations
+      if constexpr (ACT) {
+        // the step's result: the last ponder state; the tile's inner trip count
+        if (act) HH[(long)(off_t + r) * H + ju] = Op<T>::from_f32(hs[mt]);
+        if (a.y && cellt) {
+          const int b = sperm[mt * 16 + crow];
+          if (b >= 0) a.y[((long)t * B + b) * H + ju] = act ? hs[mt] : 0.f;
+        }
+        if (a.stack && rank == 0 && threadIdx.x == 0) a.ntrip[(long)t * 8 * a.MRT + grp * a.MRT + mt] = k;
+      }
     }
   }
 
@@ -435,7 +510,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
   }
 }
 
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int G, bool SKIP>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int G, bool SKIP, bool ACT = false>
 __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
@@ -449,7 +524,7 @@ __global__ __launch_bounds__(XNT, 1) void xfwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  xfwd_body<T, NCT, KSW, KSR, MRT_MAX, false, G, SKIP>(a, grp, rank, lds);
+  xfwd_body<T, NCT, KSW, KSR, MRT_MAX, false, G, SKIP, ACT>(a, grp, rank, lds);
 }
 
 // Two-layer wavefront, forward: members 0 .. P-1 of every XCD run the lower
@@ -497,8 +572,15 @@ __global__ __launch_bounds__(XNT, 1) void xfwd2_kernel(XLoopArgs a0, XLoopArgs a
 // SKIP: the LSTM body with a cond (see xfwd_body); the popped guard picks
 // each row's branch gradient: the LSTM step's, or the identity (dz = 0,
 // dh_{t-1} = dh_tot, dc_{t-1} = dc_t).
+// ACT: the body holds a nested loop (see xfwd_body).  Step t pops the tile's
+// inner trip count n and runs a nested gradient loop of n iterations, ponder
+// step n-1 down to 0, each one exchange round: the ponder step's values and
+// guard are popped from its stack slot (the guard picks the LSTM step's
+// gradient or the identity); dy_t enters at the last ponder step; c of the
+// step before ponder step 0 is the previous step's last ponder state.  dz of
+// ponder step k goes to dz slot k (slots the tile did not run get zeros).
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE, bool DMA = false, int G = 4,
-          bool SKIP = false>
+          bool SKIP = false, bool ACT = false>
 __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT;                 // units per work-group
@@ -520,15 +602,16 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   const int KS = (int)(G4 / (4 * KPC));
   // pops per (step, tile) and thread: LSTM i, f, g, o, c_t, c_{t-1}, dy;
   // GRU r, u, n, zh_n + b_hn, h_{t-1}, dy; RNN h_t, dy
-  constexpr int NPOP = (G == 4 ? 7 : G == 3 ? 6 : 2) + (SKIP ? 1 : 0);
-  constexpr int NPV = SKIP ? 8 : 7;   // popped values kept per (tile, thread); [7] = guard
+  constexpr bool GUARDED = SKIP || ACT;   // a popped guard picks each row's gradient
+  constexpr int NPOP = (G == 4 ? 7 : G == 3 ? 6 : 2) + (GUARDED ? 1 : 0);
+  constexpr int NPV = GUARDED ? 8 : 7;   // popped values kept per (tile, thread); [7] = guard
   // Unit-major reduction order (single-layer LSTM loop): k = 4 u + g over
   // units u and gates g, so a member's dz values of one unit are adjacent in
   // the ring and k-steps 4 r .. 4 r + 3 are member r's; the weights come
   // from W_h permuted to that order (a.W = [H, 4H], a.woff = 0).  Otherwise
   // k = g H + u and k-step g P + r is member r's gate g.
   constexpr bool UM = G == 4 && ROLE == 0;
-  static_assert(!(SKIP && (ROLE != 0 || G != 4)), "the cond body is built on the single-layer LSTM loop");
+  static_assert(!(GUARDED && (ROLE != 0 || G != 4)), "the cond and nested-loop bodies are built on the single-layer LSTM loop");
   const int ks0 = min(KS, wave * KSW), ks1 = min(KS, ks0 + KSW);
   const int nks = ks1 - ks0;                            // k-steps of this wave
   const T* W = reinterpret_cast<const T*>(a.W);
@@ -637,6 +720,54 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
     }
     (void)offp;
   };
+  // ACT: pops of ponder step kk of step tt for this thread (zeros for rows
+  // not running at tt): the step's i, f, g, o, c at slot kk, the c before it
+  // (slot kk-1, or the last ponder slot np_prev - 1 of step tt-1 at compact
+  // offset offp, or c0), dy_t only at the last ponder step (kk = n_tt - 1),
+  // and the guard
+  auto fetch_act = [&](float (&v)[NPV], int tt, int kk, int n_tt, int mt, int A, int off, int offp,
+                       int np_prev) {
+    const int r0 = (grp + 8 * mt) * 16;
+    const int nr = tt >= 0 ? max(0, min(16, A - r0)) : 0;
+    const bool ok = cellt && crow < nr;
+    const int b = sperm[mt * 16 + crow];
+    const long SL = a.sld;
+    const long vr = (long)max(kk, 0) * a.slot_rows + off + r0;     // first row of the tile's slot
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.stack + vr * SL, (unsigned)(nr * SL * 4));
+    const unsigned go = ok ? (unsigned)((crow * SL + ju) * 4) : kOOB;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = ld_f32(rg, go + c * H * 4);
+    v[4] = ld_f32(rg, go + a.scoff * 4);
+    if (kk > 0) {
+      const __amdgpu_buffer_rsrc_t rp2 =
+          make_rsrc(a.stack + (vr - a.slot_rows) * SL, (unsigned)(nr * SL * 4));
+      v[5] = ld_f32(rp2, go + a.scoff * 4);
+    } else if (tt > 0) {
+      const long pr = (long)(np_prev - 1) * a.slot_rows + offp + r0;
+      const __amdgpu_buffer_rsrc_t rp2 = make_rsrc(a.stack + pr * SL, (unsigned)(nr * SL * 4));
+      v[5] = ld_f32(rp2, go + a.scoff * 4);
+    } else {
+      const __amdgpu_buffer_rsrc_t rc = make_rsrc(a.c0, a.c0 ? (unsigned)(B * H * 4) : 0u);
+      v[5] = ld_f32(rc, ok ? (unsigned)((b * H + ju) * 4) : kOOB);
+    }
+    const bool last = kk == n_tt - 1;
+    const __amdgpu_buffer_rsrc_t rd =
+        make_rsrc(a.dy && last ? a.dy + (long)max(tt, 0) * B * H : nullptr, a.dy && last ? (unsigned)(B * H * 4) : 0u);
+    v[6] = ld_f32(rd, ok ? (unsigned)((b * H + ju) * 4) : kOOB);
+    const __amdgpu_buffer_rsrc_t rgd = make_rsrc(a.guard + vr, (unsigned)(nr * 4));
+    v[NPV - 1] = ld_f32(rgd, ok ? (unsigned)(crow * 4) : kOOB);
+  };
+  // ACT: the inner trip count of (step tt, tile mt), within [1, ponder_max]
+  auto ntrip_of = [&](int tt, int mt) -> int {
+    if (!ACT || tt < 0) return 1;
+    const int n = uni(a.ntrip[(long)tt * 8 * a.MRT + grp * a.MRT + mt]);
+    return min(max(n, 1), a.ponder_max);
+  };
+  // ACT: pops of the first ponder iteration of step tt (its last ponder step)
+  auto fetch_step = [&](float (&v)[NPV], int tt, int mt, int A, int off, int offp) {
+    const int n = ntrip_of(tt, mt);
+    fetch_act(v, tt, n - 1, n, mt, A, off, offp, ntrip_of(tt - 1, mt));
+  };
 
   const int T_eff = uni(a.meta[0]);
   const int t0 = a.t_begin, t1 = min(a.t_end, T_eff);
@@ -650,9 +781,16 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
     const int off_t = t >= 0 ? win[WIN + 1 + t - wlo] : 0;
     const int off_p = t >= 1 ? win[WIN + 1 + t - 1 - wlo] : 0;
 #pragma unroll
-    for (int mt = 0; mt < MRT_MAX; ++mt)
-      if (mt < a.MRT) fetch(pv[mt], t, mt, A_t, off_t, off_p);
+    for (int mt = 0; mt < MRT_MAX; ++mt) {
+      if (mt >= a.MRT) continue;
+      if constexpr (ACT) fetch_step(pv[mt], t, mt, A_t, off_t, off_p);
+      else fetch(pv[mt], t, mt, A_t, off_t, off_p);
+    }
   }
+  // ACT: exchange rounds per row tile so far (the flags count them)
+  int itb[MRT_MAX];
+#pragma unroll
+  for (int mt = 0; mt < MRT_MAX; ++mt) itb[mt] = 1;
 
   for (int t = t1 - 1; t >= t0; --t) {
     if (t - 2 < wlo && wlo > 0) {
@@ -670,12 +808,18 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       const int r0 = (grp + 8 * mt) * 16;
       if (r0 >= A_t) {
         // rows of this tile may start running at step t-1 (lengths >= t)
-        fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);
+        if constexpr (ACT) fetch_step(pv[mt], t - 1, mt, A_n, off_n, off_pn);
+        else fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);
         continue;
       }
       unsigned* flags = a.flags + (grp * a.MRT + mt) * 32;
-      char* slot = ring_tile(a, t & 1, grp, mt);
       const bool act = cellt && r0 + crow < A_t;
+      // ACT: the nested gradient loop over ponder steps n-1 .. 0 of step t;
+      // one iteration otherwise
+      const int n_t = ntrip_of(t, mt);
+      for (int kk = ACT ? n_t - 1 : 0; kk >= 0; --kk) {
+      const int cnt = ACT ? itb[mt] : T_eff - t;   // flag value of this exchange round
+      char* slot = ring_tile(a, ACT ? cnt & 1 : t & 1, grp, mt);
       // dyx ring slot of this tile for step t: [16 rows][H] floats
       const long dyx_off = ((long)(((t & 1) * 8 + grp) * a.MRT + mt) * 16) * H;
       float dyl = 0.f;   // lower wavefront layer: dy of its output from the upper layer
@@ -702,7 +846,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
           dz[1] = dct * cp * (fg * (1.f - fg));
           dz[2] = dct * ig * (1.f - gg * gg);
           dz[3] = d_o * (og * (1.f - og));
-          if (SKIP && pv[mt][NPV - 1] == 0.f) {   // the row kept its state at step t
+          if (GUARDED && pv[mt][NPV - 1] == 0.f) {   // the row kept its state at step t (ponder step kk)
             dz[0] = dz[1] = dz[2] = dz[3] = 0.f;
             dhu = dht;
           } else {
@@ -739,9 +883,17 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
             *reinterpret_cast<T*>(slot + ((g * P + rank) << 10) + rbo) = Op<T>::from_f32(dz[g]);
         }
       }
-      publish(flags + rank, (unsigned)(T_eff - t));
+      publish(flags + rank, (unsigned)cnt);
+      if (ACT && act && kk == n_t - 1) {
+        // dz slots of ponder steps the tile did not run at step t: zeros
+        for (int k2 = n_t; k2 < a.ponder_max; ++k2) {
+          T* dzz = DZ + ((long)k2 * a.slot_rows + off_t + r0 + crow) * GBH + ju;
+#pragma unroll
+          for (int g = 0; g < G; ++g) dzz[(long)g * H] = Op<T>::from_f32(0.f);
+        }
+      }
       if (act) {
-        T* dzr = DZ + (long)(off_t + r0 + crow) * GBH + ju;
+        T* dzr = DZ + ((long)(ACT ? kk : 0) * a.slot_rows + off_t + r0 + crow) * GBH + ju;
         if constexpr (G == 3) {   // [da_r, da_u, da_n, da_n * r]
           dzr[0] = Op<T>::from_f32(dz[0]);
           dzr[H] = Op<T>::from_f32(dz[1]);
@@ -761,9 +913,19 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       }
       // phase 2
       if constexpr (UM)   // k-steps 4 r .. 4 r + 3 come from member r
-        wait_flags(a, flags, ks0 / 4, (nks + 3) / 4, P, (unsigned)(T_eff - t));
+        wait_flags(a, flags, ks0 / 4, (nks + 3) / 4, P, (unsigned)cnt);
       else
-        wait_flags(a, flags, ks0, nks < 64 ? nks : 64, P, (unsigned)(T_eff - t));
+        wait_flags(a, flags, ks0, nks < 64 ? nks : 64, P, (unsigned)cnt);
+      // the pops of the next iteration: ponder step kk-1 of this step, or the
+      // previous step's last ponder step (ACT); the previous step otherwise
+      auto fetch_next = [&]() {
+        if constexpr (ACT) {
+          if (kk > 0) fetch_act(pv[mt], t, kk - 1, n_t, mt, A_t, off_t, off_n, ntrip_of(t - 1, mt));
+          else fetch_step(pv[mt], t - 1, mt, A_n, off_n, off_pn);
+        } else {
+          fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);
+        }
+      };
       const __amdgpu_buffer_rsrc_t rs = make_rsrc(slot, (unsigned)(a.ring_ks << 10));
       f32x4 acc[NCO];
 #pragma unroll
@@ -776,7 +938,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
         for (int i = 0; i < KSW; ++i)
           ld_chunk_to_lds(rs, i < nks ? (unsigned)(((ks0 + i) << 10) + lane * 16) : kOOB, dzl + i * 64);
         asm volatile("" ::: "memory");
-        fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);
+        fetch_next();
         asm volatile("" ::: "memory");
       }
       const unsigned dza = lds_addr(dzl) + lane * 16;
@@ -794,7 +956,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
 #pragma unroll
           for (int i = 0; i < KB; ++i)
             av[i] = ld_chunk_l2(rs, b0 + i < nks ? (unsigned)(((ks0 + b0 + i) << 10) + lane * 16) : kOOB);
-          if (b0 + KB >= KSW) fetch(pv[mt], t - 1, mt, A_n, off_n, off_pn);   // next step's pops
+          if (b0 + KB >= KSW) fetch_next();   // next iteration's pops
         }
 #pragma unroll
         for (int i = 0; i < KB; ++i) {
@@ -820,8 +982,9 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
         float s = rp[0];
 #pragma unroll
         for (int w2 = 1; w2 < XNW; ++w2) s += rp[w2 * 4 * IS];
-        dh[mt] = (G == 3 || SKIP) ? s + dhu : s;
+        dh[mt] = (G == 3 || GUARDED) ? s + dhu : s;
       }
+      if constexpr (ACT) itb[mt] = cnt + 1;
       if constexpr (ROLE == 2) {
         // dy of the lower layer's output at step t for the own units; the
         // slot held step t+2, which the lower partner has read once it has
@@ -837,6 +1000,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
         }
         publish(a.dyx_flags + (grp * a.MRT + mt) * 32 + rank, (unsigned)(T_eff - t));
       }
+      }   // ponder iterations
     }
   }
 
@@ -866,7 +1030,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   }
 }
 
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool DMA, int G, bool SKIP>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool DMA, int G, bool SKIP, bool ACT = false>
 __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
@@ -880,7 +1044,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, DMA, G, SKIP>(a, grp, rank, lds);
+  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, DMA, G, SKIP, ACT>(a, grp, rank, lds);
 }
 
 // Two-layer wavefront, gradient: members 0 .. P-1 of every XCD run the lower
@@ -980,18 +1144,19 @@ hipError_t launch_zero_u32(unsigned* p, int n, hipStream_t s) {
 // hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
 // row tiles per XCD.
 namespace {
-template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT, int G = 4, bool SKIP = false>
+template <typename T, int NF, int NB, int HC, int RF, int RB, int MRT, int G = 4, bool SKIP = false,
+          bool ACT = false>
 XKernels x_make() {
   XKernels k{};
-  k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT, G, SKIP>);
-  k.lds_fwd = xfwd_lds(HC, RF, NF, MRT, SKIP ? xfwd_skip_floats() : 0);
+  k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT, G, SKIP, ACT>);
+  k.lds_fwd = xfwd_lds(HC, RF, NF, MRT, (SKIP || ACT) ? xfwd_skip_floats() : 0);
   // the gradient loop loads its dz k-steps straight into LDS when they fit
   const size_t dma_lds = xbwd_lds(G * HC, RB, NB, MRT, true);
   if (dma_lds <= 160 * 1024) {
-    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, true, G, SKIP>);
+    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, true, G, SKIP, ACT>);
     k.lds_bwd = dma_lds;
   } else {
-    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, false, G, SKIP>);
+    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, false, G, SKIP, ACT>);
     k.lds_bwd = xbwd_lds(G * HC, RB, NB, MRT);
   }
   return k;
@@ -1007,12 +1172,21 @@ XKernels x_make() {
 // 6 / 3, backward KSW = 3H/256 / 3H/128.)
 // hc in {1, 2, 4} is the forward KSW (k-steps per wave, 8 waves); mrt <= 4
 template <typename T>
-XKernels x_kernels(int hc, int mrt, int gates, bool skip) {
+XKernels x_kernels(int hc, int mrt, int gates, bool skip, bool act) {
   constexpr bool bf = sizeof(T) == 2;
   constexpr int NF = bf ? 8 : 4;
   constexpr int NB = bf ? 2 : 1;
   const bool one = mrt <= 1;
   if (mrt > 4) return XKernels{};
+  if (act) {   // the LSTM tiling with the nested-loop body
+    if (gates != 4 || skip) return XKernels{};
+    switch (hc) {
+      case 1: return one ? x_make<T, NF, NB, 1, 1, 4, 1, 4, false, true>() : x_make<T, NF, NB, 1, 1, 4, 4, 4, false, true>();
+      case 2: return one ? x_make<T, NF, NB, 2, 2, 8, 1, 4, false, true>() : x_make<T, NF, NB, 2, 2, 6, 4, 4, false, true>();
+      case 4: return one ? x_make<T, NF, NB, 4, 4, 16, 1, 4, false, true>() : x_make<T, NF, NB, 4, 3, 8, 4, 4, false, true>();
+      default: return XKernels{};
+    }
+  }
   if (skip) {   // the LSTM tiling with the cond body
     if (gates != 4) return XKernels{};
     switch (hc) {
@@ -1049,8 +1223,8 @@ XKernels x_kernels(int hc, int mrt, int gates, bool skip) {
   }
 }
 
-template XKernels x_kernels<float>(int, int, int, bool);
-template XKernels x_kernels<bf16_t>(int, int, int, bool);
+template XKernels x_kernels<float>(int, int, int, bool, bool);
+template XKernels x_kernels<bf16_t>(int, int, int, bool, bool);
 
 // Two-layer wavefront kernels: the lower layer as in x_kernels, the upper one
 // with twice the forward k-steps (K = I_l + H = 2H) and, in the gradient, twice

@@ -20,7 +20,9 @@ LL_OK, LL_EINVAL, LL_ENOMEM, LL_EHIP, LL_ESTATE, LL_EUNSUPPORTED = range(6)
 LL_F32, LL_BF16 = 0, 1
 LL_DEVERR_SEQ_LEN, LL_DEVERR_BARRIER = 1, 2
 LL_LOOPS_GRID, LL_LOOPS_XCD, LL_LOOPS_CHIP = 0, 1, 2
-LL_CELL_LSTM, LL_CELL_RNN, LL_CELL_GRU, LL_CELL_LSTM_SKIP = 0, 1, 2, 3
+LL_CELL_LSTM, LL_CELL_RNN, LL_CELL_GRU, LL_CELL_LSTM_SKIP, LL_CELL_LSTM_ACT = 0, 1, 2, 3, 4
+LL_ACT_EPS = 0.01
+LL_ACT_PONDER_MAX = 8
 STATUS_NAMES = {0: "LL_OK", 1: "LL_EINVAL", 2: "LL_ENOMEM", 3: "LL_EHIP",
                 4: "LL_ESTATE", 5: "LL_EUNSUPPORTED"}
 
@@ -40,7 +42,7 @@ class ll_desc(ctypes.Structure):
                 ("spill", ctypes.c_int32), ("spill_chunk_steps", ctypes.c_int32),
                 ("device_stack_budget_bytes", ctypes.c_int64),
                 ("recompute", ctypes.c_int32), ("cell", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("ponder_max", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class LoopError(RuntimeError):
@@ -172,11 +174,11 @@ class Plan:
     def __init__(self, T_max: int, B: int, I: int, H: int, layers: int = 1,
                  dtype: str = "f32", spill: int = 0, spill_chunk_steps: int = 0,
                  device_stack_budget_bytes: int = 0, device: int = 0, recompute: int = 0,
-                 cell: int = 0):
+                 cell: int = 0, ponder_max: int = 0):
         lib = load_library()
         self._lib = lib
         self.desc = make_desc(T_max, B, I, H, layers, dtype, spill, spill_chunk_steps,
-                              device_stack_budget_bytes, recompute, cell)
+                              device_stack_budget_bytes, recompute, cell, ponder_max)
         self.dtype = dtype
         self.device = device
         h = ctypes.c_void_p()
@@ -278,10 +280,10 @@ NOALLOC_SCRATCH_BYTES = 128 << 20   # LL_NOALLOC_SCRATCH_BYTES
 
 def make_desc(T_max: int, B: int, I: int, H: int, layers: int = 1, dtype: str = "f32",
               spill: int = 0, spill_chunk_steps: int = 0, device_stack_budget_bytes: int = 0,
-              recompute: int = 0, cell: int = 0) -> ll_desc:
+              recompute: int = 0, cell: int = 0, ponder_max: int = 0) -> ll_desc:
     return ll_desc(T_max, B, I, H, layers,
                    LL_BF16 if dtype == "bf16" else LL_F32 if dtype == "f32" else int(dtype),
-                   spill, spill_chunk_steps, device_stack_budget_bytes, recompute, cell, 0)
+                   spill, spill_chunk_steps, device_stack_budget_bytes, recompute, cell, ponder_max, 0)
 
 
 def lstm_loop_fwd_noalloc(desc: ll_desc, x, seq_len, W: Sequence, bias: Sequence, h0, c0, y, hT,

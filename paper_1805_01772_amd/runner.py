@@ -12,16 +12,17 @@ from typing import Optional
 import numpy as np
 import torch
 
-from .lstmloop import LL_CELL_GRU, LL_CELL_LSTM, LL_CELL_LSTM_SKIP, LL_CELL_RNN, Plan
+from .lstmloop import LL_CELL_GRU, LL_CELL_LSTM, LL_CELL_LSTM_ACT, LL_CELL_LSTM_SKIP, LL_CELL_RNN, Plan
 
 
 class DeviceCase:
     def __init__(self, inputs: dict, H: int, I: int, layers: int, dtype: str,
-                 device: str = "cuda:0", cell: str = "lstm"):
+                 device: str = "cuda:0", cell: str = "lstm", ponder_max: int = 0):
         dev = torch.device(device)
         self.dev = dev
         self.dtype = dtype
         self.cell = cell
+        self.ponder_max = ponder_max
         op = torch.bfloat16 if dtype == "bf16" else torch.float32
         f32 = torch.float32
         T, B, _ = inputs["x"].shape
@@ -53,8 +54,9 @@ class DeviceCase:
 
     def plan(self, **kw) -> Plan:
         cell = {"lstm": LL_CELL_LSTM, "rnn": LL_CELL_RNN, "gru": LL_CELL_GRU,
-                "skip": LL_CELL_LSTM_SKIP}[self.cell]
-        return Plan(self.T, self.B, self.I, self.H, layers=self.L, dtype=self.dtype, cell=cell, **kw)
+                "skip": LL_CELL_LSTM_SKIP, "act": LL_CELL_LSTM_ACT}[self.cell]
+        return Plan(self.T, self.B, self.I, self.H, layers=self.L, dtype=self.dtype, cell=cell,
+                    ponder_max=self.ponder_max if self.cell == "act" else 0, **kw)
 
     def fwd(self, plan: Plan, save: bool = True, use_h0: bool = True) -> None:
         plan.fwd(self.x, self.seq_len, self.W, self.bias,

@@ -38,7 +38,9 @@ class Workload:
     spill: bool = False
     seed: int = 0
     cell: str = "lstm"                # "lstm" (4 gate blocks), "gru" (3), "rnn" (Elman, 1),
-                                      # "skip" (the LSTM body with a cond)
+                                      # "skip" (the LSTM body with a cond), "act" (the
+                                      # LSTM body with a nested loop)
+    ponder_max: int = 4               # "act": at most this many ponder steps per step
     extra: dict = field(default_factory=dict)
 
     def with_(self, **kw) -> "Workload":
@@ -46,7 +48,7 @@ class Workload:
 
     @property
     def gates(self) -> int:
-        return {"lstm": 4, "gru": 3, "rnn": 1, "skip": 4}[self.cell]
+        return {"lstm": 4, "gru": 3, "rnn": 1, "skip": 4, "act": 4}[self.cell]
 
     def bias_len(self, layer: int = 0) -> int:
         """Bias entries of a layer: G*H, the GRU's extra b_hn block, the cond
@@ -55,6 +57,8 @@ class Workload:
             return 4 * self.H
         if self.cell == "skip":
             return 4 * self.H + (self.I if layer == 0 else self.H) + self.H + 1
+        if self.cell == "act":
+            return 5 * self.H + 1
         return self.gates * self.H
 
 
@@ -89,8 +93,14 @@ SKIP_VAR_H1024 = Workload("skip_b128_h1024_tmax200_varlen_bf16", B=128, I=1024, 
                           T_max=200, dtype="bf16", len_lo=20, len_hi=200, cell="skip",
                           seed=1008)
 
+# ... and with the LSTM body holding a nested loop (ACT's halting rule: each
+# input pondered 1 to 4 times; the halting weights are drawn with the bias).
+ACT_VAR_H1024 = Workload("act_b128_h1024_tmax200_varlen_bf16", B=128, I=1024, H=1024,
+                         T_max=200, dtype="bf16", len_lo=20, len_hi=200, cell="act",
+                         ponder_max=4, seed=1009)
+
 ALL = (TINY, FIXED_H512, VAR_H1024, LONG_SPILL, TWO_LAYER, RNN_VAR_H1024, GRU_VAR_H1024,
-       SKIP_VAR_H1024)
+       SKIP_VAR_H1024, ACT_VAR_H1024)
 BY_NAME = {w.name: w for w in ALL}
 
 

@@ -14,7 +14,7 @@ def say(msg):
     sys.stdout.flush()
 
 
-def oracle_reference(inp, layers, dtype, cell="lstm"):
+def oracle_reference(inp, layers, dtype, cell="lstm", ponder_max=4):
     """fp64 oracle (bf16-emulating for bf16 workloads) of the full fwd + bwd.
     For the RNN and GRU cells, cT and dc0 are zeros (the library writes zeros
     there)."""
@@ -37,6 +37,14 @@ def oracle_reference(inp, layers, dtype, cell="lstm"):
     h0 = inp["h0"].astype(np.float64)
     c0 = inp["c0"].astype(np.float64)
     dy = None if inp["dy"] is None else inp["dy"].astype(np.float64)
+    if cell == "act":
+        y, hT, cT, tapes = oracle.stacked_act_forward(x, inp["seq_len"], Ws, bs, h0, c0, precision,
+                                                      ponder_max)
+        g = oracle.stacked_act_backward(tapes, dy, inp["dhT"].astype(np.float64),
+                                        inp["dcT"].astype(np.float64))
+        return dict(y=y, hT=hT, cT=cT, dx=g["dx"], dW=g["dW"], dbias=g["dbias"], dh0=g["dh0"],
+                    dc0=g["dc0"], T_eff=tapes[0]["T_eff"], trips=[t["trips"] for t in tapes],
+                    min_margin=min(t["min_margin"] for t in tapes))
     fwd, bwd = ((oracle.stacked_skip_forward, oracle.stacked_skip_backward) if cell == "skip"
                 else (oracle.stacked_forward, oracle.stacked_backward))
     y, hT, cT, tapes = fwd(x, inp["seq_len"], Ws, bs, h0, c0, precision)

@@ -55,7 +55,6 @@ def test_version_string():
     (dict(B=0), ll.LL_EINVAL),
     (dict(layers=3), ll.LL_EINVAL),
     (dict(dtype=7), ll.LL_EINVAL),
-    (dict(cell=4), ll.LL_EINVAL),
     (dict(cell=3, spill=1), ll.LL_EUNSUPPORTED),
     (dict(cell=3, recompute=1), ll.LL_EUNSUPPORTED),
     (dict(cell=-1), ll.LL_EINVAL),
@@ -69,12 +68,19 @@ def test_version_string():
     (dict(I=6), ll.LL_EUNSUPPORTED),
     (dict(B=5000), ll.LL_EUNSUPPORTED),
     (dict(reserved=1), ll.LL_EINVAL),
+    (dict(cell=4, ponder_max=0), ll.LL_EINVAL),
+    (dict(cell=4, ponder_max=9), ll.LL_EINVAL),
+    (dict(cell=4, ponder_max=3, layers=2), ll.LL_EUNSUPPORTED),
+    (dict(cell=4, ponder_max=3, spill=1), ll.LL_EUNSUPPORTED),
+    (dict(cell=0, ponder_max=2), ll.LL_EINVAL),
+    (dict(cell=5), ll.LL_EINVAL),
     (dict(reserved=-7), ll.LL_EINVAL),
 ])
 def test_descriptor_validation(fields, status):
     lib = _lib()
     base = dict(T_max=8, B=4, I=32, H=32, layers=1, dtype=ll.LL_BF16, spill=0,
-                spill_chunk_steps=0, device_stack_budget_bytes=0, recompute=0, cell=0, reserved=0)
+                spill_chunk_steps=0, device_stack_budget_bytes=0, recompute=0, cell=0, ponder_max=0,
+                reserved=0)
     base.update(fields)
     d = ll.ll_desc(**base)
     h = ctypes.c_void_p(123)

@@ -960,3 +960,140 @@ def test_dw_operands_past_two_gib_take_the_transposes():
     errs, bad = compare(res, oracle_reference(inp, 1, w.dtype), TOL[w.dtype])
     say(f"    errors {errs}")
     assert not bad, bad
+
+
+# The LSTM body with a nested loop (ACT's halting rule).  The inner trip
+# count is an integer decided by floating point on both sides (float32 sums
+# in different orders, the kernel's sigmoid against the oracle's, and the
+# bf16 runs' trajectories differ within the tolerance), so every case uses a
+# seed whose decisions all sit at least MARGIN from the threshold in the
+# oracle, with several trip counts occurring.  (case, margin, post-processing
+# of the drawn inputs: halting bias and weight scale, or None)
+ACT_CASES = [
+    (W("act_f32_b20_i24_h64_t12_m3", B=20, I=24, H=64, T_max=12, dtype="f32", len_lo=0, len_hi=12,
+       w_scale=0.3, random_state=True, cell="act", ponder_max=3, seed=200), 1e-4, None),
+    (W("act_bf16_b40_i32_h128_t10_m4", B=40, I=32, H=128, T_max=10, dtype="bf16", len_lo=1, len_hi=10,
+       w_scale=0.2, random_state=True, cell="act", ponder_max=4, seed=220), 2e-3, None),
+    (W("act_bf16_b130_i64_h256_t8_m3", B=130, I=64, H=256, T_max=8, dtype="bf16", len_lo=0, len_hi=8,
+       w_scale=0.15, random_state=True, cell="act", ponder_max=3, seed=272), 2e-3, None),
+    (W("act_f32_b33_i20_h512_t6_m2", B=33, I=20, H=512, T_max=6, dtype="f32", len_lo=0, len_hi=6,
+       random_state=True, cell="act", ponder_max=2, seed=209), 1e-4, (4.6, 8.0)),
+    (W("act_bf16_b9_i8_h1024_t6_m4", B=9, I=8, H=1024, T_max=6, dtype="bf16", len_lo=0, len_hi=6,
+       random_state=True, cell="act", ponder_max=4, seed=200), 2e-3, None),
+    (W("act_f32_b5_i8_h32_t9_m1", B=5, I=8, H=32, T_max=9, dtype="f32", len_lo=0, len_hi=9,
+       w_scale=0.3, random_state=True, cell="act", ponder_max=1, seed=200), 1e-4, None),
+]
+
+
+def _act_inputs(w, post):
+    inp = wl.generate(w)
+    if post is not None:
+        bp, wscale = post
+        inp["bias"][0][-1] = bp
+        inp["bias"][0][4 * w.H:5 * w.H] *= wscale
+    return inp
+
+
+def _act_run(w, inp):
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell="act", ponder_max=w.ponder_max)
+    plan = dc.plan()
+    geom = plan.geometry()
+    assert geom["xcd_local"], geom
+    dc.fwd(plan)
+    dc.bwd(plan)
+    err = plan.status_sync()
+    res = dc.results()
+    plan.close()
+    return res, err
+
+
+@pytest.mark.parametrize("w,margin,post", ACT_CASES, ids=[c[0].name for c in ACT_CASES])
+def test_act_cell_parity(w, margin, post):
+    """The loop engine with a nested loop in the body: inner trip counts
+    decided on the device, pushed with every ponder step, popped by the
+    nested gradient loop; every output within the tolerance of the oracle,
+    dbias zero in the halting part."""
+    say(f"[act] {w.name}")
+    inp = _act_inputs(w, post)
+    ref = oracle_reference(inp, w.layers, w.dtype, cell="act", ponder_max=w.ponder_max)
+    assert ref["min_margin"] > margin, "ill-conditioned case: a decision sits at the threshold"
+    valid = np.arange(w.T_max)[:, None] < inp["seq_len"][None, :]
+    trips = ref["trips"][0][valid]
+    assert trips.min() >= 1 and trips.max() <= w.ponder_max
+    if w.ponder_max > 1:
+        assert len(np.unique(trips)) >= 2, "one inner trip count only"
+    res, err = _act_run(w, inp)
+    assert err == 0
+    assert res["T_eff"] == ref["T_eff"] == int(inp["seq_len"].max())
+    errs, bad = compare(res, ref, TOL[w.dtype])
+    say(f"    trips {np.unique(trips, return_counts=True)} errors {errs}")
+    assert not bad, bad
+    assert not res["dbias"][0][4 * w.H:].any() and res["dbias"][0].shape[0] == 5 * w.H + 1
+
+
+def test_act_cell_zero_trip():
+    """Every length 0: no iteration of either loop; inits returned, state
+    gradients passed through, dW, db, dx zero (bitwise)."""
+    w = W("act_zero_trip", B=20, I=16, H=64, T_max=5, dtype="bf16", len_lo=0, len_hi=0,
+          random_state=True, cell="act", ponder_max=3, seed=71)
+    inp = wl.generate(w)
+    res, err = _act_run(w, inp)
+    assert err == 0 and res["T_eff"] == 0
+    np.testing.assert_array_equal(res["hT"], inp["h0"])
+    np.testing.assert_array_equal(res["cT"], inp["c0"])
+    np.testing.assert_array_equal(res["dh0"], inp["dhT"])
+    np.testing.assert_array_equal(res["dc0"], inp["dcT"])
+    for k in ("y", "dx"):
+        assert not res[k].any(), k
+    assert not any(d.any() for d in res["dW"]) and not any(b.any() for b in res["dbias"])
+
+
+def test_act_cell_inference_matches_training_forward():
+    """The nested-loop forward without a saved stack (inference) gives the
+    same outputs bitwise as the forward that pushes it."""
+    w, margin, post = ACT_CASES[1]
+    inp = _act_inputs(w, post)
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell="act", ponder_max=w.ponder_max)
+    plan = dc.plan()
+    dc.fwd(plan, save=True)
+    a = dc.results()
+    dc.fwd(plan, save=False)
+    b = dc.results()
+    assert plan.status_sync() == 0
+    plan.close()
+    for k in ("y", "hT", "cT"):
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+def test_act_full_size_rows_with_clear_decisions():
+    """The nested-loop workload at full size (B = 128, I = H = 1024,
+    T_max = 200, bf16, at most 4 ponder steps).  Its ~4e4 halting decisions
+    include many within the two sides' differing float32 sums and bf16
+    trajectories of the threshold, and a row that decides differently follows
+    another trajectory, so the comparison is per row (rows do not interact):
+    every row whose decisions all sit at least 1e-3 from the threshold in the
+    oracle must match it within the tolerance in y, dx, hT, cT, dh0 and dc0;
+    at least 10 rows must qualify."""
+    w = wl.ACT_VAR_H1024
+    say(f"[full] {w.name}")
+    inp = wl.generate(w)
+    res, err = _act_run(w, inp)
+    assert err == 0
+    say("    oracle running")
+    import oracle as orc
+    x = inp["x"].astype(np.float64)
+    y, hT, cT, tape = orc.act_forward(x, inp["seq_len"], inp["W"][0].astype(np.float64),
+                                      inp["bias"][0].astype(np.float64), inp["h0"][0].astype(np.float64),
+                                      inp["c0"][0].astype(np.float64), "bf16", w.ponder_max)
+    g = orc.act_backward(tape, inp["dy"].astype(np.float64), inp["dhT"][0].astype(np.float64),
+                         inp["dcT"][0].astype(np.float64))
+    good = tape["row_margin"] >= 1e-3
+    say(f"    rows with clear decisions: {int(good.sum())} of {w.B}")
+    assert good.sum() >= 10
+    tol = TOL[w.dtype]
+    ref = dict(y=y, dx=g["dx"], hT=hT[None], cT=cT[None], dh0=g["dh0"][None], dc0=g["dc0"][None])
+    for key in ("y", "dx", "hT", "cT", "dh0", "dc0"):
+        e = rel_err(res[key][:, good], ref[key][:, good])
+        say(f"    {key}: {e:.3e}")
+        assert e <= tol, (key, e)
+
