@@ -319,7 +319,7 @@ __global__ __launch_bounds__(CNT, 1) void cfwd_kernel(CLoopArgs a) {
       if (m + 1 < nt) tile(m + 1, a1, a0);
       if (m + 2 < nt) tile(m + 2, a2, a1);
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_all_vm();
     __syncthreads();
     if (tid < nt)
       __hip_atomic_store(a.pflags + (x * MRT + tid) * 32 + rank, (unsigned)(t + 2), __ATOMIC_RELAXED,
@@ -365,7 +365,7 @@ __global__ __launch_bounds__(CNT, 1) void cfwd_kernel(CLoopArgs a) {
         st_dev(rring, ring_off<T>(sl, MRT, KS, m, crow, jc), Op<T>::from_f32(hs[p]));
       }
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_all_vm();
     __syncthreads();
     if (tid < nt)
       __hip_atomic_store(a.xflags + tid * 256 + x * 32 + rank, (unsigned)(t + 2), __ATOMIC_RELAXED,
@@ -541,7 +541,7 @@ __global__ __launch_bounds__(CNT, 1) void cbwd_kernel(CLoopArgs a) {
           st_dev(rring, ring_off<T>(sl, MRT, KS, m, crow, g * H + jc), Op<T>::from_f32(dz[p][g]));
       }
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_all_vm();
     __syncthreads();
     if (tid < nt)
       __hip_atomic_store(a.xflags + tid * 256 + x * 32 + rank, (unsigned)(T_eff - t), __ATOMIC_RELAXED,
@@ -602,7 +602,7 @@ __global__ __launch_bounds__(CNT, 1) void cbwd_kernel(CLoopArgs a) {
       if (m + 1 < nt) tile(m + 1, a1, a0);
       if (m + 2 < nt) tile(m + 2, a2, a1);
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_all_vm();
     __syncthreads();
     if (tid < nt)
       __hip_atomic_store(a.pflags + (x * MRT + tid) * 32 + rank, (unsigned)(T_eff - t), __ATOMIC_RELAXED,

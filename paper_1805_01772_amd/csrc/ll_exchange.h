@@ -126,6 +126,18 @@ __device__ __forceinline__ void wait_lgkm() {
   asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Every vector memory operation of the wave done (vmcnt(0)), through the
+// builtin: the compiler's own wait tracking then knows that every earlier
+// load has landed.  (An inline-asm wait is opaque to it: after one, it waited
+// again for loads issued before it, at a point where that also meant waiting
+// for every store issued since.)  The empty asm statements keep the
+// compiler from moving memory operations across the wait.
+__device__ __forceinline__ void wait_all_vm() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xF70);   // vmcnt(0); expcnt, lgkmcnt: no wait
+  asm volatile("" ::: "memory");
+}
+
 // Group of this work-group: (XCD, rank within the XCD).
 __device__ __forceinline__ void join_group(unsigned* rank_ctr, int* s_info) {
   if (threadIdx.x == 0) {
@@ -145,7 +157,7 @@ __device__ __forceinline__ void join_group(unsigned* rank_ctr, int* s_info) {
 // (forward 0.58 -> 0.75 ms, gradient 0.75 -> 1.47 ms at the H = 1024
 // workload); consumers on other XCDs use publish_dev.
 __device__ __forceinline__ void publish(unsigned* flag, unsigned value) {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  wait_all_vm();
   __syncthreads();
   if (threadIdx.x == 0) __hip_atomic_store(flag, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
@@ -153,7 +165,7 @@ __device__ __forceinline__ void publish(unsigned* flag, unsigned value) {
 // Publish to every XCD: as publish, with a device-scope flag store (the
 // data must have been stored with st_dev).
 __device__ __forceinline__ void publish_dev(unsigned* flag, unsigned value) {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  wait_all_vm();
   __syncthreads();
   if (threadIdx.x == 0) __hip_atomic_store(flag, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
