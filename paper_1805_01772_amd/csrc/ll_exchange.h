@@ -45,87 +45,6 @@ __device__ __forceinline__ float ld_f32(__amdgpu_buffer_rsrc_t r, unsigned off) 
 // loads from it and gets zeros, so no load needs a per-lane branch.
 constexpr unsigned kOOB = 0x80000000u;
 
-// ----- loads straight into LDS (buffer loads with the LDS destination).
-// Lane l of a 16-byte load writes base + 16 l; base must be the same on every
-// lane of the wave.  The compiler cannot tell which LDS bytes such a load
-// writes, so the reads of that data go through ds_rd (not seen by the
-// compiler as LDS accesses) and the caller waits for both counters itself:
-// wait_vm until the loads landed, wait_lgkm until the reads returned, then
-// touch() the results so nothing uses them earlier.
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((ext_vector_type(4))) unsigned lds_u32x4;
-__device__ __forceinline__ void ld_chunk_to_lds(__amdgpu_buffer_rsrc_t r, unsigned off, void* lds_base) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_base, 16, off, 0, 0, kCpolSc1);
-}
-__device__ __forceinline__ unsigned lds_addr(const void* p) {
-  return (unsigned)(unsigned long)(const __attribute__((address_space(3))) void*)p;
-}
-__device__ __forceinline__ uint4 ds_rd(unsigned addr) {
-  lds_u32x4 v;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
-  return __builtin_bit_cast(uint4, v);
-}
-__device__ __forceinline__ void touch(uint4& v) {
-  lds_u32x4 w = __builtin_bit_cast(lds_u32x4, v);
-  asm volatile("" : "+v"(w));
-  v = __builtin_bit_cast(uint4, w);
-}
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-// wait_vm with a count known only after unrolling (folds to one wait);
-// counts above 39 wait for everything.
-__device__ __forceinline__ void wait_vm_n(int n) {
-  switch (n) {
-    case 0: wait_vm<0>(); break;
-    case 1: wait_vm<1>(); break;
-    case 2: wait_vm<2>(); break;
-    case 3: wait_vm<3>(); break;
-    case 4: wait_vm<4>(); break;
-    case 5: wait_vm<5>(); break;
-    case 6: wait_vm<6>(); break;
-    case 7: wait_vm<7>(); break;
-    case 8: wait_vm<8>(); break;
-    case 9: wait_vm<9>(); break;
-    case 10: wait_vm<10>(); break;
-    case 11: wait_vm<11>(); break;
-    case 12: wait_vm<12>(); break;
-    case 13: wait_vm<13>(); break;
-    case 14: wait_vm<14>(); break;
-    case 15: wait_vm<15>(); break;
-    case 16: wait_vm<16>(); break;
-    case 17: wait_vm<17>(); break;
-    case 18: wait_vm<18>(); break;
-    case 19: wait_vm<19>(); break;
-    case 20: wait_vm<20>(); break;
-    case 21: wait_vm<21>(); break;
-    case 22: wait_vm<22>(); break;
-    case 23: wait_vm<23>(); break;
-    case 24: wait_vm<24>(); break;
-    case 25: wait_vm<25>(); break;
-    case 26: wait_vm<26>(); break;
-    case 27: wait_vm<27>(); break;
-    case 28: wait_vm<28>(); break;
-    case 29: wait_vm<29>(); break;
-    case 30: wait_vm<30>(); break;
-    case 31: wait_vm<31>(); break;
-    case 32: wait_vm<32>(); break;
-    case 33: wait_vm<33>(); break;
-    case 34: wait_vm<34>(); break;
-    case 35: wait_vm<35>(); break;
-    case 36: wait_vm<36>(); break;
-    case 37: wait_vm<37>(); break;
-    case 38: wait_vm<38>(); break;
-    case 39: wait_vm<39>(); break;
-    default: wait_vm<0>(); break;
-  }
-}
-template <int N>
-__device__ __forceinline__ void wait_lgkm() {
-  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
-}
-
 // Every vector memory operation of the wave done (vmcnt(0)), through the
 // builtin: the compiler's own wait tracking then knows that every earlier
 // load has landed.  (An inline-asm wait is opaque to it: after one, it waited

@@ -64,15 +64,13 @@ size_t xfwd_lds(int KSW, int KSR, int NCT, int mrt_max, int skip_floats = 0) {
 // floats of the cond body's LDS: XNW x 16 partial sums
 constexpr int xfwd_skip_floats() { return XNW * 16; }
 // LDS of the gradient kernel: weight k-steps not in registers, partial
-// products (reused for the db rows at the end), metadata window, perm rows,
-// and with DMA the dz tile (KSW k-steps of 1 KB per wave).
+// products (reused for the db rows at the end), metadata window, perm rows.
 __host__ __device__ constexpr int xbwd_tail_chunks(int NCT, int mrt_max) {
   return (xbwd_red_floats(NCT) * 4 + 2 * (WIN + 1) * 4 + mrt_max * 16 * 4 + 15) / 16;
 }
-size_t xbwd_lds(int KSW, int KSR, int NCT, int mrt_max, bool dma = false) {
+size_t xbwd_lds(int KSW, int KSR, int NCT, int mrt_max) {
   const int KSL = KSW > KSR ? KSW - KSR : 0;
-  return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)xbwd_tail_chunks(NCT, mrt_max) * 16 +
-         (dma ? (size_t)XNW * KSW * 1024 : 0);
+  return (size_t)XNW * KSL * NCT * 64 * 16 + (size_t)xbwd_tail_chunks(NCT, mrt_max) * 16;
 }
 
 __device__ __forceinline__ void load_window(const XLoopArgs& a, int* win, int lo) {
@@ -579,8 +577,8 @@ __global__ __launch_bounds__(XNT, 1) void xfwd2_kernel(XLoopArgs a0, XLoopArgs a
 // gradient or the identity); dy_t enters at the last ponder step; c of the
 // step before ponder step 0 is the previous step's last ponder state.  dz of
 // ponder step k goes to dz slot k (slots the tile did not run get zeros).
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE, bool DMA = false, int G = 4,
-          bool SKIP = false, bool ACT = false>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int ROLE, int G = 4, bool SKIP = false,
+          bool ACT = false>
 __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank, uint4* lds) {
   constexpr int KPC = Op<T>::kPerChunk;
   constexpr int HJ = 16 * NCT;                 // units per work-group
@@ -636,8 +634,6 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   float* red = reinterpret_cast<float*>(lds + XNW * KSL * NCO * 64);   // [XNW][4][IS]
   int* win = reinterpret_cast<int*>(red + xbwd_red_floats(NCO));       // [2][WIN+1]
   int* sperm = win + 2 * (WIN + 1);                                   // [MRT][16]
-  // DMA: this wave's KSW k-steps of the dz tile, loaded straight into LDS
-  uint4* dzl = lds + XNW * KSL * NCO * 64 + xbwd_tail_chunks(NCO, MRT_MAX) + wave * KSW * 64;
 
   // (row, unit) of this thread: 16 lanes take 16 consecutive units of one
   // row, a wave four rows (the four MFMA result elements of a lane group)
@@ -930,34 +926,16 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
       f32x4 acc[NCO];
 #pragma unroll
       for (int ct = 0; ct < NCO; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if constexpr (DMA) {
-        // every k-step of the wave in flight at once (no registers held):
-        // KSW loads into LDS, then the NPOP pops of the next step behind them
-        asm volatile("" ::: "memory");
-#pragma unroll
-        for (int i = 0; i < KSW; ++i)
-          ld_chunk_to_lds(rs, i < nks ? (unsigned)(((ks0 + i) << 10) + lane * 16) : kOOB, dzl + i * 64);
-        asm volatile("" ::: "memory");
-        fetch_next();
-        asm volatile("" ::: "memory");
-      }
-      const unsigned dza = lds_addr(dzl) + lane * 16;
+      // the wave's k-steps of the dz tile straight into registers, KB at a
+      // time (measured faster than loading them all into LDS at once); the
+      // next iteration's pops behind the last batch
 #pragma unroll
       for (int b0 = 0; b0 < KSW; b0 += KB) {
         uint4 av[KB];
-        if constexpr (DMA) {
-          wait_vm_n(NPOP + KSW - (b0 + KB < KSW ? b0 + KB : KSW));   // this batch has landed
 #pragma unroll
-          for (int i = 0; i < KB; ++i) av[i] = b0 + i < KSW ? ds_rd(dza + (b0 + i) * 1024) : zero4();
-          wait_lgkm<0>();
-#pragma unroll
-          for (int i = 0; i < KB; ++i) touch(av[i]);
-        } else {
-#pragma unroll
-          for (int i = 0; i < KB; ++i)
-            av[i] = ld_chunk_l2(rs, b0 + i < nks ? (unsigned)(((ks0 + b0 + i) << 10) + lane * 16) : kOOB);
-          if (b0 + KB >= KSW) fetch_next();   // next iteration's pops
-        }
+        for (int i = 0; i < KB; ++i)
+          av[i] = ld_chunk_l2(rs, b0 + i < nks ? (unsigned)(((ks0 + b0 + i) << 10) + lane * 16) : kOOB);
+        if (b0 + KB >= KSW) fetch_next();
 #pragma unroll
         for (int i = 0; i < KB; ++i) {
           const int ii = b0 + i;
@@ -1030,7 +1008,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   }
 }
 
-template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, bool DMA, int G, bool SKIP, bool ACT = false>
+template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int G, bool SKIP, bool ACT = false>
 __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
   extern __shared__ uint4 lds[];
   __shared__ int s_info[2];
@@ -1044,7 +1022,7 @@ __global__ __launch_bounds__(XNT, 1) void xbwd_kernel(XLoopArgs a) {
     return;
   }
   if (rank >= a.P) return;
-  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, DMA, G, SKIP, ACT>(a, grp, rank, lds);
+  xbwd_body<T, NCT, KSW, KSR, MRT_MAX, 0, G, SKIP, ACT>(a, grp, rank, lds);
 }
 
 // Two-layer wavefront, gradient: members 0 .. P-1 of every XCD run the lower
@@ -1150,15 +1128,8 @@ XKernels x_make() {
   XKernels k{};
   k.fwd = reinterpret_cast<const void*>(&xfwd_kernel<T, NF, HC, RF, MRT, G, SKIP, ACT>);
   k.lds_fwd = xfwd_lds(HC, RF, NF, MRT, (SKIP || ACT) ? xfwd_skip_floats() : 0);
-  // the gradient loop loads its dz k-steps straight into LDS when they fit
-  const size_t dma_lds = xbwd_lds(G * HC, RB, NB, MRT, true);
-  if (dma_lds <= 160 * 1024) {
-    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, true, G, SKIP, ACT>);
-    k.lds_bwd = dma_lds;
-  } else {
-    k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, false, G, SKIP, ACT>);
-    k.lds_bwd = xbwd_lds(G * HC, RB, NB, MRT);
-  }
+  k.bwd = reinterpret_cast<const void*>(&xbwd_kernel<T, NB, G * HC, RB, MRT, G, SKIP, ACT>);
+  k.lds_bwd = xbwd_lds(G * HC, RB, NB, MRT);
   return k;
 }
 }  // namespace
