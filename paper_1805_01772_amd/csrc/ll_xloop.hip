@@ -584,7 +584,7 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
   constexpr int HJ = 16 * NCT;                 // units per work-group
   constexpr int NCO = ROLE == 2 ? 2 * NCT : NCT;   // output column tiles
   constexpr int KSL = KSW > KSR ? KSW - KSR : 0;
-  constexpr int KB = KSW < 8 ? KSW : 8;        // k-steps per load batch
+  constexpr int KB = KSW < 4 ? KSW : 4;        // k-steps per load batch
   constexpr int IS = xbwd_is(NCO);
   static_assert(16 * HJ <= XNT, "one thread per (row, unit) of a tile");
   static_assert(HJ == 4 * KPC, "a member's units of one gate are one k-step");
