@@ -1,11 +1,13 @@
 // Small kernels around the loops: trip count and length ordering, operand
 // transposes, zero fill of finished rows, deterministic reductions.
+#include <algorithm>
+
 #include "ll_kernels.h"
 
 namespace ll {
 
 // ---------------------------------------------------------------------------
-// Loop preparation (one work-group of 1024 threads).
+// Loop preparation (one work-group; any size up to 1024 threads).
 //   * range check of seq_len; a bad length sets LL_DEVERR_SEQ_LEN and makes
 //     the loops run zero iterations (every length treated as 0);
 //   * T_eff = max_b seq_len[b]: the loop predicate is t < T_eff, decided here
@@ -19,12 +21,15 @@ namespace ll {
 //   * rowmap[k] = t * B + perm[r] for compact row k = off[t] + r.
 //   * clears the barrier counters and the abort flag of this launch sequence.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void prep_kernel(const int* __restrict__ seq_len, int B,
-                                                    int T_max, int* __restrict__ perm,
-                                                    int* __restrict__ active, int* __restrict__ off,
-                                                    int* __restrict__ rowmap, int* __restrict__ meta,
-                                                    int* __restrict__ trip_out, int t_in_lds, int n_pow2) {
-  extern __shared__ int smem[];
+__device__ void prep_body(const PrepArgs& a, int* smem) {
+  const int* __restrict__ seq_len = a.seq_len;
+  const int B = a.B, T_max = a.T_max, t_in_lds = a.t_in_lds, n_pow2 = a.n_pow2;
+  int* __restrict__ perm = a.perm;
+  int* __restrict__ active = a.active;
+  int* __restrict__ off = a.off;
+  int* __restrict__ rowmap = a.rowmap;
+  int* __restrict__ meta = a.meta;
+  int* __restrict__ trip_out = a.trip_out;
   // sort keys: (T_max - length) << 32 | row, ascending = decreasing length,
   // ties by row index; entries n_pow2 > B pad with the largest key
   unsigned long long* s_key = reinterpret_cast<unsigned long long*>(smem);   // [n_pow2]
@@ -205,19 +210,26 @@ __global__ __launch_bounds__(256) void gather_transpose_kernel(GatherTArgs g) {
 
 // Zero the rows (t, b) of a [T_max, B, C] float array with t >= seq_len[b]
 // (all rows if the lengths failed the range check).  C % 4 == 0.
-__global__ __launch_bounds__(256) void zero_finished_rows_kernel(float* __restrict__ dst, int T_max,
-                                                                 int B, int C,
-                                                                 const int* __restrict__ seq_len,
-                                                                 const int* __restrict__ meta) {
+// (The bodies of the small kernels take their work-group index and count,
+// so that one launch can run several of them side by side.)
+__device__ void zero_finished_rows_body(float* __restrict__ dst, int T_max, int B, int C,
+                                        const int* __restrict__ seq_len, const int* __restrict__ meta,
+                                        int bid, int nb) {
   const int bad = meta[2] & LL_DEVERR_SEQ_LEN_BIT;
   const long rows = (long)T_max * B;
   const int c4 = C >> 2;
-  for (long row = blockIdx.x * 4L + (threadIdx.x >> 6); row < rows; row += gridDim.x * 4L) {
+  for (long row = bid * 4L + (threadIdx.x >> 6); row < rows; row += nb * 4L) {
     const int t = (int)(row / B), b = (int)(row % B);
     if (!bad && t < seq_len[b]) continue;
     float4* p = reinterpret_cast<float4*>(dst + row * C);
     for (int i = threadIdx.x & 63; i < c4; i += 64) p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
+}
+__global__ __launch_bounds__(256) void zero_finished_rows_kernel(float* __restrict__ dst, int T_max,
+                                                                 int B, int C,
+                                                                 const int* __restrict__ seq_len,
+                                                                 const int* __restrict__ meta) {
+  zero_finished_rows_body(dst, T_max, B, C, seq_len, meta, blockIdx.x, gridDim.x);
 }
 
 // Row maps of the gate recomputation (one thread per padded row (t, r)).
@@ -236,37 +248,50 @@ __global__ __launch_bounds__(256) void rc_maps_kernel(const int* __restrict__ ac
   }
 }
 
-__global__ __launch_bounds__(256) void prev_rows_kernel(const int* __restrict__ active,
-                                                        const int* __restrict__ off, int B, int T_max,
-                                                        long cap, int* __restrict__ prev) {
+__device__ void prev_rows_body(const int* __restrict__ active, const int* __restrict__ off, int B,
+                               int T_max, long cap, int* __restrict__ prev, int bid, int nb) {
   const long n = (long)T_max * B;
-  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+  for (long i = bid * 256L + threadIdx.x; i < n; i += nb * 256L) {
     const int t = (int)(i / B), r = (int)(i % B);
     if (r < active[t]) prev[off[t] + r] = t > 0 ? off[t - 1] + r : (int)(cap + r);
   }
 }
+__global__ __launch_bounds__(256) void prev_rows_kernel(const int* __restrict__ active,
+                                                        const int* __restrict__ off, int B, int T_max,
+                                                        long cap, int* __restrict__ prev) {
+  prev_rows_body(active, off, B, T_max, cap, prev, blockIdx.x, gridDim.x);
+}
 
 template <typename T>
-__global__ __launch_bounds__(256) void h0_rows_kernel(const float* __restrict__ h0,
-                                                      const int* __restrict__ perm, int B, int H,
-                                                      T* __restrict__ dst) {
+__device__ void h0_rows_body(const float* __restrict__ h0, const int* __restrict__ perm, int B, int H,
+                             T* __restrict__ dst, int bid, int nb) {
   const long n = (long)B * H;
-  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+  for (long i = bid * 256L + threadIdx.x; i < n; i += nb * 256L) {
     const int r = (int)(i / H), j = (int)(i % H);
     dst[i] = Op<T>::from_f32(h0 ? h0[(long)perm[r] * H + j] : 0.f);
   }
 }
+template <typename T>
+__global__ __launch_bounds__(256) void h0_rows_kernel(const float* __restrict__ h0,
+                                                      const int* __restrict__ perm, int B, int H,
+                                                      T* __restrict__ dst) {
+  h0_rows_body<T>(h0, perm, B, H, dst, blockIdx.x, gridDim.x);
+}
 
 // out[i] = sum_{s < S} ws[s * stride + i], fixed order.
-__global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict__ ws, int S,
-                                                         long stride, long n, long cols, long ldo,
-                                                         float* __restrict__ out) {
-  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+__device__ void sum_slices_body(const float* __restrict__ ws, int S, long stride, long n, long cols,
+                                long ldo, float* __restrict__ out, int bid, int nb) {
+  for (long i = bid * 256L + threadIdx.x; i < n; i += nb * 256L) {
     float acc = 0.0f;
     for (int s = 0; s < S; ++s) acc += ws[s * stride + i];
     const long r = i / cols;
     out[r * ldo + (i - r * cols)] = acc;
   }
+}
+__global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict__ ws, int S,
+                                                         long stride, long n, long cols, long ldo,
+                                                         float* __restrict__ out) {
+  sum_slices_body(ws, S, stride, n, cols, ldo, out, blockIdx.x, gridDim.x);
 }
 
 // out[r] = sum_k A[row(r)][k] * op(w[k]) for the compact rows r < meta[1]
@@ -296,10 +321,10 @@ __global__ __launch_bounds__(256) void row_dot_kernel(const T* __restrict__ A, i
 // One thread per (j, u): four coalesced reads (consecutive threads take
 // consecutive u) and one 4-element store.
 template <typename T>
-__global__ __launch_bounds__(256) void permute_um_kernel(const T* __restrict__ W, int row0, int H,
-                                                         T* __restrict__ dst) {
+__device__ void permute_um_body(const T* __restrict__ W, int row0, int H, T* __restrict__ dst, int bid,
+                                int nb) {
   const long n = (long)H * H;
-  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += gridDim.x * 256L) {
+  for (long i = bid * 256L + threadIdx.x; i < n; i += nb * 256L) {
     const long j = i / H;
     const int u = (int)(i - j * H);
     const T* src = W + (row0 + j) * 4L * H + u;
@@ -308,6 +333,11 @@ __global__ __launch_bounds__(256) void permute_um_kernel(const T* __restrict__ W
     for (int g = 0; g < 4; ++g) q.v[g] = src[(long)g * H];
     *reinterpret_cast<Quad*>(dst + 4 * i) = q;
   }
+}
+template <typename T>
+__global__ __launch_bounds__(256) void permute_um_kernel(const T* __restrict__ W, int row0, int H,
+                                                         T* __restrict__ dst) {
+  permute_um_body<T>(W, row0, H, dst, blockIdx.x, gridDim.x);
 }
 
 // float -> operand type copy (used for bf16(h0) and similar small arrays).
@@ -318,9 +348,111 @@ __global__ __launch_bounds__(256) void convert_kernel(const float* __restrict__ 
     out[i] = Op<T>::from_f32(in[i]);
 }
 
+// Tile (r0, c0) of the transpose out[c * ldo + r] = in[r * ldi + c], r < R,
+// c < C, 64 x 64 elements in 16-byte chunks both ways: thread (row, chunk)
+// loads KPC consecutive columns of one input row into LDS (row pitch padded
+// by one chunk), thread (column, chunk) stores KPC consecutive rows of one
+// output row.  R, C, ldi and ldo are multiples of KPC and both arrays
+// 16-byte aligned (the plan checks I and H; W and W^T are 16-byte aligned).
+template <typename T>
+__device__ void transpose_tile(const T* __restrict__ in, int R, int C, int ldi, T* __restrict__ out,
+                               int ldo, int r0, int c0, T (*tile)[64 + Op<T>::kPerChunk]) {
+  constexpr int KPC = Op<T>::kPerChunk;
+  constexpr int CPR = 64 / KPC;
+  for (int idx = threadIdx.x; idx < 64 * CPR; idx += blockDim.x) {
+    const int i = idx / CPR, j = idx - i * CPR;
+    const int r = r0 + i, c = c0 + j * KPC;
+    uint4 v = zero4();
+    if (r < R && c < C) v = *reinterpret_cast<const uint4*>(in + (long)r * ldi + c);
+    T tmp[KPC];
+    __builtin_memcpy(tmp, &v, 16);
+#pragma unroll
+    for (int e = 0; e < KPC; ++e) tile[i][j * KPC + e] = tmp[e];
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 64 * CPR; idx += blockDim.x) {
+    const int cl = idx / CPR, j = idx - cl * CPR;
+    const int c = c0 + cl, r = r0 + j * KPC;
+    if (c < C && r < R) {
+      T tmp[KPC];
+#pragma unroll
+      for (int e = 0; e < KPC; ++e) tmp[e] = tile[j * KPC + e][cl];
+      uint4 v;
+      __builtin_memcpy(&v, tmp, 16);
+      *reinterpret_cast<uint4*>(out + (long)c * ldo + r) = v;
+    }
+  }
+  __syncthreads();   // the tile is free for the next one
+}
+
+// The forward's set-up in one launch: work-group 0 runs prep; the others
+// transpose W of every layer into W^T (row n = gate column n), tile by tile.
+template <typename T>
+__global__ __launch_bounds__(512) void fwd_setup_kernel(FwdSetupArgs a) {
+  extern __shared__ int smem[];
+  if (blockIdx.x == 0) {
+    prep_body(a.prep, smem);
+    return;
+  }
+  __shared__ T tile[64][64 + Op<T>::kPerChunk];
+  const int tiles = a.job[0].tiles + (a.njobs > 1 ? a.job[1].tiles : 0);
+  for (int k = blockIdx.x - 1; k < tiles; k += gridDim.x - 1) {
+    const int j = k < a.job[0].tiles ? 0 : 1;
+    const TransposeJob& q = a.job[j];
+    const int kk = k - (j ? a.job[0].tiles : 0);
+    const int tr = kk / q.tiles_c, tc = kk - tr * q.tiles_c;
+    transpose_tile<T>(static_cast<const T*>(q.in), q.R, q.C, q.ldi, static_cast<T*>(q.out), q.ldo, tr * 64,
+                      tc * 64, tile);
+  }
+}
+
+// Several independent small tasks in one launch, each on its own range of
+// work-groups (a grid-stride loop over its range).
+template <typename T>
+__global__ __launch_bounds__(256) void small_tasks_kernel(SmallTasks ts) {
+  int b = blockIdx.x, i = 0;
+  while (i + 1 < ts.n && b >= ts.t[i].blocks) {
+    b -= ts.t[i].blocks;
+    ++i;
+  }
+  const SmallTask& k = ts.t[i];
+  switch (k.kind) {
+    case kTaskZeroU32: {
+      unsigned* p = static_cast<unsigned*>(k.out);
+      for (long j = b * 256L + threadIdx.x; j < k.l0; j += k.blocks * 256L) p[j] = 0u;
+      break;
+    }
+    case kTaskZeroFinishedRows:
+      zero_finished_rows_body(static_cast<float*>(k.out), k.i0, k.i1, k.i2, static_cast<const int*>(k.a),
+                              static_cast<const int*>(k.b), b, k.blocks);
+      break;
+    case kTaskPermuteUm:
+      permute_um_body<T>(static_cast<const T*>(k.a), k.i0, k.i1, static_cast<T*>(k.out), b, k.blocks);
+      break;
+    case kTaskSumSlices:
+      sum_slices_body(static_cast<const float*>(k.a), k.i0, k.l0, k.l1, k.l2, k.l3, static_cast<float*>(k.out), b,
+                      k.blocks);
+      break;
+    case kTaskPrevRows:
+      prev_rows_body(static_cast<const int*>(k.a), static_cast<const int*>(k.b), k.i0, k.i1, k.l0,
+                     static_cast<int*>(k.out), b, k.blocks);
+      break;
+    case kTaskH0Rows:
+      h0_rows_body<T>(static_cast<const float*>(k.a), static_cast<const int*>(k.b), k.i0, k.i1,
+                      static_cast<T*>(k.out), b, k.blocks);
+      break;
+    default:
+      break;
+  }
+}
+
 // ------------------------------------------------------------ launchers
-hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
-                       int* rowmap, int* meta, int* trip_out, hipStream_t s) {
+template <typename T>
+hipError_t launch_fwd_setup(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
+                            int* rowmap, int* meta, int* trip_out, int nw, const T* const* W, const int* R,
+                            int C, T* const* WT, hipStream_t s) {
+  if (nw < 0 || nw > 2) return hipErrorInvalidValue;
+  FwdSetupArgs a{};
   int n_pow2 = 1;
   while (n_pow2 < B) n_pow2 <<= 1;
   // sort keys (8 bytes per row, B <= 4096: at most 32 KB), and the per-step
@@ -328,8 +460,33 @@ hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* act
   const size_t keys = (size_t)n_pow2 * 8;
   const int t_in_lds = keys + 2 * ((size_t)T_max + 1) * sizeof(int) <= 64 * 1024;
   const size_t smem = keys + (t_in_lds ? 2 * ((size_t)T_max + 1) * sizeof(int) : 0);
-  hipLaunchKernelGGL(prep_kernel, dim3(1), dim3(1024), smem, s, seq_len, B, T_max, perm, active,
-                     off, rowmap, meta, trip_out, t_in_lds, n_pow2);
+  a.prep = PrepArgs{seq_len, B, T_max, perm, active, off, rowmap, meta, trip_out, t_in_lds, n_pow2};
+  a.njobs = nw;
+  long tiles = 0;
+  for (int l = 0; l < nw; ++l) {
+    TransposeJob& q = a.job[l];
+    q.in = W[l];
+    q.out = WT[l];
+    q.R = R[l];
+    q.C = C;
+    q.ldi = C;
+    q.ldo = R[l];
+    q.tiles_c = (C + 63) / 64;
+    q.tiles = ((R[l] + 63) / 64) * q.tiles_c;
+    tiles += q.tiles;
+  }
+  // (four work-groups of 512 per compute unit fit the LDS of small shapes)
+  const long nblk = 1 + std::min(tiles, 1024L);
+  hipLaunchKernelGGL(fwd_setup_kernel<T>, dim3((unsigned)nblk), dim3(512), smem, s, a);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_small_tasks(const SmallTasks& ts, hipStream_t s) {
+  if (ts.n <= 0) return hipSuccess;
+  long nblk = 0;
+  for (int i = 0; i < ts.n; ++i) nblk += ts.t[i].blocks;
+  hipLaunchKernelGGL(small_tasks_kernel<T>, dim3((unsigned)nblk), dim3(256), 0, s, ts);
   return hipGetLastError();
 }
 
@@ -535,6 +692,12 @@ hipError_t launch_convert(const float* in, long n, T* out, hipStream_t s) {
   return hipGetLastError();
 }
 
+template hipError_t launch_fwd_setup<float>(const int*, int, int, int*, int*, int*, int*, int*, int*, int,
+                                             const float* const*, const int*, int, float* const*, hipStream_t);
+template hipError_t launch_fwd_setup<bf16_t>(const int*, int, int, int*, int*, int*, int*, int*, int*, int,
+                                              const bf16_t* const*, const int*, int, bf16_t* const*, hipStream_t);
+template hipError_t launch_small_tasks<float>(const SmallTasks&, hipStream_t);
+template hipError_t launch_small_tasks<bf16_t>(const SmallTasks&, hipStream_t);
 template hipError_t launch_transpose<float>(const float*, int, int, int, float*, int, hipStream_t);
 template hipError_t launch_transpose<bf16_t>(const bf16_t*, int, int, int, bf16_t*, int,
                                              hipStream_t);

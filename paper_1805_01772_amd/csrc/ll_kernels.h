@@ -294,8 +294,149 @@ hipError_t measure_mfma_peak(int n_cu, bool shape32, double* tflops);
 // sigmoid (fn 0) or tanh (fn 1) of n floats, as the loop kernels compute them
 hipError_t eval_activations(const float* in, float* out, long n, int fn, hipStream_t s);
 
-hipError_t launch_prep(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
-                       int* rowmap, int* meta, int* trip_out, hipStream_t s);
+// The forward's set-up in one launch: prep (length order, active rows and
+// compact offsets per step, row map, T_eff into meta[0] and *trip_out, the
+// range check, the cleared barrier counters) on one work-group, beside the
+// transposes W[l] [R[l], C] -> WT[l] [C, R[l]] of nw <= 2 layers.
+struct PrepArgs {
+  const int* seq_len;
+  int B, T_max;
+  int* perm;
+  int* active;
+  int* off;
+  int* rowmap;
+  int* meta;
+  int* trip_out;
+  int t_in_lds, n_pow2;
+};
+struct TransposeJob {
+  const void* in;
+  void* out;
+  int R, C, ldi, ldo, tiles_c, tiles;
+};
+struct FwdSetupArgs {
+  PrepArgs prep;
+  int njobs;
+  TransposeJob job[2];
+};
+template <typename T>
+hipError_t launch_fwd_setup(const int* seq_len, int B, int T_max, int* perm, int* active, int* off,
+                            int* rowmap, int* meta, int* trip_out, int nw, const T* const* W, const int* R,
+                            int C, T* const* WT, hipStream_t s);
+
+// Several independent small kernels in one launch (kernel launches cost a few
+// microseconds each on this GPU, small ones mostly that): each task runs on
+// its own range of work-groups.
+enum SmallTaskKind : int {
+  kTaskZeroU32,            // out[0 .. l0) = 0 (unsigned)
+  kTaskZeroFinishedRows,   // zero rows t >= seq_len[b] of out [i0 = T_max, i1 = B, i2 = C] (a = seq_len, b = meta)
+  kTaskPermuteUm,          // W_h (a, rows i0 ..) in unit-major order into out (i1 = H)
+  kTaskSumSlices,          // out = sum of i0 slices of a (l0 = stride, l1 = n, l2 = cols, l3 = ldo)
+  kTaskPrevRows,           // out[k] = history row of h_{t-1} of compact row k (a = active, b = off, i0 = B, i1 = T_max, l0 = cap)
+  kTaskH0Rows,             // out = h0 rows (a, float) in length order (b = perm, i0 = B, i1 = H), operand type
+};
+struct SmallTask {
+  int kind, blocks;
+  const void* a;
+  const void* b;
+  void* out;
+  long l0, l1, l2, l3;
+  int i0, i1, i2;
+};
+constexpr int kMaxSmallTasks = 6;
+struct SmallTasks {
+  int n;
+  SmallTask t[kMaxSmallTasks];
+};
+template <typename T>
+hipError_t launch_small_tasks(const SmallTasks& ts, hipStream_t s);
+
+template <typename T>
+struct SmallBatch {
+  SmallTasks ts{};
+  static int blocks_for(long n, long per, long cap) {
+    const long b = (n + per - 1) / per;
+    return (int)(b < 1 ? 1 : b > cap ? cap : b);
+  }
+  hipError_t add(SmallTask t) {
+    if (ts.n >= kMaxSmallTasks) return hipErrorInvalidValue;
+    ts.t[ts.n++] = t;
+    return hipSuccess;
+  }
+  hipError_t zero_u32(unsigned* p, long n) {
+    SmallTask t{};
+    t.kind = kTaskZeroU32;
+    t.out = p;
+    t.l0 = n;
+    t.blocks = blocks_for(n, 256, 1024);
+    return add(t);
+  }
+  hipError_t zero_finished_rows(float* dst, int T_max, int B, int C, const int* seq_len, const int* meta) {
+    SmallTask t{};
+    t.kind = kTaskZeroFinishedRows;
+    t.out = dst;
+    t.a = seq_len;
+    t.b = meta;
+    t.i0 = T_max;
+    t.i1 = B;
+    t.i2 = C;
+    t.blocks = blocks_for((long)T_max * B, 4, 4096);
+    return add(t);
+  }
+  hipError_t permute_um(const T* W, int row0, int H, T* dst) {
+    SmallTask t{};
+    t.kind = kTaskPermuteUm;
+    t.a = W;
+    t.out = dst;
+    t.i0 = row0;
+    t.i1 = H;
+    t.blocks = blocks_for((long)H * H, 256, 4096);
+    return add(t);
+  }
+  hipError_t sum_slices(const float* ws, int S, long stride, long rows, long cols, float* out, long ldo) {
+    if (cols < 1 || ldo < cols) return hipErrorInvalidValue;
+    SmallTask t{};
+    t.kind = kTaskSumSlices;
+    t.a = ws;
+    t.out = out;
+    t.i0 = S;
+    t.l0 = stride;
+    t.l1 = rows * cols;
+    t.l2 = cols;
+    t.l3 = ldo;
+    t.blocks = blocks_for(rows * cols, 256, 4096);
+    return add(t);
+  }
+  hipError_t prev_rows(const int* active, const int* off, int B, int T_max, long cap, int* prev) {
+    SmallTask t{};
+    t.kind = kTaskPrevRows;
+    t.a = active;
+    t.b = off;
+    t.out = prev;
+    t.i0 = B;
+    t.i1 = T_max;
+    t.l0 = cap;
+    t.blocks = blocks_for((long)T_max * B, 256, 4096);
+    return add(t);
+  }
+  hipError_t h0_rows(const float* h0, const int* perm, int B, int H, T* dst) {
+    SmallTask t{};
+    t.kind = kTaskH0Rows;
+    t.a = h0;
+    t.b = perm;
+    t.out = dst;
+    t.i0 = B;
+    t.i1 = H;
+    t.blocks = blocks_for((long)B * H, 256, 4096);
+    return add(t);
+  }
+  // one launch of every task added since the last one (none: nothing)
+  hipError_t launch(hipStream_t s) {
+    const hipError_t e = launch_small_tasks<T>(ts, s);
+    ts.n = 0;
+    return e;
+  }
+};
 template <typename T>
 hipError_t launch_transpose(const T* in, int R, int C, int ldi, T* out, int ldo, hipStream_t s);
 template <typename T>

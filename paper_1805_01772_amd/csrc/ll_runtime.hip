@@ -64,6 +64,11 @@ class DeviceGuard {
 
 long round_up(long v, long m) { return (v + m - 1) / m * m; }
 
+// Events that only order work on this device (streams of one device, the
+// host waiting for completion): no system-scope fences (measured: each such
+// fence left the GPU idle for several microseconds).
+constexpr unsigned kOrderEventFlags = hipEventDisableTiming | hipEventDisableSystemFence;
+
 // Loop launches of every plan on one device form one chain: each waits for
 // the previous one (whatever plan or stream enqueued it) to complete.  The
 // loops need all compute units co-resident, so two of them must never run
@@ -73,6 +78,7 @@ struct LoopChain {
   std::mutex mu;
   hipEvent_t last = nullptr;
   bool recorded = false;
+  hipStream_t last_stream = nullptr;   // the stream `last` was recorded on
 };
 LoopChain g_loop_chain[64];
 
@@ -84,20 +90,23 @@ hipError_t chained_loop_launch(int device, hipStream_t s, Launch&& launch) {
   LoopChain& c = g_loop_chain[device];
   std::lock_guard<std::mutex> lock(c.mu);
   if (!c.last) {
-    hipError_t e = hipEventCreateWithFlags(&c.last, hipEventDisableTiming);
+    hipError_t e = hipEventCreateWithFlags(&c.last, kOrderEventFlags);
     if (e != hipSuccess) {
       c.last = nullptr;
       return e;
     }
   }
-  if (c.recorded) {
+  if (c.recorded && c.last_stream != s) {   // (on the same stream, stream order suffices)
     hipError_t e = hipStreamWaitEvent(s, c.last, 0);
     if (e != hipSuccess) return e;
   }
   hipError_t e = launch();
   if (e != hipSuccess) return e;
   e = hipEventRecord(c.last, s);
-  if (e == hipSuccess) c.recorded = true;
+  if (e == hipSuccess) {
+    c.recorded = true;
+    c.last_stream = s;
+  }
   return e;
 }
 
@@ -179,7 +188,6 @@ struct ll_plan {
   // the gradient loop (forked from and joined back into the call's stream)
   hipStream_t gstream = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
-  hipEvent_t ev_side = nullptr;   // side-stream work started at a call's beginning
   hipEvent_t ev_compute = nullptr;
   hipEvent_t ev_done = nullptr;   // recorded on the call's stream at the end of every call
   bool done_recorded = false;
@@ -346,7 +354,6 @@ void free_plan_memory(ll_plan* p) {
   if (p->cstream2) (void)hipStreamDestroy(p->cstream2);
   if (p->ev_fork) (void)hipEventDestroy(p->ev_fork);
   if (p->ev_join) (void)hipEventDestroy(p->ev_join);
-  if (p->ev_side) (void)hipEventDestroy(p->ev_side);
   if (p->ev_done) (void)hipEventDestroy(p->ev_done);
   if (p->gstream) (void)hipStreamDestroy(p->gstream);
 }
@@ -854,10 +861,9 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     return fail(LL_EHIP, "hipMemset of the plan's meta words failed");
   }
   if (hipStreamCreateWithFlags(&p->gstream, hipStreamNonBlocking) != hipSuccess ||
-      hipEventCreateWithFlags(&p->ev_fork, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&p->ev_join, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&p->ev_side, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&p->ev_done, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&p->ev_fork, kOrderEventFlags) != hipSuccess ||
+      hipEventCreateWithFlags(&p->ev_join, kOrderEventFlags) != hipSuccess ||
+      hipEventCreateWithFlags(&p->ev_done, kOrderEventFlags) != hipSuccess) {
     free_plan_memory(p);
     delete p;
     return fail(LL_EHIP, "creating the plan's side stream failed");
@@ -1027,11 +1033,7 @@ ll_status enqueue_fwd_wave(ll_plan* p, hipStream_t s, const void* x, const void*
   const int H = d.H, B = d.B, I = d.I;
   const long BH = (long)B * H;
   hipEvent_t ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
-  for (int l = 0; l < 2; ++l) {
-    const int Il = in_width(p, l);
-    LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, 4 * H, 4 * H,
-                                   reinterpret_cast<T*>(p->WT[l]), Il + H, s));
-  }
+  (void)W;   // (transposed by the set-up launch)
   ll::GemmArgs g{};
   g.A = x;
   g.lda = I;
@@ -1105,36 +1107,24 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
                       bool save) {
   const ll_desc& d = p->d;
   const int H = d.H, B = d.B, L = d.layers;
-  // W^T of every layer (row n = gate column n, the K-contiguous operand of
-  // the input projection and the loop) on the side stream, beside prep,
-  // which runs on one compute unit
-  // (without a side stream, in the forward that allocates nothing: on the
-  // call's stream, after prep)
-  const bool side = !p->wave && p->gstream;
-  if (side) {
-    LL_HIP(hipEventRecord(p->ev_fork, s));
-    LL_HIP(hipStreamWaitEvent(p->gstream, p->ev_fork, 0));
-    for (int l = 0; l < L; ++l) {
-      const int Il = in_width(p, l);
-      LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, p->G * H, p->G * H,
-                                     reinterpret_cast<T*>(p->WT[l]), Il + H, p->gstream));
-    }
-    LL_HIP(hipEventRecord(p->ev_side, p->gstream));
-  }
+  // prep (one work-group) beside the transposes W^T of every layer (row n =
+  // gate column n, the K-contiguous operand of the input projection and the
+  // loop), in one launch
   hipEvent_t ev = tbeg(p, s, LL_STAGE_PREP);
-  LL_HIP(ll::launch_prep(seq_len, B, d.T_max, p->perm, p->active, p->off, p->rowmap, p->meta,
-                         trip, s));
+  {
+    const T* Wl[2] = {nullptr, nullptr};
+    T* WTl[2] = {nullptr, nullptr};
+    int R[2] = {0, 0};
+    for (int l = 0; l < L; ++l) {
+      Wl[l] = reinterpret_cast<const T*>(W[l]);
+      WTl[l] = reinterpret_cast<T*>(p->WT[l]);
+      R[l] = in_width(p, l) + H;
+    }
+    LL_HIP(ll::launch_fwd_setup<T>(seq_len, B, d.T_max, p->perm, p->active, p->off, p->rowmap, p->meta,
+                                   trip, L, Wl, R, p->G * H, WTl, s));
+  }
   tend(p, s, LL_STAGE_PREP, ev);
   if (p->wave) return enqueue_fwd_wave<T>(p, s, x, W, bias, h0, c0, y, hT, cT, save);
-  if (side) {
-    LL_HIP(hipStreamWaitEvent(s, p->ev_side, 0));
-  } else {
-    for (int l = 0; l < L; ++l) {
-      const int Il = in_width(p, l);
-      LL_HIP(ll::launch_transpose<T>(reinterpret_cast<const T*>(W[l]), Il + H, p->G * H, p->G * H,
-                                     reinterpret_cast<T*>(p->WT[l]), Il + H, s));
-    }
-  }
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
     ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
@@ -1361,20 +1351,24 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
     LL_STATUS(dx_product(p->gstream));
     LL_HIP(hipEventRecord(p->ev_join, p->gstream));
   }
-  // db = sum of the row-group partials
-  ev = tbeg(p, s, LL_STAGE_DW);
-  LL_HIP(ll::launch_sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, GBH, GBH, dbias[l], s));
-  // cond body: the predicate's parameters get no gradient (a step function)
-  if (p->skip) LL_HIP(ll::launch_zero_u32(reinterpret_cast<unsigned*>(dbias[l] + GBH), Il + H + 1, s));
-  tend(p, s, LL_STAGE_DW, ev);
+  // one launch: db = sum of the row-group partials; (cond body) no gradient
+  // for the predicate's parameters (a step function); for dW straight from
+  // the row-major operands, the h history row of every compact row's
+  // h_{t-1}, and h0 (length order) after the history
+  ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
+  {
+    ll::SmallBatch<T> ops;
+    LL_HIP(ops.sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, GBH, 1, GBH, dbias[l], GBH));
+    if (p->skip) LL_HIP(ops.zero_u32(reinterpret_cast<unsigned*>(dbias[l] + GBH), Il + H + 1));
+    if (p->dw_rows[l]) {
+      LL_HIP(ops.prev_rows(p->active, p->off, B, d.T_max, p->cap, p->prevc));
+      LL_HIP(ops.h0_rows(p->h0 ? p->h0 + (long)l * B * H : nullptr, p->perm, B, H,
+                         reinterpret_cast<T*>(p->HH[l]) + p->cap * H));
+    }
+    LL_HIP(ops.launch(s));
+  }
+  tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
   if (p->dw_rows[l]) {
-    // dW straight from the row-major operands: the h history row of every
-    // compact row's h_{t-1}, and h0 (length order) after the history
-    ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
-    LL_HIP(ll::launch_prev_rows(p->active, p->off, B, d.T_max, p->cap, p->prevc, s));
-    LL_HIP(ll::launch_h0_rows<T>(p->h0 ? p->h0 + (long)l * B * H : nullptr, p->perm, B, H,
-                                 reinterpret_cast<T*>(p->HH[l]) + p->cap * H, s));
-    tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
     ev = tbeg(p, s, LL_STAGE_DW);
     DwPart parts[3];
     const int np = dw_parts_rows(p, l, parts);
@@ -1506,15 +1500,20 @@ ll_status act_products(ll_plan* p, hipStream_t s, float* dx, float* const* dW, f
   const int GH = 4 * H;
   const T* DZ = static_cast<const T*>(p->DZ);
   const T* HI = static_cast<const T*>(p->HI);
-  hipEvent_t ev = tbeg(p, s, LL_STAGE_DW);
-  LL_HIP(ll::launch_sum_slices(p->db_part, 8, GH, GH, dbias[0], s));
-  LL_HIP(ll::launch_zero_u32(reinterpret_cast<unsigned*>(dbias[0] + GH), H + 1, s));
-  tend(p, s, LL_STAGE_DW, ev);
+  // one launch: db, zero in the halting part, the dW operand maps
+  hipEvent_t ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
+  {
+    ll::SmallBatch<T> ops;
+    LL_HIP(ops.sum_slices(p->db_part, 8, GH, 1, GH, dbias[0], GH));
+    LL_HIP(ops.zero_u32(reinterpret_cast<unsigned*>(dbias[0] + GH), H + 1));
+    if (p->dw_rows[0]) {
+      LL_HIP(ops.prev_rows(p->active, p->off, B, d.T_max, cap, p->prevc));
+      LL_HIP(ops.h0_rows(p->h0, p->perm, B, H, reinterpret_cast<T*>(p->HH[0]) + cap * H));
+    }
+    LL_HIP(ops.launch(s));
+  }
+  tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
   if (p->dw_rows[0]) {
-    ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
-    LL_HIP(ll::launch_prev_rows(p->active, p->off, B, d.T_max, cap, p->prevc, s));
-    LL_HIP(ll::launch_h0_rows<T>(p->h0, p->perm, B, H, reinterpret_cast<T*>(p->HH[0]) + cap * H, s));
-    tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
     ev = tbeg(p, s, LL_STAGE_DW);
     DwPart parts[3];
     const int np = dw_parts_rows(p, 0, parts);
@@ -1668,8 +1667,14 @@ ll_status enqueue_bwd_wave(ll_plan* p, hipStream_t s, const float* dy, const flo
   unsigned* F0 = p->xflags + 8;
   unsigned* F1 = F0 + fw;
   unsigned* FY = F1 + fw;
+  // one launch: the dx rows of finished steps to zero, the flags
   hipEvent_t ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
-  LL_HIP(ll::launch_zero_u32(p->xflags, p->xflag_words, s));
+  {
+    ll::SmallBatch<T> setup;
+    if (dx) LL_HIP(setup.zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta));
+    LL_HIP(setup.zero_u32(p->xflags, p->xflag_words));
+    LL_HIP(setup.launch(s));
+  }
   tend(p, s, LL_STAGE_LOOP_SETUP, ev);
   const int ring_ks = (int)(4L * H * p->es / 64);
   ll::XLoopArgs a0 = x_common(p), a1 = x_common(p);
@@ -1791,22 +1796,11 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
   const ll_desc& d = p->d;
   const int H = d.H, B = d.B, L = d.layers;
   hipEvent_t ev = nullptr;
-  if (p->wave) {
-    ev = tbeg(p, s, LL_STAGE_DX);
-    if (dx) LL_HIP(ll::launch_zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta, s));
-    tend(p, s, LL_STAGE_DX, ev);
-    return enqueue_bwd_wave<T>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
-  }
-  // dx rows of finished steps to zero on the side stream, beside the set-up
-  // and the start of the gradient loop (joined before layer 0's products)
-  if (dx) {
-    LL_HIP(hipEventRecord(p->ev_fork, s));
-    LL_HIP(hipStreamWaitEvent(p->gstream, p->ev_fork, 0));
-    ev = tbeg(p, p->gstream, LL_STAGE_DX);
-    LL_HIP(ll::launch_zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta, p->gstream));
-    tend(p, p->gstream, LL_STAGE_DX, ev);
-    LL_HIP(hipEventRecord(p->ev_side, p->gstream));
-  }
+  if (p->wave) return enqueue_bwd_wave<T>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
+  // the set-up before each loop launch, in one launch: the dx rows of
+  // finished steps to zero (once), W_h in unit-major order, the flags
+  ll::SmallBatch<T> setup;
+  if (dx) LL_HIP(setup.zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta));
   for (int l = L - 1; l >= 0; --l) {
     const int Il = in_width(p, l);
     if (p->xmode) {
@@ -1827,9 +1821,7 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       xa.W = p->W[l];
       xa.woff = Il;
       if (p->G == 4) {   // the LSTM loop reduces in unit-major order
-        ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
-        LL_HIP(ll::launch_permute_um<T>(static_cast<const T*>(p->W[l]), Il, H, static_cast<T*>(p->Wum[l]), s));
-        tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+        LL_HIP(setup.permute_um(static_cast<const T*>(p->W[l]), Il, H, static_cast<T*>(p->Wum[l])));
         xa.W = p->Wum[l];
         xa.woff = 0;
       }
@@ -1886,7 +1878,8 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
         ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
         LL_HIP(wait_loaded(k));
         LL_HIP(wait_loaded(k - 1));
-        LL_HIP(ll::launch_zero_u32(p->xflags, p->xflag_words, s));
+        LL_HIP(setup.zero_u32(p->xflags, p->xflag_words));
+        LL_HIP(setup.launch(s));
         tend(p, s, LL_STAGE_LOOP_SETUP, ev);
         if (p->recompute) LL_STATUS(recompute_gates<T>(p, s, l, t0, t1));
         ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
@@ -1913,7 +1906,8 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     }
     if (p->cmode) {
       ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
-      LL_HIP(ll::launch_zero_u32(p->cflags, p->cflag_words, s));
+      LL_HIP(setup.zero_u32(p->cflags, p->cflag_words));
+      LL_HIP(setup.launch(s));
       tend(p, s, LL_STAGE_LOOP_SETUP, ev);
       ll::CLoopArgs ca = c_common(p);
       ca.W = p->W[l];
@@ -1966,11 +1960,11 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
     a.err = p->meta + 2;
     a.limit = p->barrier_ticks;
     if (!p->xmode && !p->cmode) {
+      LL_HIP(setup.launch(s));
       ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
       LL_HIP(chained_loop_launch(p->device, s, [&] { return ll::launch_bwd_loop<T>(a, p->geom.nwg, p->geom.lds_bwd, s); }));
       tend(p, s, LL_STAGE_BWD_LOOP, ev);
     }
-    if (l == 0 && dx) LL_HIP(hipStreamWaitEvent(s, p->ev_side, 0));
     if (p->act) {
       LL_STATUS(act_products<T>(p, s, dx, dW, dbias));
       continue;
