@@ -46,7 +46,11 @@
  *     compute unit of the device at once: the library chains the loop
  *     launches of all plans on one device (each waits for the previous one to
  *     complete, whichever stream enqueued it), so plans on different streams
- *     are safe; other work that holds compute units for long (another
+ *     are safe.  While all loop launches on a device come from one stream,
+ *     stream order does this at no cost; the first loop launch from a
+ *     second stream synchronises the device once (host-side), and later
+ *     launches order themselves with events.  Other work that holds compute
+ *     units for long (another
  *     process's kernels) delays a loop's start (waits are bounded: 5 s, then
  *     LL_DEVERR_BARRIER).  Under graph capture the chain is not used: the
  *     caller orders captured loops itself.

@@ -69,16 +69,24 @@ long round_up(long v, long m) { return (v + m - 1) / m * m; }
 // fence left the GPU idle for several microseconds).
 constexpr unsigned kOrderEventFlags = hipEventDisableTiming | hipEventDisableSystemFence;
 
-// Loop launches of every plan on one device form one chain: each waits for
-// the previous one (whatever plan or stream enqueued it) to complete.  The
-// loops need all compute units co-resident, so two of them must never run
-// at once.  (Skipped on a stream that is being captured into a graph: an
-// event recorded outside the capture cannot be waited on there.)
+// Loop launches of every plan on one device form one chain: each starts
+// after the previous one (whatever plan or stream enqueued it) has
+// completed.  The loops need all compute units co-resident, so two of them
+// must never run at once.  While every loop launch on the device has come
+// from one stream, stream order alone keeps them apart and nothing is
+// recorded (each event record cost the GPU several microseconds of idle
+// time); the first launch from another stream waits for the device to
+// finish its work (a host-side synchronisation, once per device), and from
+// then on every launch records an event that the next one, on another
+// stream, waits for.  (Skipped on a stream that is being captured into a
+// graph: an event recorded outside the capture cannot be waited on there.)
 struct LoopChain {
   std::mutex mu;
   hipEvent_t last = nullptr;
   bool recorded = false;
-  hipStream_t last_stream = nullptr;   // the stream `last` was recorded on
+  bool any = false;                    // a loop launch has happened
+  bool multi = false;                  // loop launches have come from more than one stream
+  hipStream_t last_stream = nullptr;   // the stream of the last loop launch
 };
 LoopChain g_loop_chain[64];
 
@@ -89,6 +97,20 @@ hipError_t chained_loop_launch(int device, hipStream_t s, Launch&& launch) {
   if (cap != hipStreamCaptureStatusNone || device < 0 || device >= 64) return launch();
   LoopChain& c = g_loop_chain[device];
   std::lock_guard<std::mutex> lock(c.mu);
+  if (!c.multi) {
+    if (!c.any || c.last_stream == s) {
+      const hipError_t e = launch();
+      if (e == hipSuccess) {
+        c.any = true;
+        c.last_stream = s;
+      }
+      return e;
+    }
+    // a second stream: the loops enqueued so far (on the first one) end first
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return e;
+    c.multi = true;
+  }
   if (!c.last) {
     hipError_t e = hipEventCreateWithFlags(&c.last, kOrderEventFlags);
     if (e != hipSuccess) {
@@ -103,10 +125,8 @@ hipError_t chained_loop_launch(int device, hipStream_t s, Launch&& launch) {
   hipError_t e = launch();
   if (e != hipSuccess) return e;
   e = hipEventRecord(c.last, s);
-  if (e == hipSuccess) {
-    c.recorded = true;
-    c.last_stream = s;
-  }
+  if (e == hipSuccess) c.recorded = true;
+  c.last_stream = s;
   return e;
 }
 
@@ -294,7 +314,9 @@ hipEvent_t take_event(ll_plan* p) {
     return e;
   }
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  // (timing only: no system-scope fence, which would idle the GPU for
+  // several microseconds at every bracket)
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 

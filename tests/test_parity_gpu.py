@@ -253,6 +253,37 @@ def test_repeat_calls_are_deterministic():
             np.testing.assert_array_equal(u, v)
 
 
+def test_plans_on_two_streams_match_one_stream():
+    """Two plans whose calls alternate between two streams: the loop launches
+    stay ordered across streams (the first one from the second stream
+    synchronises the device, later ones wait on the previous launch's
+    event), and every output equals, bitwise, the same calls on one stream."""
+    w = W("streams", B=24, I=32, H=64, T_max=9, dtype="f32", len_lo=0, len_hi=9,
+          random_state=True, seed=41)
+    inp = wl.generate(w)
+    say("[edge] two streams")
+    ref, err = run_case(w, inp)
+    assert err == 0
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    dcs = [DeviceCase(inp, w.H, w.I, w.layers, w.dtype) for _ in streams]
+    plans = [dc.plan() for dc in dcs]
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for dc, plan, st in zip(dcs, plans, streams):
+            with torch.cuda.stream(st):
+                dc.fwd(plan)
+                dc.bwd(plan)
+    torch.cuda.synchronize()
+    for dc, plan in zip(dcs, plans):
+        assert plan.status_sync() == 0
+        res = dc.results()
+        plan.close()
+        for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+            np.testing.assert_array_equal(res[k], ref[k], err_msg=k)
+        for u, v in zip(res["dW"] + res["dbias"], ref["dW"] + ref["dbias"]):
+            np.testing.assert_array_equal(u, v)
+
+
 def test_two_layers_equal_two_single_layer_calls(monkeypatch):
     # layer by layer, the two-layer plan makes the same calls as two plans
     monkeypatch.setenv("LSTMLOOP_WAVEFRONT", "off")
