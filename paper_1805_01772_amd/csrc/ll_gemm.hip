@@ -616,6 +616,77 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_tn_bf16_lds_kernel(GemmTn
 
   // result register r of lane l: row (r % 4) + 8 (r / 4) + 4 (l / 32), column l % 32
   const int l32 = lane & 31, kc = lane >> 5;
+  if (g.tile_flags && g.splits == 2) {
+    // The two splits of this tile meet on its counter: the first to arrive
+    // stores its sums to its slice of C and then sets the tile's ready word;
+    // the second waits for that word (the first is already running, so the
+    // wait ends), adds the slice to its own sums and writes the result.  The
+    // sum of two terms does not depend on which came first.
+    __shared__ int s_first;
+    unsigned* arrive = g.tile_flags + 2L * tt;
+    unsigned* ready = arrive + 1;
+    if (tid == 0)
+      s_first = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u;
+    __syncthreads();
+    const bool first = s_first != 0;
+    const unsigned slice_bytes = (unsigned)((long)M * g.ldc * 4);
+    if (first) {
+      const __amdgpu_buffer_rsrc_t rc = make_rsrc(g.C + (long)z * g.split_stride, slice_bytes);
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + wm * WM + i * 32 + (r & 3) + 8 * (r >> 2) + 4 * kc;
+#pragma unroll
+          for (int j = 0; j < NI; ++j) {
+            const int n = n0 + wn * WN + j * 32 + l32;
+            st_dev(rc, m < M && n < g.N ? (unsigned)(((long)m * g.ldc + n) * 4) : kOOB, acc[i][j][r]);
+          }
+        }
+      wait_all_vm();
+      __syncthreads();
+      if (tid == 0) __hip_atomic_store(ready, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    if (tid == 0) {   // (bounded: about a second of polls, far past any store burst)
+      for (unsigned polls = 0; polls < (1u << 24); ++polls) {
+        if (__hip_atomic_load(ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) break;
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    __syncthreads();
+    const __amdgpu_buffer_rsrc_t ro = make_rsrc(g.C + (long)(1 - z) * g.split_stride, slice_bytes);
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      float other[16][NI];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * WM + i * 32 + (r & 3) + 8 * (r >> 2) + 4 * kc;
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+          const int n = n0 + wn * WN + j * 32 + l32;
+          other[r][j] = ld_f32_l2(ro, m < M && n < g.N ? (unsigned)(((long)m * g.ldc + n) * 4) : kOOB);
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xF70);   // vmcnt(0): those loads, ahead of the stores
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * WM + i * 32 + (r & 3) + 8 * (r >> 2) + 4 * kc;
+        if (m >= M) continue;
+        float* orow = g.out + (long)m * g.ldo;
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+          const int n = n0 + wn * WN + j * 32 + l32;
+          if (n < g.N) orow[n] = z == 0 ? acc[i][j][r] + other[r][j] : other[r][j] + acc[i][j][r];
+        }
+      }
+    }
+    if (tid == 0) {   // both splits are past the counter: clear it for the next launch
+      __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(ready, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
+  }
   float* Cb = g.C + (g.splits > 1 ? (long)z * g.split_stride : 0L);
 #pragma unroll
   for (int i = 0; i < MI; ++i) {

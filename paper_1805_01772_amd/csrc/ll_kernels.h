@@ -505,6 +505,13 @@ struct GemmTnArgs {
   const int* a2_rowmap;
   int a2_rows;
   int M1;
+  // two splits summed in place (splits == 2, tile_flags non-NULL): per output
+  // tile two words (zero between launches; each launch leaves them zero); the
+  // split that finishes first writes its slice of C (device-scope stores),
+  // the second adds it to its own sums and writes out[m * ldo + n]
+  unsigned* tile_flags;
+  float* out;
+  long ldo;
 };
 bool gemm_tn_applies(const GemmTnArgs& g);
 hipError_t launch_gemm_tn(const GemmTnArgs& g, hipStream_t s);

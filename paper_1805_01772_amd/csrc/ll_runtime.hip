@@ -235,6 +235,9 @@ struct ll_plan {
   // h_{t-1} (h0 rows after the history), and the split-K of each product
   int* prevc = nullptr;
   int tn_splits[2][3] = {{1, 1, 1}, {1, 1, 1}};
+  // products over rows split in two sum in place: two words per output tile
+  unsigned* tn_flags = nullptr;
+  long tn_flag_words = 0;
   bool dw_rows[2] = {false, false};   // layer's dW from the row-major operands
   int64_t stack_device_bytes = 0;
   int64_t stack_host_bytes = 0;
@@ -362,7 +365,7 @@ void free_plan_memory(ll_plan* p) {
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
                   p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags,
                   p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias, p->sx, p->guards, p->Wum[0],
-                  p->Wum[1], p->prevc, p->HI, p->ntrip};
+                  p->Wum[1], p->prevc, p->HI, p->ntrip, p->tn_flags};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -650,6 +653,7 @@ ll_status plan_configure(ll_plan* p, const ll_desc* desc, int device, const hipD
       sp = std::max(1L, std::min(16L, std::min(sp, std::max(1L, p->cap / 256))));
       p->tn_splits[l][k] = (int)sp;
       if (sp > 1) p->ws_floats = std::max(p->ws_floats, sp * parts[k].m * parts[k].n);
+      if (sp == 2) p->tn_flag_words = std::max(p->tn_flag_words, 2 * tiles);
     }
   }
   for (int l = 0; l < L; ++l) {
@@ -777,6 +781,7 @@ ll_status plan_layout(ll_plan* p, bool fwd_only, Take&& take) {
   if (p->dw_rows[0] || p->dw_rows[1]) ALLOC(p->prevc, sizeof(int) * cap, "previous-row map");
   if (p->skip || p->act) ALLOC(p->guards, sizeof(float) * L * p->M * cap, "guard stack");
   if (p->ws_floats > 0) ALLOC(p->ws, sizeof(float) * p->ws_floats, "split-K workspace");
+  if (p->tn_flag_words > 0) ALLOC(p->tn_flags, sizeof(unsigned) * p->tn_flag_words, "split-K tile counters");
 #undef ALLOC
   return LL_OK;
 }
@@ -877,10 +882,11 @@ ll_status ll_plan_create(const ll_desc* desc, int device, ll_plan** out) {
     delete p;
     return fail(LL_EHIP, "hipMemset of the ponder states failed");
   }
-  if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess) {
+  if (hipMemset(p->meta, 0, sizeof(int) * ll::META_INTS) != hipSuccess ||
+      (p->tn_flags && hipMemset(p->tn_flags, 0, sizeof(unsigned) * p->tn_flag_words) != hipSuccess)) {
     free_plan_memory(p);
     delete p;
-    return fail(LL_EHIP, "hipMemset of the plan's meta words failed");
+    return fail(LL_EHIP, "hipMemset of the plan's meta words or tile counters failed");
   }
   if (hipStreamCreateWithFlags(&p->gstream, hipStreamNonBlocking) != hipSuccess ||
       hipEventCreateWithFlags(&p->ev_fork, kOrderEventFlags) != hipSuccess ||
@@ -1428,7 +1434,15 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
       if (!ll::gemm_tn_applies(g))
         return fail(LL_EHIP, "internal: the dW product over rows does not apply to layer %d", l);
       float* out = dW[l] + (long)q.a_row * GH + q.c_col;
-      if (g.splits > 1) {
+      if (g.splits == 2 && p->tn_flags) {   // the two splits sum in place
+        g.C = p->ws;
+        g.ldc = q.n;
+        g.split_stride = (long)q.m * q.n;
+        g.tile_flags = p->tn_flags;
+        g.out = out;
+        g.ldo = GH;
+        LL_HIP(ll::launch_gemm_tn(g, s));
+      } else if (g.splits > 1) {
         g.C = p->ws;
         g.ldc = q.n;
         g.split_stride = (long)q.m * q.n;
