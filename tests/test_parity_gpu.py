@@ -965,6 +965,33 @@ def test_misaligned_arrays_rejected_before_anything_is_enqueued():
     assert not bad, bad
 
 
+def test_dw_split_halves_summed_in_place():
+    """bf16 I = H = 1024, B = 128: the dW product over rows runs as two
+    split-K halves per 256x256 tile that meet on the tile's counter (the
+    first stores its sums, the second adds them and writes dW); few steps
+    keep the oracle quick.  Every output against the oracle, and a second
+    call bitwise equal to the first (the counters reset themselves)."""
+    w = W("dwsplit_bf16_b128_i1024_h1024_t6", B=128, I=1024, H=1024, T_max=6, dtype="bf16",
+          len_lo=1, len_hi=6, random_state=True, seed=83)
+    inp = wl.generate(w)
+    say(f"[dw] {w.name}")
+    dc = DeviceCase(inp, w.H, w.I, 1, w.dtype)
+    plan = dc.plan()
+    assert plan.geometry()["dw_in_place"] == [True]
+    outs = []
+    for _ in range(2):
+        dc.fwd(plan)
+        dc.bwd(plan)
+        outs.append(dc.results())
+    assert plan.status_sync() == 0
+    plan.close()
+    for u, v in zip(outs[1]["dW"] + outs[1]["dbias"], outs[0]["dW"] + outs[0]["dbias"]):
+        np.testing.assert_array_equal(u, v)
+    errs, bad = compare(outs[0], oracle_reference(inp, 1, w.dtype), TOL[w.dtype])
+    say(f"    errors {errs}")
+    assert not bad, bad
+
+
 def test_dw_operands_past_two_gib_take_the_transposes():
     """bf16 I = H = 1024, B = 128, T_max = 2048: the dz rows of the row
     capacity reach 2 GiB, past the 32-bit offsets of the dW product over rows,
