@@ -358,8 +358,9 @@ const char* ll_last_error(void);
  * NULL.
  */
 typedef enum {
-  LL_STAGE_PREP = 0,          /* trip count, length order, compact offsets   */
-  LL_STAGE_INPUT_PROJ = 1,    /* W transpose + x_t W_x + b of all rows        */
+  LL_STAGE_PREP = 0,          /* trip count, length order, compact offsets,  */
+                              /* and the W transposes in the same launch     */
+  LL_STAGE_INPUT_PROJ = 1,    /* x_t W_x + b of all rows                     */
   LL_STAGE_FWD_LOOP = 2,      /* forward recurrence (one launch per layer)   */
   LL_STAGE_BWD_LOOP = 3,      /* gradient recurrence (one launch per layer)  */
   LL_STAGE_BWD_OPERANDS = 4,  /* transposed operands of the dW products      */
