@@ -41,6 +41,10 @@ __device__ __forceinline__ float ld_f32_l2(__amdgpu_buffer_rsrc_t r, unsigned of
 __device__ __forceinline__ float ld_f32(__amdgpu_buffer_rsrc_t r, unsigned off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
+// Plain 16-byte read of four floats through a buffer descriptor.
+__device__ __forceinline__ float4 ld_f32x4(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
 // Offset past every buffer range used here: a lane with nothing to read
 // loads from it and gets zeros, so no load needs a per-lane branch.
 constexpr unsigned kOOB = 0x80000000u;

@@ -185,7 +185,7 @@ struct XLoopArgs {
   // saved values: the c field of row (t, r) at stack + stack_row(t, r) * sld
   // + scoff; i, f, g, o at gstk + grow(t, r) * gld + {0, H, 2H, 3H}, where
   // grow maps like stack_row with gchunk / gslots (gstk NULL: the gates sit
-  // in the stack rows, at offsets 0 .. 3H)
+  // in the stack rows, those of unit u at 4u .. 4u+3)
   int sld, scoff;
   int sgates;             // forward: 1 = push i, f, g, o with c (0: c only); the
                           // GRU pushes r, u, n, zh_n + b_hn and h_{t-1} in their places

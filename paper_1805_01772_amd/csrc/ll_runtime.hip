@@ -1041,8 +1041,9 @@ ll::XLoopArgs x_common(const ll_plan* p) {
   a.t_end = p->d.T_max;
   a.chunk_steps = p->d.T_max;
   a.nslots = 1;
-  // stack rows: LSTM i, f, g, o, c_t (5H); GRU r, u, n, zh_n + b_hn,
-  // h_{t-1} (5H); the RNN pushes h_t only
+  // stack rows: LSTM i, f, g, o, c_t (5H: the four gate values of unit u at
+  // 4u .. 4u+3, then c_t); GRU r, u, n, zh_n + b_hn, h_{t-1} (the same
+  // layout); the RNN pushes h_t only
   const bool five = p->G == 4 || p->G == 3;
   a.sld = five ? 5 * p->d.H : p->d.H;
   a.scoff = five ? 4 * p->d.H : 0;

@@ -447,12 +447,9 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         // ponder step k's values at stack slot k, its guard, and h^{k+1}
         if (act && a.stack) {
           const long vr = (long)k * a.slot_rows + off_t + r;
-          float* st = a.stack + vr * a.sld + ju;
-          st[0] = ig;
-          st[H] = fg;
-          st[2 * H] = gg;
-          st[3 * H] = og;
-          st[a.scoff] = cn;
+          float* srow = a.stack + vr * a.sld;
+          *reinterpret_cast<float4*>(srow + 4 * ju) = make_float4(ig, fg, gg, og);
+          srow[a.scoff + ju] = cn;
           reinterpret_cast<T*>(a.HI)[vr * H + ju] = Op<T>::from_f32(hn);
           if (rank == 0 && cu == 0) a.guard[vr] = run ? 1.f : 0.f;
         }
@@ -462,19 +459,15 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
         const long cr = off_t + r;
         HH[cr * H + ju] = Op<T>::from_f32(hn);
         if (a.stack) {
-          float* st = a.stack + stack_row(a, t, r) * a.sld + ju;
+          float* srow = a.stack + stack_row(a, t, r) * a.sld;
           if constexpr (G == 4 || G == 3) {
-            // (c only: the gate stores all land on the c field, which the last
-            // store overwrites; no branch on the common path)
-            const int gs = a.sgates ? H : 0;
-            st[0] = ig;
-            st[gs] = fg;
-            st[2 * gs] = gg;
-            st[3 * gs] = og;
-            st[a.scoff] = cn;
+            // the unit's four gate values side by side (stack row: 4H gate
+            // values unit by unit, then c): one 16-byte store
+            if (a.sgates) *reinterpret_cast<float4*>(srow + 4 * ju) = make_float4(ig, fg, gg, og);
+            srow[a.scoff + ju] = cn;
             if (SKIP && rank == 0 && cu == 0) a.guard[cr] = run ? 1.f : 0.f;
           } else {
-            st[a.scoff] = hn;   // the RNN's gradient needs only h_t
+            srow[a.scoff + ju] = hn;   // the RNN's gradient needs only h_t
           }
         }
       }
@@ -687,9 +680,17 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
     } else {
     const float* gbase = a.gstk ? a.gstk : a.stack;
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(gbase + gate_row(a, ts, r0) * GL, (unsigned)(nr * GL * 4));
-    const unsigned go = ok ? (unsigned)((crow * GL + ju) * 4) : kOOB;
+    if (a.gstk) {   // recomputed gates: gate-major rows
+      const unsigned go = ok ? (unsigned)((crow * GL + ju) * 4) : kOOB;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) v[c] = ld_f32(rg, go + c * H * 4);
+      for (int c = 0; c < 4; ++c) v[c] = ld_f32(rg, go + c * H * 4);
+    } else {        // the stack's gate values, unit by unit: one 16-byte read
+      const float4 g4 = ld_f32x4(rg, ok ? (unsigned)((crow * GL + 4 * ju) * 4) : kOOB);
+      v[0] = g4.x;
+      v[1] = g4.y;
+      v[2] = g4.z;
+      v[3] = g4.w;
+    }
     v[4] = ld_f32(rs, so);
     if constexpr (G == 3) {   // GRU: h_{t-1} was pushed with the step
       v[5] = 0.f;
@@ -731,8 +732,11 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
     const long vr = (long)max(kk, 0) * a.slot_rows + off + r0;     // first row of the tile's slot
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(a.stack + vr * SL, (unsigned)(nr * SL * 4));
     const unsigned go = ok ? (unsigned)((crow * SL + ju) * 4) : kOOB;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) v[c] = ld_f32(rg, go + c * H * 4);
+    const float4 g4 = ld_f32x4(rg, ok ? (unsigned)((crow * SL + 4 * ju) * 4) : kOOB);
+    v[0] = g4.x;
+    v[1] = g4.y;
+    v[2] = g4.z;
+    v[3] = g4.w;
     v[4] = ld_f32(rg, go + a.scoff * 4);
     if (kk > 0) {
       const __amdgpu_buffer_rsrc_t rp2 =
