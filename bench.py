@@ -223,7 +223,7 @@ def main():
         plan_kw = dict(spill=1, spill_chunk_steps=C,
                        device_stack_budget_bytes=4 * C * w.B * 5 * w.H * 4)
 
-    def timed(kw, timing, steps=None):
+    def timed(kw, timing, steps=None, per_step_events=False):
         steps = steps or args.steps
         plan = dc.plan(**kw)
         for _ in range(args.warmup):
@@ -234,17 +234,22 @@ def main():
             raise RuntimeError("device error during warmup")
         plan.set_timing(timing)
         stream = torch.cuda.current_stream()
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        # an event after every step only where per-step times are wanted (each
+        # costs a few microseconds of stream time)
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1 if per_step_events else 2)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         evs[0].record(stream)
         for k in range(steps):
             dc.fwd(plan)
             dc.bwd(plan)
-            evs[k + 1].record(stream)
+            if per_step_events:
+                evs[k + 1].record(stream)
+        if not per_step_events:
+            evs[1].record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        per_step = [evs[k].elapsed_time(evs[k + 1]) for k in range(steps)]
+        per_step = [evs[k].elapsed_time(evs[k + 1]) for k in range(len(evs) - 1)]
         stages = plan.read_timing()
         plan.set_timing(False)
         err = plan.status_sync()
@@ -260,7 +265,10 @@ def main():
     breakdown_steps = min(args.steps, 10)
     stages_all = timed(plan_kw, True, breakdown_steps)[2]
     dom = max(("fwd_loop", "bwd_loop", "input_proj", "dw", "dx"), key=lambda k: stages_all[k][0])
-    gpu_ms, wall, stages, geom, sbytes, per_step = timed(plan_kw, [dom])
+    gpu_ms, wall, stages, geom, sbytes, _ = timed(plan_kw, [dom])
+    # the spread of single steps, from a pass of its own with an event after
+    # every step and no stage events
+    per_step = timed(plan_kw, False, breakdown_steps, per_step_events=True)[5]
     spill = None
     if w.spill:
         res_ms = timed({}, False)[0]
@@ -319,7 +327,8 @@ def main():
         "mfma_util_of_measured_peak": flops / (ms_per_step / 1e3) / (measured_peak * 1e12),
         "measured_mfma_peak_tflops": measured_peak,
         "measured_mfma_rate_16x16_tflops": measured_16,
-        "step_ms": {"median": q[1], "p5": q[0], "p95": q[2]},
+        "step_ms": {"median": q[1], "p5": q[0], "p95": q[2],
+                    "from": f"separate pass of {breakdown_steps} steps with an event after each"},
         "padded_flops_per_step": padded,
         "flops_skipped_vs_padded_T_eff": 1.0 - flops / padded["T_eff"],
         "per_iteration_us": ms_per_step * 1e3 / T_eff if T_eff else None,
