@@ -457,18 +457,14 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       }
       if (act) {
         const long cr = off_t + r;
-        __builtin_nontemporal_store(Op<T>::from_f32(hn), HH + cr * H + ju);
+        HH[cr * H + ju] = Op<T>::from_f32(hn);
         if (a.stack) {
           float* srow = a.stack + stack_row(a, t, r) * a.sld;
           if constexpr (G == 4 || G == 3) {
             // the unit's four gate values side by side (stack row: 4H gate
-            // values unit by unit, then c): one 16-byte store.  The stack,
-            // history and y stores are non-temporal: nothing reads them in
-            // this launch (measured: forward loop -0.5 %; the same for the
-            // gradient loop's dz rows, read by the products after it, +2 %)
-            typedef float f4v __attribute__((ext_vector_type(4)));
-            if (a.sgates) __builtin_nontemporal_store(f4v{ig, fg, gg, og}, reinterpret_cast<f4v*>(srow + 4 * ju));
-            __builtin_nontemporal_store(cn, srow + a.scoff + ju);
+            // values unit by unit, then c): one 16-byte store
+            if (a.sgates) *reinterpret_cast<float4*>(srow + 4 * ju) = make_float4(ig, fg, gg, og);
+            srow[a.scoff + ju] = cn;
             if (SKIP && rank == 0 && cu == 0) a.guard[cr] = run ? 1.f : 0.f;
           } else {
             srow[a.scoff + ju] = hn;   // the RNN's gradient needs only h_t
@@ -477,7 +473,7 @@ __device__ __forceinline__ void xfwd_body(const XLoopArgs& a, int grp, int rank,
       }
       if (a.y && cellt) {
         const int b = sperm[mt * 16 + crow];
-        if (b >= 0) __builtin_nontemporal_store(act ? hn : 0.f, a.y + ((long)t * B + b) * H + ju);
+        if (b >= 0) a.y[((long)t * B + b) * H + ju] = act ? hn : 0.f;
       }
       }   // ponder iterations
       if constexpr (ACT) {
