@@ -198,6 +198,12 @@ struct XLoopArgs {
   long slot_rows;
   int* ntrip;             // [T_max][8 * MRT] inner trip count per (step, row tile)
   void* HI;
+  // gradient: dx [T_max, B, I] floats to zero at every row's finished steps
+  // (t >= seq_len[b]; all steps if the lengths failed the range check), or
+  // NULL; XCDs 1 .. 7 zero them after their last step
+  float* dx_zero;
+  const int* seq_len;
+  int I;
 };
 
 // Chip-wide loops (ll_cloop.hip), for shapes whose recurrent weights need

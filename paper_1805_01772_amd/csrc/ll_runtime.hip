@@ -1835,9 +1835,10 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
   hipEvent_t ev = nullptr;
   if (p->wave) return enqueue_bwd_wave<T>(p, s, dy, dhT, dcT, dx, dW, dbias, dh0, dc0);
   // the set-up before each loop launch, in one launch: the dx rows of
-  // finished steps to zero (once), W_h in unit-major order, the flags
+  // finished steps to zero (once; the XCD-local gradient loop of layer 0
+  // zeroes them itself), W_h in unit-major order, the flags
   ll::SmallBatch<T> setup;
-  if (dx) LL_HIP(setup.zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta));
+  if (dx && !p->xmode) LL_HIP(setup.zero_finished_rows(dx, d.T_max, B, d.I, p->seq_len, p->meta));
   for (int l = L - 1; l >= 0; --l) {
     const int Il = in_width(p, l);
     if (p->xmode) {
@@ -1863,6 +1864,11 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
         xa.woff = 0;
       }
       xa.X = p->DZ;
+      if (l == 0 && dx) {   // dx at finished steps, zeroed by XCDs 1 .. 7 after their last step
+        xa.dx_zero = dx;
+        xa.seq_len = p->seq_len;
+        xa.I = d.I;
+      }
       xa.c0 = p->c0 && p->G == 4 ? p->c0 + (long)l * B * H : nullptr;
       xa.stack = p->stack[l];
       xa.guard = p->skip ? p->guards + (long)l * p->cap : p->act ? p->guards : nullptr;

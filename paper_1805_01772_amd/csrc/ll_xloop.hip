@@ -1010,6 +1010,21 @@ __device__ __forceinline__ void xbwd_body(const XLoopArgs& a, int grp, int rank,
     const int g = c / HJ, u = c - (c / HJ) * HJ;
     a.db_part[(long)grp * GBH + (long)g * H + j0 + u] = s;
   }
+  // dx at the finished steps of every row: zeros, written by XCDs 1 .. 7
+  // once their own steps are done (XCD 0 holds the longest rows, tile 0, so
+  // the others end first): XCD x takes the batch rows b = x - 1 (mod 7), its
+  // waves the rows, its members the steps
+  if (a.dx_zero && t0 == 0 && grp > 0) {
+    const bool bad = (a.err[0] & LL_DEVERR_SEQ_LEN_BIT) != 0;
+    const int I4 = a.I >> 2;
+    for (int b = grp - 1 + 7 * wave; b < B; b += 7 * XNW) {
+      const int len = bad ? 0 : a.seq_len[b];
+      for (int t = len + rank; t < a.T_max; t += P) {
+        float4* row = reinterpret_cast<float4*>(a.dx_zero + ((long)t * B + b) * a.I);
+        for (int i = lane; i < I4; i += 64) row[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  }
 }
 
 template <typename T, int NCT, int KSW, int KSR, int MRT_MAX, int G, bool SKIP, bool ACT = false>
