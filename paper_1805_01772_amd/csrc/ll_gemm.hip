@@ -256,13 +256,17 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_nt_bf16_lds_kernel(GemmAr
   constexpr int LI = BM / 8 / NW;            // load instructions per wave and operand
   __shared__ uint4 sA0[CH], sA1[CH], sB0[CH], sB1[CH];
 
+  if ((int)blockIdx.x < g.pre_blocks) {   // the forward loop's entering state and flags
+    x_prepare_body<bf16_t>(g.pre, blockIdx.x, g.pre_blocks, kBigThreads);
+    return;
+  }
   const int M = g.M_dev ? min(*g.M_dev, g.M) : g.M;
   const int K = g.K_dev ? *g.K_dev : g.K;
   const int nmt = (M + BM - 1) / BM, nnt = (g.N + BN - 1) / BN;
   const int per_split = nmt * nnt;
   const int ntiles = per_split * g.splits;
   const int share = (ntiles + 7) / 8;
-  const int L = blockIdx.x;
+  const int L = blockIdx.x - g.pre_blocks;
   const int t = (L & 7) * share + (L >> 3);
   if ((L >> 3) >= share || t >= ntiles) return;
   const int z = t / per_split;
@@ -758,14 +762,21 @@ long gemm_rounds(const GemmArgs& g, int elem_bytes, int n_cu) {
 template <typename T>
 hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s) {
   if (g.act_h > 0 && (g.splits != 1 || g.bias)) return hipErrorInvalidValue;
-  if (gemm_big_applies(g, (int)sizeof(T))) {
+  if (g.pre_blocks < 0) return hipErrorInvalidValue;
+  if (gemm_big_applies(g, (int)sizeof(T)) && sizeof(T) == 2) {
     long ab, bb;
     big_ranges(g, &ab, &bb);
     const long tiles = (long)((g.M + kBigTile - 1) / kBigTile) * ((g.N + kBigTile - 1) / kBigTile) * g.splits;
     const long share = (tiles + 7) / 8;
-    hipLaunchKernelGGL(gemm_nt_bf16_lds_kernel, dim3((unsigned)(share * 8)), dim3(kBigThreads), 0, s, g,
-                       (unsigned)ab, (unsigned)bb);
+    hipLaunchKernelGGL(gemm_nt_bf16_lds_kernel, dim3((unsigned)(share * 8 + g.pre_blocks)), dim3(kBigThreads), 0,
+                       s, g, (unsigned)ab, (unsigned)bb);
     return hipGetLastError();
+  }
+  if (g.pre_blocks > 0) {   // (the other kernels take no extra work-groups)
+    const XPrepArgs& q = g.pre;
+    const hipError_t e = launch_x_prepare_fwd<T>(q.h0, q.perm, q.B, q.H, q.MRT, q.ring_ks, q.slot, q.ring,
+                                                 q.flags, q.nflags, s);
+    if (e != hipSuccess) return e;
   }
   dim3 grid((g.N + 127) / 128, (g.M + 127) / 128, g.splits);
   hipLaunchKernelGGL(gemm_nt_kernel<T>, grid, dim3(256), 0, s, g);

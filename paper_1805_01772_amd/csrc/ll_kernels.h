@@ -32,6 +32,39 @@ struct GatherTArgs {
 
 // C[crow(m), n] = sum_k A[arow(m), k] * Bm[n, k] (+ bias[n]), both operands
 // K-contiguous ("NT").  M, K may come from device memory (sum of lengths).
+// The forward loop's entering state in its ring (slot `slot`, the operand
+// layout: row r = (x + 8 mt) * 16 + l % 16 of XCD x, unit u = ks * 4 KPC +
+// (l / 16) * KPC + e for lane l, element e of k-step ks; rows in length order
+// through perm, zeros past B or without h0) and its flags cleared.
+struct XPrepArgs {
+  const float* h0;
+  const int* perm;
+  int B, H, MRT, ring_ks, slot;
+  void* ring;
+  unsigned* flags;
+  int nflags;
+};
+template <typename T>
+__device__ inline void x_prepare_body(const XPrepArgs& a, long bid, long nb, int nthreads) {
+  constexpr int KPC = Op<T>::kPerChunk;
+  const int KS = a.H / (4 * KPC);
+  const long n = 8L * a.MRT * KS * 64 * KPC;
+  T* slot1 = reinterpret_cast<T*>(reinterpret_cast<char*>(a.ring) + ((long)a.slot * 8 * a.MRT * a.ring_ks << 10));
+  for (long f = bid * nthreads + threadIdx.x; f < n; f += nb * nthreads) {
+    const int e = (int)(f % KPC);
+    const int l = (int)((f / KPC) % 64);
+    const int ks = (int)((f / (64 * KPC)) % KS);
+    const int tile = (int)(f / (64L * KPC * KS));
+    const int x = tile / a.MRT, mt = tile - x * a.MRT;
+    const int r = (x + 8 * mt) * 16 + (l & 15);
+    const int u = ks * 4 * KPC + (l >> 4) * KPC + e;
+    const float v = (a.h0 && r < a.B) ? a.h0[(long)a.perm[r] * a.H + u] : 0.f;
+    // block ks of tile `tile` in the slot (tiles are ring_ks blocks apart)
+    slot1[(((long)tile * a.ring_ks + ks) * 64 + l) * KPC + e] = Op<T>::from_f32(v);
+  }
+  for (long i = bid * nthreads + threadIdx.x; i < a.nflags; i += nb * nthreads) a.flags[i] = 0u;
+}
+
 struct GemmArgs {
   const void* A;
   long lda;
@@ -59,6 +92,11 @@ struct GemmArgs {
   const float* addend;
   const int* add_rowmap;
   long ld_add;
+  // pre_blocks > 0: the launch also fills the forward loop's ring with its
+  // entering state and clears the loop's flags (x_prepare_body), in
+  // pre_blocks work-groups of its own (bf16 operands only)
+  int pre_blocks;
+  XPrepArgs pre;
 };
 
 struct LoopGeom {

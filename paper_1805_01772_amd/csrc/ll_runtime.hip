@@ -1172,6 +1172,13 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     g.N = p->G * H;
     g.K = Il;
     g.splits = 1;
+    // the XCD-local loop's entering state (ring slot 1, read at step 0) and
+    // flags, prepared in work-groups of this launch beside the product's
+    if (p->xmode) {
+      g.pre_blocks = 16;
+      g.pre = ll::XPrepArgs{h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->xMRT,
+                            (int)((long)H * p->es / 64), 1, p->xring, p->xflags, p->xflag_words};
+    }
     LL_HIP(ll::launch_gemm_nt<T>(g, s));
     // cond body: the input part of the predicate, x_t . w_px per compact row
     if (p->skip)
@@ -1243,12 +1250,16 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
         const int t0 = k * C, t1 = std::min(d.T_max, t0 + C);
         const int slot = k % xa.nslots;
         const bool last = k == nch - 1;
-        ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
-        // the chunk that used this ring slot before has reached host memory
-        if (p->spill && save && k >= p->nslots) LL_HIP(hipStreamWaitEvent(s, p->ev_d2h[l * p->nslots + slot], 0));
-        LL_HIP(ll::launch_x_prepare_fwd<T>(hin, p->perm, B, H, p->xMRT, ring_ks, (t0 + 1) & 1, p->xring,
-                                           p->xflags, p->xflag_words, s));
-        tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+        // (the first launch's entering state: prepared by the input projection's launch)
+        if (k > 0) {
+          ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
+          // the chunk that used this ring slot before has reached host memory
+          if (p->spill && save && k >= p->nslots)
+            LL_HIP(hipStreamWaitEvent(s, p->ev_d2h[l * p->nslots + slot], 0));
+          LL_HIP(ll::launch_x_prepare_fwd<T>(hin, p->perm, B, H, p->xMRT, ring_ks, (t0 + 1) & 1, p->xring,
+                                             p->xflags, p->xflag_words, s));
+          tend(p, s, LL_STAGE_LOOP_SETUP, ev);
+        }
         ev = tbeg(p, s, LL_STAGE_FWD_LOOP);
         xa.t_begin = t0;
         xa.t_end = t1;

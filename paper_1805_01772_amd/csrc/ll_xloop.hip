@@ -1072,27 +1072,8 @@ __global__ __launch_bounds__(XNT, 1) void xbwd2_kernel(XLoopArgs a0, XLoopArgs a
 //   f = (((x * MRT + mt) * KS + ks) * 64 + l) * KPC + e
 //   row r = (x + 8 mt) * 16 + l % 16, unit u = ks * 4 KPC + (l / 16) * KPC + e.
 template <typename T>
-__global__ __launch_bounds__(256) void x_prepare_fwd_kernel(const float* __restrict__ h0,
-                                                            const int* __restrict__ perm, int B, int H,
-                                                            int MRT, int ring_ks, int slot, void* ring,
-                                                            unsigned* flags, int nflags) {
-  constexpr int KPC = Op<T>::kPerChunk;
-  const int KS = H / (4 * KPC);
-  const long n = 8L * MRT * KS * 64 * KPC;
-  T* slot1 = reinterpret_cast<T*>(reinterpret_cast<char*>(ring) + ((long)slot * 8 * MRT * ring_ks << 10));
-  for (long f = blockIdx.x * 256L + threadIdx.x; f < n; f += gridDim.x * 256L) {
-    const int e = (int)(f % KPC);
-    const int l = (int)((f / KPC) % 64);
-    const int ks = (int)((f / (64 * KPC)) % KS);
-    const int tile = (int)(f / (64L * KPC * KS));
-    const int x = tile / MRT, mt = tile - x * MRT;
-    const int r = (x + 8 * mt) * 16 + (l & 15);
-    const int u = ks * 4 * KPC + (l >> 4) * KPC + e;
-    const float v = (h0 && r < B) ? h0[(long)perm[r] * H + u] : 0.f;
-    // block ks of tile `tile` in slot 1 (tiles are ring_ks blocks apart)
-    slot1[(((long)tile * ring_ks + ks) * 64 + l) * KPC + e] = Op<T>::from_f32(v);
-  }
-  for (long i = blockIdx.x * 256L + threadIdx.x; i < nflags; i += gridDim.x * 256L) flags[i] = 0u;
+__global__ __launch_bounds__(256) void x_prepare_fwd_kernel(XPrepArgs a) {
+  x_prepare_body<T>(a, blockIdx.x, gridDim.x, 256);
 }
 
 __global__ __launch_bounds__(256) void zero_u32_kernel(unsigned* p, int n) {
@@ -1107,8 +1088,8 @@ hipError_t launch_x_prepare_fwd(const float* h0, const int* perm, int B, int H, 
   long blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(x_prepare_fwd_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, h0, perm, B, H, mrt,
-                     ring_ks, slot, ring, flags, nflags);
+  hipLaunchKernelGGL(x_prepare_fwd_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s,
+                     XPrepArgs{h0, perm, B, H, mrt, ring_ks, slot, ring, flags, nflags});
   return hipGetLastError();
 }
 template hipError_t launch_x_prepare_fwd<float>(const float*, const int*, int, int, int, int, int, void*,
