@@ -248,50 +248,23 @@ __global__ __launch_bounds__(256) void rc_maps_kernel(const int* __restrict__ ac
   }
 }
 
-__device__ void prev_rows_body(const int* __restrict__ active, const int* __restrict__ off, int B,
-                               int T_max, long cap, int* __restrict__ prev, int bid, int nb) {
-  const long n = (long)T_max * B;
-  for (long i = bid * 256L + threadIdx.x; i < n; i += nb * 256L) {
-    const int t = (int)(i / B), r = (int)(i % B);
-    if (r < active[t]) prev[off[t] + r] = t > 0 ? off[t - 1] + r : (int)(cap + r);
-  }
-}
 __global__ __launch_bounds__(256) void prev_rows_kernel(const int* __restrict__ active,
                                                         const int* __restrict__ off, int B, int T_max,
                                                         long cap, int* __restrict__ prev) {
-  prev_rows_body(active, off, B, T_max, cap, prev, blockIdx.x, gridDim.x);
+  prev_rows_body(active, off, B, T_max, cap, prev, blockIdx.x, gridDim.x, 256);
 }
 
-template <typename T>
-__device__ void h0_rows_body(const float* __restrict__ h0, const int* __restrict__ perm, int B, int H,
-                             T* __restrict__ dst, int bid, int nb) {
-  const long n = (long)B * H;
-  for (long i = bid * 256L + threadIdx.x; i < n; i += nb * 256L) {
-    const int r = (int)(i / H), j = (int)(i % H);
-    dst[i] = Op<T>::from_f32(h0 ? h0[(long)perm[r] * H + j] : 0.f);
-  }
-}
 template <typename T>
 __global__ __launch_bounds__(256) void h0_rows_kernel(const float* __restrict__ h0,
                                                       const int* __restrict__ perm, int B, int H,
                                                       T* __restrict__ dst) {
-  h0_rows_body<T>(h0, perm, B, H, dst, blockIdx.x, gridDim.x);
+  h0_rows_body<T>(h0, perm, B, H, dst, blockIdx.x, gridDim.x, 256);
 }
 
-// out[i] = sum_{s < S} ws[s * stride + i], fixed order.
-__device__ void sum_slices_body(const float* __restrict__ ws, int S, long stride, long n, long cols,
-                                long ldo, float* __restrict__ out, int bid, int nb) {
-  for (long i = bid * 256L + threadIdx.x; i < n; i += nb * 256L) {
-    float acc = 0.0f;
-    for (int s = 0; s < S; ++s) acc += ws[s * stride + i];
-    const long r = i / cols;
-    out[r * ldo + (i - r * cols)] = acc;
-  }
-}
 __global__ __launch_bounds__(256) void sum_slices_kernel(const float* __restrict__ ws, int S,
                                                          long stride, long n, long cols, long ldo,
                                                          float* __restrict__ out) {
-  sum_slices_body(ws, S, stride, n, cols, ldo, out, blockIdx.x, gridDim.x);
+  sum_slices_body(ws, S, stride, n, cols, ldo, out, blockIdx.x, gridDim.x, 256);
 }
 
 // out[r] = sum_k A[row(r)][k] * op(w[k]) for the compact rows r < meta[1]
@@ -431,15 +404,15 @@ __global__ __launch_bounds__(256) void small_tasks_kernel(SmallTasks ts) {
       break;
     case kTaskSumSlices:
       sum_slices_body(static_cast<const float*>(k.a), k.i0, k.l0, k.l1, k.l2, k.l3, static_cast<float*>(k.out), b,
-                      k.blocks);
+                      k.blocks, 256);
       break;
     case kTaskPrevRows:
       prev_rows_body(static_cast<const int*>(k.a), static_cast<const int*>(k.b), k.i0, k.i1, k.l0,
-                     static_cast<int*>(k.out), b, k.blocks);
+                     static_cast<int*>(k.out), b, k.blocks, 256);
       break;
     case kTaskH0Rows:
       h0_rows_body<T>(static_cast<const float*>(k.a), static_cast<const int*>(k.b), k.i0, k.i1,
-                      static_cast<T*>(k.out), b, k.blocks);
+                      static_cast<T*>(k.out), b, k.blocks, 256);
       break;
     default:
       break;
@@ -696,6 +669,17 @@ template hipError_t launch_fwd_setup<float>(const int*, int, int, int*, int*, in
                                              const float* const*, const int*, int, float* const*, hipStream_t);
 template hipError_t launch_fwd_setup<bf16_t>(const int*, int, int, int*, int*, int*, int*, int*, int*, int,
                                               const bf16_t* const*, const int*, int, bf16_t* const*, hipStream_t);
+template <typename T>
+__global__ __launch_bounds__(256) void pre_jobs_kernel(PreJobs j) {
+  pre_jobs_body<T>(j, blockIdx.x, gridDim.x, 256);
+}
+template <typename T>
+hipError_t launch_pre_jobs(const PreJobs& j, hipStream_t s) {
+  hipLaunchKernelGGL(pre_jobs_kernel<T>, dim3(64), dim3(256), 0, s, j);
+  return hipGetLastError();
+}
+template hipError_t launch_pre_jobs<float>(const PreJobs&, hipStream_t);
+template hipError_t launch_pre_jobs<bf16_t>(const PreJobs&, hipStream_t);
 template hipError_t launch_small_tasks<float>(const SmallTasks&, hipStream_t);
 template hipError_t launch_small_tasks<bf16_t>(const SmallTasks&, hipStream_t);
 template hipError_t launch_transpose<float>(const float*, int, int, int, float*, int, hipStream_t);

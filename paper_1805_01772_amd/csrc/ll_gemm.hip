@@ -256,8 +256,8 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_nt_bf16_lds_kernel(GemmAr
   constexpr int LI = BM / 8 / NW;            // load instructions per wave and operand
   __shared__ uint4 sA0[CH], sA1[CH], sB0[CH], sB1[CH];
 
-  if ((int)blockIdx.x < g.pre_blocks) {   // the forward loop's entering state and flags
-    x_prepare_body<bf16_t>(g.pre, blockIdx.x, g.pre_blocks, kBigThreads);
+  if ((int)blockIdx.x < g.pre_blocks) {   // the jobs carried by this launch
+    pre_jobs_body<bf16_t>(g.pre, blockIdx.x, g.pre_blocks, kBigThreads);
     return;
   }
   const int M = g.M_dev ? min(*g.M_dev, g.M) : g.M;
@@ -773,9 +773,7 @@ hipError_t launch_gemm_nt(const GemmArgs& g, hipStream_t s) {
     return hipGetLastError();
   }
   if (g.pre_blocks > 0) {   // (the other kernels take no extra work-groups)
-    const XPrepArgs& q = g.pre;
-    const hipError_t e = launch_x_prepare_fwd<T>(q.h0, q.perm, q.B, q.H, q.MRT, q.ring_ks, q.slot, q.ring,
-                                                 q.flags, q.nflags, s);
+    const hipError_t e = launch_pre_jobs<T>(g.pre, s);
     if (e != hipSuccess) return e;
   }
   dim3 grid((g.N + 127) / 128, (g.M + 127) / 128, g.splits);

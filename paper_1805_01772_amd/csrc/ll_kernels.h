@@ -65,6 +65,65 @@ __device__ inline void x_prepare_body(const XPrepArgs& a, long bid, long nb, int
   for (long i = bid * nthreads + threadIdx.x; i < a.nflags; i += nb * nthreads) a.flags[i] = 0u;
 }
 
+// Row map of the h_{t-1} operand of dW over rows: prev[off[t] + r] = the
+// history row of the same sequence one step earlier (rows cap + r hold h0).
+__device__ inline void prev_rows_body(const int* __restrict__ active, const int* __restrict__ off, int B,
+                                      int T_max, long cap, int* __restrict__ prev, long bid, long nb,
+                                      int nthreads) {
+  const long n = (long)T_max * B;
+  for (long i = bid * nthreads + threadIdx.x; i < n; i += nb * nthreads) {
+    const int t = (int)(i / B), r = (int)(i % B);
+    if (r < active[t]) prev[off[t] + r] = t > 0 ? off[t - 1] + r : (int)(cap + r);
+  }
+}
+// h0 rows in length order, operand type.
+template <typename T>
+__device__ inline void h0_rows_body(const float* __restrict__ h0, const int* __restrict__ perm, int B, int H,
+                                    T* __restrict__ dst, long bid, long nb, int nthreads) {
+  const long n = (long)B * H;
+  for (long i = bid * nthreads + threadIdx.x; i < n; i += nb * nthreads) {
+    const int r = (int)(i / H), j = (int)(i % H);
+    dst[i] = Op<T>::from_f32(h0 ? h0[(long)perm[r] * H + j] : 0.f);
+  }
+}
+// out[r * ldo + c] = sum_{s < S} ws[s * stride + r * cols + c], fixed order.
+__device__ inline void sum_slices_body(const float* __restrict__ ws, int S, long stride, long n, long cols,
+                                       long ldo, float* __restrict__ out, long bid, long nb, int nthreads) {
+  for (long i = bid * nthreads + threadIdx.x; i < n; i += nb * nthreads) {
+    float acc = 0.0f;
+    for (int s = 0; s < S; ++s) acc += ws[s * stride + i];
+    const long r = i / cols;
+    out[r * ldo + (i - r * cols)] = acc;
+  }
+}
+
+// Small jobs a product's launch can carry in work-groups of its own
+// (pre_blocks of them, ahead of the product's): each is skipped when its
+// output is NULL.
+struct PreJobs {
+  XPrepArgs xp;                          // the forward loop's entering state (xp.ring)
+  const int* active;                     // the h_{t-1} row map of dW over rows (prev)
+  const int* off;
+  int B, T_max;
+  long cap;
+  int* prev;
+  const float* h0;                       // h0 rows in length order (h0dst, operand type)
+  const int* perm;
+  int H;
+  void* h0dst;
+  const float* ws;                       // a sum of S slices (sum_out)
+  int S;
+  long stride, n, cols, ldo;
+  float* sum_out;
+};
+template <typename T>
+__device__ inline void pre_jobs_body(const PreJobs& j, long bid, long nb, int nthreads) {
+  if (j.xp.ring) x_prepare_body<T>(j.xp, bid, nb, nthreads);
+  if (j.prev) prev_rows_body(j.active, j.off, j.B, j.T_max, j.cap, j.prev, bid, nb, nthreads);
+  if (j.h0dst) h0_rows_body<T>(j.h0, j.perm, j.B, j.H, static_cast<T*>(j.h0dst), bid, nb, nthreads);
+  if (j.sum_out) sum_slices_body(j.ws, j.S, j.stride, j.n, j.cols, j.ldo, j.sum_out, bid, nb, nthreads);
+}
+
 struct GemmArgs {
   const void* A;
   long lda;
@@ -92,12 +151,14 @@ struct GemmArgs {
   const float* addend;
   const int* add_rowmap;
   long ld_add;
-  // pre_blocks > 0: the launch also fills the forward loop's ring with its
-  // entering state and clears the loop's flags (x_prepare_body), in
-  // pre_blocks work-groups of its own (bf16 operands only)
+  // pre_blocks > 0: the launch also runs the jobs of `pre` (the forward
+  // loop's entering state and flags, dW's row maps, a slice sum), in
+  // pre_blocks work-groups of its own
   int pre_blocks;
-  XPrepArgs pre;
+  PreJobs pre;
 };
+template <typename T>
+hipError_t launch_pre_jobs(const PreJobs& j, hipStream_t s);
 
 struct LoopGeom {
   int HJ;       // hidden units per work-group (multiple of 4)

@@ -211,6 +211,9 @@ struct ll_plan {
   hipEvent_t ev_compute = nullptr;
   hipEvent_t ev_done = nullptr;   // recorded on the call's stream at the end of every call
   bool done_recorded = false;
+  // the saved forward's input-projection launches also wrote dW's h_{t-1}
+  // row map and h0 rows (the gradient pass then skips those tasks)
+  bool rows_prepared = false;
   std::vector<hipEvent_t> ev_d2h, ev_h2d;   // per (layer, slot)
   float* carry = nullptr;      // [4][B, H]: h, c (forward) / dh, dc (backward) between chunks
   float* db_state = nullptr;   // per-thread db sums between backward chunks
@@ -1153,7 +1156,9 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
                                    trip, L, Wl, R, p->G * H, WTl, s));
   }
   tend(p, s, LL_STAGE_PREP, ev);
+  p->rows_prepared = false;
   if (p->wave) return enqueue_fwd_wave<T>(p, s, x, W, bias, h0, c0, y, hT, cT, save);
+  p->rows_prepared = save;   // (the input projections below carry them)
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
     ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
@@ -1173,11 +1178,26 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
     g.K = Il;
     g.splits = 1;
     // the XCD-local loop's entering state (ring slot 1, read at step 0) and
-    // flags, prepared in work-groups of this launch beside the product's
+    // flags, and for a gradient pass with dW over rows the h_{t-1} row map
+    // and this layer's h0 rows, prepared in work-groups of this launch beside
+    // the product's (they depend only on prep and h0)
     if (p->xmode) {
       g.pre_blocks = 16;
-      g.pre = ll::XPrepArgs{h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->xMRT,
-                            (int)((long)H * p->es / 64), 1, p->xring, p->xflags, p->xflag_words};
+      g.pre.xp = ll::XPrepArgs{h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->xMRT,
+                               (int)((long)H * p->es / 64), 1, p->xring, p->xflags, p->xflag_words};
+    }
+    if (save && p->dw_rows[l]) {
+      g.pre_blocks = 16;
+      g.pre.active = p->active;
+      g.pre.off = p->off;
+      g.pre.B = B;
+      g.pre.T_max = d.T_max;
+      g.pre.cap = p->cap;
+      g.pre.prev = p->prevc;
+      g.pre.h0 = h0 ? h0 + (long)l * B * H : nullptr;
+      g.pre.perm = p->perm;
+      g.pre.H = H;
+      g.pre.h0dst = reinterpret_cast<T*>(p->HH[l]) + p->cap * H;
     }
     LL_HIP(ll::launch_gemm_nt<T>(g, s));
     // cond body: the input part of the predicate, x_t . w_px per compact row
@@ -1376,6 +1396,20 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   } else {
     gx.ldc = H;
   }
+  // db = the sum of the gradient loop's row-group partials, carried by the
+  // dx product's launch when there is one
+  const int db_slices = p->xmode ? 8 : p->cmode ? 1 : p->geom.RG;
+  const bool db_in_dx = dx != nullptr;
+  if (db_in_dx) {
+    gx.pre_blocks = 4;
+    gx.pre.ws = db_part;
+    gx.pre.S = db_slices;
+    gx.pre.stride = GBH;
+    gx.pre.n = GBH;
+    gx.pre.cols = GBH;
+    gx.pre.ldo = GBH;
+    gx.pre.sum_out = dbias[l];
+  }
   auto dx_product = [&](hipStream_t st) -> ll_status {
     hipEvent_t evx = tbeg(p, st, LL_STAGE_DX);
     LL_HIP(ll::launch_gemm_nt<T>(gx, st));
@@ -1398,14 +1432,15 @@ ll_status bwd_products(ll_plan* p, hipStream_t s, int l, const void* dz, const f
   ev = tbeg(p, s, LL_STAGE_BWD_OPERANDS);
   {
     ll::SmallBatch<T> ops;
-    LL_HIP(ops.sum_slices(db_part, p->xmode ? 8 : p->cmode ? 1 : p->geom.RG, GBH, 1, GBH, dbias[l], GBH));
+    if (!db_in_dx)
+      LL_HIP(ops.sum_slices(db_part, db_slices, GBH, 1, GBH, dbias[l], GBH));
     if (p->skip) LL_HIP(ops.zero_u32(reinterpret_cast<unsigned*>(dbias[l] + GBH), Il + H + 1));
-    if (p->dw_rows[l]) {
+    if (p->dw_rows[l] && !p->rows_prepared) {
       LL_HIP(ops.prev_rows(p->active, p->off, B, d.T_max, p->cap, p->prevc));
       LL_HIP(ops.h0_rows(p->h0 ? p->h0 + (long)l * B * H : nullptr, p->perm, B, H,
                          reinterpret_cast<T*>(p->HH[l]) + p->cap * H));
     }
-    LL_HIP(ops.launch(s));
+    LL_HIP(ops.launch(s));   // (nothing left: no launch)
   }
   tend(p, s, LL_STAGE_BWD_OPERANDS, ev);
   if (p->dw_rows[l]) {
