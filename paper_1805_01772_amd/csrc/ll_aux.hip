@@ -294,23 +294,9 @@ __global__ __launch_bounds__(256) void row_dot_kernel(const T* __restrict__ A, i
 // One thread per (j, u): four coalesced reads (consecutive threads take
 // consecutive u) and one 4-element store.
 template <typename T>
-__device__ void permute_um_body(const T* __restrict__ W, int row0, int H, T* __restrict__ dst, int bid,
-                                int nb) {
-  const long n = (long)H * H;
-  for (long i = bid * 256L + threadIdx.x; i < n; i += nb * 256L) {
-    const long j = i / H;
-    const int u = (int)(i - j * H);
-    const T* src = W + (row0 + j) * 4L * H + u;
-    struct alignas(4 * sizeof(T)) Quad { T v[4]; } q;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) q.v[g] = src[(long)g * H];
-    *reinterpret_cast<Quad*>(dst + 4 * i) = q;
-  }
-}
-template <typename T>
 __global__ __launch_bounds__(256) void permute_um_kernel(const T* __restrict__ W, int row0, int H,
                                                          T* __restrict__ dst) {
-  permute_um_body<T>(W, row0, H, dst, blockIdx.x, gridDim.x);
+  permute_um_body<T>(W, row0, H, dst, blockIdx.x, gridDim.x, 256);
 }
 
 // float -> operand type copy (used for bf16(h0) and similar small arrays).
@@ -400,7 +386,7 @@ __global__ __launch_bounds__(256) void small_tasks_kernel(SmallTasks ts) {
                               static_cast<const int*>(k.b), b, k.blocks);
       break;
     case kTaskPermuteUm:
-      permute_um_body<T>(static_cast<const T*>(k.a), k.i0, k.i1, static_cast<T*>(k.out), b, k.blocks);
+      permute_um_body<T>(static_cast<const T*>(k.a), k.i0, k.i1, static_cast<T*>(k.out), b, k.blocks, 256);
       break;
     case kTaskSumSlices:
       sum_slices_body(static_cast<const float*>(k.a), k.i0, k.l0, k.l1, k.l2, k.l3, static_cast<float*>(k.out), b,

@@ -97,6 +97,23 @@ __device__ inline void sum_slices_body(const float* __restrict__ ws, int S, long
   }
 }
 
+// W_h (rows row0 .. row0 + H - 1 of W [rows, 4H]) in unit-major column
+// order: dst[j][4u + g] = W[row0 + j][g H + u].
+template <typename T>
+__device__ inline void permute_um_body(const T* __restrict__ W, int row0, int H, T* __restrict__ dst, long bid,
+                                       long nb, int nthreads) {
+  const long n = (long)H * H;
+  for (long i = bid * nthreads + threadIdx.x; i < n; i += nb * nthreads) {
+    const long j = i / H;
+    const int u = (int)(i - j * H);
+    const T* src = W + (row0 + j) * 4L * H + u;
+    struct alignas(4 * sizeof(T)) Quad { T v[4]; } q;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) q.v[g] = src[(long)g * H];
+    *reinterpret_cast<Quad*>(dst + 4 * i) = q;
+  }
+}
+
 // Small jobs a product's launch can carry in work-groups of its own
 // (pre_blocks of them, ahead of the product's): each is skipped when its
 // output is NULL.
@@ -115,6 +132,11 @@ struct PreJobs {
   int S;
   long stride, n, cols, ldo;
   float* sum_out;
+  const void* pw;                        // W_h in unit-major order (pdst, operand type)
+  int prow0, pH;
+  void* pdst;
+  unsigned* zero;                        // nzero words to zero
+  int nzero;
 };
 template <typename T>
 __device__ inline void pre_jobs_body(const PreJobs& j, long bid, long nb, int nthreads) {
@@ -122,6 +144,9 @@ __device__ inline void pre_jobs_body(const PreJobs& j, long bid, long nb, int nt
   if (j.prev) prev_rows_body(j.active, j.off, j.B, j.T_max, j.cap, j.prev, bid, nb, nthreads);
   if (j.h0dst) h0_rows_body<T>(j.h0, j.perm, j.B, j.H, static_cast<T*>(j.h0dst), bid, nb, nthreads);
   if (j.sum_out) sum_slices_body(j.ws, j.S, j.stride, j.n, j.cols, j.ldo, j.sum_out, bid, nb, nthreads);
+  if (j.pdst)
+    permute_um_body<T>(static_cast<const T*>(j.pw), j.prow0, j.pH, static_cast<T*>(j.pdst), bid, nb, nthreads);
+  for (long i = bid * nthreads + threadIdx.x; i < j.nzero; i += nb * nthreads) j.zero[i] = 0u;
 }
 
 struct GemmArgs {

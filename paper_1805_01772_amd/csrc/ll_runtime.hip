@@ -182,6 +182,9 @@ struct ll_plan {
   // wavefront: lower layer, upper layer, dy exchange)
   unsigned* xflags = nullptr;
   int xflag_words = 0;
+  // single-layer plans whose gradient loop is one launch: its flags, of
+  // their own, cleared by the forward's input-projection launch
+  unsigned* xflags_b = nullptr;
   void* xring2 = nullptr;      // wavefront: the upper layer's exchange ring
   void* DZ2 = nullptr;         // wavefront: dz of the upper layer
   float* dyx = nullptr;        // wavefront: dy exchange [2][8][MRT][16][H]
@@ -214,6 +217,8 @@ struct ll_plan {
   // the saved forward's input-projection launches also wrote dW's h_{t-1}
   // row map and h0 rows (the gradient pass then skips those tasks)
   bool rows_prepared = false;
+  // ... and W_h in unit-major order and, with xflags_b, the gradient loop's flags
+  bool bwd_prepared = false;
   std::vector<hipEvent_t> ev_d2h, ev_h2d;   // per (layer, slot)
   float* carry = nullptr;      // [4][B, H]: h, c (forward) / dh, dc (backward) between chunks
   float* db_state = nullptr;   // per-thread db sums between backward chunks
@@ -368,7 +373,7 @@ void free_plan_memory(ll_plan* p) {
                   p->dyc, p->xring, p->xflags, p->db_part, p->ws, p->carry, p->db_state,
                   p->xring2, p->DZ2, p->dyx, p->db_part2, p->cring, p->cpart, p->cflags,
                   p->gslot, p->rc_inmap, p->rc_prevmap, p->rc_bias, p->sx, p->guards, p->Wum[0],
-                  p->Wum[1], p->prevc, p->HI, p->ntrip, p->tn_flags};
+                  p->Wum[1], p->prevc, p->HI, p->ntrip, p->tn_flags, p->xflags_b};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   for (float* h : p->host_stack)
@@ -750,6 +755,8 @@ ll_status plan_layout(ll_plan* p, bool fwd_only, Take&& take) {
     ALLOC(p->xring, 2L * 8 * p->xMRT * ks_b * 1024, "exchange ring");
     p->xflag_words = 8 + (p->wave ? 3 : 1) * 8 * p->xMRT * 32;
     ALLOC(p->xflags, sizeof(unsigned) * p->xflag_words, "exchange flags");
+    if (!fwd_only && L == 1 && !p->spill && !p->recompute)
+      ALLOC(p->xflags_b, sizeof(unsigned) * p->xflag_words, "gradient loop flags");
     if (p->wave) {
       ALLOC(p->xring2, 2L * 8 * p->xMRT * ks_b * 1024, "exchange ring");
       if (!fwd_only) {
@@ -1157,8 +1164,10 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
   }
   tend(p, s, LL_STAGE_PREP, ev);
   p->rows_prepared = false;
+  p->bwd_prepared = false;
   if (p->wave) return enqueue_fwd_wave<T>(p, s, x, W, bias, h0, c0, y, hT, cT, save);
   p->rows_prepared = save;   // (the input projections below carry them)
+  p->bwd_prepared = save && p->xmode && p->G == 4;
   for (int l = 0; l < L; ++l) {
     const int Il = in_width(p, l);
     ev = tbeg(p, s, LL_STAGE_INPUT_PROJ);
@@ -1186,8 +1195,20 @@ ll_status enqueue_fwd(ll_plan* p, hipStream_t s, const void* x, const int32_t* s
       g.pre.xp = ll::XPrepArgs{h0 ? h0 + (long)l * B * H : nullptr, p->perm, B, H, p->xMRT,
                                (int)((long)H * p->es / 64), 1, p->xring, p->xflags, p->xflag_words};
     }
+    // (and for the gradient pass: W_h in unit-major order, its flags)
+    if (save && p->xmode && p->G == 4) {
+      g.pre_blocks = 32;
+      g.pre.pw = W[l];
+      g.pre.prow0 = Il;
+      g.pre.pH = H;
+      g.pre.pdst = p->Wum[l];
+      if (p->xflags_b) {
+        g.pre.zero = p->xflags_b;
+        g.pre.nzero = p->xflag_words;
+      }
+    }
     if (save && p->dw_rows[l]) {
-      g.pre_blocks = 16;
+      g.pre_blocks = std::max(g.pre_blocks, 16);
       g.pre.active = p->active;
       g.pre.off = p->off;
       g.pre.B = B;
@@ -1891,8 +1912,10 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       ll::XLoopArgs xa = x_common(p);
       xa.ring = p->xring;
       xa.ring_ks = (int)((long)p->G * H * p->es / 64);
-      xa.rank_ctr = p->xflags;
-      xa.flags = p->xflags + 8;
+      // flags cleared by the saved forward's input projection, or here
+      unsigned* fl = p->bwd_prepared && p->xflags_b ? p->xflags_b : p->xflags;
+      xa.rank_ctr = fl;
+      xa.flags = fl + 8;
       xa.B = B;
       xa.H = H;
       xa.T_max = d.T_max;
@@ -1904,8 +1927,9 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
       xa.perm = p->perm;
       xa.W = p->W[l];
       xa.woff = Il;
-      if (p->G == 4) {   // the LSTM loop reduces in unit-major order
-        LL_HIP(setup.permute_um(static_cast<const T*>(p->W[l]), Il, H, static_cast<T*>(p->Wum[l])));
+      if (p->G == 4) {   // the LSTM loop reduces in unit-major order (permuted by the forward)
+        if (!p->bwd_prepared)
+          LL_HIP(setup.permute_um(static_cast<const T*>(p->W[l]), Il, H, static_cast<T*>(p->Wum[l])));
         xa.W = p->Wum[l];
         xa.woff = 0;
       }
@@ -1967,8 +1991,8 @@ ll_status enqueue_bwd(ll_plan* p, hipStream_t s, const float* dy, const float* d
         ev = tbeg(p, s, LL_STAGE_LOOP_SETUP);
         LL_HIP(wait_loaded(k));
         LL_HIP(wait_loaded(k - 1));
-        LL_HIP(setup.zero_u32(p->xflags, p->xflag_words));
-        LL_HIP(setup.launch(s));
+        if (fl == p->xflags) LL_HIP(setup.zero_u32(p->xflags, p->xflag_words));
+        LL_HIP(setup.launch(s));   // (nothing left: no launch)
         tend(p, s, LL_STAGE_LOOP_SETUP, ev);
         if (p->recompute) LL_STATUS(recompute_gates<T>(p, s, l, t0, t1));
         ev = tbeg(p, s, LL_STAGE_BWD_LOOP);
