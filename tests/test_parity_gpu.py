@@ -253,6 +253,33 @@ def test_repeat_calls_are_deterministic():
             np.testing.assert_array_equal(u, v)
 
 
+@pytest.mark.parametrize("dtype,layers", [("bf16", 1), ("f32", 1), ("bf16", 2)])
+def test_inference_forward_between_saved_forwards_changes_nothing(dtype, layers):
+    """A saved forward prepares part of the gradient pass's set-up (flags,
+    row maps, permuted weights) in its own launches; an inference forward in
+    between, and the saved forward it replaces, leave the next saved
+    forward's gradient pass bitwise unchanged."""
+    w = W("interleave", B=64, I=64, H=256, T_max=12, dtype=dtype, layers=layers, len_lo=0,
+          len_hi=12, random_state=True, seed=31)
+    inp = wl.generate(w)
+    say(f"[edge] saved / inference / saved forwards, {dtype}, {layers} layer(s)")
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
+    plan = dc.plan()
+    dc.fwd(plan)
+    dc.bwd(plan)
+    ref = dc.results()
+    dc.fwd(plan)
+    dc.fwd(plan, save=False)
+    dc.fwd(plan)
+    dc.bwd(plan)
+    got = dc.results()
+    plan.close()
+    for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+        np.testing.assert_array_equal(got[k], ref[k])
+    for u, v in zip(got["dW"] + got["dbias"], ref["dW"] + ref["dbias"]):
+        np.testing.assert_array_equal(u, v)
+
+
 def test_plans_on_two_streams_match_one_stream():
     """Two plans whose calls alternate between two streams: the loop launches
     stay ordered across streams (the first one from the second stream
