@@ -280,6 +280,40 @@ def test_inference_forward_between_saved_forwards_changes_nothing(dtype, layers)
         np.testing.assert_array_equal(u, v)
 
 
+@pytest.mark.parametrize("dtype,layers", [("bf16", 1), ("f32", 1), ("bf16", 2)])
+def test_plan_reused_with_new_lengths_matches_a_fresh_plan(dtype, layers):
+    """Everything a call derives from the lengths (trip count, order, compact
+    offsets, row maps, loop flags) is rebuilt on the device by each call: a
+    plan reused with other lengths in the same seq_len buffer gives the
+    results of a fresh plan bitwise, also when the new trip count is
+    shorter or zero."""
+    w = W("new_lengths", B=48, I=64, H=128, T_max=15, dtype=dtype, layers=layers, len_lo=0,
+          len_hi=15, random_state=True, with_dy=True, seed=33)
+    say(f"[edge] plan reuse with new lengths, {dtype}, {layers} layer(s)")
+    inp = wl.generate(w)
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
+    plan = dc.plan()
+    dc.fwd(plan)
+    dc.bwd(plan)
+    rng = np.random.default_rng(34)
+    for new_len in (rng.integers(0, 8, size=w.B).astype(np.int32),      # shorter trip count
+                    rng.integers(3, 16, size=w.B).astype(np.int32),     # longer again
+                    np.zeros(w.B, dtype=np.int32)):                     # zero trip
+        inp2 = dict(inp, seq_len=new_len)
+        dc.seq_len.copy_(torch.from_numpy(new_len))
+        dc.fwd(plan)
+        dc.bwd(plan)
+        assert plan.status_sync() == 0
+        got = dc.results()
+        ref, err = run_case(w, inp2)
+        assert err == 0
+        for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+            np.testing.assert_array_equal(got[k], ref[k])
+        for u, v in zip(got["dW"] + got["dbias"], ref["dW"] + ref["dbias"]):
+            np.testing.assert_array_equal(u, v)
+    plan.close()
+
+
 def test_plans_on_two_streams_match_one_stream():
     """Two plans whose calls alternate between two streams: the loop launches
     stay ordered across streams (the first one from the second stream
@@ -667,6 +701,39 @@ def test_spill_matches_resident_stack_bitwise(w, C, R, monkeypatch):
     # and the resident run is right
     errs, bad = compare(ref, oracle_reference(inp, w.layers, w.dtype), TOL[w.dtype])
     assert not bad, bad
+
+
+@pytest.mark.parametrize("dtype,mode", [("f32", "spill"), ("bf16", "spill"), ("f32", "recompute")])
+def test_memory_policy_repeat_calls_bitwise(dtype, mode, monkeypatch):
+    """Consecutive training steps on one plan that swaps the stack (device
+    ring, host stack, copy events) or recomputes the gates (chunk buffers)
+    reuse its state; every step's results equal the first's bitwise, and a
+    forward-only call in between changes nothing."""
+    monkeypatch.setenv("LSTMLOOP_WAVEFRONT", "off")
+    w = W("policy_repeat", B=24, I=32, H=64, T_max=41, dtype=dtype, len_lo=0, len_hi=41,
+          w_scale=0.3, random_state=True, seed=26)
+    say(f"[{mode}] repeat calls, {dtype}")
+    inp = wl.generate(w)
+    C, R = 6, 3
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
+    if mode == "spill":
+        plan = dc.plan(spill=1, spill_chunk_steps=C, device_stack_budget_bytes=R * C * w.B * 5 * w.H * 4)
+    else:
+        plan = dc.plan(recompute=1, spill_chunk_steps=C)
+    outs = []
+    for k in range(3):
+        dc.fwd(plan)
+        dc.bwd(plan)
+        assert plan.status_sync() == 0
+        outs.append(dc.results())
+        if k == 0:
+            dc.fwd(plan, save=False)
+    plan.close()
+    for o in outs[1:]:
+        for key in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+            np.testing.assert_array_equal(o[key], outs[0][key])
+        for u, v in zip(o["dW"] + o["dbias"], outs[0]["dW"] + outs[0]["dbias"]):
+            np.testing.assert_array_equal(u, v)
 
 
 def test_spill_long_sequences():
