@@ -280,14 +280,15 @@ def test_inference_forward_between_saved_forwards_changes_nothing(dtype, layers)
         np.testing.assert_array_equal(u, v)
 
 
-@pytest.mark.parametrize("dtype,layers", [("bf16", 1), ("f32", 1), ("bf16", 2)])
-def test_plan_reused_with_new_lengths_matches_a_fresh_plan(dtype, layers):
+@pytest.mark.parametrize("dtype,layers,B,I,H", [("bf16", 1, 48, 64, 128), ("f32", 1, 48, 64, 128),
+                                               ("bf16", 2, 48, 64, 128), ("bf16", 1, 128, 1024, 1024)])
+def test_plan_reused_with_new_lengths_matches_a_fresh_plan(dtype, layers, B, I, H):
     """Everything a call derives from the lengths (trip count, order, compact
     offsets, row maps, loop flags) is rebuilt on the device by each call: a
     plan reused with other lengths in the same seq_len buffer gives the
     results of a fresh plan bitwise, also when the new trip count is
-    shorter or zero."""
-    w = W("new_lengths", B=48, I=64, H=128, T_max=15, dtype=dtype, layers=layers, len_lo=0,
+    shorter or zero (the last case has the benchmark's widths)."""
+    w = W("new_lengths", B=B, I=I, H=H, T_max=15, dtype=dtype, layers=layers, len_lo=0,
           len_hi=15, random_state=True, with_dy=True, seed=33)
     say(f"[edge] plan reuse with new lengths, {dtype}, {layers} layer(s)")
     inp = wl.generate(w)
