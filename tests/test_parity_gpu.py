@@ -290,9 +290,23 @@ def test_plan_reused_with_new_lengths_matches_a_fresh_plan(dtype, layers, B, I, 
     shorter or zero (the last case has the benchmark's widths)."""
     w = W("new_lengths", B=B, I=I, H=H, T_max=15, dtype=dtype, layers=layers, len_lo=0,
           len_hi=15, random_state=True, with_dy=True, seed=33)
-    say(f"[edge] plan reuse with new lengths, {dtype}, {layers} layer(s)")
+    _check_reuse_with_new_lengths(w, "lstm")
+
+
+@pytest.mark.parametrize("cell", ["gru", "rnn", "skip", "act"])
+def test_other_cells_plan_reused_with_new_lengths(cell):
+    """As above for the other bodies (the cond body's guards, the nested
+    loop's ponder slots and inner trip counts are per call too)."""
+    w = W("new_lengths_" + cell, B=48, I=64, H=128, T_max=15, dtype="bf16", len_lo=0, len_hi=15,
+          random_state=True, with_dy=True, cell=cell, seed=35)
+    _check_reuse_with_new_lengths(w, cell)
+
+
+def _check_reuse_with_new_lengths(w, cell):
+    pm = w.ponder_max if cell == "act" else 0
+    say(f"[edge] plan reuse with new lengths, {cell}, {w.dtype}, {w.layers} layer(s), H={w.H}")
     inp = wl.generate(w)
-    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype)
+    dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell=cell, ponder_max=pm)
     plan = dc.plan()
     dc.fwd(plan)
     dc.bwd(plan)
@@ -306,8 +320,13 @@ def test_plan_reused_with_new_lengths_matches_a_fresh_plan(dtype, layers, B, I, 
         dc.bwd(plan)
         assert plan.status_sync() == 0
         got = dc.results()
-        ref, err = run_case(w, inp2)
-        assert err == 0
+        fresh = DeviceCase(inp2, w.H, w.I, w.layers, w.dtype, cell=cell, ponder_max=pm)
+        plan2 = fresh.plan()
+        fresh.fwd(plan2)
+        fresh.bwd(plan2)
+        assert plan2.status_sync() == 0
+        ref = fresh.results()
+        plan2.close()
         for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
             np.testing.assert_array_equal(got[k], ref[k])
         for u, v in zip(got["dW"] + got["dbias"], ref["dW"] + ref["dbias"]):
