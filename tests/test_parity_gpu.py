@@ -280,14 +280,22 @@ def test_inference_forward_between_saved_forwards_changes_nothing(dtype, layers)
         np.testing.assert_array_equal(u, v)
 
 
-@pytest.mark.parametrize("dtype,layers,B,I,H", [("bf16", 1, 48, 64, 128), ("f32", 1, 48, 64, 128),
-                                               ("bf16", 2, 48, 64, 128), ("bf16", 1, 128, 1024, 1024)])
-def test_plan_reused_with_new_lengths_matches_a_fresh_plan(dtype, layers, B, I, H):
+@pytest.mark.parametrize("dtype,layers,B,I,H,loops", [
+    ("bf16", 1, 48, 64, 128, "auto"), ("f32", 1, 48, 64, 128, "auto"), ("bf16", 2, 48, 64, 128, "auto"),
+    ("bf16", 1, 128, 1024, 1024, "auto"), ("bf16", 1, 64, 64, 2048, "auto"), ("f32", 1, 64, 64, 1024, "auto"),
+    ("f32", 1, 48, 64, 128, "grid")])
+def test_plan_reused_with_new_lengths_matches_a_fresh_plan(dtype, layers, B, I, H, loops, monkeypatch):
     """Everything a call derives from the lengths (trip count, order, compact
-    offsets, row maps, loop flags) is rebuilt on the device by each call: a
-    plan reused with other lengths in the same seq_len buffer gives the
-    results of a fresh plan bitwise, also when the new trip count is
-    shorter or zero (the last case has the benchmark's widths)."""
+    offsets, row maps, loop flags, barrier counters) is rebuilt on the device
+    by each call: a plan reused with other lengths in the same seq_len
+    buffer gives the results of a fresh plan bitwise, also when the new trip
+    count is shorter or zero (XCD-local loops, the benchmark's widths, the
+    chip-wide loops of bf16 H = 2048 and f32 H = 1024, the grid-barrier
+    loops)."""
+    if loops == "grid":
+        monkeypatch.setenv("LSTMLOOP_LOOPS", "grid")
+    else:
+        monkeypatch.delenv("LSTMLOOP_LOOPS", raising=False)
     w = W("new_lengths", B=B, I=I, H=H, T_max=15, dtype=dtype, layers=layers, len_lo=0,
           len_hi=15, random_state=True, with_dy=True, seed=33)
     _check_reuse_with_new_lengths(w, "lstm")
@@ -308,6 +316,7 @@ def _check_reuse_with_new_lengths(w, cell):
     inp = wl.generate(w)
     dc = DeviceCase(inp, w.H, w.I, w.layers, w.dtype, cell=cell, ponder_max=pm)
     plan = dc.plan()
+    say(f"    loops {plan.geometry()}")
     dc.fwd(plan)
     dc.bwd(plan)
     rng = np.random.default_rng(34)
